@@ -1,0 +1,113 @@
+/*
+ * hcmix -- rotating-hypercube mixing layers on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libhcmix.so.  Plain pointers and sizes only; no HIP or framework
+ * types appear here (a stream is passed as `void*` holding a hipStream_t,
+ * NULL meaning the default stream).
+ *
+ * The operation (paper "Reaching Every Position Without Searching"):
+ *   Section 3.1 -- a window of n = 2^b positions is a b-dimensional hypercube;
+ *   at layer l position i is linked to its partner i XOR 2^(l mod b).  In the
+ *   causal form only the earlier endpoint of each link is kept: position i
+ *   takes its partner's vector only when bit (l mod b) of i is set.
+ *   Section 3.2, Eq. (1) -- y_i = W_self x_i + W_off x_partner(i): two linear
+ *   maps and a shift, with no bias, residual or nonlinearity.
+ *
+ * Layouts (all row-major, contiguous, no padding):
+ *   x, y, dx, dy   [batch][n][width] in `dtype` (bf16 or fp32).  Windows are
+ *                  independent; position i of window t is row t*n + i.
+ *   w_self, w_off  [width_out][width_in] in `dtype`, so y = W x reads
+ *                  y[o] = sum_c W[o][c] x[c].
+ *   dw_self, dw_off  [width_out][width_in] fp32.
+ *
+ * Ownership and ordering: the caller owns every buffer (device memory) and
+ * keeps it alive until the enqueued work finishes.  The library allocates and
+ * frees nothing, keeps no state between calls, never synchronises, and
+ * enqueues all work on `stream` in call order.  Calls on different streams
+ * that share an output buffer race.
+ *
+ * Errors: arguments are validated before anything is enqueued; a rejected
+ * call has no effect.  HCMIX_ERR_INVALID_VALUE: null pointer, batch < 1, n not
+ * a power of two >= 2, width < 1, layer < 0, unknown mode or dtype, an output
+ * that overlaps an input, workspace smaller than the query, sizes beyond
+ * 2^31 rows.  HCMIX_ERR_UNSUPPORTED: a shape or alignment this build has no
+ * kernel for (bf16 needs width a multiple of 64 and 16-byte aligned
+ * pointers; fp32 needs 4-byte aligned pointers).  HCMIX_ERR_HIP: a HIP call
+ * or kernel launch failed; the message is available from
+ * hcmix_last_hip_error().
+ */
+#ifndef HCMIX_H
+#define HCMIX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HCMIX_OK = 0,
+  HCMIX_ERR_INVALID_VALUE = 1,
+  HCMIX_ERR_UNSUPPORTED = 2,
+  HCMIX_ERR_HIP = 3
+} hcmix_status;
+
+typedef enum { HCMIX_F32 = 0, HCMIX_BF16 = 1 } hcmix_dtype;
+
+/* HCMIX_BIDIR: every position takes its partner (Section 3.1, 2n links per
+ * layer counting self).  HCMIX_CAUSAL: only the later endpoint of a link
+ * receives, i.e. position i receives when bit d of i is 1 (n + n/2 links). */
+typedef enum { HCMIX_BIDIR = 0, HCMIX_CAUSAL = 1 } hcmix_mode;
+
+/* Human-readable name of a status code (static storage). */
+const char* hcmix_status_string(int32_t status);
+
+/* Text of the last HIP error seen by this thread ("" if none). */
+const char* hcmix_last_hip_error(void);
+
+/* Hypercube dimension used at layer `layer` for windows of n positions
+ * (Section 3.1): layer mod log2(n).  Returns -1 if n is not a power of two
+ * >= 2 or layer < 0.  A fixed (un-rotated) schedule simply passes the same
+ * layer index every time; any dimension d < log2(n) is selected by layer = d. */
+int32_t hcmix_dim(int32_t layer, int64_t n);
+
+/* Forward of one layer, Eq. (1):
+ *   y[t][i] = W_self x[t][i] + m(i) W_off x[t][i XOR 2^d],   d = hcmix_dim(layer, n)
+ * with m(i) = 1 (HCMIX_BIDIR) or bit d of i (HCMIX_CAUSAL).
+ * bf16: inputs bf16, products accumulated in fp32, y rounded to bf16 (nearest
+ * even).  fp32: fp32 throughout, no reduced-precision matrix instructions.
+ * y must not overlap x. */
+hcmix_status hcmix_forward(int64_t batch, int64_t n, int64_t width, int32_t layer,
+                           int32_t mode, int32_t dtype, const void* x,
+                           const void* w_self, const void* w_off, void* y,
+                           void* stream);
+
+/* Bytes of device workspace hcmix_backward needs for this shape (0 if none),
+ * or 0 for invalid arguments. The workspace must be 256-byte aligned. */
+size_t hcmix_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                      int32_t dtype);
+
+/* Backward of one layer: the adjoint of hcmix_forward.  Given dy = dL/dy,
+ *   dx[t][j]  = W_self^T dy[t][j] + m'(j) W_off^T dy[t][j XOR 2^d]
+ *               with m'(j) = 1 (bidir) or 1 - bit d of j (causal: j is the
+ *               earlier endpoint of the link it sends on)
+ *   dw_self   = sum over (t, i) of dy[t][i] x[t][i]^T
+ *   dw_off    = sum over (t, i) of m(i) dy[t][i] x[t][i XOR 2^d]^T
+ * dx is in `dtype` (bf16: fp32 accumulation, rounded once); dw_* are fp32,
+ * overwritten when accumulate == 0 and added to when accumulate != 0.
+ * dx, dw_self, dw_off and workspace must not overlap each other or any input.
+ * The weight-gradient reduction over rows runs in a fixed order, so repeated
+ * calls give bitwise-identical results. */
+hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t layer,
+                            int32_t mode, int32_t dtype, const void* x,
+                            const void* w_self, const void* w_off, const void* dy,
+                            void* dx, float* dw_self, float* dw_off,
+                            int32_t accumulate, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HCMIX_H */

@@ -1,0 +1,60 @@
+// Internal declarations shared by the hcmix HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hcmix {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Row bookkeeping for one layer along hypercube dimension d (stride s = 2^d).
+// A flattened row r = t*n + i (window t, position i) keeps bit d of i as bit d
+// of r because n is a power of two above s, so r XOR s is the partner in the
+// same window.  The rows with bit d clear ("lower" rows: the earlier endpoint
+// of each link) are enumerated by q = 0 .. rows/2-1 by inserting a zero bit at
+// position d; the partner "upper" row is lower_row(q) + s.
+__device__ __forceinline__ int lower_row(int q, int d) {
+  const int lo = q & ((1 << d) - 1);
+  return ((q >> d) << (d + 1)) | lo;
+}
+
+// fp32 -> bf16, round to nearest even (the gfx950 conversion instruction).
+__device__ __forceinline__ bf16 to_bf16(float v) { return (bf16)v; }
+
+// ---- launchers (each returns hipGetLastError() of its launch) ----
+
+// out[r][j] = sum_k A[r][k] B1(j,k) + m(r) sum_k A[r^s][k] B2(j,k), fp32.
+// B(j,k) = W[j*width+k] when !transpose_w, W[k*width+j] when transpose_w.
+// m(r) = partner_lower for rows with bit d clear, partner_upper otherwise.
+hipError_t launch_mix_f32(const float* A, const float* W1, const float* W2, float* out,
+                          int rows, int width, int d, int partner_lower, int partner_upper,
+                          bool transpose_w, hipStream_t st);
+
+// dW_self = dY^T X ; dW_off = sum over receiving rows of dY[r] X[r^s]^T, fp32.
+hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo,
+                         int rows, int width, int d, int bidir, int accumulate,
+                         hipStream_t st);
+
+// bf16 MFMA: same contraction as launch_mix_f32 with B1/B2 given as
+// [width_out][width_in] (k contiguous).  width % 64 == 0.
+hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out,
+                           int rows, int width, int d, int partner_lower, int partner_upper,
+                           hipStream_t st);
+
+// WT[c][o] = W[o][c] for two width x width bf16 matrices.
+hipError_t launch_transpose2_bf16(const bf16* W1, const bf16* W2, bf16* W1T, bf16* W2T,
+                                  int width, hipStream_t st);
+
+// Split-K weight gradients into `partial` ([splits][2][width][width] fp32),
+// then a fixed-order reduction into dws / dwo.
+int dw_bf16_splits(int rows, int width);
+hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* dws, float* dwo,
+                          int rows, int width, int d, int bidir, int accumulate,
+                          hipStream_t st);
+
+}  // namespace hcmix

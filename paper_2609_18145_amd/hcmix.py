@@ -1,0 +1,194 @@
+"""Python binding of libhcmix.so (ctypes; argument marshalling only).
+
+Every step of the layer runs in the HIP library; PyTorch supplies device
+memory and the current stream.  If the library is not built this module
+raises on first use: there is no CPU or PyTorch fallback.
+
+    y = forward(x, w_self, w_off, layer, causal)
+    dx, dws, dwo = backward(x, w_self, w_off, dy, layer, causal)
+    y = Stack.apply(x, layers, causal, *w_selfs, *w_offs)   # autograd over L layers
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhcmix.so")
+
+HCMIX_OK, HCMIX_ERR_INVALID_VALUE, HCMIX_ERR_UNSUPPORTED, HCMIX_ERR_HIP = 0, 1, 2, 3
+HCMIX_F32, HCMIX_BF16 = 0, 1
+HCMIX_BIDIR, HCMIX_CAUSAL = 0, 1
+
+# every symbol declared in include/hcmix.h
+EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_forward",
+           "hcmix_backward_workspace_bytes", "hcmix_backward")
+
+_lib = None
+
+
+class HcmixError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        lib = load()
+        msg = lib.hcmix_status_string(status).decode()
+        if status == HCMIX_ERR_HIP:
+            msg += ": " + lib.hcmix_last_hip_error().decode()
+        super().__init__(f"{what}: {msg}")
+        self.status = status
+
+
+def load():
+    """Load libhcmix.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_18145_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        i64, i32, vp, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+        fp = ctypes.POINTER(ctypes.c_float)
+        lib.hcmix_status_string.argtypes, lib.hcmix_status_string.restype = [i32], ctypes.c_char_p
+        lib.hcmix_last_hip_error.argtypes, lib.hcmix_last_hip_error.restype = [], ctypes.c_char_p
+        lib.hcmix_dim.argtypes, lib.hcmix_dim.restype = [i32, i64], i32
+        lib.hcmix_forward.argtypes = [i64, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp]
+        lib.hcmix_forward.restype = i32
+        lib.hcmix_backward_workspace_bytes.argtypes = [i64, i64, i64, i32]
+        lib.hcmix_backward_workspace_bytes.restype = sz
+        lib.hcmix_backward.argtypes = [i64, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, fp, fp,
+                                       i32, vp, sz, vp]
+        lib.hcmix_backward.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return HCMIX_BF16
+    if t.dtype == torch.float32:
+        return HCMIX_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _fptr(t):
+    return ctypes.cast(ctypes.c_void_p(t.data_ptr()), ctypes.POINTER(ctypes.c_float))
+
+
+def _check(x, *others):
+    if not x.is_cuda:
+        raise ValueError("hcmix works on GPU tensors only")
+    for t in (x, *others):
+        if t.device != x.device or t.dtype != x.dtype or not t.is_contiguous():
+            raise ValueError("all operands must be contiguous, on one device, of one dtype")
+
+
+def _stream(x):
+    return ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
+
+
+def dim(layer: int, n: int) -> int:
+    return load().hcmix_dim(layer, n)
+
+
+def forward(x: torch.Tensor, w_self: torch.Tensor, w_off: torch.Tensor, layer: int,
+            causal: bool, out: torch.Tensor | None = None) -> torch.Tensor:
+    """y = W_self x_i + m(i) W_off x_(i xor 2^d) over x of shape [batch, n, width]."""
+    _check(x, w_self, w_off)
+    batch, n, width = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    rc = load().hcmix_forward(batch, n, width, layer, int(bool(causal)), _dtype_code(x),
+                              _ptr(x), _ptr(w_self), _ptr(w_off), _ptr(out), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_forward")
+    return out
+
+
+def workspace_bytes(batch: int, n: int, width: int, dtype: torch.dtype) -> int:
+    code = HCMIX_BF16 if dtype == torch.bfloat16 else HCMIX_F32
+    return load().hcmix_backward_workspace_bytes(batch, n, width, code)
+
+
+def alloc_workspace(batch, n, width, dtype, device) -> torch.Tensor | None:
+    nbytes = workspace_bytes(batch, n, width, dtype)
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def backward(x, w_self, w_off, dy, layer: int, causal: bool, dx=None, dw_self=None,
+             dw_off=None, accumulate: bool = False, workspace=None):
+    """Adjoint of ``forward``: returns (dx, dw_self, dw_off); dw_* are fp32."""
+    _check(x, w_self, w_off, dy)
+    batch, n, width = x.shape
+    if dx is None:
+        dx = torch.empty_like(x)
+    if dw_self is None:
+        dw_self = torch.empty((width, width), dtype=torch.float32, device=x.device)
+    if dw_off is None:
+        dw_off = torch.empty((width, width), dtype=torch.float32, device=x.device)
+    if workspace is None:
+        workspace = alloc_workspace(batch, n, width, x.dtype, x.device)
+    ws_bytes = workspace.numel() if workspace is not None else 0
+    rc = load().hcmix_backward(batch, n, width, layer, int(bool(causal)), _dtype_code(x),
+                               _ptr(x), _ptr(w_self), _ptr(w_off), _ptr(dy), _ptr(dx),
+                               _fptr(dw_self), _fptr(dw_off), int(bool(accumulate)),
+                               _ptr(workspace), ws_bytes, _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_backward")
+    return dx, dw_self, dw_off
+
+
+def stack_forward(x, w_selfs, w_offs, layers, causal, outs=None):
+    """Run the layers in order; returns the list [x_0, x_1, ..., x_L]."""
+    xs = [x]
+    for l, (ws, wo, layer) in enumerate(zip(w_selfs, w_offs, layers)):
+        xs.append(forward(xs[-1], ws, wo, layer, causal, out=None if outs is None else outs[l]))
+    return xs
+
+
+def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dxs=None, dws=None, dwo=None,
+                   workspace=None):
+    """Backward through the stack in reverse; returns (dx_0, [dW_self], [dW_off])."""
+    L = len(layers)
+    x0 = xs[0]
+    batch, n, width = x0.shape
+    if workspace is None:
+        workspace = alloc_workspace(batch, n, width, x0.dtype, x0.device)
+    g = dy
+    dws = dws if dws is not None else [None] * L
+    dwo = dwo if dwo is not None else [None] * L
+    for l in reversed(range(L)):
+        out = None if dxs is None else dxs[l]
+        g, dws[l], dwo[l] = backward(xs[l], w_selfs[l], w_offs[l], g, layers[l], causal, dx=out,
+                                     dw_self=dws[l], dw_off=dwo[l], workspace=workspace)
+    return g, dws, dwo
+
+
+class Stack(torch.autograd.Function):
+    """Autograd over a stack of mixing layers.
+
+    Stack.apply(x, layers, causal, *w_selfs, *w_offs) -> x_L"""
+
+    @staticmethod
+    def forward(ctx, x, layers, causal, *weights):
+        L = len(layers)
+        w_selfs, w_offs = weights[:L], weights[L:]
+        xs = stack_forward(x.contiguous(), w_selfs, w_offs, layers, causal)
+        ctx.layers, ctx.causal = list(layers), causal
+        ctx.save_for_backward(*xs[:-1], *weights)
+        return xs[-1]
+
+    @staticmethod
+    def backward(ctx, gy):
+        L = len(ctx.layers)
+        saved = ctx.saved_tensors
+        xs, w_selfs, w_offs = saved[:L], saved[L:2 * L], saved[2 * L:]
+        dx, dws, dwo = stack_backward(list(xs), w_selfs, w_offs, ctx.layers, gy.contiguous(),
+                                      ctx.causal)
+        grads_w = [g.to(w.dtype) for g, w in zip(dws + dwo, list(w_selfs) + list(w_offs))]
+        return (dx, None, None, *grads_w)

@@ -1,0 +1,173 @@
+"""Whole-stack parity of the HIP path against the CPU oracle, at the
+workloads' real shapes (through the C ABI via the Python binding)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_18145_amd import hcmix, inputs
+from tests.util import TOL, fro_rel_err, row_rel_err, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    hcmix.load()
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def run_gpu_stack(s, with_backward=True):
+    dt = s.dtype
+    x = to_dev(s.x, dt)
+    ws = [to_dev(w, dt) for w in s.w_self]
+    wo = [to_dev(w, dt) for w in s.w_off]
+    xs = hcmix.stack_forward(x, ws, wo, s.layers, s.causal)
+    out = {"y": xs[-1]}
+    if with_backward:
+        dx, dws, dwo = hcmix.stack_backward(xs, ws, wo, s.layers, to_dev(s.dy, dt), s.causal)
+        out.update(dx=dx, dws=dws, dwo=dwo)
+    torch.cuda.synchronize()
+    return {k: ([to_host(t) for t in v] if isinstance(v, list) else to_host(v))
+            for k, v in out.items()}
+
+
+def check_stack(s, got, windows=None, with_dw=True):
+    tol = TOL[s.dtype]
+    sel = slice(None) if windows is None else windows
+    x = s.x[sel]
+    xs = oracle.stack_forward(x, s.w_self, s.w_off, s.layers, s.causal)
+    e_y = row_rel_err(got["y"][sel], xs[-1])
+    log(f"  y row err {e_y:.3e}")
+    assert e_y <= tol
+    if "dx" in got:
+        dx, dws, dwo = oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, s.dy[sel], s.causal)
+        e_dx = row_rel_err(got["dx"][sel], dx)
+        log(f"  dx row err {e_dx:.3e}")
+        assert e_dx <= tol
+        if with_dw:
+            e_w = max(max(fro_rel_err(g, r) for g, r in zip(got["dws"], dws)),
+                      max(fro_rel_err(g, r) for g, r in zip(got["dwo"], dwo)))
+            log(f"  dW fro err {e_w:.3e}")
+            assert e_w <= tol
+
+
+@pytest.mark.parametrize("schedule", ["rot", "fixed"])
+def test_tiny_stack_fp32(schedule):
+    """n=16, width 32, batch 2, 4 layers in fp32: the rotated stack (d = 0..3)
+    and the un-rotated control that repeats d = 0."""
+    layers = oracle.schedule_rot(4) if schedule == "rot" else oracle.schedule_fixed(4)
+    s = inputs.make_preset("tiny", layers=layers)
+    log(f"tiny fp32 {schedule}")
+    check_stack(s, run_gpu_stack(s))
+
+
+def test_tiny_impulse_reaches_everyone_only_when_rotated():
+    """Impulse at one position: after log2 n rotated layers every position of
+    its window is nonzero; under the fixed control only the pair {j, j^1}."""
+    n, width = 16, 32
+    for j in [0, 5, 15]:
+        x = np.zeros((1, n, width), dtype=np.float32)
+        x[0, j] = 1.0
+        one = np.eye(width, dtype=np.float32)
+        tx = to_dev(x, "f32")
+        te = to_dev(one, "f32")
+        for layers, expect_all in ((oracle.schedule_rot(4), True), (oracle.schedule_fixed(4), False)):
+            xs = hcmix.stack_forward(tx, [te] * 4, [te] * 4, layers, False)
+            y = to_host(xs[-1])[0]
+            reached = set(np.flatnonzero(np.abs(y).sum(axis=1)))
+            assert reached == (set(range(n)) if expect_all else {j, j ^ 1})
+
+
+@pytest.mark.parametrize("schedule", ["rot", "fixed"])
+def test_reach_stack_bf16_full_size(schedule):
+    """n=256, width 64, batch 64, 8 bidirectional layers, bf16: whole stack,
+    forward and backward, every output compared."""
+    layers = oracle.schedule_rot(8) if schedule == "rot" else oracle.schedule_fixed(8)
+    s = inputs.make_preset("reach", layers=layers)
+    log(f"reach bf16 {schedule}")
+    check_stack(s, run_gpu_stack(s))
+
+
+def test_lm256_stack_bf16_sampled_windows():
+    """n=256, width 512, batch 64, 16 causal layers, bf16, in the launch
+    configuration of the benchmark; the oracle recomputes three of the 64
+    windows (windows are independent, so this is their exact reference)."""
+    s = inputs.make_preset("lm256")
+    log("lm256 bf16 full batch")
+    got = run_gpu_stack(s)
+    check_stack(s, got, windows=[0, 31, 63], with_dw=False)
+
+
+def test_lm256_stack_bf16_weight_gradients():
+    """Same stack at batch 4 so the oracle can form every weight gradient."""
+    s = inputs.make_preset("lm256", batch=4)
+    log("lm256 bf16 batch 4")
+    check_stack(s, run_gpu_stack(s))
+
+
+def test_lm256_layer_full_size_with_weight_gradients():
+    """One layer at the benchmark's full shape and launch configuration
+    (64 windows of 256 x 512): every output, including both weight gradients,
+    against the oracle."""
+    s = inputs.make_preset("lm256", num_layers=1)
+    x, ws, wo, dy = (to_dev(a, "bf16") for a in (s.x, s.w_self[0], s.w_off[0], s.dy))
+    for layer in (7, 0):
+        log(f"lm256 full-size layer {layer}")
+        y = hcmix.forward(x, ws, wo, layer, True)
+        dx, dws, dwo = hcmix.backward(x, ws, wo, dy, layer, True)
+        torch.cuda.synchronize()
+        ry = oracle.forward(s.x, s.w_self[0], s.w_off[0], layer, True)
+        rdx, rws, rwo = oracle.backward(s.x, s.w_self[0], s.w_off[0], s.dy, layer, True)
+        assert row_rel_err(to_host(y), ry) <= TOL["bf16"]
+        assert row_rel_err(to_host(dx), rdx) <= TOL["bf16"]
+        assert fro_rel_err(to_host(dws), rws) <= 1e-4
+        assert fro_rel_err(to_host(dwo), rwo) <= 1e-4
+
+
+def test_long4096_layers_bf16_sampled():
+    """n=4096, width 1024 (strides up to 2048 rows): the layers with the
+    largest and smallest strides at full shape (batch 8), outputs of window 0
+    against the oracle; weight gradients from a one-window call."""
+    s = inputs.make_preset("long4096", num_layers=1)
+    x = to_dev(s.x, "bf16")
+    dy = to_dev(s.dy, "bf16")
+    ws = to_dev(s.w_self[0], "bf16")
+    wo = to_dev(s.w_off[0], "bf16")
+    for layer in (11, 0):
+        log(f"long4096 layer {layer}")
+        y = hcmix.forward(x, ws, wo, layer, True)
+        dx, _, _ = hcmix.backward(x, ws, wo, dy, layer, True)
+        _, dws1, dwo1 = hcmix.backward(x[:1].contiguous(), ws, wo, dy[:1].contiguous(), layer, True)
+        torch.cuda.synchronize()
+        ry = oracle.forward(s.x[:1], s.w_self[0], s.w_off[0], layer, True)
+        rdx, rws, rwo = oracle.backward(s.x[:1], s.w_self[0], s.w_off[0], s.dy[:1], layer, True)
+        assert row_rel_err(to_host(y)[:1], ry) <= TOL["bf16"]
+        assert row_rel_err(to_host(dx)[:1], rdx) <= TOL["bf16"]
+        assert fro_rel_err(to_host(dws1), rws) <= 1e-4
+        assert fro_rel_err(to_host(dwo1), rwo) <= 1e-4
+
+
+def test_autograd_stack_matches_oracle():
+    s = inputs.make_preset("reach", batch=4, num_layers=8)
+    dt = torch.bfloat16
+    x = to_dev(s.x, "bf16").requires_grad_(True)
+    ws = [to_dev(w, "bf16").requires_grad_(True) for w in s.w_self]
+    wo = [to_dev(w, "bf16").requires_grad_(True) for w in s.w_off]
+    y = hcmix.Stack.apply(x, s.layers, s.causal, *ws, *wo)
+    y.backward(to_dev(s.dy, "bf16"))
+    torch.cuda.synchronize()
+    xs = oracle.stack_forward(s.x, s.w_self, s.w_off, s.layers, s.causal)
+    dx, dws, dwo = oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, s.dy, s.causal)
+    assert y.dtype == dt
+    assert row_rel_err(to_host(y), xs[-1]) <= TOL["bf16"]
+    assert row_rel_err(to_host(x.grad), dx) <= TOL["bf16"]
+    for g, r in zip(ws, dws):
+        assert fro_rel_err(to_host(g.grad), r) <= TOL["bf16"]
+    for g, r in zip(wo, dwo):
+        assert fro_rel_err(to_host(g.grad), r) <= TOL["bf16"]
