@@ -166,21 +166,25 @@ def main():
 
 def cpu_baseline(s, n, w, L, causal, windows):
     """The CPU oracle (plain fp64 loops) on a bounded sample: `windows` windows
-    of the same workload through every layer, forward and backward."""
+    of the same workload through every layer, forward and backward.  With
+    windows == 0 one window is timed first and the sample is sized to about
+    15 s of CPU work from that."""
     import oracle
+
+    def run(k):
+        t0 = time.perf_counter()
+        xs = oracle.stack_forward(s.x[:k], s.w_self, s.w_off, s.layers, causal)
+        oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, s.dy[:k], causal)
+        return time.perf_counter() - t0
+
     if windows <= 0:
-        # ~9 w^2 flops per position-layer at a few GFLOP/s: aim for ~15 s
-        windows = max(1, min(s.x.shape[0], int(15 * 4e9 / (9 * w * w * n * L))))
-    x = s.x[:windows]
-    dy = s.dy[:windows]
-    t0 = time.perf_counter()
-    xs = oracle.stack_forward(x, s.w_self, s.w_off, s.layers, causal)
-    oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, dy, causal)
-    dt = time.perf_counter() - t0
+        t1 = run(1)
+        windows = max(1, min(s.x.shape[0], int(15.0 / max(t1, 1e-3))))
+    dt = run(windows)
     return {"value": round(windows * n * L / dt, 1), "unit": UNIT, "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"{windows} of the workload's windows, all {L} layers, forward+backward, "
-                      f"{dt:.1f} s"}
+            "sample": f"{windows} of the workload's {s.x.shape[0]} windows, all {L} layers, "
+                      f"forward+backward, {dt:.1f} s"}
 
 
 if __name__ == "__main__":

@@ -1,7 +1,7 @@
 // C ABI of libhcmix.so: argument validation and kernel dispatch.
 // Every check runs before anything is enqueued, so a rejected call has no
 // effect; there is one kernel path per dtype and no fallback.
-#include "../../include/hcmix.h"
+#include "hcmix.h"
 #include "hcmix_internal.h"
 
 #include <string.h>
@@ -43,16 +43,14 @@ hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer,
   return HCMIX_OK;
 }
 
-// Backward workspace layout (bf16): [W_self^T | W_off^T] bf16, then the
-// split-K partial sums [splits][2][width][width] fp32, each 256-byte aligned.
+// Backward workspace (bf16): the split-K partial sums of the weight gradients,
+// [splits][2][width][width] fp32.
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
-
-size_t bf16_wt_bytes(int64_t width) { return align256((size_t)2 * width * width * 2); }
 
 size_t workspace_bytes_checked(int64_t batch, int64_t n, int64_t width, int32_t dtype) {
   if (dtype != HCMIX_BF16) return 0;
   const int splits = dw_bf16_splits((int)(batch * n), (int)width);
-  return bf16_wt_bytes(width) + align256((size_t)splits * 2 * width * width * sizeof(float));
+  return align256((size_t)splits * 2 * width * width * sizeof(float));
 }
 
 }  // namespace
@@ -99,7 +97,8 @@ hcmix_status hcmix_forward(int64_t batch, int64_t n, int64_t width, int32_t laye
   hipError_t e;
   if (dtype == HCMIX_BF16)
     e = launch_mix_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y, rows,
-                        w, d, /*partner_lower=*/bidir, /*partner_upper=*/1, s);
+                        w, d, /*partner_lower=*/bidir, /*partner_upper=*/1,
+                        /*transpose_b=*/false, s);
   else
     e = launch_mix_f32((const float*)x, (const float*)w_self, (const float*)w_off, (float*)y,
                        rows, w, d, bidir, 1, /*transpose_w=*/false, s);
@@ -150,13 +149,10 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;
   if (dtype == HCMIX_BF16) {
-    bf16* wsT = (bf16*)workspace;
-    bf16* woT = wsT + (size_t)w * w;
-    float* partial = (float*)((char*)workspace + bf16_wt_bytes(width));
-    e = launch_transpose2_bf16((const bf16*)w_self, (const bf16*)w_off, wsT, woT, w, s);
-    if (e == hipSuccess)
-      e = launch_mix_bf16((const bf16*)dy, wsT, woT, (bf16*)dx, rows, w, d,
-                          /*partner_lower=*/1, /*partner_upper=*/bidir, s);
+    float* partial = (float*)workspace;
+    e = launch_mix_bf16((const bf16*)dy, (const bf16*)w_self, (const bf16*)w_off, (bf16*)dx,
+                        rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
+                        /*transpose_b=*/true, s);
     if (e == hipSuccess)
       e = launch_dw_bf16((const bf16*)x, (const bf16*)dy, partial, dw_self, dw_off, rows, w, d,
                          bidir, accumulate != 0, s);

@@ -40,15 +40,12 @@ hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo
                          int rows, int width, int d, int bidir, int accumulate,
                          hipStream_t st);
 
-// bf16 MFMA: same contraction as launch_mix_f32 with B1/B2 given as
-// [width_out][width_in] (k contiguous).  width % 64 == 0.
+// bf16 MFMA: same contraction as launch_mix_f32.  B(j,k) = B[j*width+k] when
+// !transpose_b, B[k*width+j] when transpose_b (read transposed from LDS).
+// width % 64 == 0.
 hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out,
                            int rows, int width, int d, int partner_lower, int partner_upper,
-                           hipStream_t st);
-
-// WT[c][o] = W[o][c] for two width x width bf16 matrices.
-hipError_t launch_transpose2_bf16(const bf16* W1, const bf16* W2, bf16* W1T, bf16* W2T,
-                                  int width, hipStream_t st);
+                           bool transpose_b, hipStream_t st);
 
 // Split-K weight gradients into `partial` ([splits][2][width][width] fp32),
 // then a fixed-order reduction into dws / dwo.

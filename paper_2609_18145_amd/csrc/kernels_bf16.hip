@@ -6,311 +6,460 @@
 // block's row set is closed under XOR 2^d for every stride 1 .. n/2, so the
 // partner of LDS row m is LDS row m +- BMP and the XOR gather is just a
 // different LDS base address; no permuted copy of the activations is ever
-// written.  Each 16-byte global load is a whole 16-byte piece of one row, so
-// every stride is fetched at full line efficiency.
+// written.  Each 16-byte load is a whole 16-byte piece of one row, so every
+// stride is fetched at full line efficiency.
+//
+// Tiles move global -> LDS with global_load_lds_dwordx4 (lane i of a wave
+// writes 16 bytes at LDS base + 16*i), so the swizzled LDS layouts below are
+// produced by choosing each lane's source address.
+//
+// Operands whose contraction index is not the contiguous one (the weights in
+// the dX product, both operands of the weight gradients) stay in their
+// natural row-major layout in LDS and are read transposed with
+// ds_read_b64_tr_b16: within each group of 16 lanes, source lane j points at
+// row (base + j/4), column (c0 + 4*(j%4)); lane i then receives column c0 + i
+// of those 4 rows.
 #include "hcmix_internal.h"
 
 namespace hcmix {
 
 namespace {
 
-constexpr int BK = 64;       // contraction slice held in LDS (128 bytes per row)
-constexpr int CH = BK / 8;   // 16-byte pieces per row of a slice
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr int BK = 64;       // contraction slice per pipeline stage (128-byte rows)
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// LDS offset (in elements) of 16-byte piece `ch` of tile row `m`; the piece
-// index is XOR-swizzled with the row so that 8 consecutive rows read at the
-// same piece hit 8 different bank groups.
-__device__ __forceinline__ int swz(int m, int ch) { return m * BK + ((ch ^ (m & 7)) << 3); }
+// 16 bytes global -> LDS; `lds` is the wave-uniform base, lane i lands at +16*i.
+__device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Scheduling hint for one MFMA sub-step: alternate its NMFMA matrix
+// instructions with the NDS LDS reads that fetch the next sub-step's
+// fragments, spreading the reads evenly, so LDS latency hides under MFMAs.
+template <int NMFMA, int NDS>
+__device__ __forceinline__ void interleave_mfma_ds() {
+#pragma unroll
+  for (int i = 0; i < NMFMA; i++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+    const int nds = (NDS * (i + 1)) / NMFMA - (NDS * i) / NMFMA;
+    if (nds == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    if (nds == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if (nds == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+  }
+}
+
+// LDS has 64 banks of 4 bytes: a 128-bit access is conflict-free when each
+// group of 16 lanes covers 256 distinct bytes (mod 256), a 64-bit access when
+// each group of 32 lanes does.
+//
+// k-contiguous tile [rows][BK] (128-byte rows): 16-byte piece `ch` of row m
+// sits at piece ch ^ ((m >> 1) & 7), so 16 consecutive rows reading the same
+// piece land in 16 distinct 16-byte slots.  Offsets in elements.
+__device__ __forceinline__ int swz(int m, int ch) {
+  return m * BK + ((ch ^ ((m >> 1) & 7)) << 3);
+}
+
+// Row-major tile read transposed, RB bytes per row (256 or 128): 64-byte
+// segment `seg` of row `row` is stored at segment seg ^ f(row), so the 4 rows
+// x 64 bytes that 32 lanes of a tr read touch fall in distinct bank quarters.
+template <int RB>
+__device__ __forceinline__ int trswz(int row, int seg) {
+  static_assert(RB == 256 || RB == 128, "row of 64 or 128 bf16");
+  return RB == 256 ? (seg ^ (row & 3)) : (seg ^ ((row >> 1) & 1));
+}
+
+// Transposed 32x32x16 operand fragment from a row-major tile T[k][col] with
+// RB-byte rows: lane l gets T[k0 + 8*(l/32) + t][c0 + l%32], t = 0..7, the same
+// k order as a ds_read_b128 fragment of a k-contiguous tile.  c0 % 32 == 0.
+template <int RB>
+__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, int k0, int c0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const int row = k0 + 8 * (g >> 1) + (j >> 2);
+  const int seg = c0 >> 5;                                   // 32 columns = 64 bytes
+  const int in = 16 * (g & 1) + 4 * (j & 3);                 // column within the segment
+  const bf16* p = tile + row * (RB / 2) + trswz<RB>(row, seg) * 32 + in;
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * (RB / 2)));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Source element offset (row, column) for lane i of DMA block b of a tr tile.
+template <int RB>
+__device__ __forceinline__ void tr_dma_coord(int b, int i, int* row, int* col) {
+  const int o = b * 1024 + 16 * i;          // byte offset in the tile
+  const int r = o / RB, ob = o % RB;
+  const int seg = trswz<RB>(r, ob >> 6);    // the swizzle is an involution
+  *row = r;
+  *col = seg * 32 + ((ob & 63) >> 1);
+}
+
+// Block index -> tile index, keeping consecutive tiles (the column tiles of
+// one row tile) on one XCD: blocks are dealt to the 8 XCDs round-robin.
+__device__ __forceinline__ int xcd_tile(int bid, int total) {
+  if (total % 8 != 0) return bid;
+  return (bid % 8) * (total / 8) + bid / 8;
+}
 
 // ---------------------------------------------------------------------------
 // Mix GEMM.  For the block's lower rows L and upper rows U:
-//   out_L = A_L B1^T + [partner_lower] A_U B2^T
-//   out_U = A_U B1^T + [partner_upper] A_L B2^T
-// Forward: A = x, B1 = W_self, B2 = W_off, partner_upper = 1, partner_lower = bidir.
-// dX:      A = dy, B1 = W_self^T, B2 = W_off^T, partner_lower = 1, partner_upper = bidir.
+//   out_L = A_L B1^T + [PL] A_U B2^T
+//   out_U = A_U B1^T + [PU] A_L B2^T
+// B(n, k) is B[n*width + k] (k contiguous), or B[k*width + n] when TRANS_B.
+// Forward: A = x, B1 = W_self, B2 = W_off, PU = 1, PL = bidir.
+// dX:      A = dy, B = W read transposed, PL = 1, PU = bidir.
 // ---------------------------------------------------------------------------
-template <int BMP, int BN, int WAVES_M, int WAVES_N>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void mix_bf16_kernel(
-    const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
-    bf16* __restrict__ out, int pairs, int width, int d, int partner_lower, int partner_upper) {
-  constexpr int NT = 64 * WAVES_M * WAVES_N;
-  constexpr int BM = 2 * BMP;
-  constexpr int TMP = BMP / (32 * WAVES_M);  // 32-row pair blocks per wave
-  constexpr int TN = BN / (32 * WAVES_N);    // 32-column blocks per wave
-  constexpr int A_IT = BM * CH / NT;
-  constexpr int B_IT = BN * CH / NT;
+template <int BMP, int BN, int WM, int WN>
+struct MixCfg {
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int NW = WM * WN;
+  static constexpr int BM = 2 * BMP;
+  static constexpr int TMP = BMP / (32 * WM);   // 32-row pair blocks per wave
+  static constexpr int TN = BN / (32 * WN);     // 32-column blocks per wave
+  static constexpr int A_ELEMS = BM * BK;
+  static constexpr int B_ELEMS = BN * BK;       // same size in both layouts
+  static constexpr int STAGE = A_ELEMS + 2 * B_ELEMS;
+  static constexpr int LDO = BN + 8;            // row stride of the output staging tile
+  static constexpr int LDS_ELEMS = (2 * STAGE > BM * LDO) ? 2 * STAGE : BM * LDO;
+  static constexpr int A_DMA = A_ELEMS * 2 / 1024 / NW;   // 1 KB DMA blocks per wave
+  static constexpr int B_DMA = B_ELEMS * 2 / 1024 / NW;
+  static constexpr int O_IT = BM * (BN / 8) / NT;
   static_assert(TMP >= 1 && TN >= 1, "tile too small for the wave grid");
-  static_assert(A_IT * NT == BM * CH && B_IT * NT == BN * CH, "loads must tile evenly");
+  static_assert(A_DMA * NW * 1024 == A_ELEMS * 2 && B_DMA * NW * 1024 == B_ELEMS * 2, "");
+  static_assert(O_IT * NT == BM * (BN / 8), "stores must tile evenly");
+};
 
-  __shared__ __attribute__((aligned(16))) bf16 sA[BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB1[BN * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB2[BN * BK];
+template <int BMP, int BN, int WM, int WN, bool PL, bool PU, bool TRANS_B>
+__global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
+    bf16* __restrict__ out, int pairs, int width, int d) {
+  using C = MixCfg<BMP, BN, WM, WN>;
+  constexpr int RB = BN * 2;   // bytes per row of a transposed B tile
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int wm = wave % WM, wn = wave / WM;
   const int s = 1 << d;
-  const int q0 = blockIdx.x * BMP;
-  const int n0 = blockIdx.y * BN;
+  const int tiles_n = width / BN;
+  const int tiles_m = (pairs + BMP - 1) / BMP;
+  const int tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  const int q0 = (tile / tiles_n) * BMP;
+  const int n0 = (tile % tiles_n) * BN;
 
-  // Source pointers and LDS slots of this thread's 16-byte pieces.
-  const bf16* a_src[A_IT];
-  int a_dst[A_IT];
+  // DMA sources (element offsets at k-slice 0) of this lane for each 1 KB block.
+  const bf16* a_src[C::A_DMA];
 #pragma unroll
-  for (int j = 0; j < A_IT; j++) {
-    const int idx = tid + NT * j;
-    const int m = idx / CH, ch = idx % CH;
+  for (int j = 0; j < C::A_DMA; j++) {
+    const int b = j * C::NW + wave;
+    const int m = b * 8 + (lane >> 3);                // tile row
+    const int ch = (lane & 7) ^ ((m >> 1) & 7);       // logical 16-byte piece
     int q = q0 + (m % BMP);
     if (q >= pairs) q = pairs - 1;  // ragged last block: load a valid row, never store it
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
     a_src[j] = A + (size_t)r * width + ch * 8;
-    a_dst[j] = swz(m, ch);
   }
-  const bf16* b1_src[B_IT];
-  const bf16* b2_src[B_IT];
-  int b_dst[B_IT];
+  size_t b_src[C::B_DMA];
 #pragma unroll
-  for (int j = 0; j < B_IT; j++) {
-    const int idx = tid + NT * j;
-    const int nr = idx / CH, ch = idx % CH;
-    b1_src[j] = B1 + (size_t)(n0 + nr) * width + ch * 8;
-    b2_src[j] = B2 + (size_t)(n0 + nr) * width + ch * 8;
-    b_dst[j] = swz(nr, ch);
+  for (int j = 0; j < C::B_DMA; j++) {
+    const int b = j * C::NW + wave;
+    if constexpr (TRANS_B) {  // tile rows are k, columns n
+      int kr, col;
+      tr_dma_coord<RB>(b, lane, &kr, &col);
+      b_src[j] = (size_t)kr * width + n0 + col;
+    } else {                  // tile rows are n, columns k
+      const int nr = b * 8 + (lane >> 3);
+      const int ch = (lane & 7) ^ ((nr >> 1) & 7);
+      b_src[j] = (size_t)(n0 + nr) * width + ch * 8;
+    }
   }
+  const size_t b_step = TRANS_B ? (size_t)BK * width : BK;
 
-  f32x16 accL[TMP][TN], accU[TMP][TN];
+  auto issue = [&](int kt, int stage) {
+    bf16* sA = smem + stage * C::STAGE;
+    bf16* sB1 = sA + C::A_ELEMS;
+    bf16* sB2 = sB1 + C::B_ELEMS;
 #pragma unroll
-  for (int p = 0; p < TMP; p++)
+    for (int j = 0; j < C::A_DMA; j++) dma16(a_src[j] + kt * BK, sA + (j * C::NW + wave) * 512);
 #pragma unroll
-    for (int t = 0; t < TN; t++)
+    for (int j = 0; j < C::B_DMA; j++) {
+      dma16(B1 + b_src[j] + kt * b_step, sB1 + (j * C::NW + wave) * 512);
+      dma16(B2 + b_src[j] + kt * b_step, sB2 + (j * C::NW + wave) * 512);
+    }
+  };
+
+  f32x16 accL[C::TMP][C::TN], accU[C::TMP][C::TN];
+#pragma unroll
+  for (int p = 0; p < C::TMP; p++)
+#pragma unroll
+    for (int t = 0; t < C::TN; t++)
 #pragma unroll
       for (int e = 0; e < 16; e++) { accL[p][t][e] = 0.f; accU[p][t][e] = 0.f; }
 
-  for (int k0 = 0; k0 < width; k0 += BK) {
-    uint4 ra[A_IT], rb1[B_IT], rb2[B_IT];
+  struct Frags { bf16x8 aL[C::TMP], aU[C::TMP], b1[C::TN], b2[C::TN]; };
+  auto load_frags = [&](Frags& f, const bf16* sA, int kk) {
+    const bf16* sB1 = sA + C::A_ELEMS;
+    const bf16* sB2 = sB1 + C::B_ELEMS;
+    const int ch = kk * 2 + (lane >> 5);
 #pragma unroll
-    for (int j = 0; j < A_IT; j++) ra[j] = *(const uint4*)(a_src[j] + k0);
-#pragma unroll
-    for (int j = 0; j < B_IT; j++) {
-      rb1[j] = *(const uint4*)(b1_src[j] + k0);
-      rb2[j] = *(const uint4*)(b2_src[j] + k0);
+    for (int p = 0; p < C::TMP; p++) {
+      const int m = (wm * C::TMP + p) * 32 + (lane & 31);
+      f.aL[p] = *(const bf16x8*)(sA + swz(m, ch));
+      f.aU[p] = *(const bf16x8*)(sA + swz(m + BMP, ch));
     }
-    __syncthreads();
 #pragma unroll
-    for (int j = 0; j < A_IT; j++) *(uint4*)(sA + a_dst[j]) = ra[j];
-#pragma unroll
-    for (int j = 0; j < B_IT; j++) {
-      *(uint4*)(sB1 + b_dst[j]) = rb1[j];
-      *(uint4*)(sB2 + b_dst[j]) = rb2[j];
-    }
-    __syncthreads();
-
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; kk++) {
-      const int ch = kk * 2 + (lane >> 5);
-      bf16x8 aL[TMP], aU[TMP], b1[TN], b2[TN];
-#pragma unroll
-      for (int p = 0; p < TMP; p++) {
-        const int m = (wm * TMP + p) * 32 + (lane & 31);
-        aL[p] = *(const bf16x8*)(sA + swz(m, ch));
-        aU[p] = *(const bf16x8*)(sA + swz(m + BMP, ch));
-      }
-#pragma unroll
-      for (int t = 0; t < TN; t++) {
-        const int nr = (wn * TN + t) * 32 + (lane & 31);
-        b1[t] = *(const bf16x8*)(sB1 + swz(nr, ch));
-        b2[t] = *(const bf16x8*)(sB2 + swz(nr, ch));
-      }
-#pragma unroll
-      for (int p = 0; p < TMP; p++)
-#pragma unroll
-        for (int t = 0; t < TN; t++) {
-          accL[p][t] = mfma32(aL[p], b1[t], accL[p][t]);
-          accU[p][t] = mfma32(aU[p], b1[t], accU[p][t]);
-          if (partner_upper) accU[p][t] = mfma32(aL[p], b2[t], accU[p][t]);
-          if (partner_lower) accL[p][t] = mfma32(aU[p], b2[t], accL[p][t]);
-        }
-    }
-  }
-
-  // Epilogue: accumulator element e of lane l is C[8*(e/4) + 4*(l/32) + e%4][l%32].
-#pragma unroll
-  for (int p = 0; p < TMP; p++) {
-#pragma unroll
-    for (int e = 0; e < 16; e++) {
-      const int i = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-      const int q = q0 + (wm * TMP + p) * 32 + i;
-      if (q >= pairs) continue;
-      const int rL = lower_row(q, d), rU = rL + s;
-#pragma unroll
-      for (int t = 0; t < TN; t++) {
-        const int col = n0 + (wn * TN + t) * 32 + (lane & 31);
-        out[(size_t)rL * width + col] = to_bf16(accL[p][t][e]);
-        out[(size_t)rU * width + col] = to_bf16(accU[p][t][e]);
+    for (int t = 0; t < C::TN; t++) {
+      const int nb = (wn * C::TN + t) * 32;
+      if constexpr (TRANS_B) {
+        f.b1[t] = tr_frag<RB>(sB1, kk * 16, nb, lane);
+        f.b2[t] = tr_frag<RB>(sB2, kk * 16, nb, lane);
+      } else {
+        f.b1[t] = *(const bf16x8*)(sB1 + swz(nb + (lane & 31), ch));
+        f.b2[t] = *(const bf16x8*)(sB2 + swz(nb + (lane & 31), ch));
       }
     }
-  }
-}
+  };
+  auto mma = [&](const Frags& f) {
+    // self terms first, partner terms after, so no MFMA waits on the one before it
+#pragma unroll
+    for (int p = 0; p < C::TMP; p++)
+#pragma unroll
+      for (int t = 0; t < C::TN; t++) {
+        accL[p][t] = mfma32(f.aL[p], f.b1[t], accL[p][t]);
+        accU[p][t] = mfma32(f.aU[p], f.b1[t], accU[p][t]);
+      }
+#pragma unroll
+    for (int p = 0; p < C::TMP; p++)
+#pragma unroll
+      for (int t = 0; t < C::TN; t++) {
+        if (PU) accU[p][t] = mfma32(f.aL[p], f.b2[t], accU[p][t]);
+        if (PL) accL[p][t] = mfma32(f.aU[p], f.b2[t], accL[p][t]);
+      }
+  };
 
-// ---------------------------------------------------------------------------
-// Transpose of two width x width bf16 matrices (for the dX contraction).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void transpose2_kernel(const bf16* __restrict__ W1,
-                                                         const bf16* __restrict__ W2,
-                                                         bf16* __restrict__ W1T,
-                                                         bf16* __restrict__ W2T, int width) {
-  __shared__ bf16 tile[32][33];
-  const bf16* src = blockIdx.z ? W2 : W1;
-  bf16* dst = blockIdx.z ? W2T : W1T;
-  const int c0 = blockIdx.x * 32, o0 = blockIdx.y * 32;
-  const int tx = threadIdx.x % 32, ty = threadIdx.x / 32;  // 32 x 8
-  for (int i = ty; i < 32; i += 8) tile[i][tx] = src[(size_t)(o0 + i) * width + c0 + tx];
+  constexpr int KK = BK / 16;
+  constexpr int NMFMA = C::TMP * C::TN * (2 + (PL ? 1 : 0) + (PU ? 1 : 0));
+  constexpr int NDS = 2 * C::TMP + 2 * C::TN * (TRANS_B ? 2 : 1);
+  const int nk = width / BK;
+  issue(0, 0);
+  wait_dma();
   __syncthreads();
-  for (int i = ty; i < 32; i += 8) dst[(size_t)(c0 + i) * width + o0 + tx] = tile[tx][i];
+  Frags f[2];
+  load_frags(f[0], smem, 0);
+  for (int kt = 0; kt < nk; kt++) {
+    const bf16* sA = smem + (kt & 1) * C::STAGE;
+    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++) {
+      if (kk + 1 < KK) {
+        load_frags(f[(kk + 1) & 1], sA, kk + 1);
+        mma(f[kk & 1]);
+        interleave_mfma_ds<NMFMA, NDS>();
+      } else {
+        mma(f[kk & 1]);
+      }
+    }
+    wait_dma();
+    __syncthreads();
+    if (kt + 1 < nk) load_frags(f[0], smem + ((kt + 1) & 1) * C::STAGE, 0);
+  }
+
+  // Epilogue: round to bf16 into an LDS tile [BM][LDO], then 16-byte row stores.
+  // Accumulator element e of lane l holds C[8*(e/4) + 4*(l/32) + e%4][l%32].
+  bf16* sO = smem;
+#pragma unroll
+  for (int p = 0; p < C::TMP; p++)
+#pragma unroll
+    for (int t = 0; t < C::TN; t++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) {
+        const int i = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int m = (wm * C::TMP + p) * 32 + i;
+        const int col = (wn * C::TN + t) * 32 + (lane & 31);
+        sO[m * C::LDO + col] = to_bf16(accL[p][t][e]);
+        sO[(m + BMP) * C::LDO + col] = to_bf16(accU[p][t][e]);
+      }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < C::O_IT; j++) {
+    const int idx = tid + C::NT * j;
+    const int m = idx / (BN / 8), ch = idx % (BN / 8);
+    const int q = q0 + (m % BMP);
+    if (q >= pairs) continue;
+    const int r = lower_row(q, d) + (m >= BMP ? s : 0);
+    *(u32x4*)(out + (size_t)r * width + n0 + ch * 8) = *(const u32x4*)(sO + m * C::LDO + ch * 8);
+  }
 }
 
 // ---------------------------------------------------------------------------
-// Weight gradients, split over rows.  Block (x, y, z) computes the BO x BC
-// tile (o0 = y*BO, c0 = x*BC) of dW_self and dW_off over the pairs of split z:
+// Weight gradients, split over rows.  Block (tile, split) computes the BO x BC
+// tile of dW_self and dW_off over the row pairs of its split:
 //   dW_self += dY_L^T X_L + dY_U^T X_U
 //   dW_off  += dY_U^T X_L            (+ dY_L^T X_U when bidirectional)
-// K-step = KP pairs = 2*KP rows, staged transposed in LDS ([column][row slot],
-// slots 0..KP-1 lower rows, KP..2KP-1 their partners) so both MFMA operands
-// are read as 16 contiguous bytes along the row (contraction) index.
+// A K-step stages KP pairs = 2*KP rows of dY and X in LDS in their natural
+// layout (slots 0..KP-1 the lower rows, KP..2KP-1 their partners); both MFMA
+// operands are read transposed, the row (slot) index being the contraction.
 // ---------------------------------------------------------------------------
 constexpr int KP = 32;
 constexpr int SLOTS = 2 * KP;
-constexpr int LDT = SLOTS + 8;  // padded LDS row, elements (144 bytes)
 
-template <int BO, int BC, int WAVES_O, int WAVES_C>
-__global__ __launch_bounds__(64 * WAVES_O * WAVES_C) void dw_bf16_kernel(
+template <int BO, int BC, int WO, int WC>
+struct DwCfg {
+  static constexpr int NT = 64 * WO * WC;
+  static constexpr int NW = WO * WC;
+  static constexpr int TO = BO / (32 * WO);
+  static constexpr int TC = BC / (32 * WC);
+  static constexpr int G_ELEMS = SLOTS * BO;
+  static constexpr int X_ELEMS = SLOTS * BC;
+  static constexpr int STAGE = G_ELEMS + X_ELEMS;
+  static constexpr int G_DMA = G_ELEMS * 2 / 1024 / NW;
+  static constexpr int X_DMA = X_ELEMS * 2 / 1024 / NW;
+  static_assert(G_DMA * NW * 1024 == G_ELEMS * 2 && X_DMA * NW * 1024 == X_ELEMS * 2, "");
+};
+
+template <int BO, int BC, int WO, int WC, bool BIDIR>
+__global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
     const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
-    int pairs, int width, int d, int bidir, int pairs_per_split) {
-  constexpr int NT = 64 * WAVES_O * WAVES_C;
-  constexpr int TO = BO / (32 * WAVES_O);
-  constexpr int TC = BC / (32 * WAVES_C);
-  constexpr int G_IT = SLOTS * (BO / 8) / NT;
-  constexpr int X_IT = SLOTS * (BC / 8) / NT;
-  static_assert(G_IT * NT == SLOTS * (BO / 8) && X_IT * NT == SLOTS * (BC / 8), "");
-  __shared__ __attribute__((aligned(16))) bf16 sG[BO * LDT];
-  __shared__ __attribute__((aligned(16))) bf16 sX[BC * LDT];
+    int pairs, int width, int d, int pairs_per_split) {
+  using C = DwCfg<BO, BC, WO, WC>;
+  constexpr int RBG = BO * 2, RBX = BC * 2;
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wo = wave % WAVES_O, wc = wave / WAVES_O;
-  const int c0 = blockIdx.x * BC, o0 = blockIdx.y * BO;
+  const int wo = wave % WO, wc = wave / WO;
+  const int tiles_c = width / BC;
+  const int tiles = (width / BO) * tiles_c;
+  const int tile = blockIdx.x % tiles;
+  const int split = blockIdx.x / tiles;
+  const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
   const int s = 1 << d;
-  const int pbeg = blockIdx.z * pairs_per_split;
+  const int pbeg = split * pairs_per_split;
   const int pend = min(pairs, pbeg + pairs_per_split);
 
-  f32x16 accS[TO][TC], accO[TO][TC];
+  // Per-lane (slot, column) of each DMA block.
+  int g_slot[C::G_DMA], g_col[C::G_DMA], x_slot[C::X_DMA], x_col[C::X_DMA];
 #pragma unroll
-  for (int a = 0; a < TO; a++)
+  for (int j = 0; j < C::G_DMA; j++) tr_dma_coord<RBG>(j * C::NW + wave, lane, &g_slot[j], &g_col[j]);
 #pragma unroll
-    for (int b = 0; b < TC; b++)
+  for (int j = 0; j < C::X_DMA; j++) tr_dma_coord<RBX>(j * C::NW + wave, lane, &x_slot[j], &x_col[j]);
+
+  auto row_of = [&](int p0, int slot) {
+    return lower_row(p0 + (slot % KP), d) + (slot >= KP ? s : 0);
+  };
+  // Whole K-step: every slot valid, straight DMA.
+  auto issue = [&](int p0, int stage) {
+    bf16* sG = smem + stage * C::STAGE;
+    bf16* sX = sG + C::G_ELEMS;
+#pragma unroll
+    for (int j = 0; j < C::G_DMA; j++)
+      dma16(dY + (size_t)row_of(p0, g_slot[j]) * width + o0 + g_col[j], sG + (j * C::NW + wave) * 512);
+#pragma unroll
+    for (int j = 0; j < C::X_DMA; j++)
+      dma16(X + (size_t)row_of(p0, x_slot[j]) * width + c0 + x_col[j], sX + (j * C::NW + wave) * 512);
+  };
+  // Ragged last K-step: slots past the end of the split are zero-filled.
+  auto fill_tail = [&](int p0, int stage) {
+    bf16* sG = smem + stage * C::STAGE;
+    bf16* sX = sG + C::G_ELEMS;
+#pragma unroll
+    for (int j = 0; j < C::G_DMA; j++) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (p0 + (g_slot[j] % KP) < pend)
+        v = *(const u32x4*)(dY + (size_t)row_of(p0, g_slot[j]) * width + o0 + g_col[j]);
+      *(u32x4*)(sG + (j * C::NW + wave) * 512 + lane * 8) = v;
+    }
+#pragma unroll
+    for (int j = 0; j < C::X_DMA; j++) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (p0 + (x_slot[j] % KP) < pend)
+        v = *(const u32x4*)(X + (size_t)row_of(p0, x_slot[j]) * width + c0 + x_col[j]);
+      *(u32x4*)(sX + (j * C::NW + wave) * 512 + lane * 8) = v;
+    }
+  };
+  auto stage_in = [&](int p0, int stage) {
+    if (p0 + KP <= pend) issue(p0, stage);
+    else fill_tail(p0, stage);
+  };
+
+  f32x16 accS[C::TO][C::TC], accO[C::TO][C::TC];
+#pragma unroll
+  for (int a = 0; a < C::TO; a++)
+#pragma unroll
+    for (int b = 0; b < C::TC; b++)
 #pragma unroll
       for (int e = 0; e < 16; e++) { accS[a][b][e] = 0.f; accO[a][b][e] = 0.f; }
 
-  for (int p0 = pbeg; p0 < pend; p0 += KP) {
-    uint4 rg[G_IT], rx[X_IT];
+  struct Frags { bf16x8 gL[C::TO], gU[C::TO], xL[C::TC], xU[C::TC]; };
+  auto load_frags = [&](Frags& f, const bf16* sG, int kk) {
+    const bf16* sX = sG + C::G_ELEMS;
 #pragma unroll
-    for (int j = 0; j < G_IT; j++) {
-      const int idx = tid + NT * j;
-      const int slot = idx / (BO / 8), ch = idx % (BO / 8);
-      const int q = p0 + (slot % KP);
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (q < pend) {
-        const int r = lower_row(q, d) + (slot >= KP ? s : 0);
-        v = *(const uint4*)(dY + (size_t)r * width + o0 + ch * 8);
+    for (int a = 0; a < C::TO; a++) {
+      const int ob = (wo * C::TO + a) * 32;
+      f.gL[a] = tr_frag<RBG>(sG, kk * 16, ob, lane);
+      f.gU[a] = tr_frag<RBG>(sG, KP + kk * 16, ob, lane);
+    }
+#pragma unroll
+    for (int b = 0; b < C::TC; b++) {
+      const int cb = (wc * C::TC + b) * 32;
+      f.xL[b] = tr_frag<RBX>(sX, kk * 16, cb, lane);
+      f.xU[b] = tr_frag<RBX>(sX, KP + kk * 16, cb, lane);
+    }
+  };
+  auto mma = [&](const Frags& f) {
+#pragma unroll
+    for (int a = 0; a < C::TO; a++)
+#pragma unroll
+      for (int b = 0; b < C::TC; b++) {
+        accS[a][b] = mfma32(f.gL[a], f.xL[b], accS[a][b]);
+        accO[a][b] = mfma32(f.gU[a], f.xL[b], accO[a][b]);
       }
-      rg[j] = v;
-    }
 #pragma unroll
-    for (int j = 0; j < X_IT; j++) {
-      const int idx = tid + NT * j;
-      const int slot = idx / (BC / 8), ch = idx % (BC / 8);
-      const int q = p0 + (slot % KP);
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (q < pend) {
-        const int r = lower_row(q, d) + (slot >= KP ? s : 0);
-        v = *(const uint4*)(X + (size_t)r * width + c0 + ch * 8);
+    for (int a = 0; a < C::TO; a++)
+#pragma unroll
+      for (int b = 0; b < C::TC; b++) {
+        accS[a][b] = mfma32(f.gU[a], f.xU[b], accS[a][b]);
+        if (BIDIR) accO[a][b] = mfma32(f.gL[a], f.xU[b], accO[a][b]);
       }
-      rx[j] = v;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < G_IT; j++) {
-      const int idx = tid + NT * j;
-      const int slot = idx / (BO / 8), ch = idx % (BO / 8);
-      const bf16* v = (const bf16*)&rg[j];
-#pragma unroll
-      for (int e = 0; e < 8; e++) sG[(ch * 8 + e) * LDT + slot] = v[e];
-    }
-#pragma unroll
-    for (int j = 0; j < X_IT; j++) {
-      const int idx = tid + NT * j;
-      const int slot = idx / (BC / 8), ch = idx % (BC / 8);
-      const bf16* v = (const bf16*)&rx[j];
-#pragma unroll
-      for (int e = 0; e < 8; e++) sX[(ch * 8 + e) * LDT + slot] = v[e];
-    }
-    __syncthreads();
+  };
 
-    const int half = 8 * (lane >> 5);
-    // dW_self: all 64 slots
-#pragma unroll
-    for (int kk = 0; kk < SLOTS / 16; kk++) {
-      bf16x8 ga[TO], xb[TC];
-#pragma unroll
-      for (int a = 0; a < TO; a++)
-        ga[a] = *(const bf16x8*)(sG + ((wo * TO + a) * 32 + (lane & 31)) * LDT + kk * 16 + half);
-#pragma unroll
-      for (int b = 0; b < TC; b++)
-        xb[b] = *(const bf16x8*)(sX + ((wc * TC + b) * 32 + (lane & 31)) * LDT + kk * 16 + half);
-#pragma unroll
-      for (int a = 0; a < TO; a++)
-#pragma unroll
-        for (int b = 0; b < TC; b++) accS[a][b] = mfma32(ga[a], xb[b], accS[a][b]);
-    }
-    // dW_off: receiver gradient slots x sender activation slots
-#pragma unroll
-    for (int kk = 0; kk < KP / 16; kk++) {
-      bf16x8 gU[TO], xL[TC], gL[TO], xU[TC];
-#pragma unroll
-      for (int a = 0; a < TO; a++) {
-        const int row = ((wo * TO + a) * 32 + (lane & 31)) * LDT + kk * 16 + half;
-        gU[a] = *(const bf16x8*)(sG + row + KP);
-        gL[a] = *(const bf16x8*)(sG + row);
-      }
-#pragma unroll
-      for (int b = 0; b < TC; b++) {
-        const int row = ((wc * TC + b) * 32 + (lane & 31)) * LDT + kk * 16 + half;
-        xL[b] = *(const bf16x8*)(sX + row);
-        xU[b] = *(const bf16x8*)(sX + row + KP);
-      }
-#pragma unroll
-      for (int a = 0; a < TO; a++)
-#pragma unroll
-        for (int b = 0; b < TC; b++) {
-          accO[a][b] = mfma32(gU[a], xL[b], accO[a][b]);
-          if (bidir) accO[a][b] = mfma32(gL[a], xU[b], accO[a][b]);
-        }
-    }
+  constexpr int NMFMA = C::TO * C::TC * (3 + (BIDIR ? 1 : 0));
+  constexpr int NDS = 4 * (C::TO + C::TC);   // two tr reads per fragment
+  const int nsteps = pend > pbeg ? (pend - pbeg + KP - 1) / KP : 0;
+  if (nsteps > 0) stage_in(pbeg, 0);
+  wait_dma();
+  __syncthreads();
+  Frags f0, f1;
+  if (nsteps > 0) load_frags(f0, smem, 0);
+  for (int it = 0; it < nsteps; it++) {
+    const bf16* sG = smem + (it & 1) * C::STAGE;
+    if (it + 1 < nsteps) stage_in(pbeg + (it + 1) * KP, (it + 1) & 1);
+    load_frags(f1, sG, 1);
+    mma(f0);
+    interleave_mfma_ds<NMFMA, NDS>();
+    mma(f1);
+    wait_dma();
+    __syncthreads();
+    if (it + 1 < nsteps) load_frags(f0, smem + ((it + 1) & 1) * C::STAGE, 0);
   }
 
   const size_t ww = (size_t)width * width;
-  float* outS = partial + (size_t)blockIdx.z * 2 * ww;
+  float* outS = partial + (size_t)split * 2 * ww;
   float* outO = outS + ww;
 #pragma unroll
-  for (int a = 0; a < TO; a++)
+  for (int a = 0; a < C::TO; a++)
 #pragma unroll
-    for (int b = 0; b < TC; b++)
+    for (int b = 0; b < C::TC; b++)
 #pragma unroll
       for (int e = 0; e < 16; e++) {
-        const int o = o0 + (wo * TO + a) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int c = c0 + (wc * TC + b) * 32 + (lane & 31);
+        const int o = o0 + (wo * C::TO + a) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int c = c0 + (wc * C::TC + b) * 32 + (lane & 31);
         outS[(size_t)o * width + c] = accS[a][b][e];
         outO[(size_t)o * width + c] = accO[a][b][e];
       }
@@ -326,52 +475,54 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
        i += (size_t)gridDim.x * blockDim.x) {
     const int m = i >= n4;
     const size_t j = i - m * n4;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sp = 0; sp < splits; sp++) {
-      const float4 v = ((const float4*)(partial + ((size_t)sp * 2 + m) * ww))[j];
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
-    float4* dst = (float4*)(m ? dwo : dws) + j;
-    if (accumulate) {
-      const float4 o = *dst;
-      acc.x += o.x; acc.y += o.y; acc.z += o.z; acc.w += o.w;
-    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < splits; sp++)
+      acc += ((const f32x4*)(partial + ((size_t)sp * 2 + m) * ww))[j];
+    f32x4* dst = (f32x4*)(m ? dwo : dws) + j;
+    if (accumulate) acc += *dst;
     *dst = acc;
   }
 }
 
+// ---- launch configurations ----
+constexpr int MIX_BMP = 128;          // 256 rows per block
 constexpr int DW_BO = 128, DW_BC = 128;
 
-}  // namespace
-
-hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
-                           int width, int d, int partner_lower, int partner_upper,
-                           hipStream_t st) {
-  const int pairs = rows / 2;
-  if (width % 128 == 0) {
-    constexpr int BMP = 64, BN = 128;
-    dim3 grid((pairs + BMP - 1) / BMP, width / BN);
-    mix_bf16_kernel<BMP, BN, 2, 2><<<grid, 256, 0, st>>>(A, B1, B2, out, pairs, width, d,
-                                                         partner_lower, partner_upper);
-  } else {
-    constexpr int BMP = 64, BN = 64;
-    dim3 grid((pairs + BMP - 1) / BMP, width / BN);
-    mix_bf16_kernel<BMP, BN, 2, 2><<<grid, 256, 0, st>>>(A, B1, B2, out, pairs, width, d,
-                                                         partner_lower, partner_upper);
+template <int BMP, int BN, int WM, int WN, bool TRANS_B>
+hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int pairs,
+                      int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
+  using C = MixCfg<BMP, BN, WM, WN>;
+  const int blocks = ((pairs + BMP - 1) / BMP) * (width / BN);
+  const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
+#define HCMIX_MIX(PL, PU)                                                                   \
+  {                                                                                         \
+    auto k = mix_bf16_kernel<BMP, BN, WM, WN, PL, PU, TRANS_B>;                             \
+    static const hipError_t attr = hipFuncSetAttribute(                                     \
+        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+    if (attr != hipSuccess) return attr;                                                    \
+    k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, pairs, width, d);                         \
   }
+  if (partner_lower && partner_upper) HCMIX_MIX(true, true)
+  else if (partner_upper) HCMIX_MIX(false, true)
+  else HCMIX_MIX(true, false)
+#undef HCMIX_MIX
   return hipGetLastError();
 }
 
-hipError_t launch_transpose2_bf16(const bf16* W1, const bf16* W2, bf16* W1T, bf16* W2T,
-                                  int width, hipStream_t st) {
-  dim3 grid(width / 32, width / 32, 2);
-  transpose2_kernel<<<grid, 256, 0, st>>>(W1, W2, W1T, W2T, width);
-  return hipGetLastError();
+template <bool TRANS_B>
+hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                        int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
+  const int pairs = rows / 2;
+  if (width % 128 == 0)
+    return mix_launch<MIX_BMP, 128, 2, 2, TRANS_B>(A, B1, B2, out, pairs, width, d,
+                                                   partner_lower, partner_upper, st);
+  return mix_launch<MIX_BMP, 64, 4, 1, TRANS_B>(A, B1, B2, out, pairs, width, d, partner_lower,
+                                                partner_upper, st);
 }
 
 // Split-K plan: enough blocks to fill the chip (about 512), each split a whole
 // number of K-steps.  Returns the split count; *pps gets pairs per split.
-static int dw_plan(int rows, int width, int* pps) {
+int dw_plan(int rows, int width, int* pps) {
   const int pairs = rows / 2;
   const int bo = width % DW_BO == 0 ? DW_BO : 64;
   const int tiles = (width / bo) * (width / bo);
@@ -381,6 +532,36 @@ static int dw_plan(int rows, int width, int* pps) {
   if (splits < 1) splits = 1;
   *pps = ((ksteps + splits - 1) / splits) * KP;
   return (pairs + *pps - 1) / *pps;
+}
+
+template <int BO, int BC, int WO, int WC>
+hipError_t dw_launch(const bf16* X, const bf16* dY, float* partial, int pairs, int width, int d,
+                     int bidir, int splits, int pps, hipStream_t st) {
+  using C = DwCfg<BO, BC, WO, WC>;
+  const int blocks = (width / BO) * (width / BC) * splits;
+  const size_t lds = (size_t)2 * C::STAGE * sizeof(bf16);
+#define HCMIX_DW(BIDIR)                                                                     \
+  {                                                                                         \
+    auto k = dw_bf16_kernel<BO, BC, WO, WC, BIDIR>;                                         \
+    static const hipError_t attr = hipFuncSetAttribute(                                     \
+        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+    if (attr != hipSuccess) return attr;                                                    \
+    k<<<blocks, C::NT, lds, st>>>(X, dY, partial, pairs, width, d, pps);                    \
+  }
+  if (bidir) HCMIX_DW(true)
+  else HCMIX_DW(false)
+#undef HCMIX_DW
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                           int width, int d, int partner_lower, int partner_upper,
+                           bool transpose_b, hipStream_t st) {
+  if (transpose_b)
+    return mix_dispatch<true>(A, B1, B2, out, rows, width, d, partner_lower, partner_upper, st);
+  return mix_dispatch<false>(A, B1, B2, out, rows, width, d, partner_lower, partner_upper, st);
 }
 
 int dw_bf16_splits(int rows, int width) {
@@ -394,16 +575,11 @@ hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* 
   const int pairs = rows / 2;
   int pps;
   const int splits = dw_plan(rows, width, &pps);
-  if (width % DW_BO == 0) {
-    dim3 grid(width / DW_BC, width / DW_BO, splits);
-    dw_bf16_kernel<DW_BO, DW_BC, 2, 2><<<grid, 256, 0, st>>>(X, dY, partial, pairs, width, d,
-                                                             bidir, pps);
-  } else {
-    dim3 grid(width / 64, width / 64, splits);
-    dw_bf16_kernel<64, 64, 2, 2><<<grid, 256, 0, st>>>(X, dY, partial, pairs, width, d, bidir,
-                                                       pps);
-  }
-  hipError_t e = hipGetLastError();
+  hipError_t e;
+  if (width % DW_BO == 0)
+    e = dw_launch<DW_BO, DW_BC, 2, 2>(X, dY, partial, pairs, width, d, bidir, splits, pps, st);
+  else
+    e = dw_launch<64, 64, 2, 2>(X, dY, partial, pairs, width, d, bidir, splits, pps, st);
   if (e != hipSuccess) return e;
   const size_t ww = (size_t)width * width;
   int blocks = (int)((2 * ww / 4 + 255) / 256);
