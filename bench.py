@@ -54,7 +54,33 @@ def parse():
     ap.add_argument("--cpu-windows", type=int, default=0,
                     help="windows in the oracle sample (0: sized for ~10-30 s)")
     ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources; a traffic figure is valid only for the same sources."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_18145_amd", "csrc", "*"))):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary (profiles/traffic_<workload>.json), or None if it was taken on
+    different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def main():
@@ -135,6 +161,12 @@ def main():
         torch.cuda.synchronize()
         mix_s = k0.elapsed_time(k1) / 1e3 / (reps * L)
 
+    if args.calib_copy_mb > 0:
+        src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
     flops, nbytes = algorithmic_work(B, n, w, L, causal)
     pl_per_step = B * n * L
     value = pl_per_step * args.steps / t
@@ -143,7 +175,8 @@ def main():
     mix_tflops = mix_flops / mix_s / 1e12
     roofline = {"bound": "mfma", "kernel": "mix_bf16_kernel (forward launch)",
                 "achieved": round(mix_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(mix_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(mix_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": profiled_traffic(args.workload),
                 "avg_launch_us": round(mix_s * 1e6, 2)}
 
     out = {

@@ -29,8 +29,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr int BK = 64;       // contraction slice per pipeline stage (128-byte rows)
-
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -41,6 +39,20 @@ __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
 }
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Wait for all but the `ahead` most recently issued pipeline stages (DPS DMA
+// instructions each) of this wave; ahead < NA.
+template <int NA, int DPS>
+__device__ __forceinline__ void wait_stages(int ahead) {
+  if constexpr (NA > 0) {
+    if (ahead >= NA - 1) { wait_vmcnt<(NA - 1) * DPS>(); return; }
+    wait_stages<NA - 1, DPS>(ahead);
+  }
+}
 
 // Scheduling hint for one MFMA sub-step: alternate its NMFMA matrix
 // instructions with the NDS LDS reads that fetch the next sub-step's
@@ -61,11 +73,14 @@ __device__ __forceinline__ void interleave_mfma_ds() {
 // group of 16 lanes covers 256 distinct bytes (mod 256), a 64-bit access when
 // each group of 32 lanes does.
 //
-// k-contiguous tile [rows][BK] (128-byte rows): 16-byte piece `ch` of row m
-// sits at piece ch ^ ((m >> 1) & 7), so 16 consecutive rows reading the same
-// piece land in 16 distinct 16-byte slots.  Offsets in elements.
+// k-contiguous tile [rows][BK] (2*BK-byte rows, BK = 32 or 64): 16-byte piece
+// `ch` of row m sits at piece ch ^ ((m / (128/BK)) % (BK/8)), so 16 consecutive
+// rows reading the same piece land in 16 distinct 16-byte slots.  Elements.
+template <int BK>
 __device__ __forceinline__ int swz(int m, int ch) {
-  return m * BK + ((ch ^ ((m >> 1) & 7)) << 3);
+  static_assert(BK == 32 || BK == 64, "");
+  constexpr int RPQ = 128 / BK;   // rows sharing one 256-byte bank window
+  return m * BK + ((ch ^ ((m / RPQ) & (BK / 8 - 1))) << 3);
 }
 
 // Row-major tile read transposed, RB bytes per row (256 or 128): 64-byte
@@ -117,7 +132,7 @@ __device__ __forceinline__ int xcd_tile(int bid, int total) {
 // Forward: A = x, B1 = W_self, B2 = W_off, PU = 1, PL = bidir.
 // dX:      A = dy, B = W read transposed, PL = 1, PU = bidir.
 // ---------------------------------------------------------------------------
-template <int BMP, int BN, int WM, int WN>
+template <int BMP, int BN, int WM, int WN, int BK, int NS>
 struct MixCfg {
   static constexpr int NT = 64 * WM * WN;
   static constexpr int NW = WM * WN;
@@ -128,20 +143,22 @@ struct MixCfg {
   static constexpr int B_ELEMS = BN * BK;       // same size in both layouts
   static constexpr int STAGE = A_ELEMS + 2 * B_ELEMS;
   static constexpr int LDO = BN + 8;            // row stride of the output staging tile
-  static constexpr int LDS_ELEMS = (2 * STAGE > BM * LDO) ? 2 * STAGE : BM * LDO;
+  static constexpr int LDS_ELEMS = (NS * STAGE > BM * LDO) ? NS * STAGE : BM * LDO;
   static constexpr int A_DMA = A_ELEMS * 2 / 1024 / NW;   // 1 KB DMA blocks per wave
   static constexpr int B_DMA = B_ELEMS * 2 / 1024 / NW;
   static constexpr int O_IT = BM * (BN / 8) / NT;
   static_assert(TMP >= 1 && TN >= 1, "tile too small for the wave grid");
   static_assert(A_DMA * NW * 1024 == A_ELEMS * 2 && B_DMA * NW * 1024 == B_ELEMS * 2, "");
+  static constexpr int DPS = A_DMA + 2 * B_DMA;  // DMA instructions per wave per stage
   static_assert(O_IT * NT == BM * (BN / 8), "stores must tile evenly");
+  static_assert(NS >= 2 && (NS - 2) * DPS <= 63, "vmcnt range");
 };
 
-template <int BMP, int BN, int WM, int WN, bool PL, bool PU, bool TRANS_B>
+template <int BMP, int BN, int WM, int WN, int BK, int NS, bool PL, bool PU, bool TRANS_B>
 __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
     bf16* __restrict__ out, int pairs, int width, int d) {
-  using C = MixCfg<BMP, BN, WM, WN>;
+  using C = MixCfg<BMP, BN, WM, WN, BK, NS>;
   constexpr int RB = BN * 2;   // bytes per row of a transposed B tile
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
 
@@ -159,8 +176,9 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 #pragma unroll
   for (int j = 0; j < C::A_DMA; j++) {
     const int b = j * C::NW + wave;
-    const int m = b * 8 + (lane >> 3);                // tile row
-    const int ch = (lane & 7) ^ ((m >> 1) & 7);       // logical 16-byte piece
+    const int o = b * 1024 + 16 * lane;               // byte offset in the tile
+    const int m = o / (2 * BK);                       // tile row
+    const int ch = (swz<BK>(m, (o % (2 * BK)) / 16) - m * BK) / 8;   // swizzle is an involution
     int q = q0 + (m % BMP);
     if (q >= pairs) q = pairs - 1;  // ragged last block: load a valid row, never store it
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
@@ -175,8 +193,9 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
       tr_dma_coord<RB>(b, lane, &kr, &col);
       b_src[j] = (size_t)kr * width + n0 + col;
     } else {                  // tile rows are n, columns k
-      const int nr = b * 8 + (lane >> 3);
-      const int ch = (lane & 7) ^ ((nr >> 1) & 7);
+      const int o = b * 1024 + 16 * lane;
+      const int nr = o / (2 * BK);
+      const int ch = (swz<BK>(nr, (o % (2 * BK)) / 16) - nr * BK) / 8;
       b_src[j] = (size_t)(n0 + nr) * width + ch * 8;
     }
   }
@@ -211,8 +230,8 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 #pragma unroll
     for (int p = 0; p < C::TMP; p++) {
       const int m = (wm * C::TMP + p) * 32 + (lane & 31);
-      f.aL[p] = *(const bf16x8*)(sA + swz(m, ch));
-      f.aU[p] = *(const bf16x8*)(sA + swz(m + BMP, ch));
+      f.aL[p] = *(const bf16x8*)(sA + swz<BK>(m, ch));
+      f.aU[p] = *(const bf16x8*)(sA + swz<BK>(m + BMP, ch));
     }
 #pragma unroll
     for (int t = 0; t < C::TN; t++) {
@@ -221,8 +240,8 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
         f.b1[t] = tr_frag<RB>(sB1, kk * 16, nb, lane);
         f.b2[t] = tr_frag<RB>(sB2, kk * 16, nb, lane);
       } else {
-        f.b1[t] = *(const bf16x8*)(sB1 + swz(nb + (lane & 31), ch));
-        f.b2[t] = *(const bf16x8*)(sB2 + swz(nb + (lane & 31), ch));
+        f.b1[t] = *(const bf16x8*)(sB1 + swz<BK>(nb + (lane & 31), ch));
+        f.b2[t] = *(const bf16x8*)(sB2 + swz<BK>(nb + (lane & 31), ch));
       }
     }
   };
@@ -248,14 +267,18 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
   constexpr int NMFMA = C::TMP * C::TN * (2 + (PL ? 1 : 0) + (PU ? 1 : 0));
   constexpr int NDS = 2 * C::TMP + 2 * C::TN * (TRANS_B ? 2 : 1);
   const int nk = width / BK;
-  issue(0, 0);
-  wait_dma();
-  __syncthreads();
+  // NS-stage ring: stage kt lives in buffer kt % NS; while stage kt is being
+  // multiplied, stages kt+1 .. kt+NS-1 are in flight.
+#pragma unroll
+  for (int st = 0; st < NS - 1; st++)
+    if (st < nk) issue(st, st);
   Frags f[2];
-  load_frags(f[0], smem, 0);
   for (int kt = 0; kt < nk; kt++) {
-    const bf16* sA = smem + (kt & 1) * C::STAGE;
-    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+    wait_stages<NS - 1, C::DPS>(min(nk, kt + NS - 1) - (kt + 1));
+    __syncthreads();  // stage kt visible to all waves; buffer (kt-1) % NS free
+    if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+    const bf16* sA = smem + (kt % NS) * C::STAGE;
+    load_frags(f[0], sA, 0);
 #pragma unroll
     for (int kk = 0; kk < KK; kk++) {
       if (kk + 1 < KK) {
@@ -266,10 +289,8 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
         mma(f[kk & 1]);
       }
     }
-    wait_dma();
-    __syncthreads();
-    if (kt + 1 < nk) load_frags(f[0], smem + ((kt + 1) & 1) * C::STAGE, 0);
   }
+  __syncthreads();  // every wave done with the stage buffers
 
   // Epilogue: round to bf16 into an LDS tile [BM][LDO], then 16-byte row stores.
   // Accumulator element e of lane l holds C[8*(e/4) + 4*(l/32) + e%4][l%32].
@@ -336,8 +357,11 @@ __global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
   const int wo = wave % WO, wc = wave / WO;
   const int tiles_c = width / BC;
   const int tiles = (width / BO) * tiles_c;
-  const int tile = blockIdx.x % tiles;
-  const int split = blockIdx.x / tiles;
+  // split-major order through the XCD deal: every tile of one split (they all
+  // read the same rows of X and dY) runs on one XCD and shares its L2
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = lin % tiles;
+  const int split = lin / tiles;
   const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
   const int s = 1 << d;
   const int pbeg = split * pairs_per_split;
@@ -486,17 +510,20 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
 
 // ---- launch configurations ----
 constexpr int MIX_BMP = 128;          // 256 rows per block
+constexpr int MIX_BK = 64;            // contraction slice per pipeline stage
+constexpr int MIX_NS = 2;             // pipeline stages in LDS
 constexpr int DW_BO = 128, DW_BC = 128;
+constexpr int DW_TARGET_BLOCKS = 512;  // split-K blocks aimed for
 
-template <int BMP, int BN, int WM, int WN, bool TRANS_B>
+template <int BMP, int BN, int WM, int WN, int BK, int NS, bool TRANS_B>
 hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int pairs,
                       int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
-  using C = MixCfg<BMP, BN, WM, WN>;
+  using C = MixCfg<BMP, BN, WM, WN, BK, NS>;
   const int blocks = ((pairs + BMP - 1) / BMP) * (width / BN);
   const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
 #define HCMIX_MIX(PL, PU)                                                                   \
   {                                                                                         \
-    auto k = mix_bf16_kernel<BMP, BN, WM, WN, PL, PU, TRANS_B>;                             \
+    auto k = mix_bf16_kernel<BMP, BN, WM, WN, BK, NS, PL, PU, TRANS_B>;                     \
     static const hipError_t attr = hipFuncSetAttribute(                                     \
         (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
     if (attr != hipSuccess) return attr;                                                    \
@@ -514,10 +541,10 @@ hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out
                         int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
   const int pairs = rows / 2;
   if (width % 128 == 0)
-    return mix_launch<MIX_BMP, 128, 2, 2, TRANS_B>(A, B1, B2, out, pairs, width, d,
-                                                   partner_lower, partner_upper, st);
-  return mix_launch<MIX_BMP, 64, 4, 1, TRANS_B>(A, B1, B2, out, pairs, width, d, partner_lower,
-                                                partner_upper, st);
+    return mix_launch<MIX_BMP, 128, 2, 2, MIX_BK, MIX_NS, TRANS_B>(
+        A, B1, B2, out, pairs, width, d, partner_lower, partner_upper, st);
+  return mix_launch<MIX_BMP, 64, 4, 1, MIX_BK, MIX_NS, TRANS_B>(
+      A, B1, B2, out, pairs, width, d, partner_lower, partner_upper, st);
 }
 
 // Split-K plan: enough blocks to fill the chip (about 512), each split a whole
@@ -527,7 +554,7 @@ int dw_plan(int rows, int width, int* pps) {
   const int bo = width % DW_BO == 0 ? DW_BO : 64;
   const int tiles = (width / bo) * (width / bo);
   const int ksteps = (pairs + KP - 1) / KP;
-  int splits = (512 + tiles - 1) / tiles;
+  int splits = (DW_TARGET_BLOCKS + tiles - 1) / tiles;
   if (splits > ksteps) splits = ksteps;
   if (splits < 1) splits = 1;
   *pps = ((ksteps + splits - 1) / splits) * KP;
