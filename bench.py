@@ -117,11 +117,11 @@ def main():
     dx_out = [torch.empty_like(x0) for _ in range(L)]
     dws = [torch.empty((w, w), dtype=torch.float32, device=dev) for _ in range(L)]
     dwo = [torch.empty((w, w), dtype=torch.float32, device=dev) for _ in range(L)]
-    workspace = hcmix.alloc_workspace(B, n, w, dt, dev)
+    workspace = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
 
     def step():
         xs = hcmix.stack_forward(x0, ws, wo, s.layers, causal, outs=xs_out)
-        hcmix.stack_backward(xs, ws, wo, s.layers, dy, causal, dxs=dx_out, dws=dws, dwo=dwo,
+        hcmix.stack_backward(xs, ws, wo, s.layers, dy, causal, dx=dx_out[0], dws=dws, dwo=dwo,
                              workspace=workspace)
 
     stream = torch.cuda.Stream(device=dev)

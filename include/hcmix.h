@@ -106,6 +106,49 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
                             int32_t accumulate, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* ---- Whole stacks (Section 3.3: a schedule is a list of layer indices) ----
+ *
+ * layers:        host array of num_layers layer indices (layer l uses
+ *                dimension hcmix_dim(layers[l], n)); the rotated schedule is
+ *                0, 1, 2, ..., the fixed control repeats one index.
+ * w_self, w_off: host arrays of num_layers device pointers, one pair per layer.
+ *
+ * For bf16, width 64 and n in {64, 128, 256} (a window of at most 32 KB) the
+ * whole stack runs in one kernel with every window resident in LDS (one
+ * block per window); otherwise the layers run one launch each, with results
+ * identical to calling hcmix_forward / hcmix_backward layer by layer up to
+ * the order of floating-point summation.  num_layers may be at most 64 for
+ * the fused kernels; longer stacks run layer by layer.
+ */
+
+/* Forward through the stack: xs is a host array of num_layers device
+ * pointers receiving x_1 .. x_L, where x_0 = x and x_{l+1} is layer l
+ * applied to x_l.  Every xs[l] must be distinct from each other and from
+ * the inputs. */
+hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                 const int32_t* layers, int32_t mode, int32_t dtype,
+                                 const void* x, const void* const* w_self,
+                                 const void* const* w_off, void* const* xs, void* stream);
+
+/* Bytes of device workspace hcmix_stack_backward needs (0 for invalid
+ * arguments).  256-byte aligned. */
+size_t hcmix_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                            int32_t num_layers, int32_t dtype);
+
+/* Backward through the stack: xs_in is a host array of the num_layers layer
+ * inputs x_0 .. x_{L-1} (device pointers), dy the gradient of x_L.  Writes dx
+ * (gradient of x_0, in dtype) and, for every layer, dw_self[l] and dw_off[l]
+ * (host arrays of device pointers to fp32 [width][width]), overwritten when
+ * accumulate == 0, added to otherwise.  Weight gradients are summed in a
+ * fixed order (bitwise-repeatable). */
+hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                  const int32_t* layers, int32_t mode, int32_t dtype,
+                                  const void* const* xs_in, const void* const* w_self,
+                                  const void* const* w_off, const void* dy, void* dx,
+                                  float* const* dw_self, float* const* dw_off,
+                                  int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
 #ifdef __cplusplus
 }
 #endif

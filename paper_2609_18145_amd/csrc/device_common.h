@@ -1,0 +1,101 @@
+// Device helpers shared by the bf16 kernels: MFMA wrapper, LDS DMA, waits,
+// scheduling hints, LDS swizzles and transposed LDS fragment reads.
+#pragma once
+
+#include "hcmix_internal.h"
+
+namespace hcmix {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 16 bytes global -> LDS; `lds` is the wave-uniform base, lane i lands at +16*i.
+__device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+// Wait for all but the `ahead` most recently issued pipeline stages (DPS DMA
+// instructions each) of this wave; ahead < NA.
+template <int NA, int DPS>
+__device__ __forceinline__ void wait_stages(int ahead) {
+  if constexpr (NA > 0) {
+    if (ahead >= NA - 1) { wait_vmcnt<(NA - 1) * DPS>(); return; }
+    wait_stages<NA - 1, DPS>(ahead);
+  }
+}
+
+// Scheduling hint for one MFMA sub-step: alternate its NMFMA matrix
+// instructions with the NDS LDS reads that fetch the next sub-step's
+// fragments, spreading the reads evenly, so LDS latency hides under MFMAs.
+template <int NMFMA, int NDS>
+__device__ __forceinline__ void interleave_mfma_ds() {
+#pragma unroll
+  for (int i = 0; i < NMFMA; i++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+    const int nds = (NDS * (i + 1)) / NMFMA - (NDS * i) / NMFMA;
+    if (nds == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    if (nds == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if (nds == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+  }
+}
+
+// LDS has 64 banks of 4 bytes: a 128-bit access is conflict-free when each
+// group of 16 lanes covers 256 distinct bytes (mod 256), a 64-bit access when
+// each group of 32 lanes does.
+//
+// k-contiguous tile [rows][BK] (2*BK-byte rows, BK = 32 or 64): 16-byte piece
+// `ch` of row m sits at piece ch ^ ((m / (128/BK)) % (BK/8)), so 16 consecutive
+// rows reading the same piece land in 16 distinct 16-byte slots.  Elements.
+template <int BK>
+__device__ __forceinline__ int swz(int m, int ch) {
+  static_assert(BK == 32 || BK == 64, "");
+  constexpr int RPQ = 128 / BK;   // rows sharing one 256-byte bank window
+  return m * BK + ((ch ^ ((m / RPQ) & (BK / 8 - 1))) << 3);
+}
+
+// Row-major tile read transposed, RB bytes per row (256 or 128): 64-byte
+// segment `seg` of row `row` is stored at segment seg ^ f(row), so the 4 rows
+// x 64 bytes that 32 lanes of a tr read touch fall in distinct bank quarters.
+template <int RB>
+__device__ __forceinline__ int trswz(int row, int seg) {
+  static_assert(RB == 256 || RB == 128, "row of 64 or 128 bf16");
+  return RB == 256 ? (seg ^ (row & 3)) : (seg ^ ((row >> 1) & 1));
+}
+
+// Transposed 32x32x16 operand fragment from a row-major tile T[k][col] with
+// RB-byte rows: lane l gets T[k0 + 8*(l/32) + t][c0 + l%32], t = 0..7, the same
+// k order as a ds_read_b128 fragment of a k-contiguous tile.  c0 % 32 == 0.
+template <int RB>
+__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, int k0, int c0, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const int row = k0 + 8 * (g >> 1) + (j >> 2);
+  const int seg = c0 >> 5;                                   // 32 columns = 64 bytes
+  const int in = 16 * (g & 1) + 4 * (j & 3);                 // column within the segment
+  const bf16* p = tile + row * (RB / 2) + trswz<RB>(row, seg) * 32 + in;
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * (RB / 2)));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Source element offset (row, column) for lane i of DMA block b of a tr tile.
+template <int RB>
+__device__ __forceinline__ void tr_dma_coord(int b, int i, int* row, int* col) {
+  const int o = b * 1024 + 16 * i;          // byte offset in the tile
+  const int r = o / RB, ob = o % RB;
+  const int seg = trswz<RB>(r, ob >> 6);    // the swizzle is an involution
+  *row = r;
+  *col = seg * 32 + ((ob & 63) >> 1);
+}
+
+}  // namespace hcmix

@@ -1,6 +1,6 @@
 // C ABI of libhcmix.so: argument validation and kernel dispatch.
 // Every check runs before anything is enqueued, so a rejected call has no
-// effect; there is one kernel path per dtype and no fallback.
+// effect; there is one kernel path per shape class and no fallback.
 #include "hcmix.h"
 #include "hcmix_internal.h"
 
@@ -20,6 +20,7 @@ hcmix_status hip_fail(hipError_t e) {
 
 constexpr int64_t kMaxRows = (int64_t)1 << 30;      // row indices stay in int32
 constexpr int64_t kMaxElems = (int64_t)1 << 40;     // element offsets in size_t
+constexpr int32_t kMaxLayers = 1 << 16;
 
 size_t elem_size(int32_t dtype) { return dtype == HCMIX_BF16 ? 2 : 4; }
 
@@ -30,7 +31,9 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Shape checks shared by forward and backward; returns HCMIX_OK or the error.
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Shape checks shared by every entry point; returns HCMIX_OK or the error.
 hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer, int32_t mode,
                          int32_t dtype) {
   if (hcmix_dim(layer, n) < 0) return HCMIX_ERR_INVALID_VALUE;
@@ -43,14 +46,84 @@ hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer,
   return HCMIX_OK;
 }
 
-// Backward workspace (bf16): the split-K partial sums of the weight gradients,
-// [splits][2][width][width] fp32.
-size_t align256(size_t v) { return (v + 255) / 256 * 256; }
-
-size_t workspace_bytes_checked(int64_t batch, int64_t n, int64_t width, int32_t dtype) {
+// Backward workspace (bf16): the split-K partial sums of the weight
+// gradients, [splits][2][width][width] fp32.
+size_t layer_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t dtype) {
   if (dtype != HCMIX_BF16) return 0;
   const int splits = dw_bf16_splits((int)(batch * n), (int)width);
   return align256((size_t)splits * 2 * width * width * sizeof(float));
+}
+
+// Stack backward workspace: the per-window partials of the fused path, or two
+// gradient buffers plus one layer's workspace for the layer-by-layer path.
+size_t stack_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                             int32_t dtype) {
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers))
+    return align256(fused_partial_bytes(batch, num_layers));
+  const size_t act = align256((size_t)(batch * n * width) * elem_size(dtype));
+  return (num_layers > 1 ? 2 * act : 0) + layer_workspace_bytes(batch, n, width, dtype);
+}
+
+// ---- unchecked per-layer dispatch (arguments already validated) ----
+
+hipError_t run_forward(int rows, int w, int d, int bidir, int32_t dtype, const void* x,
+                       const void* w_self, const void* w_off, void* y, hipStream_t s) {
+  if (dtype == HCMIX_BF16)
+    return launch_mix_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y,
+                           rows, w, d, /*partner_lower=*/bidir, /*partner_upper=*/1,
+                           /*transpose_b=*/false, s);
+  return launch_mix_f32((const float*)x, (const float*)w_self, (const float*)w_off, (float*)y,
+                        rows, w, d, bidir, 1, /*transpose_w=*/false, s);
+}
+
+hipError_t run_backward(int rows, int w, int d, int bidir, int32_t dtype, const void* x,
+                        const void* w_self, const void* w_off, const void* dy, void* dx,
+                        float* dw_self, float* dw_off, int accumulate, void* workspace,
+                        hipStream_t s) {
+  hipError_t e;
+  if (dtype == HCMIX_BF16) {
+    e = launch_mix_bf16((const bf16*)dy, (const bf16*)w_self, (const bf16*)w_off, (bf16*)dx,
+                        rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
+                        /*transpose_b=*/true, s);
+    if (e == hipSuccess)
+      e = launch_dw_bf16((const bf16*)x, (const bf16*)dy, (float*)workspace, dw_self, dw_off,
+                         rows, w, d, bidir, accumulate, s);
+  } else {
+    e = launch_mix_f32((const float*)dy, (const float*)w_self, (const float*)w_off, (float*)dx,
+                       rows, w, d, 1, bidir, /*transpose_w=*/true, s);
+    if (e == hipSuccess)
+      e = launch_dw_f32((const float*)x, (const float*)dy, dw_self, dw_off, rows, w, d, bidir,
+                        accumulate, s);
+  }
+  return e;
+}
+
+// A buffer in a call: its address and extent in bytes.
+struct Span {
+  const void* p;
+  size_t n;
+};
+
+// Inputs must be non-null; outputs (with nonzero extent) non-null and
+// overlapping no input and no other output; everything aligned to `al`.
+hcmix_status check_spans(const Span* ins, int nin, const Span* outs, int nout, size_t al) {
+  for (int i = 0; i < nin; i++)
+    if (!ins[i].p) return HCMIX_ERR_INVALID_VALUE;
+  for (int i = 0; i < nout; i++)
+    if (!outs[i].p && outs[i].n) return HCMIX_ERR_INVALID_VALUE;
+  for (int i = 0; i < nout; i++) {
+    if (!outs[i].n) continue;
+    for (int j = 0; j < nin; j++)
+      if (overlaps(outs[i].p, outs[i].n, ins[j].p, ins[j].n)) return HCMIX_ERR_INVALID_VALUE;
+    for (int j = i + 1; j < nout; j++)
+      if (outs[j].n && overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n))
+        return HCMIX_ERR_INVALID_VALUE;
+  }
+  for (int i = 0; i < nin; i++)
+    if (!aligned(ins[i].p, al)) return HCMIX_ERR_UNSUPPORTED;
+  for (int i = 0; i < nout; i++)
+    if (outs[i].n && !aligned(outs[i].p, al)) return HCMIX_ERR_UNSUPPORTED;
+  return HCMIX_OK;
 }
 
 }  // namespace
@@ -84,30 +157,19 @@ hcmix_status hcmix_forward(int64_t batch, int64_t n, int64_t width, int32_t laye
   if (st != HCMIX_OK) return st;
   const size_t es = elem_size(dtype);
   const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
-  if (overlaps(y, act, x, act) || overlaps(y, act, w_self, wgt) || overlaps(y, act, w_off, wgt))
-    return HCMIX_ERR_INVALID_VALUE;
-  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
-  if (!aligned(x, al) || !aligned(w_self, al) || !aligned(w_off, al) || !aligned(y, al))
-    return HCMIX_ERR_UNSUPPORTED;
-
-  const int d = hcmix_dim(layer, n);
-  const int rows = (int)(batch * n), w = (int)width;
-  const int bidir = mode == HCMIX_BIDIR;
-  hipStream_t s = (hipStream_t)stream;
-  hipError_t e;
-  if (dtype == HCMIX_BF16)
-    e = launch_mix_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y, rows,
-                        w, d, /*partner_lower=*/bidir, /*partner_upper=*/1,
-                        /*transpose_b=*/false, s);
-  else
-    e = launch_mix_f32((const float*)x, (const float*)w_self, (const float*)w_off, (float*)y,
-                       rows, w, d, bidir, 1, /*transpose_w=*/false, s);
+  const Span ins[3] = {{x, act}, {w_self, wgt}, {w_off, wgt}};
+  const Span outs[1] = {{y, act}};
+  st = check_spans(ins, 3, outs, 1, dtype == HCMIX_BF16 ? 16 : 4);
+  if (st != HCMIX_OK) return st;
+  hipError_t e = run_forward((int)(batch * n), (int)width, hcmix_dim(layer, n),
+                             mode == HCMIX_BIDIR, dtype, x, w_self, w_off, y,
+                             (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
 size_t hcmix_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t dtype) {
   if (check_shape(batch, n, width, 0, HCMIX_BIDIR, dtype) != HCMIX_OK) return 0;
-  return workspace_bytes_checked(batch, n, width, dtype);
+  return layer_workspace_bytes(batch, n, width, dtype);
 }
 
 hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t layer, int32_t mode,
@@ -119,49 +181,171 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
     return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_shape(batch, n, width, layer, mode, dtype);
   if (st != HCMIX_OK) return st;
-  const size_t need = workspace_bytes_checked(batch, n, width, dtype);
+  const size_t need = layer_workspace_bytes(batch, n, width, dtype);
   if (need > 0 && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
   const size_t es = elem_size(dtype);
   const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
   const size_t gw = (size_t)(width * width) * sizeof(float);
-  // outputs must not overlap each other or any input
-  const void* outs[4] = {dx, dw_self, dw_off, workspace};
-  const size_t out_n[4] = {act, gw, gw, need};
-  const void* ins[4] = {x, w_self, w_off, dy};
-  const size_t in_n[4] = {act, wgt, wgt, act};
-  for (int i = 0; i < 4; i++) {
-    if (out_n[i] == 0) continue;
-    for (int j = 0; j < 4; j++)
-      if (overlaps(outs[i], out_n[i], ins[j], in_n[j])) return HCMIX_ERR_INVALID_VALUE;
-    for (int j = i + 1; j < 4; j++)
-      if (out_n[j] && overlaps(outs[i], out_n[i], outs[j], out_n[j]))
-        return HCMIX_ERR_INVALID_VALUE;
-  }
-  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
-  if (!aligned(x, al) || !aligned(w_self, al) || !aligned(w_off, al) || !aligned(dy, al) ||
-      !aligned(dx, al) || !aligned(dw_self, 16) || !aligned(dw_off, 16))
+  const Span ins[4] = {{x, act}, {w_self, wgt}, {w_off, wgt}, {dy, act}};
+  const Span outs[4] = {{dx, act}, {dw_self, gw}, {dw_off, gw}, {workspace, need}};
+  st = check_spans(ins, 4, outs, 4, dtype == HCMIX_BF16 ? 16 : 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(dw_self, 16) || !aligned(dw_off, 16) || (need && !aligned(workspace, 256)))
     return HCMIX_ERR_UNSUPPORTED;
-  if (need > 0 && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = run_backward((int)(batch * n), (int)width, hcmix_dim(layer, n),
+                              mode == HCMIX_BIDIR, dtype, x, w_self, w_off, dy, dx, dw_self,
+                              dw_off, accumulate != 0, workspace, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
 
-  const int d = hcmix_dim(layer, n);
+hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                 const int32_t* layers, int32_t mode, int32_t dtype,
+                                 const void* x, const void* const* w_self,
+                                 const void* const* w_off, void* const* xs, void* stream) {
+  if (!x || !layers || !w_self || !w_off || !xs) return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], mode, dtype);
+    if (st != HCMIX_OK) return st;
+  }
+  const size_t es = elem_size(dtype);
+  const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
+  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
+  for (int l = 0; l < num_layers; l++) {
+    const Span ins[3] = {{x, act}, {w_self[l], wgt}, {w_off[l], wgt}};
+    const Span outs[1] = {{xs[l], act}};
+    hcmix_status st = check_spans(ins, 3, outs, 1, al);
+    if (st != HCMIX_OK) return st;
+    for (int j = 0; j < num_layers; j++) {
+      if (j != l && overlaps(xs[l], act, xs[j], act)) return HCMIX_ERR_INVALID_VALUE;
+      if (overlaps(xs[l], act, w_self[j], wgt) || overlaps(xs[l], act, w_off[j], wgt))
+        return HCMIX_ERR_INVALID_VALUE;
+    }
+  }
   const int rows = (int)(batch * n), w = (int)width;
   const int bidir = mode == HCMIX_BIDIR;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e;
-  if (dtype == HCMIX_BF16) {
-    float* partial = (float*)workspace;
-    e = launch_mix_bf16((const bf16*)dy, (const bf16*)w_self, (const bf16*)w_off, (bf16*)dx,
-                        rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
-                        /*transpose_b=*/true, s);
-    if (e == hipSuccess)
-      e = launch_dw_bf16((const bf16*)x, (const bf16*)dy, partial, dw_self, dw_off, rows, w, d,
-                         bidir, accumulate != 0, s);
+  hipError_t e = hipSuccess;
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
+    FusedFwdArgs a = {};
+    a.x0 = (const bf16*)x;
+    for (int l = 0; l < num_layers; l++) {
+      a.ws[l] = (const bf16*)w_self[l];
+      a.wo[l] = (const bf16*)w_off[l];
+      a.xs[l] = (bf16*)xs[l];
+      a.dim[l] = hcmix_dim(layers[l], n);
+    }
+    a.n = (int)n;
+    a.num_layers = num_layers;
+    e = launch_fused_forward(a, (int)batch, bidir, s);
   } else {
-    e = launch_mix_f32((const float*)dy, (const float*)w_self, (const float*)w_off, (float*)dx,
-                       rows, w, d, 1, bidir, /*transpose_w=*/true, s);
-    if (e == hipSuccess)
-      e = launch_dw_f32((const float*)x, (const float*)dy, dw_self, dw_off, rows, w, d, bidir,
-                        accumulate != 0, s);
+    const void* in = x;
+    for (int l = 0; l < num_layers && e == hipSuccess; l++) {
+      e = run_forward(rows, w, hcmix_dim(layers[l], n), bidir, dtype, in, w_self[l], w_off[l],
+                      xs[l], s);
+      in = xs[l];
+    }
+  }
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+size_t hcmix_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                            int32_t num_layers, int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers) return 0;
+  if (check_shape(batch, n, width, 0, HCMIX_BIDIR, dtype) != HCMIX_OK) return 0;
+  return stack_workspace_bytes(batch, n, width, num_layers, dtype);
+}
+
+hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                  const int32_t* layers, int32_t mode, int32_t dtype,
+                                  const void* const* xs_in, const void* const* w_self,
+                                  const void* const* w_off, const void* dy, void* dx,
+                                  float* const* dw_self, float* const* dw_off,
+                                  int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  if (!layers || !xs_in || !w_self || !w_off || !dy || !dx || !dw_self || !dw_off)
+    return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], mode, dtype);
+    if (st != HCMIX_OK) return st;
+    if (!xs_in[l] || !w_self[l] || !w_off[l] || !dw_self[l] || !dw_off[l])
+      return HCMIX_ERR_INVALID_VALUE;
+  }
+  const size_t need = stack_workspace_bytes(batch, n, width, num_layers, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
+  const size_t es = elem_size(dtype);
+  const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
+  const size_t gw = (size_t)(width * width) * sizeof(float);
+  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
+  // Outputs: dx, the workspace and every weight gradient.  Inputs: dy, every
+  // layer input and weight.  No output may overlap any input or other output.
+  const Span outs_fixed[2] = {{dx, act}, {workspace, need}};
+  {
+    const Span ins[1] = {{dy, act}};
+    hcmix_status st = check_spans(ins, 1, outs_fixed, 2, al);
+    if (st != HCMIX_OK) return st;
+  }
+  for (int l = 0; l < num_layers; l++) {
+    const Span ins[3] = {{xs_in[l], act}, {w_self[l], wgt}, {w_off[l], wgt}};
+    const Span outs[4] = {outs_fixed[0], outs_fixed[1], {dw_self[l], gw}, {dw_off[l], gw}};
+    hcmix_status st = check_spans(ins, 3, outs, 4, al);
+    if (st != HCMIX_OK) return st;
+    for (int j = 0; j < num_layers; j++) {
+      if (j == l) continue;
+      const Span other_ins[3] = {{xs_in[j], act}, {w_self[j], wgt}, {w_off[j], wgt}};
+      const Span other_outs[2] = {{dw_self[j], gw}, {dw_off[j], gw}};
+      for (int k = 2; k < 4; k++) {
+        for (int m = 0; m < 3; m++)
+          if (overlaps(outs[k].p, outs[k].n, other_ins[m].p, other_ins[m].n))
+            return HCMIX_ERR_INVALID_VALUE;
+        for (int m = 0; m < 2; m++)
+          if (overlaps(outs[k].p, outs[k].n, other_outs[m].p, other_outs[m].n))
+            return HCMIX_ERR_INVALID_VALUE;
+      }
+    }
+    if (!aligned(dw_self[l], 16) || !aligned(dw_off[l], 16)) return HCMIX_ERR_UNSUPPORTED;
+  }
+  if (need && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+
+  const int rows = (int)(batch * n), w = (int)width;
+  const int bidir = mode == HCMIX_BIDIR;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
+    FusedBwdArgs a = {};
+    FusedReduceArgs r = {};
+    for (int l = 0; l < num_layers; l++) {
+      a.xs[l] = (const bf16*)xs_in[l];
+      a.ws[l] = (const bf16*)w_self[l];
+      a.wo[l] = (const bf16*)w_off[l];
+      a.dim[l] = hcmix_dim(layers[l], n);
+      r.dws[l] = dw_self[l];
+      r.dwo[l] = dw_off[l];
+    }
+    a.dy = (const bf16*)dy;
+    a.dx = (bf16*)dx;
+    a.partial = (float*)workspace;
+    a.n = (int)n;
+    a.num_layers = num_layers;
+    r.partial = (const float*)workspace;
+    r.batch = (int)batch;
+    r.num_layers = num_layers;
+    r.accumulate = accumulate != 0;
+    e = launch_fused_backward(a, r, (int)batch, bidir, s);
+  } else {
+    // layer by layer; intermediate gradients ping-pong in the workspace
+    const size_t act_al = align256(act);
+    char* ws = (char*)workspace;
+    void* gbuf[2] = {ws, ws + act_al};
+    void* layer_ws = ws + (num_layers > 1 ? 2 * act_al : 0);
+    const void* g = dy;
+    for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
+      void* out = l == 0 ? dx : gbuf[l & 1];
+      e = run_backward(rows, w, hcmix_dim(layers[l], n), bidir, dtype, xs_in[l], w_self[l],
+                       w_off[l], g, out, dw_self[l], dw_off[l], accumulate != 0, layer_ws, s);
+      g = out;
+    }
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }

@@ -54,4 +54,40 @@ hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* 
                           int rows, int width, int d, int bidir, int accumulate,
                           hipStream_t st);
 
+// ---- fused small-width stack (width 64, n in {64, 128, 256}) ----
+constexpr int kFusedMaxLayers = 64;
+
+struct FusedFwdArgs {
+  const bf16* x0;
+  const bf16* ws[kFusedMaxLayers];
+  const bf16* wo[kFusedMaxLayers];
+  bf16* xs[kFusedMaxLayers];       // x_1 .. x_L
+  int dim[kFusedMaxLayers];        // hypercube dimension of each layer
+  int n, num_layers;
+};
+
+struct FusedBwdArgs {
+  const bf16* xs[kFusedMaxLayers];  // input of each layer, x_0 .. x_{L-1}
+  const bf16* ws[kFusedMaxLayers];
+  const bf16* wo[kFusedMaxLayers];
+  int dim[kFusedMaxLayers];
+  const bf16* dy;                   // gradient of x_L
+  bf16* dx;                         // gradient of x_0
+  float* partial;                   // [batch][L][2][64][64] per-window weight gradients
+  int n, num_layers;
+};
+
+struct FusedReduceArgs {
+  const float* partial;
+  float* dws[kFusedMaxLayers];
+  float* dwo[kFusedMaxLayers];
+  int batch, num_layers, accumulate;
+};
+
+bool fused_stack_eligible(int64_t n, int64_t width, int32_t num_layers);
+size_t fused_partial_bytes(int64_t batch, int32_t num_layers);
+hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hipStream_t st);
+hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
+                                 bool bidir, hipStream_t st);
+
 }  // namespace hcmix

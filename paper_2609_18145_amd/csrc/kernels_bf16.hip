@@ -20,102 +20,11 @@
 // row (base + j/4), column (c0 + 4*(j%4)); lane i then receives column c0 + i
 // of those 4 rows.
 #include "hcmix_internal.h"
+#include "device_common.h"
 
 namespace hcmix {
 
 namespace {
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-
-__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-// 16 bytes global -> LDS; `lds` is the wave-uniform base, lane i lands at +16*i.
-__device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
-  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
-}
-
-__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// Wait until at most N vector-memory operations of this wave are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
-
-// Wait for all but the `ahead` most recently issued pipeline stages (DPS DMA
-// instructions each) of this wave; ahead < NA.
-template <int NA, int DPS>
-__device__ __forceinline__ void wait_stages(int ahead) {
-  if constexpr (NA > 0) {
-    if (ahead >= NA - 1) { wait_vmcnt<(NA - 1) * DPS>(); return; }
-    wait_stages<NA - 1, DPS>(ahead);
-  }
-}
-
-// Scheduling hint for one MFMA sub-step: alternate its NMFMA matrix
-// instructions with the NDS LDS reads that fetch the next sub-step's
-// fragments, spreading the reads evenly, so LDS latency hides under MFMAs.
-template <int NMFMA, int NDS>
-__device__ __forceinline__ void interleave_mfma_ds() {
-#pragma unroll
-  for (int i = 0; i < NMFMA; i++) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
-    const int nds = (NDS * (i + 1)) / NMFMA - (NDS * i) / NMFMA;
-    if (nds == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
-    if (nds == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    if (nds == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-  }
-}
-
-// LDS has 64 banks of 4 bytes: a 128-bit access is conflict-free when each
-// group of 16 lanes covers 256 distinct bytes (mod 256), a 64-bit access when
-// each group of 32 lanes does.
-//
-// k-contiguous tile [rows][BK] (2*BK-byte rows, BK = 32 or 64): 16-byte piece
-// `ch` of row m sits at piece ch ^ ((m / (128/BK)) % (BK/8)), so 16 consecutive
-// rows reading the same piece land in 16 distinct 16-byte slots.  Elements.
-template <int BK>
-__device__ __forceinline__ int swz(int m, int ch) {
-  static_assert(BK == 32 || BK == 64, "");
-  constexpr int RPQ = 128 / BK;   // rows sharing one 256-byte bank window
-  return m * BK + ((ch ^ ((m / RPQ) & (BK / 8 - 1))) << 3);
-}
-
-// Row-major tile read transposed, RB bytes per row (256 or 128): 64-byte
-// segment `seg` of row `row` is stored at segment seg ^ f(row), so the 4 rows
-// x 64 bytes that 32 lanes of a tr read touch fall in distinct bank quarters.
-template <int RB>
-__device__ __forceinline__ int trswz(int row, int seg) {
-  static_assert(RB == 256 || RB == 128, "row of 64 or 128 bf16");
-  return RB == 256 ? (seg ^ (row & 3)) : (seg ^ ((row >> 1) & 1));
-}
-
-// Transposed 32x32x16 operand fragment from a row-major tile T[k][col] with
-// RB-byte rows: lane l gets T[k0 + 8*(l/32) + t][c0 + l%32], t = 0..7, the same
-// k order as a ds_read_b128 fragment of a k-contiguous tile.  c0 % 32 == 0.
-template <int RB>
-__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, int k0, int c0, int lane) {
-  const int g = lane >> 4, j = lane & 15;
-  const int row = k0 + 8 * (g >> 1) + (j >> 2);
-  const int seg = c0 >> 5;                                   // 32 columns = 64 bytes
-  const int in = 16 * (g & 1) + 4 * (j & 3);                 // column within the segment
-  const bf16* p = tile + row * (RB / 2) + trswz<RB>(row, seg) * 32 + in;
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
-  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * (RB / 2)));
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// Source element offset (row, column) for lane i of DMA block b of a tr tile.
-template <int RB>
-__device__ __forceinline__ void tr_dma_coord(int b, int i, int* row, int* col) {
-  const int o = b * 1024 + 16 * i;          // byte offset in the tile
-  const int r = o / RB, ob = o % RB;
-  const int seg = trswz<RB>(r, ob >> 6);    // the swizzle is an involution
-  *row = r;
-  *col = seg * 32 + ((ob & 63) >> 1);
-}
 
 // Block index -> tile index, keeping consecutive tiles (the column tiles of
 // one row tile) on one XCD: blocks are dealt to the 8 XCDs round-robin.
@@ -245,21 +154,24 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
       }
     }
   };
+  // The accumulators hold the transposed product (weights as the MFMA "A"
+  // operand, activation rows as "B"), so each lane owns one output row and 16
+  // of its columns: the epilogue writes 8-byte runs instead of single values.
   auto mma = [&](const Frags& f) {
     // self terms first, partner terms after, so no MFMA waits on the one before it
 #pragma unroll
     for (int p = 0; p < C::TMP; p++)
 #pragma unroll
       for (int t = 0; t < C::TN; t++) {
-        accL[p][t] = mfma32(f.aL[p], f.b1[t], accL[p][t]);
-        accU[p][t] = mfma32(f.aU[p], f.b1[t], accU[p][t]);
+        accL[p][t] = mfma32(f.b1[t], f.aL[p], accL[p][t]);
+        accU[p][t] = mfma32(f.b1[t], f.aU[p], accU[p][t]);
       }
 #pragma unroll
     for (int p = 0; p < C::TMP; p++)
 #pragma unroll
       for (int t = 0; t < C::TN; t++) {
-        if (PU) accU[p][t] = mfma32(f.aL[p], f.b2[t], accU[p][t]);
-        if (PL) accL[p][t] = mfma32(f.aU[p], f.b2[t], accL[p][t]);
+        if (PU) accU[p][t] = mfma32(f.b2[t], f.aL[p], accU[p][t]);
+        if (PL) accL[p][t] = mfma32(f.b2[t], f.aU[p], accL[p][t]);
       }
   };
 
@@ -293,20 +205,25 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
   __syncthreads();  // every wave done with the stage buffers
 
   // Epilogue: round to bf16 into an LDS tile [BM][LDO], then 16-byte row stores.
-  // Accumulator element e of lane l holds C[8*(e/4) + 4*(l/32) + e%4][l%32].
+  // Accumulator element e of lane l holds output row (lane's row l%32) and
+  // column 8*(e/4) + 4*(l/32) + e%4 of its 32 x 32 block.
   bf16* sO = smem;
 #pragma unroll
   for (int p = 0; p < C::TMP; p++)
 #pragma unroll
-    for (int t = 0; t < C::TN; t++)
+    for (int t = 0; t < C::TN; t++) {
+      const int m = (wm * C::TMP + p) * 32 + (lane & 31);
+      const int col = (wn * C::TN + t) * 32 + 4 * (lane >> 5);
 #pragma unroll
-      for (int e = 0; e < 16; e++) {
-        const int i = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int m = (wm * C::TMP + p) * 32 + i;
-        const int col = (wn * C::TN + t) * 32 + (lane & 31);
-        sO[m * C::LDO + col] = to_bf16(accL[p][t][e]);
-        sO[(m + BMP) * C::LDO + col] = to_bf16(accU[p][t][e]);
+      for (int g = 0; g < 4; g++) {
+        const bf16x4 vl = {to_bf16(accL[p][t][4 * g]), to_bf16(accL[p][t][4 * g + 1]),
+                           to_bf16(accL[p][t][4 * g + 2]), to_bf16(accL[p][t][4 * g + 3])};
+        const bf16x4 vu = {to_bf16(accU[p][t][4 * g]), to_bf16(accU[p][t][4 * g + 1]),
+                           to_bf16(accU[p][t][4 * g + 2]), to_bf16(accU[p][t][4 * g + 3])};
+        *(bf16x4*)(sO + m * C::LDO + col + 8 * g) = vl;
+        *(bf16x4*)(sO + (m + BMP) * C::LDO + col + 8 * g) = vu;
       }
+    }
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < C::O_IT; j++) {

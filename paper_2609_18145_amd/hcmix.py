@@ -23,7 +23,8 @@ HCMIX_BIDIR, HCMIX_CAUSAL = 0, 1
 
 # every symbol declared in include/hcmix.h
 EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_forward",
-           "hcmix_backward_workspace_bytes", "hcmix_backward")
+           "hcmix_backward_workspace_bytes", "hcmix_backward", "hcmix_stack_forward",
+           "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward")
 
 _lib = None
 
@@ -58,6 +59,15 @@ def load():
         lib.hcmix_backward.argtypes = [i64, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, fp, fp,
                                        i32, vp, sz, vp]
         lib.hcmix_backward.restype = i32
+        pp = ctypes.POINTER(ctypes.c_void_p)
+        ip = ctypes.POINTER(ctypes.c_int32)
+        lib.hcmix_stack_forward.argtypes = [i64, i64, i64, i32, ip, i32, i32, vp, pp, pp, pp, vp]
+        lib.hcmix_stack_forward.restype = i32
+        lib.hcmix_stack_backward_workspace_bytes.argtypes = [i64, i64, i64, i32, i32]
+        lib.hcmix_stack_backward_workspace_bytes.restype = sz
+        lib.hcmix_stack_backward.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp, vp, vp,
+                                             pp, pp, i32, vp, sz, vp]
+        lib.hcmix_stack_backward.restype = i32
         _lib = lib
     return _lib
 
@@ -143,30 +153,64 @@ def backward(x, w_self, w_off, dy, layer: int, causal: bool, dx=None, dw_self=No
     return dx, dw_self, dw_off
 
 
+def _ptrs(ts):
+    return (ctypes.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
+
+
+def _layers(layers):
+    return (ctypes.c_int32 * len(layers))(*[int(v) for v in layers])
+
+
 def stack_forward(x, w_selfs, w_offs, layers, causal, outs=None):
-    """Run the layers in order; returns the list [x_0, x_1, ..., x_L]."""
-    xs = [x]
-    for l, (ws, wo, layer) in enumerate(zip(w_selfs, w_offs, layers)):
-        xs.append(forward(xs[-1], ws, wo, layer, causal, out=None if outs is None else outs[l]))
-    return xs
+    """Run the layers in order in one library call; returns [x_0, x_1, ..., x_L]."""
+    L = len(layers)
+    _check(x, *w_selfs, *w_offs)
+    if outs is None:
+        outs = [torch.empty_like(x) for _ in range(L)]
+    _check(x, *outs)
+    batch, n, width = x.shape
+    rc = load().hcmix_stack_forward(batch, n, width, L, _layers(layers), int(bool(causal)),
+                                    _dtype_code(x), _ptr(x), _ptrs(w_selfs), _ptrs(w_offs),
+                                    _ptrs(outs), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_stack_forward")
+    return [x, *outs]
 
 
-def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dxs=None, dws=None, dwo=None,
-                   workspace=None):
-    """Backward through the stack in reverse; returns (dx_0, [dW_self], [dW_off])."""
+def stack_workspace_bytes(batch, n, width, num_layers, dtype) -> int:
+    code = HCMIX_BF16 if dtype == torch.bfloat16 else HCMIX_F32
+    return load().hcmix_stack_backward_workspace_bytes(batch, n, width, num_layers, code)
+
+
+def alloc_stack_workspace(batch, n, width, num_layers, dtype, device):
+    nbytes = stack_workspace_bytes(batch, n, width, num_layers, dtype)
+    return None if nbytes == 0 else torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dx=None, dws=None, dwo=None,
+                   accumulate=False, workspace=None):
+    """Backward through the stack in one library call, using the saved layer
+    inputs xs[0..L-1]; returns (dx_0, [dW_self], [dW_off])."""
     L = len(layers)
     x0 = xs[0]
+    _check(x0, *xs[:L], *w_selfs, *w_offs, dy)
     batch, n, width = x0.shape
+    if dx is None:
+        dx = torch.empty_like(x0)
+    if dws is None:
+        dws = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+    if dwo is None:
+        dwo = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
     if workspace is None:
-        workspace = alloc_workspace(batch, n, width, x0.dtype, x0.device)
-    g = dy
-    dws = dws if dws is not None else [None] * L
-    dwo = dwo if dwo is not None else [None] * L
-    for l in reversed(range(L)):
-        out = None if dxs is None else dxs[l]
-        g, dws[l], dwo[l] = backward(xs[l], w_selfs[l], w_offs[l], g, layers[l], causal, dx=out,
-                                     dw_self=dws[l], dw_off=dwo[l], workspace=workspace)
-    return g, dws, dwo
+        workspace = alloc_stack_workspace(batch, n, width, L, x0.dtype, x0.device)
+    ws_bytes = workspace.numel() if workspace is not None else 0
+    rc = load().hcmix_stack_backward(batch, n, width, L, _layers(layers), int(bool(causal)),
+                                     _dtype_code(x0), _ptrs(xs[:L]), _ptrs(w_selfs), _ptrs(w_offs),
+                                     _ptr(dy), _ptr(dx), _ptrs(dws), _ptrs(dwo),
+                                     int(bool(accumulate)), _ptr(workspace), ws_bytes, _stream(x0))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_stack_backward")
+    return dx, dws, dwo
 
 
 class Stack(torch.autograd.Function):

@@ -117,3 +117,35 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(hcmix, "LIB_PATH", str(tmp_path / "libhcmix.so"))
     with pytest.raises(RuntimeError, match="missing"):
         hcmix.load()
+
+
+LP = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+PP = lambda *ps: (ctypes.c_void_p * len(ps))(*[p.value for p in ps])  # noqa: E731
+
+
+def sfwd(batch=2, n=16, width=64, L=4, layers=LP, mode=0, dtype=1, x=P[0], ws=None, wo=None, xs=None):
+    ws = ws if ws is not None else PP(P[1], P[1], P[1], P[1])
+    wo = wo if wo is not None else PP(P[2], P[2], P[2], P[2])
+    xs = xs if xs is not None else PP(P[3], P[4], P[5], P[6])
+    return hcmix.load().hcmix_stack_forward(batch, n, width, L, layers, mode, dtype, x, ws, wo, xs, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), INVALID), (dict(n=12), INVALID), (dict(layers=(ctypes.c_int32 * 4)(0, -1, 2, 3)), INVALID),
+    (dict(x=None), INVALID), (dict(xs=PP(P[3], P[3], P[5], P[6])), INVALID),   # two outputs alias
+    (dict(xs=PP(P[0], P[4], P[5], P[6])), INVALID),                            # output aliases x
+    (dict(xs=PP(P[3], P[4], P[1], P[6])), INVALID),                            # output aliases a weight
+    (dict(width=96), UNSUPPORTED),
+])
+def test_stack_forward_rejects_bad_arguments(kw, code):
+    assert sfwd(**kw) == code
+
+
+def test_stack_workspace_query():
+    lib = hcmix.load()
+    fused = lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 8, hcmix.HCMIX_BF16)
+    assert fused == 64 * 8 * 2 * 64 * 64 * 4          # per-window partial weight gradients
+    wide = lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16)
+    assert wide >= 2 * 64 * 256 * 512 * 2              # two gradient buffers + one layer's partials
+    assert lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 0, hcmix.HCMIX_BF16) == 0
+    assert lib.hcmix_stack_backward_workspace_bytes(2, 16, 32, 1, hcmix.HCMIX_F32) == 0
