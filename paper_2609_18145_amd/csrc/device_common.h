@@ -19,6 +19,15 @@ __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
 }
 
+// 16-byte store through the global address space.  Pointers that were read
+// from memory (rather than taken from kernel arguments) are generic, and a
+// generic store becomes a FLAT instruction, which also counts on lgkmcnt and
+// so serialises with the LDS reads that feed it.
+typedef __attribute__((address_space(1))) u32x4 global_u32x4;
+__device__ __forceinline__ void store_global16(void* dst, const u32x4& v) {
+  *(global_u32x4*)dst = v;
+}
+
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
@@ -45,6 +54,24 @@ __device__ __forceinline__ void interleave_mfma_ds() {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
     const int nds = (NDS * (i + 1)) / NMFMA - (NDS * i) / NMFMA;
     if (nds == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    if (nds == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if (nds == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+  }
+}
+
+// Same, with the DS reads front-loaded: with NDS <= NMFMA one read follows
+// each of the first NDS MFMAs, so the last read is issued several MFMAs before
+// the region ends and the next region's first MFMA does not wait for it
+// (with more reads than MFMAs, the extra ones go to the first MFMAs).  Use
+// inside a region fenced with __builtin_amdgcn_sched_barrier(0) on both sides.
+template <int NMFMA, int NDS>
+__device__ __forceinline__ void interleave_front() {
+  static_assert(NDS <= 3 * NMFMA, "");
+#pragma unroll
+  for (int i = 0; i < NMFMA; i++) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    const int nds = NDS / NMFMA + (i < NDS % NMFMA ? 1 : 0);
+    if (nds == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     if (nds == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     if (nds == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
   }

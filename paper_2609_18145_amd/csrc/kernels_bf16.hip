@@ -193,13 +193,15 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
     load_frags(f[0], sA, 0);
 #pragma unroll
     for (int kk = 0; kk < KK; kk++) {
+      // one fenced region per kk: this kk's MFMAs with the next kk's reads
       if (kk + 1 < KK) {
         load_frags(f[(kk + 1) & 1], sA, kk + 1);
         mma(f[kk & 1]);
-        interleave_mfma_ds<NMFMA, NDS>();
+        interleave_front<NMFMA, NDS>();
       } else {
         mma(f[kk & 1]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   __syncthreads();  // every wave done with the stage buffers

@@ -7,8 +7,13 @@
 // Activation buffers use the k-contiguous swizzle (rows of 128 bytes, 16-byte
 // piece ch stored at ch ^ ((row >> 1) & 7)); weight buffers read transposed
 // (backward) use the 64-byte segment swizzle of tr_frag.  Fragments whose
-// contraction index runs over rows are gathered with ds_read_b64_tr_b16 whose
-// per-lane row addresses apply the XOR pairing directly.
+// contraction index runs over row pairs are gathered with ds_read_b64_tr_b16.
+//
+// In the forward kernel the per-layer arguments (dimension, weight and
+// activation pointers) are copied into LDS once at kernel start, so a layer
+// never waits on a scalar load of the kernel-argument block.
+#include <type_traits>
+
 #include "device_common.h"
 #include "hcmix_internal.h"
 
@@ -20,46 +25,61 @@ constexpr int FW = 64;        // width of the fused path
 constexpr int FRB = 2 * FW;   // bytes per activation / weight row
 constexpr int WW = FW * FW;   // elements per weight matrix
 
+struct LayerArg {
+  const bf16* ws;
+  const bf16* wo;
+  bf16* xs;
+  int d, pad;
+};
+constexpr int ARG_BYTES = kFusedMaxLayers * (int)sizeof(LayerArg);
+
 __device__ __forceinline__ int act_off(int row, int col) {
   return swz<FW>(row, col >> 3) + (col & 7);
 }
 
-// Transposed 32x32x16 fragment over an activation buffer: lane l receives
-// buf[row(k0 + 8*(l/32) + t)][c0 + l%32] for t = 0..7, where row(kappa) maps
-// the contraction index to a buffer row (identity, or a pair member).
-template <typename RowFn>
-__device__ __forceinline__ bf16x8 tr_act(const bf16* buf, int k0, int c0, int lane, RowFn row) {
+// ---- transposed pair fragments ------------------------------------------
+// A 16-pair step k0 .. k0+15 (k0 % 16 == 0) of dimension d covers the lower
+// rows base + off(delta), delta = 0..15, with
+//   d < 4:  base = 2 k0,               off(delta) = lower_row(delta, d)
+//   d >= 4: base = lower_row(k0, d),   off(delta) = delta
+// and base a multiple of 16, so act_off(base + r, c) = base * FW + act_off(r, c)
+// (the swizzle only sees row bits 1..3).  Each lane's two reads of a
+// fragment (contraction rows 8 (l/32) + (l%16)/4 and +4, column c0 + 16 ((l/16)%2)
+// + 4 (l%4)) therefore sit at a per-layer lane constant plus a per-step base.
+struct PairOffs {
+  int lo_l, hi_l, lo_u, hi_u;   // element offsets: lower / upper pair member
+};
+
+__device__ __forceinline__ PairOffs pair_offs(int c0, int lane, int d) {
   const int g = lane >> 4, j = lane & 15;
-  const int kap = k0 + 8 * (g >> 1) + (j >> 2);
+  const int dl = 8 * (g >> 1) + (j >> 2);
   const int col = c0 + 16 * (g & 1) + 4 * (j & 3);
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(buf + act_off(row(kap), col)));
-  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(buf + act_off(row(kap + 4), col)));
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  const int s = 1 << d;
+  const int rl = d < 4 ? lower_row(dl, d) : dl;
+  const int rh = d < 4 ? lower_row(dl + 4, d) : dl + 4;
+  return {act_off(rl, col), act_off(rh, col), act_off(rl + s, col), act_off(rh + s, col)};
 }
 
-// Rounds a wave's two 32-row output blocks to bf16 into an activation buffer.
-// The accumulators hold the transposed products (weight fragment as the MFMA
-// "A" operand), so element e of lane l belongs to row rL / rU (the lane's pair)
-// and column 32 t + 8 (e/4) + 4 (l/32) + e%4: four runs of four columns.
-__device__ __forceinline__ void store_rows(bf16* buf, const f32x16 (&accL)[2],
-                                           const f32x16 (&accU)[2], int rL, int rU, int lane) {
-#pragma unroll
-  for (int t = 0; t < 2; t++)
-#pragma unroll
-    for (int g = 0; g < 4; g++) {
-      const int col = 32 * t + 8 * g + 4 * (lane >> 5);
-      const bf16x4 vl = {to_bf16(accL[t][4 * g]), to_bf16(accL[t][4 * g + 1]),
-                         to_bf16(accL[t][4 * g + 2]), to_bf16(accL[t][4 * g + 3])};
-      const bf16x4 vu = {to_bf16(accU[t][4 * g]), to_bf16(accU[t][4 * g + 1]),
-                         to_bf16(accU[t][4 * g + 2]), to_bf16(accU[t][4 * g + 3])};
-      *(bf16x4*)(buf + act_off(rL, col)) = vl;
-      *(bf16x4*)(buf + act_off(rU, col)) = vu;
-    }
+__device__ __forceinline__ int step_base(int k0, int d) {
+  return d < 4 ? 2 * k0 : lower_row(k0, d);
 }
 
-// Window rows (n rows of 128 bytes) global -> LDS in the activation swizzle.
-__device__ __forceinline__ void dma_act(const bf16* src, bf16* dst, int n, int wave, int nw, int lane) {
-  for (int b = wave; b < n / 8; b += nw) {
+// Lane l receives buf[row(k0 + 8 (l/32) + t)][c0 + l%32], t = 0..7 (the MFMA
+// operand layout with the contraction over pairs).
+__device__ __forceinline__ bf16x8 tr_pair(const bf16* step, int lo, int hi) {
+  const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(step + lo));
+  const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(step + hi));
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// ---- staging -------------------------------------------------------------
+// Window rows (N rows of 128 bytes) global -> LDS in the activation swizzle.
+template <int N, int NW>
+__device__ __forceinline__ void dma_act(const bf16* src, bf16* dst, int wave, int lane) {
+  static_assert((N / 8) % NW == 0, "");
+#pragma unroll
+  for (int i = 0; i < N / 8 / NW; i++) {
+    const int b = wave + i * NW;
     const int o = b * 1024 + 16 * lane;
     const int row = o / FRB;
     const int ch = ((o % FRB) / 16) ^ ((row >> 1) & 7);
@@ -68,8 +88,12 @@ __device__ __forceinline__ void dma_act(const bf16* src, bf16* dst, int n, int w
 }
 
 // One weight matrix global -> LDS, k-contiguous rows (forward B operand).
-__device__ __forceinline__ void dma_w_rows(const bf16* src, bf16* dst, int wave, int nw, int lane) {
-  for (int b = wave; b < WW * 2 / 1024; b += nw) {
+template <int NW>
+__device__ __forceinline__ void dma_w_rows(const bf16* src, bf16* dst, int wave, int lane) {
+  static_assert(8 % NW == 0, "");
+#pragma unroll
+  for (int i = 0; i < 8 / NW; i++) {
+    const int b = wave + i * NW;
     const int o = b * 1024 + 16 * lane;
     const int row = o / FRB;
     const int ch = ((o % FRB) / 16) ^ ((row >> 1) & 7);
@@ -78,106 +102,175 @@ __device__ __forceinline__ void dma_w_rows(const bf16* src, bf16* dst, int wave,
 }
 
 // One weight matrix global -> LDS for transposed reads (backward B operand).
-__device__ __forceinline__ void dma_w_tr(const bf16* src, bf16* dst, int wave, int nw, int lane) {
-  for (int b = wave; b < WW * 2 / 1024; b += nw) {
+template <int NW>
+__device__ __forceinline__ void dma_w_tr(const bf16* src, bf16* dst, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < 8 / NW; i++) {
+    const int b = wave + i * NW;
     int row, col;
     tr_dma_coord<FRB>(b, lane, &row, &col);
     dma16(src + (size_t)row * FW + col, dst + b * 512);
   }
 }
 
+// Rounds column block t (32 columns) of a wave's output rows to bf16 into an
+// activation buffer (transposed accumulators: lane l holds row rL / rU and
+// columns 32 t + 8 (e/4) + 4 (l/32) + e%4).
+__device__ __forceinline__ void store_block(bf16* buf, const f32x16& accL, const f32x16& accU,
+                                            int rL, int rU, int t, int lane) {
+#pragma unroll
+  for (int g = 0; g < 4; g++) {
+    const int col = 32 * t + 8 * g + 4 * (lane >> 5);
+    const bf16x4 vl = {to_bf16(accL[4 * g]), to_bf16(accL[4 * g + 1]), to_bf16(accL[4 * g + 2]),
+                       to_bf16(accL[4 * g + 3])};
+    const bf16x4 vu = {to_bf16(accU[4 * g]), to_bf16(accU[4 * g + 1]), to_bf16(accU[4 * g + 2]),
+                       to_bf16(accU[4 * g + 3])};
+    *(bf16x4*)(buf + act_off(rL, col)) = vl;
+    *(bf16x4*)(buf + act_off(rU, col)) = vu;
+  }
+}
+
+// 16-byte pieces p0, p0 + stride, ... (K of them) of a window's activation
+// buffer -> their row-major places in global memory; all LDS reads first.
+template <int K>
+__device__ __forceinline__ void copy_out(const bf16* buf, bf16* dst, int p0, int stride) {
+  u32x4 v[K];
+#pragma unroll
+  for (int i = 0; i < K; i++) {
+    const int p = p0 + i * stride;
+    v[i] = *(const u32x4*)(buf + swz<FW>(p / (FW / 8), p % (FW / 8)));
+  }
+#pragma unroll
+  for (int i = 0; i < K; i++) {
+    const int p = p0 + i * stride;
+    store_global16(dst + (size_t)(p / (FW / 8)) * FW + (p % (FW / 8)) * 8, v[i]);
+  }
+}
+
+template <int N> constexpr size_t fwd_lds() { return (size_t)(2 * N * FW + 4 * WW) * 2 + ARG_BYTES; }
+template <int N> constexpr size_t bwd_lds() { return (size_t)(4 * N * FW + 4 * WW) * 2; }
+
 // ---------------------------------------------------------------------------
 // Forward: x_{l+1} = layer_l(x_l) for l = 0..L-1, each x_{l+1} also stored.
+//
+// 3 n / 64 waves in two roles:
+//  * 2 n / 64 compute waves (two per SIMD at n = 256): wave w multiplies the
+//    32 row pairs of block w / 2 into the 32 output columns of half w % 2 and
+//    fetches its share of the next layer's weights;
+//  * n / 64 store waves copy x_l (the layer's input, in LDS during layer l)
+//    to global memory.  A CU writes to memory at roughly half the rate it
+//    reads, so the stores take about as long as the layer's MFMAs; in waves
+//    of their own they never hold up an MFMA, and no wave waits for them to
+//    complete (the LDS reads that feed them finish before the layer ends).
 // ---------------------------------------------------------------------------
-template <bool BIDIR>
-__global__ __launch_bounds__(256) void fused_fwd_kernel(FusedFwdArgs a) {
+template <int N, bool BIDIR>
+__global__ __launch_bounds__(3 * N) void fused_fwd_kernel(FusedFwdArgs a) {
+  constexpr int CT = 2 * N, CW = CT / 64;   // compute threads / waves
+  constexpr int SPT = N * FW / 8 / N;       // 16-byte pieces per store thread (8)
+  constexpr int CPT = N * FW / 8 / CT;      // pieces per compute thread (4)
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
-  const int n = a.n, nw = n / 64, nthreads = 64 * nw;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t win = (size_t)blockIdx.x * n * FW;
+  const bool compute = wave < CW;
+  const int pb = wave >> 1, half = wave & 1;
+  const int L = a.num_layers;
+  const size_t win = (size_t)blockIdx.x * N * FW;
   bf16* X = smem;
-  bf16* Y = X + n * FW;
-  bf16* Wb = Y + n * FW;  // two sets of [W_self | W_off]
+  bf16* Y = X + N * FW;
+  bf16* Wb = Y + N * FW;  // two sets of [W_self | W_off]
+  LayerArg* tab = (LayerArg*)(Wb + 4 * WW);
 
-  dma_act(a.x0 + win, X, n, wave, nw, lane);
-  dma_w_rows(a.ws[0], Wb, wave, nw, lane);
-  dma_w_rows(a.wo[0], Wb + WW, wave, nw, lane);
-  wait_dma();
+  if (tid < L) tab[tid] = LayerArg{a.ws[tid], a.wo[tid], a.xs[tid], a.dim[tid], 0};
+  if (compute) {
+    dma_act<N, CW>(a.x0 + win, X, wave, lane);
+    dma_w_rows<CW>(a.ws[0], Wb, wave, lane);
+    dma_w_rows<CW>(a.wo[0], Wb + WW, wave, lane);
+    wait_dma();
+  }
   __syncthreads();
 
-  for (int l = 0; l < a.num_layers; l++) {
-    const int d = a.dim[l], s = 1 << d;
-    const bf16* Ws = Wb + (l & 1) * 2 * WW;
-    const bf16* Wo = Ws + WW;
-    if (l + 1 < a.num_layers) {
-      bf16* Wn = Wb + ((l + 1) & 1) * 2 * WW;
-      dma_w_rows(a.ws[l + 1], Wn, wave, nw, lane);
-      dma_w_rows(a.wo[l + 1], Wn + WW, wave, nw, lane);
+  for (int l = 0; l < L; l++) {
+    if (compute) {
+      const int d = tab[l].d, s = 1 << d;
+      const bf16* Ws = Wb + (l & 1) * 2 * WW;
+      const bf16* Wo = Ws + WW;
+      if (l + 1 < L) {
+        bf16* Wn = Wb + ((l + 1) & 1) * 2 * WW;
+        dma_w_rows<CW>(tab[l + 1].ws, Wn, wave, lane);
+        dma_w_rows<CW>(tab[l + 1].wo, Wn + WW, wave, lane);
+      }
+      const int rL = lower_row(32 * pb + (lane & 31), d), rU = rL + s;
+      const int nr = 32 * half + (lane & 31);
+      bf16x8 aL[4], aU[4], b1[4], b2[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        const int ch = kk * 2 + (lane >> 5);
+        aL[kk] = *(const bf16x8*)(X + swz<FW>(rL, ch));
+        aU[kk] = *(const bf16x8*)(X + swz<FW>(rU, ch));
+        b1[kk] = *(const bf16x8*)(Ws + swz<FW>(nr, ch));
+        b2[kk] = *(const bf16x8*)(Wo + swz<FW>(nr, ch));
+      }
+      f32x16 accL, accU;
+#pragma unroll
+      for (int e = 0; e < 16; e++) { accL[e] = 0.f; accU[e] = 0.f; }
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        accL = mfma32(b1[kk], aL[kk], accL);
+        accU = mfma32(b1[kk], aU[kk], accU);
+        accU = mfma32(b2[kk], aL[kk], accU);
+        if (BIDIR) accL = mfma32(b2[kk], aU[kk], accL);
+      }
+      store_block(Y, accL, accU, rL, rU, half, lane);
+      wait_dma();  // this wave's share of the next weights
+    } else if (l > 0) {
+      bf16* dst = tab[l - 1].xs + win;
+      copy_out<SPT>(X, dst, tid - CT, N);
     }
-    f32x16 accL[2], accU[2];
-#pragma unroll
-    for (int t = 0; t < 2; t++)
-#pragma unroll
-      for (int e = 0; e < 16; e++) { accL[t][e] = 0.f; accU[t][e] = 0.f; }
-    const int rL = lower_row(32 * wave + (lane & 31), d), rU = rL + s;
-#pragma unroll
-    for (int kk = 0; kk < FW / 16; kk++) {
-      const int ch = kk * 2 + (lane >> 5);
-      const bf16x8 aL = *(const bf16x8*)(X + swz<FW>(rL, ch));
-      const bf16x8 aU = *(const bf16x8*)(X + swz<FW>(rU, ch));
-      bf16x8 b1[2], b2[2];
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        const int nr = 32 * t + (lane & 31);
-        b1[t] = *(const bf16x8*)(Ws + swz<FW>(nr, ch));
-        b2[t] = *(const bf16x8*)(Wo + swz<FW>(nr, ch));
-      }
-      // self terms first, partner terms after: no MFMA waits on the one before it
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        accL[t] = mfma32(b1[t], aL, accL[t]);
-        accU[t] = mfma32(b1[t], aU, accU[t]);
-      }
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        accU[t] = mfma32(b2[t], aL, accU[t]);
-        if (BIDIR) accL[t] = mfma32(b2[t], aU, accL[t]);
-      }
-    }
-    store_rows(Y, accL, accU, rL, rU, lane);
-    wait_dma();
     __syncthreads();  // Y complete, next weights landed, X and this layer's weights free
-    bf16* dst = a.xs[l] + win;
-    for (int p = tid; p < n * FW / 8; p += nthreads) {
-      const int row = p / (FW / 8), ch = p % (FW / 8);
-      *(u32x4*)(dst + (size_t)row * FW + ch * 8) = *(const u32x4*)(Y + swz<FW>(row, ch));
-    }
     bf16* t = X;
     X = Y;
     Y = t;
+  }
+  if (compute) {
+    bf16* dst = tab[L - 1].xs + win;
+    copy_out<CPT>(X, dst, tid, CT);
   }
 }
 
 // ---------------------------------------------------------------------------
 // Backward: walks the layers in reverse with the gradient resident in LDS.
-// Per layer: per-window weight-gradient blocks to `partial`, then dX.
+//
+// 2 n / 64 waves in two roles that run side by side within a layer (one wave
+// of each role per SIMD at n = 256); they share only the gradient G, which
+// both read:
+//  * weight-gradient waves: block c (0..3) is the 32 x 32 piece (outputs ob,
+//    inputs cb) of both dW_self and dW_off; one pass over the row pairs reads
+//    the fragments dY_L, dY_U (outputs) and X_L, X_U (inputs) and feeds
+//      dW_self += dY_L^T X_L + dY_U^T X_U,  dW_off += dY_U^T X_L (+ dY_L^T X_U bidir),
+//    then stores the window's partial;
+//  * dX waves: 32 row pairs each, in two 32-column halves (the second half's
+//    MFMAs carry the first half's rounding and LDS writes).
+// The layer inputs are double-buffered, so the next layer's input and weights
+// are fetched from the start of the layer.  The per-layer arguments are read
+// from the kernel-argument block (the four activation buffers and two weight
+// sets fill the 160 KB of LDS at n = 256).
 // ---------------------------------------------------------------------------
-template <bool BIDIR>
-__global__ __launch_bounds__(256) void fused_bwd_kernel(FusedBwdArgs a) {
+template <int N, bool BIDIR>
+__global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
+  constexpr int NT = 2 * N, NW = NT / 64, HW = NW / 2;
+  constexpr int PCS = N * FW / 8 / NT;
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
-  const int n = a.n, nw = n / 64, nthreads = 64 * nw;
   const int L = a.num_layers;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t win = (size_t)blockIdx.x * n * FW;
-  bf16* G = smem;          // gradient of the current layer's output
-  bf16* Gn = G + n * FW;   // gradient of its input (being built)
-  bf16* Xb = Gn + n * FW;  // the current layer's input
-  bf16* Wb = Xb + n * FW;  // two sets of [W_self | W_off], transposed-read layout
+  const size_t win = (size_t)blockIdx.x * N * FW;
+  bf16* G = smem;            // gradient of the current layer's output
+  bf16* Gn = G + N * FW;     // gradient of its input (being built)
+  bf16* Xs = Gn + N * FW;    // two layer-input buffers: x_l in buffer l % 2
+  bf16* Wb = Xs + 2 * N * FW;  // two sets of [W_self | W_off], transposed-read layout
 
-  dma_act(a.dy + win, G, n, wave, nw, lane);
-  dma_act(a.xs[L - 1] + win, Xb, n, wave, nw, lane);
-  dma_w_tr(a.ws[L - 1], Wb + ((L - 1) & 1) * 2 * WW, wave, nw, lane);
-  dma_w_tr(a.wo[L - 1], Wb + ((L - 1) & 1) * 2 * WW + WW, wave, nw, lane);
+  dma_act<N, NW>(a.dy + win, G, wave, lane);
+  dma_act<N, NW>(a.xs[L - 1] + win, Xs + ((L - 1) & 1) * N * FW, wave, lane);
+  dma_w_tr<NW>(a.ws[L - 1], Wb + ((L - 1) & 1) * 2 * WW, wave, lane);
+  dma_w_tr<NW>(a.wo[L - 1], Wb + ((L - 1) & 1) * 2 * WW + WW, wave, lane);
   wait_dma();
   __syncthreads();
 
@@ -185,84 +278,101 @@ __global__ __launch_bounds__(256) void fused_bwd_kernel(FusedBwdArgs a) {
     const int d = a.dim[l], s = 1 << d;
     const bf16* Ws = Wb + (l & 1) * 2 * WW;
     const bf16* Wo = Ws + WW;
+    const bf16* Xb = Xs + (l & 1) * N * FW;
     if (l > 0) {
       bf16* Wn = Wb + ((l - 1) & 1) * 2 * WW;
-      dma_w_tr(a.ws[l - 1], Wn, wave, nw, lane);
-      dma_w_tr(a.wo[l - 1], Wn + WW, wave, nw, lane);
+      dma_w_tr<NW>(a.ws[l - 1], Wn, wave, lane);
+      dma_w_tr<NW>(a.wo[l - 1], Wn + WW, wave, lane);
+      dma_act<N, NW>(a.xs[l - 1] + win, Xs + ((l - 1) & 1) * N * FW, wave, lane);
     }
-    auto same = [](int k) { return k; };
-    auto lowr = [d](int k) { return lower_row(k, d); };
-    auto uppr = [d, s](int k) { return lower_row(k, d) + s; };
-
-    // 1. weight-gradient blocks: 0..3 of dW_self, 4..7 of dW_off (32 x 32 each)
-    float* part = a.partial + ((size_t)blockIdx.x * L + l) * 2 * WW;
-    for (int blk = wave; blk < 8; blk += nw) {
-      const int is_off = blk >> 2, ob = ((blk >> 1) & 1) * 32, cb = (blk & 1) * 32;
-      f32x16 acc;
+    if (wave < HW) {
+      // weight-gradient partials of this window
+      float* part = a.partial + ((size_t)blockIdx.x * L + l) * 2 * WW;
 #pragma unroll
-      for (int e = 0; e < 16; e++) acc[e] = 0.f;
-      if (!is_off) {
-        for (int k0 = 0; k0 < n; k0 += 16)
-          acc = mfma32(tr_act(G, k0, ob, lane, same), tr_act(Xb, k0, cb, lane, same), acc);
-      } else {
-        // receivers' gradients against their senders' inputs, over the n/2 pairs
-        for (int k0 = 0; k0 < n / 2; k0 += 16) {
-          acc = mfma32(tr_act(G, k0, ob, lane, uppr), tr_act(Xb, k0, cb, lane, lowr), acc);
-          if (BIDIR) acc = mfma32(tr_act(G, k0, ob, lane, lowr), tr_act(Xb, k0, cb, lane, uppr), acc);
+      for (int c = wave; c < 4; c += HW) {
+        const int ob = (c >> 1) * 32, cb = (c & 1) * 32;
+        const PairOffs pg = pair_offs(ob, lane, d), px = pair_offs(cb, lane, d);
+        f32x16 accS, accO;
+#pragma unroll
+        for (int e = 0; e < 16; e++) { accS[e] = 0.f; accO[e] = 0.f; }
+        // fragments of the 16-pair step at k0: dY_L, dY_U, X_L, X_U
+        auto frags = [&](bf16x8 (&f)[4], int k0) {
+          const int base = step_base(k0, d) * FW;
+          f[0] = tr_pair(G + base, pg.lo_l, pg.hi_l);
+          f[1] = tr_pair(G + base, pg.lo_u, pg.hi_u);
+          f[2] = tr_pair(Xb + base, px.lo_l, px.hi_l);
+          f[3] = tr_pair(Xb + base, px.lo_u, px.hi_u);
+        };
+        auto mma = [&](const bf16x8 (&f)[4]) {
+          accS = mfma32(f[2], f[0], accS);
+          accO = mfma32(f[2], f[1], accO);
+          accS = mfma32(f[3], f[1], accS);
+          if (BIDIR) accO = mfma32(f[3], f[0], accO);
+        };
+        // each step's reads are issued under the previous step's MFMAs
+        bf16x8 fr[2][4];
+        frags(fr[0], 0);
+#pragma unroll
+        for (int k = 0; k < N / 32; k++) {
+          if (k + 1 < N / 32) frags(fr[(k + 1) & 1], 16 * (k + 1));
+          mma(fr[k & 1]);
+        }
+        // transposed accumulators: lane l holds output ob + l%32 and inputs
+        // cb + 8 g + 4 (l/32) + 0..3
+        float* rowS = part + (size_t)(ob + (lane & 31)) * FW + cb + 4 * (lane >> 5);
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+          *(f32x4*)(rowS + 8 * g) = f32x4{accS[4 * g], accS[4 * g + 1], accS[4 * g + 2], accS[4 * g + 3]};
+          *(f32x4*)(rowS + WW + 8 * g) = f32x4{accO[4 * g], accO[4 * g + 1], accO[4 * g + 2], accO[4 * g + 3]};
         }
       }
-      float* dst = part + is_off * WW;
+    } else {
+      // dX: lower rows always take their partner's gradient through W_off^T
+      // (causal: the lower row is the sender), upper rows only when bidirectional.
+      const int rL = lower_row(32 * (wave - HW) + (lane & 31), d), rU = rL + s;
+      bf16x8 gL[4], gU[4], b1[2][4], b2[2][4];
 #pragma unroll
-      for (int e = 0; e < 16; e++) {
-        const int o = ob + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        dst[o * FW + cb + (lane & 31)] = acc[e];
+      for (int kk = 0; kk < 4; kk++) {
+        const int ch = kk * 2 + (lane >> 5);
+        gL[kk] = *(const bf16x8*)(G + swz<FW>(rL, ch));
+        gU[kk] = *(const bf16x8*)(G + swz<FW>(rU, ch));
+        b1[0][kk] = tr_frag<FRB>(Ws, kk * 16, 0, lane);
+        b2[0][kk] = tr_frag<FRB>(Wo, kk * 16, 0, lane);
       }
+      f32x16 accL[2], accU[2];
+#pragma unroll
+      for (int t = 0; t < 2; t++)
+#pragma unroll
+        for (int e = 0; e < 16; e++) { accL[t][e] = 0.f; accU[t][e] = 0.f; }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        b1[1][kk] = tr_frag<FRB>(Ws, kk * 16, 32, lane);
+        b2[1][kk] = tr_frag<FRB>(Wo, kk * 16, 32, lane);
+        accL[0] = mfma32(b1[0][kk], gL[kk], accL[0]);
+        accU[0] = mfma32(b1[0][kk], gU[kk], accU[0]);
+        accL[0] = mfma32(b2[0][kk], gU[kk], accL[0]);
+        if (BIDIR) accU[0] = mfma32(b2[0][kk], gL[kk], accU[0]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        accL[1] = mfma32(b1[1][kk], gL[kk], accL[1]);
+        accU[1] = mfma32(b1[1][kk], gU[kk], accU[1]);
+        accL[1] = mfma32(b2[1][kk], gU[kk], accL[1]);
+        if (BIDIR) accU[1] = mfma32(b2[1][kk], gL[kk], accU[1]);
+      }
+      store_block(Gn, accL[0], accU[0], rL, rU, 0, lane);
+      __builtin_amdgcn_sched_barrier(0);
+      store_block(Gn, accL[1], accU[1], rL, rU, 1, lane);
     }
-    __syncthreads();  // Xb free
-    if (l > 0) dma_act(a.xs[l - 1] + win, Xb, n, wave, nw, lane);
-
-    // 2. dX: lower rows always take their partner's gradient through W_off^T
-    //    (causal: the lower row is the sender), upper rows only when bidirectional.
-    f32x16 accL[2], accU[2];
-#pragma unroll
-    for (int t = 0; t < 2; t++)
-#pragma unroll
-      for (int e = 0; e < 16; e++) { accL[t][e] = 0.f; accU[t][e] = 0.f; }
-    const int rL = lower_row(32 * wave + (lane & 31), d), rU = rL + s;
-#pragma unroll
-    for (int kk = 0; kk < FW / 16; kk++) {
-      const int ch = kk * 2 + (lane >> 5);
-      const bf16x8 gL = *(const bf16x8*)(G + swz<FW>(rL, ch));
-      const bf16x8 gU = *(const bf16x8*)(G + swz<FW>(rU, ch));
-      bf16x8 b1[2], b2[2];
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        b1[t] = tr_frag<FRB>(Ws, kk * 16, 32 * t, lane);
-        b2[t] = tr_frag<FRB>(Wo, kk * 16, 32 * t, lane);
-      }
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        accL[t] = mfma32(b1[t], gL, accL[t]);
-        accU[t] = mfma32(b1[t], gU, accU[t]);
-      }
-#pragma unroll
-      for (int t = 0; t < 2; t++) {
-        accL[t] = mfma32(b2[t], gU, accL[t]);
-        if (BIDIR) accU[t] = mfma32(b2[t], gL, accU[t]);
-      }
-    }
-    store_rows(Gn, accL, accU, rL, rU, lane);
     wait_dma();
-    __syncthreads();  // Gn complete; next input and weights landed
+    __syncthreads();  // Gn complete, partial stored; next input and weights landed
     bf16* t = G;
     G = Gn;
     Gn = t;
   }
-  bf16* dst = a.dx + win;
-  for (int p = tid; p < n * FW / 8; p += nthreads) {
-    const int row = p / (FW / 8), ch = p % (FW / 8);
-    *(u32x4*)(dst + (size_t)row * FW + ch * 8) = *(const u32x4*)(G + swz<FW>(row, ch));
-  }
+  copy_out<PCS>(G, a.dx + win, tid, NT);
 }
 
 // dW_self[l] / dW_off[l] (+)= sum over windows of the partials.  Each block
@@ -295,8 +405,46 @@ __global__ __launch_bounds__(256) void fused_dw_reduce_kernel(FusedReduceArgs a)
   }
 }
 
-size_t fwd_lds_bytes(int n) { return ((size_t)2 * n * FW + 4 * WW) * sizeof(bf16); }
-size_t bwd_lds_bytes(int n) { return ((size_t)3 * n * FW + 4 * WW) * sizeof(bf16); }
+
+template <int N, bool BIDIR>
+hipError_t fwd_launch(const FusedFwdArgs& a, int batch, hipStream_t st) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)fused_fwd_kernel<N, BIDIR>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)fwd_lds<N>());
+  if (attr != hipSuccess) return attr;
+  fused_fwd_kernel<N, BIDIR><<<batch, 3 * N, fwd_lds<N>(), st>>>(a);
+  return hipGetLastError();
+}
+
+template <int N, bool BIDIR>
+hipError_t bwd_launch(const FusedBwdArgs& a, int batch, hipStream_t st) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)fused_bwd_kernel<N, BIDIR>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)bwd_lds<N>());
+  if (attr != hipSuccess) return attr;
+  fused_bwd_kernel<N, BIDIR><<<batch, 2 * N, bwd_lds<N>(), st>>>(a);
+  return hipGetLastError();
+}
+
+template <bool BIDIR>
+hipError_t fwd_dispatch(const FusedFwdArgs& a, int batch, hipStream_t st) {
+  switch (a.n) {
+    case 64: return fwd_launch<64, BIDIR>(a, batch, st);
+    case 128: return fwd_launch<128, BIDIR>(a, batch, st);
+    case 256: return fwd_launch<256, BIDIR>(a, batch, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <bool BIDIR>
+hipError_t bwd_dispatch(const FusedBwdArgs& a, int batch, hipStream_t st) {
+  switch (a.n) {
+    case 64: return bwd_launch<64, BIDIR>(a, batch, st);
+    case 128: return bwd_launch<128, BIDIR>(a, batch, st);
+    case 256: return bwd_launch<256, BIDIR>(a, batch, st);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 }  // namespace
 
@@ -310,38 +458,12 @@ size_t fused_partial_bytes(int64_t batch, int32_t num_layers) {
 }
 
 hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hipStream_t st) {
-  const size_t lds = fwd_lds_bytes(a.n);
-  const int threads = 64 * (a.n / 64);
-  if (bidir) {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)fused_fwd_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (attr != hipSuccess) return attr;
-    fused_fwd_kernel<true><<<batch, threads, lds, st>>>(a);
-  } else {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)fused_fwd_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (attr != hipSuccess) return attr;
-    fused_fwd_kernel<false><<<batch, threads, lds, st>>>(a);
-  }
-  return hipGetLastError();
+  return bidir ? fwd_dispatch<true>(a, batch, st) : fwd_dispatch<false>(a, batch, st);
 }
 
 hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
                                  bool bidir, hipStream_t st) {
-  const size_t lds = bwd_lds_bytes(a.n);
-  const int threads = 64 * (a.n / 64);
-  if (bidir) {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)fused_bwd_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (attr != hipSuccess) return attr;
-    fused_bwd_kernel<true><<<batch, threads, lds, st>>>(a);
-  } else {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)fused_bwd_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (attr != hipSuccess) return attr;
-    fused_bwd_kernel<false><<<batch, threads, lds, st>>>(a);
-  }
-  hipError_t e = hipGetLastError();
+  hipError_t e = bidir ? bwd_dispatch<true>(a, batch, st) : bwd_dispatch<false>(a, batch, st);
   if (e != hipSuccess) return e;
   const int blocks = r.num_layers * 2 * (WW / 4) / RED_OUT;   // exact: WW/4 = 1024
   fused_dw_reduce_kernel<<<blocks, 256, 0, st>>>(r);
