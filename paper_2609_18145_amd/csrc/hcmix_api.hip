@@ -54,14 +54,24 @@ size_t layer_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t dt
   return align256((size_t)splits * 2 * width * width * sizeof(float));
 }
 
+// Transposed copies of every layer's two weight matrices (bf16 stacks of two
+// or more layers on the layer-by-layer path): dX then multiplies by W^T with
+// the same kernel and the same 128-bit fragment reads as the forward.
+size_t transposed_weight_bytes(int64_t width, int32_t num_layers, int32_t dtype) {
+  if (dtype != HCMIX_BF16 || num_layers < 2) return 0;
+  return align256((size_t)2 * num_layers * width * width * sizeof(bf16));
+}
+
 // Stack backward workspace: the per-window partials of the fused path, or two
-// gradient buffers plus one layer's workspace for the layer-by-layer path.
+// gradient buffers, one layer's workspace and the transposed weights for the
+// layer-by-layer path.
 size_t stack_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                              int32_t dtype) {
   if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers))
     return align256(fused_partial_bytes(batch, num_layers));
   const size_t act = align256((size_t)(batch * n * width) * elem_size(dtype));
-  return (num_layers > 1 ? 2 * act : 0) + layer_workspace_bytes(batch, n, width, dtype);
+  return (num_layers > 1 ? 2 * act : 0) + layer_workspace_bytes(batch, n, width, dtype) +
+         transposed_weight_bytes(width, num_layers, dtype);
 }
 
 // ---- unchecked per-layer dispatch (arguments already validated) ----
@@ -340,10 +350,39 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
     void* gbuf[2] = {ws, ws + act_al};
     void* layer_ws = ws + (num_layers > 1 ? 2 * act_al : 0);
     const void* g = dy;
+    const size_t lws = layer_workspace_bytes(batch, n, width, dtype);
+    bf16* wt = (bf16*)((char*)layer_ws + lws);   // transposed weights (bf16, L >= 2)
+    const size_t ww = (size_t)w * w;
+    if (transposed_weight_bytes(width, num_layers, dtype) > 0) {
+      // wt[2l] = W_self[l]^T, wt[2l+1] = W_off[l]^T
+      for (int l0 = 0; l0 < num_layers && e == hipSuccess; l0 += kTransposeBatch / 2) {
+        TransposeArgs t = {};
+        t.width = w;
+        int cnt = 0;
+        for (int l = l0; l < num_layers && l < l0 + kTransposeBatch / 2; l++) {
+          t.src[cnt] = (const bf16*)w_self[l];
+          t.dst[cnt++] = wt + (2 * (size_t)l) * ww;
+          t.src[cnt] = (const bf16*)w_off[l];
+          t.dst[cnt++] = wt + (2 * (size_t)l + 1) * ww;
+        }
+        e = launch_transpose_bf16(t, cnt, s);
+      }
+    }
     for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
       void* out = l == 0 ? dx : gbuf[l & 1];
-      e = run_backward(rows, w, hcmix_dim(layers[l], n), bidir, dtype, xs_in[l], w_self[l],
-                       w_off[l], g, out, dw_self[l], dw_off[l], accumulate != 0, layer_ws, s);
+      const int d = hcmix_dim(layers[l], n);
+      if (dtype == HCMIX_BF16 && num_layers > 1) {
+        // dX = W_self^T dy (+ partner W_off^T dy): the forward kernel on W^T
+        e = launch_mix_bf16((const bf16*)g, wt + 2 * (size_t)l * ww, wt + (2 * (size_t)l + 1) * ww,
+                            (bf16*)out, rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
+                            /*transpose_b=*/false, s);
+        if (e == hipSuccess)
+          e = launch_dw_bf16((const bf16*)xs_in[l], (const bf16*)g, (float*)layer_ws, dw_self[l],
+                             dw_off[l], rows, w, d, bidir, accumulate != 0, s);
+      } else {
+        e = run_backward(rows, w, d, bidir, dtype, xs_in[l], w_self[l], w_off[l], g, out,
+                         dw_self[l], dw_off[l], accumulate != 0, layer_ws, s);
+      }
       g = out;
     }
   }

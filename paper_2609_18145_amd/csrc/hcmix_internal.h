@@ -50,6 +50,16 @@ hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* 
 // Split-K weight gradients into `partial` ([splits][2][width][width] fp32),
 // then a fixed-order reduction into dws / dwo.
 int dw_bf16_splits(int rows, int width);
+// dst[m] = src[m]^T for `count` (<= kTransposeBatch) bf16 matrices of
+// width x width, width a multiple of 64.
+constexpr int kTransposeBatch = 64;
+struct TransposeArgs {
+  const bf16* src[kTransposeBatch];
+  bf16* dst[kTransposeBatch];
+  int width;
+};
+hipError_t launch_transpose_bf16(const TransposeArgs& a, int count, hipStream_t st);
+
 hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* dws, float* dwo,
                           int rows, int width, int d, int bidir, int accumulate,
                           hipStream_t st);

@@ -466,6 +466,32 @@ hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out
       A, B1, B2, out, pairs, width, d, partner_lower, partner_upper, st);
 }
 
+// Batched bf16 transpose: dst[m] = src[m]^T for up to kTransposeBatch square
+// width x width matrices, one 64 x 64 tile per block through a padded LDS tile.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeArgs a) {
+  __shared__ bf16 t[64][64 + 8];
+  const int tiles = a.width / 64;
+  const int tr = blockIdx.x / tiles, tc = blockIdx.x % tiles;
+  const bf16* src = a.src[blockIdx.y];
+  bf16* dst = a.dst[blockIdx.y];
+#pragma unroll
+  for (int i = threadIdx.x; i < 512; i += 256) {
+    const int r = i / 8, c = (i % 8) * 8;
+    const bf16x8 v = *(const bf16x8*)(src + (size_t)(tr * 64 + r) * a.width + tc * 64 + c);
+#pragma unroll
+    for (int j = 0; j < 8; j++) t[r][c + j] = v[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = threadIdx.x; i < 512; i += 256) {
+    const int r = i / 8, c = (i % 8) * 8;
+    bf16x8 v;
+#pragma unroll
+    for (int j = 0; j < 8; j++) v[j] = t[c + j][r];
+    *(bf16x8*)(dst + (size_t)(tc * 64 + r) * a.width + tr * 64 + c) = v;
+  }
+}
+
 // Split-K plan: enough blocks to fill the chip (about 512), each split a whole
 // number of K-steps.  Returns the split count; *pps gets pairs per split.
 int dw_plan(int rows, int width, int* pps) {
@@ -508,6 +534,12 @@ hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* 
   if (transpose_b)
     return mix_dispatch<true>(A, B1, B2, out, rows, width, d, partner_lower, partner_upper, st);
   return mix_dispatch<false>(A, B1, B2, out, rows, width, d, partner_lower, partner_upper, st);
+}
+
+hipError_t launch_transpose_bf16(const TransposeArgs& a, int count, hipStream_t st) {
+  const int tiles = a.width / 64;
+  transpose_bf16_kernel<<<dim3(tiles * tiles, count), 256, 0, st>>>(a);
+  return hipGetLastError();
 }
 
 int dw_bf16_splits(int rows, int width) {
