@@ -239,21 +239,29 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Weight gradients, split over rows.  Block (tile, split) computes the BO x BC
-// tile of dW_self and dW_off over the row pairs of its split:
+// Weight gradients, split over rows.  Block (tile, slot) computes the BO x BC
+// tile of dW_self and dW_off over the row pairs of its slot:
 //   dW_self += dY_L^T X_L + dY_U^T X_U
 //   dW_off  += dY_U^T X_L            (+ dY_L^T X_U when bidirectional)
 // A K-step stages KP pairs = 2*KP rows of dY and X in LDS in their natural
 // layout (slots 0..KP-1 the lower rows, KP..2KP-1 their partners); both MFMA
 // operands are read transposed, the row (slot) index being the contraction.
+//
+// A block is two groups of WO x WC waves (two waves per SIMD): the groups walk
+// the two halves of the block's row range side by side, each with its own
+// two-stage pipeline, and at the end group 1 hands its accumulators to group 0
+// through LDS; group 0 adds them (always in that order) and stores the block's
+// partial.  One partial per block halves the partial traffic of one block per
+// half range, with the same number of waves in flight.
 // ---------------------------------------------------------------------------
 constexpr int KP = 32;
 constexpr int SLOTS = 2 * KP;
 
 template <int BO, int BC, int WO, int WC>
 struct DwCfg {
-  static constexpr int NT = 64 * WO * WC;
-  static constexpr int NW = WO * WC;
+  static constexpr int NG = 2;                  // row-range groups per block
+  static constexpr int NW = WO * WC;            // waves per group
+  static constexpr int NT = 64 * NW * NG;
   static constexpr int TO = BO / (32 * WO);
   static constexpr int TC = BC / (32 * WC);
   static constexpr int G_ELEMS = SLOTS * BO;
@@ -262,17 +270,22 @@ struct DwCfg {
   static constexpr int G_DMA = G_ELEMS * 2 / 1024 / NW;
   static constexpr int X_DMA = X_ELEMS * 2 / 1024 / NW;
   static_assert(G_DMA * NW * 1024 == G_ELEMS * 2 && X_DMA * NW * 1024 == X_ELEMS * 2, "");
+  static constexpr int ACC = 2 * TO * TC * 16;  // accumulator floats per lane
+  static constexpr size_t LDS = (size_t)NG * 2 * STAGE * 2;   // bytes: two stages per group
+  static_assert((size_t)NW * ACC * 64 * 4 <= LDS, "hand-over fits in the stage buffers");
 };
 
 template <int BO, int BC, int WO, int WC, bool BIDIR>
-__global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
+__global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
     const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
-    int pairs, int width, int d, int pairs_per_split) {
+    int pairs, int width, int d, int pairs_per_group) {
   using C = DwCfg<BO, BC, WO, WC>;
   constexpr int RBG = BO * 2, RBX = BC * 2;
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int group = (tid >> 6) / C::NW, wave = (tid >> 6) % C::NW;
+  bf16* smem = smem_all + group * 2 * C::STAGE;
   const int wo = wave % WO, wc = wave / WO;
   const int tiles_c = width / BC;
   const int tiles = (width / BO) * tiles_c;
@@ -283,8 +296,8 @@ __global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
   const int split = lin / tiles;
   const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
   const int s = 1 << d;
-  const int pbeg = split * pairs_per_split;
-  const int pend = min(pairs, pbeg + pairs_per_split);
+  const int pbeg = (2 * split + group) * pairs_per_group;
+  const int pend = min(pairs, pbeg + pairs_per_group);   // may be <= pbeg: all zero-filled
 
   // Per-lane (slot, column) of each DMA block.
   int g_slot[C::G_DMA], g_col[C::G_DMA], x_slot[C::X_DMA], x_col[C::X_DMA];
@@ -374,7 +387,9 @@ __global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
 
   constexpr int NMFMA = C::TO * C::TC * (3 + (BIDIR ? 1 : 0));
   constexpr int NDS = 4 * (C::TO + C::TC);   // two tr reads per fragment
-  const int nsteps = pend > pbeg ? (pend - pbeg + KP - 1) / KP : 0;
+  // the same step count in both groups (their barriers are shared); steps past
+  // a group's range are zero-filled
+  const int nsteps = pairs_per_group / KP;
   if (nsteps > 0) stage_in(pbeg, 0);
   wait_dma();
   __syncthreads();
@@ -390,6 +405,35 @@ __global__ __launch_bounds__(64 * WO * WC) void dw_bf16_kernel(
     wait_dma();
     __syncthreads();
     if (it + 1 < nsteps) load_frags(f0, smem + ((it + 1) & 1) * C::STAGE, 0);
+  }
+
+  // group 1 -> LDS -> group 0, which adds in a fixed order and stores
+  float* hand = (float*)smem_all + (size_t)wave * C::ACC * 64;
+  if (group == 1) {
+    int i = 0;
+#pragma unroll
+    for (int a = 0; a < C::TO; a++)
+#pragma unroll
+      for (int b = 0; b < C::TC; b++)
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+          hand[(i++) * 64 + lane] = accS[a][b][e];
+          hand[(i++) * 64 + lane] = accO[a][b][e];
+        }
+  }
+  __syncthreads();
+  if (group == 1) return;
+  {
+    int i = 0;
+#pragma unroll
+    for (int a = 0; a < C::TO; a++)
+#pragma unroll
+      for (int b = 0; b < C::TC; b++)
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+          accS[a][b][e] += hand[(i++) * 64 + lane];
+          accO[a][b][e] += hand[(i++) * 64 + lane];
+        }
   }
 
   const size_t ww = (size_t)width * width;
@@ -432,7 +476,7 @@ constexpr int MIX_BMP = 128;          // 256 rows per block
 constexpr int MIX_BK = 64;            // contraction slice per pipeline stage
 constexpr int MIX_NS = 2;             // pipeline stages in LDS
 constexpr int DW_BO = 128, DW_BC = 128;
-constexpr int DW_TARGET_BLOCKS = 512;  // split-K blocks aimed for
+constexpr int DW_TARGET_BLOCKS = 256;  // split-K blocks aimed for (8 waves each)
 
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool TRANS_B>
 hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int pairs,
@@ -492,18 +536,19 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeArgs a) {
   }
 }
 
-// Split-K plan: enough blocks to fill the chip (about 512), each split a whole
-// number of K-steps.  Returns the split count; *pps gets pairs per split.
-int dw_plan(int rows, int width, int* pps) {
+// Split-K plan: about one block per CU, each block's row range two groups of
+// whole K-steps.  Returns the number of partial slots (blocks per tile);
+// *ppg gets the pairs per group.
+int dw_plan(int rows, int width, int* ppg) {
   const int pairs = rows / 2;
   const int bo = width % DW_BO == 0 ? DW_BO : 64;
   const int tiles = (width / bo) * (width / bo);
   const int ksteps = (pairs + KP - 1) / KP;
-  int splits = (DW_TARGET_BLOCKS + tiles - 1) / tiles;
-  if (splits > ksteps) splits = ksteps;
-  if (splits < 1) splits = 1;
-  *pps = ((ksteps + splits - 1) / splits) * KP;
-  return (pairs + *pps - 1) / *pps;
+  int slots = (DW_TARGET_BLOCKS + tiles - 1) / tiles;
+  if (slots > (ksteps + 1) / 2) slots = (ksteps + 1) / 2;
+  if (slots < 1) slots = 1;
+  *ppg = ((ksteps + 2 * slots - 1) / (2 * slots)) * KP;
+  return (pairs + 2 * *ppg - 1) / (2 * *ppg);
 }
 
 template <int BO, int BC, int WO, int WC>
@@ -511,7 +556,7 @@ hipError_t dw_launch(const bf16* X, const bf16* dY, float* partial, int pairs, i
                      int bidir, int splits, int pps, hipStream_t st) {
   using C = DwCfg<BO, BC, WO, WC>;
   const int blocks = (width / BO) * (width / BC) * splits;
-  const size_t lds = (size_t)2 * C::STAGE * sizeof(bf16);
+  const size_t lds = C::LDS;
 #define HCMIX_DW(BIDIR)                                                                     \
   {                                                                                         \
     auto k = dw_bf16_kernel<BO, BC, WO, WC, BIDIR>;                                         \
