@@ -33,7 +33,12 @@ WORKLOADS = {
     "lm256": "window n=256, width 512, batch 64, 16 rotated causal layers, bf16, fwd+bwd",
     "reach": "window n=256, width 64, batch 64, 8 rotated bidirectional layers, bf16, fwd+bwd",
     "long4096": "window n=4096, width 1024, batch 8, 24 rotated causal layers, bf16, fwd+bwd",
+    "hybrid": ("window n=256, width 512, batch 64, 16 rotated causal layers with 2 causal "
+               "softmax attention layers (8 heads x 64) at slots 3 and 9 of 18, bf16, fwd+bwd"),
 }
+# hybrid: positions of the attention layers in the 18-layer list
+HYBRID_ATTN_SLOTS = (3, 9)
+HYBRID_LAYERS = 18
 
 
 def algorithmic_work(batch, n, width, layers, causal):
@@ -52,6 +57,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="lm256", choices=sorted(WORKLOADS))
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the workload's batch (windows), e.g. for a batch sweep")
     ap.add_argument("--graph", type=int, default=1, help="replay the step as a HIP graph")
     ap.add_argument("--cpu-baseline", type=int, default=1)
     ap.add_argument("--cpu-windows", type=int, default=0,
@@ -157,8 +164,11 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
-    cfg = dict(inputs.PRESETS[args.workload])
-    s = inputs.make_preset(args.workload)
+    if args.workload == "hybrid":
+        return run_hybrid(args, torch, hcmix, inputs, dev)
+    over = {"batch": args.batch} if args.batch > 0 else {}
+    cfg = dict(inputs.PRESETS[args.workload], **over)
+    s = inputs.make_preset(args.workload, **over)
     B, n, w, L, causal = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"], cfg["causal"]
     dt = torch.bfloat16
 
@@ -222,7 +232,8 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}", "batch": B,
+        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}"
+                               + (f" (batch overridden to {B})" if over else ""), "batch": B,
                    "n": n, "width": w, "layers": L, "mode": "causal" if causal else "bidir",
                    "graph": bool(args.graph)},
         "pct_bf16_peak": round(flops / t * args.steps / 1e12 / PEAK_BF16_TFLOPS * 100, 2),
@@ -231,6 +242,159 @@ def main():
     }
     if args.cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(s, n, w, L, causal, args.cpu_windows)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def run_hybrid(args, torch, hcmix, inputs, dev):
+    """The lm256 stack with two causal softmax attention layers inserted (18
+    layers, attention at slots 3 and 9; the rotated layers keep d = their index
+    among the rotated layers mod 8).  Attention is harness code (PyTorch: QKV
+    projection, scaled-dot-product attention, output projection); the sparse
+    segments are hcmix stack calls.  Forward and backward are chained by hand
+    so that every segment is timed with HIP events on one stream; the line
+    reports the sparse layers' share of the step and their own throughput."""
+    import torch.nn.functional as F
+    cfg = dict(inputs.PRESETS["lm256"])
+    if args.batch > 0:
+        cfg["batch"] = args.batch
+    s = inputs.make_preset("lm256", **({"batch": args.batch} if args.batch > 0 else {}))
+    B, n, w, Ls = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"]
+    dt = torch.bfloat16
+    heads, hd = 8, 64
+    assert heads * hd == w
+
+    def dev_t(a):
+        return torch.from_numpy(a).to(dt).to(dev)
+
+    x0, dy = dev_t(s.x), dev_t(s.dy)
+    ws = [dev_t(a) for a in s.w_self]
+    wo = [dev_t(a) for a in s.w_off]
+    gen = torch.Generator(device="cpu").manual_seed(1)
+    attn_w = [((torch.randn(3 * w, w, generator=gen) / w ** 0.5).to(dt).to(dev),
+               (torch.randn(w, w, generator=gen) / w ** 0.5).to(dt).to(dev))
+              for _ in HYBRID_ATTN_SLOTS]
+    # segments of consecutive rotated layers between the attention slots
+    segs, rot = [], 0
+    cur = []
+    for slot in range(HYBRID_LAYERS):
+        if slot in HYBRID_ATTN_SLOTS:
+            segs.append(("sparse", cur))
+            segs.append(("attn", HYBRID_ATTN_SLOTS.index(slot)))
+            cur = []
+        else:
+            cur.append(rot)
+            rot += 1
+    segs.append(("sparse", cur))
+    assert rot == Ls
+
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    backend = {"name": None}
+
+    def sdpa(q, k, v):
+        if backend["name"] is None:
+            for name, be in (("flash", SDPBackend.FLASH_ATTENTION),
+                             ("efficient", SDPBackend.EFFICIENT_ATTENTION)):
+                try:
+                    with sdpa_kernel([be]):
+                        out = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+                    backend["name"], backend["be"] = name, be
+                    return out
+                except RuntimeError:
+                    continue
+            backend["name"] = "fp32 math"
+        if backend["name"] == "fp32 math":
+            # plain fp32 products on contiguous operands
+            qf, kf, vf = (t.float().contiguous() for t in (q, k, v))
+            att = torch.matmul(qf, kf.transpose(-1, -2).contiguous()) / hd ** 0.5
+            mask = torch.ones(n, n, dtype=torch.bool, device=dev).triu(1)
+            att = att.masked_fill(mask, float("-inf")).softmax(-1)
+            return torch.matmul(att, vf).to(q.dtype)
+        with sdpa_kernel([backend["be"]]):
+            return F.scaled_dot_product_attention(q, k, v, is_causal=True)
+
+    def attention(x, i):
+        wqkv, wout = attn_w[i]
+        qkv = F.linear(x, wqkv).view(B, n, 3, heads, hd)
+        q, k, v = (qkv[:, :, j].transpose(1, 2).contiguous() for j in range(3))
+        o = sdpa(q, k, v).transpose(1, 2).reshape(B, n, w)
+        return F.linear(o, wout)
+
+    wsp = {}
+    stream = torch.cuda.current_stream(dev)
+    ev = torch.cuda.Event
+
+    def step(times):
+        saved, x = [], x0
+        for kind, arg in segs:                      # forward
+            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
+            e0.record(stream)
+            if kind == "sparse":
+                xs = hcmix.stack_forward(x, [ws[l] for l in arg], [wo[l] for l in arg],
+                                         [s.layers[l] for l in arg], True)
+                saved.append(xs)
+                x = xs[-1]
+            else:
+                xin = x.detach().requires_grad_(True)
+                params = [p.requires_grad_(True) for p in attn_w[arg]]
+                with torch.enable_grad():
+                    out = attention(xin, arg)
+                saved.append((xin, out, params))
+                x = out.detach()
+            e1.record(stream)
+            times.append((kind, "fwd", e0, e1))
+        g = dy
+        for (kind, arg), sv in zip(reversed(segs), reversed(saved)):   # backward
+            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
+            e0.record(stream)
+            if kind == "sparse":
+                L = len(arg)
+                if L not in wsp:
+                    wsp[L] = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
+                g, _, _ = hcmix.stack_backward(sv[:L], [ws[l] for l in arg], [wo[l] for l in arg],
+                                               [s.layers[l] for l in arg], g, True,
+                                               workspace=wsp[L])
+            else:
+                xin, out, params = sv
+                grads = torch.autograd.grad(out, [xin, *params], grad_outputs=g)
+                g = grads[0].contiguous()
+            e1.record(stream)
+            times.append((kind, "bwd", e0, e1))
+        return g
+
+    for _ in range(args.warmup):
+        step([])
+    torch.cuda.synchronize()
+    per_step = []
+    t0 = time.perf_counter()
+    c0, c1 = ev(enable_timing=True), ev(enable_timing=True)
+    c0.record(stream)
+    for _ in range(args.steps):
+        times = []
+        step(times)
+        per_step.append(times)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total = max(wall, c0.elapsed_time(c1) / 1e3)
+    sparse = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "sparse") / 1e3
+    attn = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "attn") / 1e3
+    pl = B * n * Ls
+    out = {
+        "metric": METRIC, "value": round(pl * args.steps / sparse, 1), "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(total / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"hybrid: {WORKLOADS['hybrid']}", "batch": B, "n": n, "width": w,
+                   "layers": Ls, "attention_layers": len(HYBRID_ATTN_SLOTS), "mode": "causal",
+                   "graph": False, "attention_backend": backend["name"]},
+        "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
+                   "sparse_ms": round(sparse / args.steps * 1e3, 4),
+                   "attention_ms": round(attn / args.steps * 1e3, 4),
+                   "sparse_share_of_step": round(sparse / total, 4),
+                   "note": "value = sparse positions*layers per second of sparse-layer time; "
+                           "eager launches, each segment timed with HIP events"},
+    }
     print(json.dumps(out), flush=True)
     return 0
 
