@@ -18,6 +18,10 @@ import subprocess
 
 import numpy as np
 
+# Layer code of the local layer (Eq. (1) with jump k = 1, partner i - 1); layer
+# codes >= 0 are hypercube layers.
+NEAR = -1
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hcmix_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
@@ -43,6 +47,7 @@ def _load():
         lib.oracle_dim.argtypes, lib.oracle_dim.restype = [i32, i64], i32
         lib.oracle_partner.argtypes, lib.oracle_partner.restype = [i64, i32, i64], i64
         lib.oracle_receives.argtypes, lib.oracle_receives.restype = [i64, i32, i64, i32], i32
+        lib.oracle_valid_layer.argtypes, lib.oracle_valid_layer.restype = [i32, i64, i32], i32
         lib.oracle_num_threads.argtypes, lib.oracle_num_threads.restype = [], i32
         lib.oracle_forward.argtypes = [i64, i64, i64, i32, i32, dp, dp, dp, dp]
         lib.oracle_forward.restype = i32
@@ -70,7 +75,8 @@ def dim(layer: int, n: int) -> int:
 
 
 def partner(i: int, layer: int, n: int) -> int:
-    """Partner of position i at layer ``layer``: i XOR 2^(layer mod b) (Section 3.1)."""
+    """Partner of position i at layer ``layer``: i XOR 2^(layer mod b) (Section 3.1),
+    or i - 1 for the local layer (NEAR; -1 at position 0)."""
     return _load().oracle_partner(i, layer, n)
 
 
@@ -158,4 +164,40 @@ def schedule_gray(num_layers: int) -> list[int]:
         while not (t >> d) & 1:
             d += 1
         out.append(d)
+    return out
+
+
+def schedule_local(num_layers: int) -> list[int]:
+    """local: the jump k = 1 layer (NEAR) at every layer (Section 3.3)."""
+    return [NEAR] * num_layers
+
+
+def schedule_mixa(n: int) -> list[int]:
+    """mixa: local layers alternating with causal hypercube jumps that visit each
+    scale once, longest first (Section 3.3: 32, 16, 8, 4, 2, 1 for n = 64).  A
+    jump of length 2^d is the hypercube layer of dimension d."""
+    b = log2n(n)
+    out = []
+    for d in range(b - 1, -1, -1):
+        out += [NEAR, d]
+    return out
+
+
+def schedule_from_names(names) -> list:
+    """Layer codes of a schedule written as layer names (Appendix A): "near",
+    "jumpK" (K a power of two: the hypercube layer of dimension log2 K) and
+    "attn" (an attention layer, which this oracle does not compute: None)."""
+    out = []
+    for name in names:
+        if name == "near":
+            out.append(NEAR)
+        elif name == "attn":
+            out.append(None)
+        elif name.startswith("jump"):
+            k = int(name[len("jump"):])
+            d = k.bit_length() - 1
+            assert k == 1 << d, name
+            out.append(d)
+        else:
+            raise ValueError(f"unknown layer name {name!r}")
     return out

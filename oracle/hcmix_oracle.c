@@ -18,6 +18,10 @@
  *    its partner only when the partner comes before it.
  *  - Section 3.2, Eq. (1): y_i = W_self x_i + W_off x_partner(i); two linear
  *    maps and a shift, nothing else (no bias, residual or activation).
+ *  - Section 3.2, Eq. (1) with jump k = 1 is the local ("near") layer of the
+ *    schedules of Section 3.3 and Appendix A: y_i = W_self x_i + W_off x_(i-1),
+ *    position 0 of a window having no predecessor.  It is causal by
+ *    construction and exists in causal mode only.  Layer code ORACLE_NEAR.
  *  - The backward pass is the adjoint of Eq. (1); the paper trains every model
  *    but prints no gradient, so it is written here from the chain rule: for
  *    every link (receiver i <- sender p) the gradient flows back from i to p.
@@ -32,6 +36,10 @@
 #ifdef _OPENMP
 #include <omp.h>
 #endif
+
+/* Layer code of the local layer (jump k = 1); layer codes >= 0 are hypercube
+ * layers with dimension code mod b. */
+#define ORACLE_NEAR (-1)
 
 /* b = log2 n for n a power of two >= 2, else -1. */
 int32_t oracle_log2n(int64_t n) {
@@ -49,19 +57,32 @@ int32_t oracle_dim(int32_t layer, int64_t n) {
     return layer % b;
 }
 
-/* Partner of position i at layer l: i XOR 2^(l mod b) (Section 3.1). */
+/* 1 if `layer` is a layer code this oracle knows for windows of n (and the
+ * mode allows it): a hypercube layer, or the local layer in causal mode. */
+int32_t oracle_valid_layer(int32_t layer, int64_t n, int32_t causal) {
+    if (oracle_log2n(n) < 0) return 0;
+    if (layer == ORACLE_NEAR) return causal ? 1 : 0;
+    return layer >= 0;
+}
+
+/* Partner of position i at layer l: i XOR 2^(l mod b) (Section 3.1); for the
+ * local layer the previous position i - 1, or -1 at position 0 (no partner). */
 int64_t oracle_partner(int64_t i, int32_t layer, int64_t n) {
+    if (i < 0 || i >= n || oracle_log2n(n) < 0) return -1;
+    if (layer == ORACLE_NEAR) return i - 1;
     int32_t d = oracle_dim(layer, n);
-    if (d < 0 || i < 0 || i >= n) return -1;
+    if (d < 0) return -1;
     return i ^ ((int64_t)1 << d);
 }
 
 /* 1 when position i takes its partner's vector at layer l.  Bidirectional:
  * always.  Causal: only the earlier endpoint of a link is kept (Section 3.1),
- * so i receives exactly when its partner precedes it. */
+ * so i receives exactly when its partner precedes it (for the local layer:
+ * whenever it has a predecessor).  -1 for an invalid layer, position or mode. */
 int32_t oracle_receives(int64_t i, int32_t layer, int64_t n, int32_t causal) {
+    if (i < 0 || i >= n || !oracle_valid_layer(layer, n, causal)) return -1;
     int64_t p = oracle_partner(i, layer, n);
-    if (p < 0) return -1;
+    if (layer == ORACLE_NEAR) return p >= 0 ? 1 : 0;
     if (!causal) return 1;
     return p < i ? 1 : 0;
 }
@@ -80,21 +101,21 @@ int32_t oracle_num_threads(void) {
 int32_t oracle_forward(int64_t batch, int64_t n, int64_t width, int32_t layer,
                        int32_t causal, const double* x, const double* w_self,
                        const double* w_off, double* y) {
-    if (oracle_dim(layer, n) < 0 || batch < 1 || width < 1) return -1;
+    if (!oracle_valid_layer(layer, n, causal) || batch < 1 || width < 1) return -1;
     int64_t rows = batch * n;
 #pragma omp parallel for schedule(static)
     for (int64_t r = 0; r < rows; r++) {
         int64_t bt = r / n, i = r % n;
-        int64_t p = oracle_partner(i, layer, n);
         int32_t take = oracle_receives(i, layer, n, causal);
         const double* xi = x + (bt * n + i) * width;
-        const double* xp = x + (bt * n + p) * width;
         double* yi = y + (bt * n + i) * width;
         for (int64_t o = 0; o < width; o++) {
             double acc = 0.0;
             for (int64_t c = 0; c < width; c++) acc += w_self[o * width + c] * xi[c];
-            if (take)
+            if (take) {
+                const double* xp = x + (bt * n + oracle_partner(i, layer, n)) * width;
                 for (int64_t c = 0; c < width; c++) acc += w_off[o * width + c] * xp[c];
+            }
             yi[o] = acc;
         }
     }
@@ -112,7 +133,7 @@ int32_t oracle_backward(int64_t batch, int64_t n, int64_t width, int32_t layer,
                         int32_t causal, const double* x, const double* w_self,
                         const double* w_off, const double* dy, double* dx,
                         double* dw_self, double* dw_off) {
-    if (oracle_dim(layer, n) < 0 || batch < 1 || width < 1) return -1;
+    if (!oracle_valid_layer(layer, n, causal) || batch < 1 || width < 1) return -1;
     int64_t rows = batch * n;
 
     /* dx: windows are independent, so parallelise over windows only. */

@@ -100,7 +100,11 @@ def links_from_oracle(n, layer, causal):
 
 
 def near_links(n):
-    return n + (n - 1)       # self plus the previous position (k = 1 shift, Eq. (1))
+    """Links of the local layer (jump k = 1), counted through the oracle; also
+    equal to n + (n - 1): self plus the previous position."""
+    count = links_from_oracle(n, oracle.NEAR, True)
+    assert count == n + (n - 1)
+    return count
 
 
 def attn_links(n):
@@ -124,6 +128,11 @@ def test_link_counts_window64(golden):
     assert rot == g["links"]["rot"]
     jump = {k: links_from_oracle(n, int(np.log2(k)), True) for k in g["mixa_jumps"]}
     assert 6 * near_links(n) + sum(jump[k] for k in g["mixa_jumps"]) == g["links"]["mixa"]
+    # the same total from the oracle's own mixa schedule (Section 3.3)
+    mixa = oracle.schedule_mixa(n)
+    assert len(mixa) == L
+    assert sum(links_from_oracle(n, c, True) for c in mixa) == g["links"]["mixa"]
+    assert sum(links_from_oracle(n, c, True) for c in oracle.schedule_local(L)) == g["links"]["local"]
     assert (6 * near_links(n) + sum(jump[k] for k in g["hybrid_jumps"]) + 2 * attn_links(n)
             == g["links"]["hybrid"])
     assert L * near_links(n) == g["links"]["local"]
@@ -142,6 +151,9 @@ def test_link_counts_window256_hybrid(golden):
         else:
             k = int(kind[len("jump"):])
             total += links_from_oracle(n, int(np.log2(k)), True)
+    assert total == g["links"]["hy"]
+    codes = oracle.schedule_from_names(g["hy_schedule"])
+    total = sum(attn_links(n) if c is None else links_from_oracle(n, c, True) for c in codes)
     assert total == g["links"]["hy"]
     assert 16 * attn_links(n) == g["links"]["attn"]
 
@@ -392,3 +404,96 @@ def test_zipf_tokens_follow_the_rank_law():
     r = np.arange(1, 33)
     slope = np.polyfit(np.log(r), np.log(counts[:32]), 1)[0]
     assert abs(slope + 1.1) < 0.05
+
+
+# --- the local layer (Eq. (1) with jump k = 1; Section 3.3, Appendix A) -------
+
+def test_near_partner_and_mask_brute_force():
+    for n in (2, 16, 256):
+        for i in range(n):
+            assert oracle.partner(i, oracle.NEAR, n) == i - 1
+            assert oracle.receives(i, oracle.NEAR, n, True) == (1 if i >= 1 else 0)
+            assert oracle.receives(i, oracle.NEAR, n, False) == -1   # causal only
+
+
+def test_near_forward_equals_dense_shift_matmul():
+    """y = X W_self^T + S X W_off^T, S the sub-diagonal shift inside a window."""
+    rng = np.random.default_rng(21)
+    for n, width, batch in [(2, 3, 1), (16, 5, 2), (64, 7, 3)]:
+        x = rng.standard_normal((batch, n, width))
+        ws = rng.standard_normal((width, width))
+        wo = rng.standard_normal((width, width))
+        S = np.eye(n, k=-1)
+        want = np.stack([x[t] @ ws.T + (S @ x[t]) @ wo.T for t in range(batch)])
+        np.testing.assert_allclose(oracle.forward(x, ws, wo, oracle.NEAR, True), want,
+                                   rtol=1e-12, atol=1e-12)
+    with pytest.raises(Exception):
+        oracle.forward(x, ws, wo, oracle.NEAR, False)
+
+
+@pytest.mark.parametrize("L", [1, 3, 7])
+def test_near_stack_with_identity_weights_is_pascals_triangle(L):
+    """W_self = W_off = I: L local layers give y_i = sum_k C(L, k) x_(i-k), the
+    sum stopping at the window's first position."""
+    from math import comb
+    n = 16
+    rng = np.random.default_rng(22)
+    x = rng.integers(-5, 6, size=(2, n, 2)).astype(np.float64)
+    eye = np.eye(2)
+    y = oracle.stack_forward(x, [eye] * L, [eye] * L, oracle.schedule_local(L), True)[-1]
+    want = np.zeros_like(x)
+    for i in range(n):
+        for k in range(min(L, i) + 1):
+            want[:, i] += comb(L, k) * x[:, i - k]
+    np.testing.assert_array_equal(y, want)
+
+
+def test_near_backward_adjoint_and_autograd():
+    rng = np.random.default_rng(23)
+    n, width, batch = 16, 5, 2
+    x = rng.standard_normal((batch, n, width))
+    g = rng.standard_normal((batch, n, width))
+    ws = rng.standard_normal((width, width))
+    wo = rng.standard_normal((width, width))
+    y = oracle.forward(x, ws, wo, oracle.NEAR, True)
+    dx, dws, dwo = oracle.backward(x, ws, wo, g, oracle.NEAR, True)
+    lhs = float((y * g).sum())
+    assert abs(float((x * dx).sum()) - lhs) <= 1e-10 * (1 + abs(lhs))
+    S = torch.tensor(np.eye(n, k=-1))
+    tx = torch.tensor(x, requires_grad=True)
+    tws = torch.tensor(ws, requires_grad=True)
+    two = torch.tensor(wo, requires_grad=True)
+    (torch.matmul(tx, tws.T) + torch.matmul(torch.matmul(S, tx), two.T)).backward(torch.tensor(g))
+    np.testing.assert_allclose(dx, tx.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dws, tws.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dwo, two.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_mixa_stack_backward_matches_central_differences_and_never_looks_ahead():
+    rng = np.random.default_rng(24)
+    n, width, batch = 16, 3, 2
+    layers = oracle.schedule_mixa(n)
+    L = len(layers)
+    ws = [rng.standard_normal((width, width)) * 0.5 for _ in range(L)]
+    wo = [rng.standard_normal((width, width)) * 0.5 for _ in range(L)]
+    x = rng.standard_normal((batch, n, width))
+    g = rng.standard_normal((batch, n, width))
+
+    def loss(x_):
+        return float((oracle.stack_forward(x_, ws, wo, layers, True)[-1] * g).sum())
+
+    xs = oracle.stack_forward(x, ws, wo, layers, True)
+    dx, _, _ = oracle.stack_backward(xs, ws, wo, layers, g, True)
+    h = 1e-6
+    for idx in [(0, 0, 0), (1, 7, 2), (0, 15, 1), (1, 3, 0)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (loss(xp) - loss(xm)) / (2 * h)
+        assert abs(fd - dx[idx]) <= 1e-6 * (1 + abs(fd))
+    base = xs[-1]
+    for k in (1, 6, 15):
+        x2 = x.copy()
+        x2[:, k] += 1.0
+        pert = oracle.stack_forward(x2, ws, wo, layers, True)[-1]
+        np.testing.assert_array_equal(pert[:, :k], base[:, :k])
