@@ -60,6 +60,15 @@ typedef enum { HCMIX_F32 = 0, HCMIX_BF16 = 1 } hcmix_dtype;
  * receives, i.e. position i receives when bit d of i is 1 (n + n/2 links). */
 typedef enum { HCMIX_BIDIR = 0, HCMIX_CAUSAL = 1 } hcmix_mode;
 
+/* Layer code of the local layer: Eq. (1) with jump k = 1, the schedules'
+ * "near" layer (Section 3.3, Appendix A):
+ *   y[t][i] = W_self x[t][i] + W_off x[t][i-1]   (i >= 1; position 0 of a
+ *                                                  window takes no partner)
+ * It exists in causal form only (mode must be HCMIX_CAUSAL).  Wherever a
+ * layer index is taken (`layer`, `layers[l]`), this value selects it; values
+ * >= 0 select the hypercube layer of dimension hcmix_dim(value, n). */
+enum { HCMIX_LAYER_NEAR = -1 };
+
 /* Human-readable name of a status code (static storage). */
 const char* hcmix_status_string(int32_t status);
 
@@ -74,7 +83,8 @@ int32_t hcmix_dim(int32_t layer, int64_t n);
 
 /* Forward of one layer, Eq. (1):
  *   y[t][i] = W_self x[t][i] + m(i) W_off x[t][i XOR 2^d],   d = hcmix_dim(layer, n)
- * with m(i) = 1 (HCMIX_BIDIR) or bit d of i (HCMIX_CAUSAL).
+ * with m(i) = 1 (HCMIX_BIDIR) or bit d of i (HCMIX_CAUSAL); for
+ * layer == HCMIX_LAYER_NEAR the partner is i - 1 and m(i) = (i >= 1).
  * bf16: inputs bf16, products accumulated in fp32, y rounded to bf16 (nearest
  * even).  fp32: fp32 throughout, no reduced-precision matrix instructions.
  * y must not overlap x. */
@@ -91,9 +101,10 @@ size_t hcmix_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
 /* Backward of one layer: the adjoint of hcmix_forward.  Given dy = dL/dy,
  *   dx[t][j]  = W_self^T dy[t][j] + m'(j) W_off^T dy[t][j XOR 2^d]
  *               with m'(j) = 1 (bidir) or 1 - bit d of j (causal: j is the
- *               earlier endpoint of the link it sends on)
+ *               earlier endpoint of the link it sends on); for the local layer
+ *               dy[t][j+1] with m'(j) = (j <= n - 2)
  *   dw_self   = sum over (t, i) of dy[t][i] x[t][i]^T
- *   dw_off    = sum over (t, i) of m(i) dy[t][i] x[t][i XOR 2^d]^T
+ *   dw_off    = sum over (t, i) of m(i) dy[t][i] x[t][partner(i)]^T
  * dx is in `dtype` (bf16: fp32 accumulation, rounded once); dw_* are fp32,
  * overwritten when accumulate == 0 and added to when accumulate != 0.
  * dx, dw_self, dw_off and workspace must not overlap each other or any input.
@@ -113,12 +124,17 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
  *                0, 1, 2, ..., the fixed control repeats one index.
  * w_self, w_off: host arrays of num_layers device pointers, one pair per layer.
  *
- * For bf16, width 64 and n in {64, 128, 256} (a window of at most 32 KB) the
- * whole stack runs in one kernel with every window resident in LDS (one
- * block per window); otherwise the layers run one launch each, with results
- * identical to calling hcmix_forward / hcmix_backward layer by layer up to
- * the order of floating-point summation.  num_layers may be at most 64 for
- * the fused kernels; longer stacks run layer by layer.
+ * layers[l] may also be HCMIX_LAYER_NEAR (causal mode), so the local, mixa
+ * and hybrid schedules of Section 3.3 are lists such as
+ * {NEAR, 5, NEAR, 4, ..., NEAR, 0} (jump 2^d = hypercube layer d).
+ *
+ * For bf16, width 64 and n in {64, 128, 256} (a window of at most 32 KB) a
+ * stack of hypercube layers runs in one kernel with every window resident in
+ * LDS (one block per window); otherwise (or with local layers) the layers run
+ * one launch each, with results identical to calling hcmix_forward /
+ * hcmix_backward layer by layer up to the order of floating-point summation.
+ * num_layers may be at most 64 for the fused kernels; longer stacks run layer
+ * by layer.
  */
 
 /* Forward through the stack: xs is a host array of num_layers device

@@ -36,7 +36,12 @@ size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 // Shape checks shared by every entry point; returns HCMIX_OK or the error.
 hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer, int32_t mode,
                          int32_t dtype) {
-  if (hcmix_dim(layer, n) < 0) return HCMIX_ERR_INVALID_VALUE;
+  if (layer == HCMIX_LAYER_NEAR) {
+    // the local layer exists in causal form only
+    if (hcmix_dim(0, n) < 0 || mode != HCMIX_CAUSAL) return HCMIX_ERR_INVALID_VALUE;
+  } else if (hcmix_dim(layer, n) < 0) {
+    return HCMIX_ERR_INVALID_VALUE;
+  }
   if (batch < 1 || width < 1) return HCMIX_ERR_INVALID_VALUE;
   if (mode != HCMIX_BIDIR && mode != HCMIX_CAUSAL) return HCMIX_ERR_INVALID_VALUE;
   if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return HCMIX_ERR_INVALID_VALUE;
@@ -67,42 +72,70 @@ size_t transposed_weight_bytes(int64_t width, int32_t num_layers, int32_t dtype)
 // layer-by-layer path.
 size_t stack_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                              int32_t dtype) {
-  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers))
-    return align256(fused_partial_bytes(batch, num_layers));
   const size_t act = align256((size_t)(batch * n * width) * elem_size(dtype));
-  return (num_layers > 1 ? 2 * act : 0) + layer_workspace_bytes(batch, n, width, dtype) +
-         transposed_weight_bytes(width, num_layers, dtype);
+  const size_t layered = (num_layers > 1 ? 2 * act : 0) +
+                         layer_workspace_bytes(batch, n, width, dtype) +
+                         transposed_weight_bytes(width, num_layers, dtype);
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
+    // the schedule is not known here: enough for the fused path and for the
+    // layer-by-layer path a schedule with local layers takes
+    const size_t fused = align256(fused_partial_bytes(batch, num_layers));
+    return fused > layered ? fused : layered;
+  }
+  return layered;
+}
+
+// The fused kernels handle hypercube layers only.
+bool any_local_layer(const int32_t* layers, int32_t num_layers) {
+  for (int l = 0; l < num_layers; l++)
+    if (layers[l] == HCMIX_LAYER_NEAR) return true;
+  return false;
 }
 
 // ---- unchecked per-layer dispatch (arguments already validated) ----
 
-hipError_t run_forward(int rows, int w, int d, int bidir, int32_t dtype, const void* x,
+// d >= 0: hypercube layer of dimension d; d < 0: the local layer (jump 1).
+hipError_t run_forward(int rows, int w, int d, int n, int bidir, int32_t dtype, const void* x,
                        const void* w_self, const void* w_off, void* y, hipStream_t s) {
-  if (dtype == HCMIX_BF16)
+  if (dtype == HCMIX_BF16) {
+    if (d < 0)
+      return launch_shift_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y,
+                               rows, w, n, /*delta=*/-1, /*transpose_b=*/false, s);
     return launch_mix_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y,
                            rows, w, d, /*partner_lower=*/bidir, /*partner_upper=*/1,
                            /*transpose_b=*/false, s);
+  }
   return launch_mix_f32((const float*)x, (const float*)w_self, (const float*)w_off, (float*)y,
-                        rows, w, d, bidir, 1, /*transpose_w=*/false, s);
+                        rows, w, d, bidir, 1, n, /*shift=*/-1, /*transpose_w=*/false, s);
 }
 
-hipError_t run_backward(int rows, int w, int d, int bidir, int32_t dtype, const void* x,
+// dX of one bf16 layer with the weights read as given (transpose_b) or from
+// transposed copies.  Hypercube layer: lower rows always take their partner's
+// gradient (causal: the lower row is the sender); local layer: every row but
+// a window's last takes the next row's gradient.
+hipError_t run_dx_bf16(int rows, int w, int d, int n, int bidir, const bf16* dy, const bf16* b1,
+                       const bf16* b2, bf16* dx, bool transpose_b, hipStream_t s) {
+  if (d < 0) return launch_shift_bf16(dy, b1, b2, dx, rows, w, n, /*delta=*/1, transpose_b, s);
+  return launch_mix_bf16(dy, b1, b2, dx, rows, w, d, /*partner_lower=*/1,
+                         /*partner_upper=*/bidir, transpose_b, s);
+}
+
+hipError_t run_backward(int rows, int w, int d, int n, int bidir, int32_t dtype, const void* x,
                         const void* w_self, const void* w_off, const void* dy, void* dx,
                         float* dw_self, float* dw_off, int accumulate, void* workspace,
                         hipStream_t s) {
   hipError_t e;
   if (dtype == HCMIX_BF16) {
-    e = launch_mix_bf16((const bf16*)dy, (const bf16*)w_self, (const bf16*)w_off, (bf16*)dx,
-                        rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
-                        /*transpose_b=*/true, s);
+    e = run_dx_bf16(rows, w, d, n, bidir, (const bf16*)dy, (const bf16*)w_self,
+                    (const bf16*)w_off, (bf16*)dx, /*transpose_b=*/true, s);
     if (e == hipSuccess)
       e = launch_dw_bf16((const bf16*)x, (const bf16*)dy, (float*)workspace, dw_self, dw_off,
-                         rows, w, d, bidir, accumulate, s);
+                         rows, w, d, n, bidir, accumulate, s);
   } else {
     e = launch_mix_f32((const float*)dy, (const float*)w_self, (const float*)w_off, (float*)dx,
-                       rows, w, d, 1, bidir, /*transpose_w=*/true, s);
+                       rows, w, d, 1, bidir, n, /*shift=*/1, /*transpose_w=*/true, s);
     if (e == hipSuccess)
-      e = launch_dw_f32((const float*)x, (const float*)dy, dw_self, dw_off, rows, w, d, bidir,
+      e = launch_dw_f32((const float*)x, (const float*)dy, dw_self, dw_off, rows, w, d, n, bidir,
                         accumulate, s);
   }
   return e;
@@ -171,7 +204,7 @@ hcmix_status hcmix_forward(int64_t batch, int64_t n, int64_t width, int32_t laye
   const Span outs[1] = {{y, act}};
   st = check_spans(ins, 3, outs, 1, dtype == HCMIX_BF16 ? 16 : 4);
   if (st != HCMIX_OK) return st;
-  hipError_t e = run_forward((int)(batch * n), (int)width, hcmix_dim(layer, n),
+  hipError_t e = run_forward((int)(batch * n), (int)width, hcmix_dim(layer, n), (int)n,
                              mode == HCMIX_BIDIR, dtype, x, w_self, w_off, y,
                              (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
@@ -202,7 +235,7 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
   if (st != HCMIX_OK) return st;
   if (!aligned(dw_self, 16) || !aligned(dw_off, 16) || (need && !aligned(workspace, 256)))
     return HCMIX_ERR_UNSUPPORTED;
-  hipError_t e = run_backward((int)(batch * n), (int)width, hcmix_dim(layer, n),
+  hipError_t e = run_backward((int)(batch * n), (int)width, hcmix_dim(layer, n), (int)n,
                               mode == HCMIX_BIDIR, dtype, x, w_self, w_off, dy, dx, dw_self,
                               dw_off, accumulate != 0, workspace, (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
@@ -236,7 +269,8 @@ hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_
   const int bidir = mode == HCMIX_BIDIR;
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = hipSuccess;
-  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers) &&
+      !any_local_layer(layers, num_layers)) {
     FusedFwdArgs a = {};
     a.x0 = (const bf16*)x;
     for (int l = 0; l < num_layers; l++) {
@@ -251,8 +285,8 @@ hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_
   } else {
     const void* in = x;
     for (int l = 0; l < num_layers && e == hipSuccess; l++) {
-      e = run_forward(rows, w, hcmix_dim(layers[l], n), bidir, dtype, in, w_self[l], w_off[l],
-                      xs[l], s);
+      e = run_forward(rows, w, hcmix_dim(layers[l], n), (int)n, bidir, dtype, in, w_self[l],
+                      w_off[l], xs[l], s);
       in = xs[l];
     }
   }
@@ -322,7 +356,8 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
   const int bidir = mode == HCMIX_BIDIR;
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = hipSuccess;
-  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
+  if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers) &&
+      !any_local_layer(layers, num_layers)) {
     FusedBwdArgs a = {};
     FusedReduceArgs r = {};
     for (int l = 0; l < num_layers; l++) {
@@ -372,15 +407,14 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
       void* out = l == 0 ? dx : gbuf[l & 1];
       const int d = hcmix_dim(layers[l], n);
       if (dtype == HCMIX_BF16 && num_layers > 1) {
-        // dX = W_self^T dy (+ partner W_off^T dy): the forward kernel on W^T
-        e = launch_mix_bf16((const bf16*)g, wt + 2 * (size_t)l * ww, wt + (2 * (size_t)l + 1) * ww,
-                            (bf16*)out, rows, w, d, /*partner_lower=*/1, /*partner_upper=*/bidir,
-                            /*transpose_b=*/false, s);
+        // dX = W_self^T dy (+ partner W_off^T dy): the forward kernels on W^T
+        e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g, wt + 2 * (size_t)l * ww,
+                        wt + (2 * (size_t)l + 1) * ww, (bf16*)out, /*transpose_b=*/false, s);
         if (e == hipSuccess)
           e = launch_dw_bf16((const bf16*)xs_in[l], (const bf16*)g, (float*)layer_ws, dw_self[l],
-                             dw_off[l], rows, w, d, bidir, accumulate != 0, s);
+                             dw_off[l], rows, w, d, (int)n, bidir, accumulate != 0, s);
       } else {
-        e = run_backward(rows, w, d, bidir, dtype, xs_in[l], w_self[l], w_off[l], g, out,
+        e = run_backward(rows, w, d, (int)n, bidir, dtype, xs_in[l], w_self[l], w_off[l], g, out,
                          dw_self[l], dw_off[l], accumulate != 0, layer_ws, s);
       }
       g = out;

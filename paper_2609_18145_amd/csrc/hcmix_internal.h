@@ -28,16 +28,18 @@ __device__ __forceinline__ bf16 to_bf16(float v) { return (bf16)v; }
 
 // ---- launchers (each returns hipGetLastError() of its launch) ----
 
-// out[r][j] = sum_k A[r][k] B1(j,k) + m(r) sum_k A[r^s][k] B2(j,k), fp32.
+// out[r][j] = sum_k A[r][k] B1(j,k) + m(r) sum_k A[p(r)][k] B2(j,k), fp32.
 // B(j,k) = W[j*width+k] when !transpose_w, W[k*width+j] when transpose_w.
-// m(r) = partner_lower for rows with bit d clear, partner_upper otherwise.
+// d >= 0: p(r) = r ^ 2^d, m(r) = partner_lower for rows with bit d clear,
+// partner_upper otherwise.  d < 0 (local layer): p(r) = r + shift over windows
+// of n rows, shift = -1 (m = 0 at a window's first row) or +1 (at its last).
+// The weight gradients of a local layer (d < 0) pair row r with r - 1.
 hipError_t launch_mix_f32(const float* A, const float* W1, const float* W2, float* out,
                           int rows, int width, int d, int partner_lower, int partner_upper,
-                          bool transpose_w, hipStream_t st);
+                          int n, int shift, bool transpose_w, hipStream_t st);
 
-// dW_self = dY^T X ; dW_off = sum over receiving rows of dY[r] X[r^s]^T, fp32.
 hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo,
-                         int rows, int width, int d, int bidir, int accumulate,
+                         int rows, int width, int d, int n, int bidir, int accumulate,
                          hipStream_t st);
 
 // bf16 MFMA: same contraction as launch_mix_f32.  B(j,k) = B[j*width+k] when
@@ -49,6 +51,11 @@ hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* 
 
 // Split-K weight gradients into `partial` ([splits][2][width][width] fp32),
 // then a fixed-order reduction into dws / dwo.
+// Local layer (jump 1), bf16: out_r = A_r B1^T + m(r) A_(r+delta) B2^T over
+// windows of n rows; delta = -1 (forward: m = 0 at a window's first row) or +1
+// (dX: m = 0 at a window's last row).  transpose_b as launch_mix_bf16.
+hipError_t launch_shift_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                             int width, int n, int delta, bool transpose_b, hipStream_t st);
 int dw_bf16_splits(int rows, int width);
 // dst[m] = src[m]^T for `count` (<= kTransposeBatch) bf16 matrices of
 // width x width, width a multiple of 64.
@@ -61,7 +68,7 @@ struct TransposeArgs {
 hipError_t launch_transpose_bf16(const TransposeArgs& a, int count, hipStream_t st);
 
 hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* dws, float* dwo,
-                          int rows, int width, int d, int bidir, int accumulate,
+                          int rows, int width, int d, int n, int bidir, int accumulate,
                           hipStream_t st);
 
 // ---- fused small-width stack (width 64, n in {64, 128, 256}) ----

@@ -239,6 +239,205 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Shift GEMM: the local layer (Eq. (1) with jump 1).  For the block's BM
+// consecutive rows r:
+//   out_r = A_r B1^T + m(r) A_(r+DELTA) B2^T
+// DELTA = -1: forward, the previous row, m(r) = 0 at a window's first row.
+// DELTA = +1: dX, the next row, m(r) = 0 at a window's last row.
+// The A tile is the block's rows plus HALO rows on the partner's side, so the
+// partner of LDS row m is LDS row m + DELTA; a lane whose output row is masked
+// zeroes its partner fragment, and both products go to one accumulator tile.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN, int BK>
+struct ShiftCfg {
+  static constexpr int NS = 2;                   // pipeline stages
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int NW = WM * WN;
+  static constexpr int HALO = 8;                 // one 1 KB DMA block of rows at BK = 64
+  static constexpr int AR = BM + HALO;           // staged A rows
+  static constexpr int TM = BM / (32 * WM);      // 32-row blocks per wave
+  static constexpr int TN = BN / (32 * WN);      // 32-column blocks per wave
+  static constexpr int A_ELEMS = AR * BK;
+  static constexpr int B_ELEMS = BN * BK;
+  static constexpr int STAGE = A_ELEMS + 2 * B_ELEMS;
+  static constexpr int LDO = BN + 8;
+  static constexpr int LDS_ELEMS = (NS * STAGE > BM * LDO) ? NS * STAGE : BM * LDO;
+  static constexpr int A_BLOCKS = A_ELEMS * 2 / 1024;
+  static constexpr int A_DMA = (A_BLOCKS + NW - 1) / NW;   // per wave; the last may idle
+  static constexpr int B_DMA = B_ELEMS * 2 / 1024 / NW;
+  static constexpr int O_IT = BM * (BN / 8) / NT;
+  static_assert(A_BLOCKS * 1024 == A_ELEMS * 2 && B_DMA * NW * 1024 == B_ELEMS * 2, "");
+  static_assert(TM >= 1 && TN >= 1 && O_IT * NT == BM * (BN / 8), "");
+};
+
+template <int BM, int BN, int WM, int WN, int BK, int DELTA, bool TRANS_B>
+__global__ __launch_bounds__(64 * WM * WN) void shift_bf16_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
+    bf16* __restrict__ out, int rows, int width, int n) {
+  using C = ShiftCfg<BM, BN, WM, WN, BK>;
+  static_assert(DELTA == -1 || DELTA == 1, "");
+  constexpr int RB = BN * 2;
+  constexpr int OFF0 = DELTA < 0 ? C::HALO : 0;   // LDS row of the block's first row
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WM, wn = wave / WM;
+  const int tiles_n = width / BN;
+  const int tiles_m = (rows + BM - 1) / BM;
+  const int tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  const int r0 = (tile / tiles_n) * BM;
+  const int n0 = (tile % tiles_n) * BN;
+
+  // DMA sources of this lane at k-slice 0; rows outside the tensor read a
+  // valid row whose products are masked or never stored.
+  const bf16* a_src[C::A_DMA];
+#pragma unroll
+  for (int j = 0; j < C::A_DMA; j++) {
+    const int b = min(j * C::NW + wave, C::A_BLOCKS - 1);
+    const int o = b * 1024 + 16 * lane;
+    const int m = o / (2 * BK);
+    const int ch = (swz<BK>(m, (o % (2 * BK)) / 16) - m * BK) / 8;
+    const int r = min(max(r0 - OFF0 + m, 0), rows - 1);
+    a_src[j] = A + (size_t)r * width + ch * 8;
+  }
+  size_t b_src[C::B_DMA];
+#pragma unroll
+  for (int j = 0; j < C::B_DMA; j++) {
+    const int b = j * C::NW + wave;
+    if constexpr (TRANS_B) {
+      int kr, col;
+      tr_dma_coord<RB>(b, lane, &kr, &col);
+      b_src[j] = (size_t)kr * width + n0 + col;
+    } else {
+      const int o = b * 1024 + 16 * lane;
+      const int nr = o / (2 * BK);
+      const int ch = (swz<BK>(nr, (o % (2 * BK)) / 16) - nr * BK) / 8;
+      b_src[j] = (size_t)(n0 + nr) * width + ch * 8;
+    }
+  }
+  const size_t b_step = TRANS_B ? (size_t)BK * width : BK;
+  auto issue = [&](int kt, int stage) {
+    bf16* sA = smem + stage * C::STAGE;
+    bf16* sB1 = sA + C::A_ELEMS;
+    bf16* sB2 = sB1 + C::B_ELEMS;
+#pragma unroll
+    for (int j = 0; j < C::A_DMA; j++)
+      if (j * C::NW + wave < C::A_BLOCKS)   // wave-uniform
+        dma16(a_src[j] + kt * BK, sA + (j * C::NW + wave) * 512);
+#pragma unroll
+    for (int j = 0; j < C::B_DMA; j++) {
+      dma16(B1 + b_src[j] + kt * b_step, sB1 + (j * C::NW + wave) * 512);
+      dma16(B2 + b_src[j] + kt * b_step, sB2 + (j * C::NW + wave) * 512);
+    }
+  };
+
+  // partner mask of this lane's output row in each 32-row block
+  bool keep[C::TM];
+#pragma unroll
+  for (int t = 0; t < C::TM; t++) {
+    const int pos = (r0 + (wm * C::TM + t) * 32 + (lane & 31)) & (n - 1);
+    keep[t] = DELTA < 0 ? pos != 0 : pos != n - 1;
+  }
+
+  f32x16 acc[C::TM][C::TN];
+#pragma unroll
+  for (int t = 0; t < C::TM; t++)
+#pragma unroll
+    for (int u = 0; u < C::TN; u++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) acc[t][u][e] = 0.f;
+
+  struct Frags { bf16x8 as[C::TM], ap[C::TM], b1[C::TN], b2[C::TN]; };
+  auto load_frags = [&](Frags& f, const bf16* sA, int kk) {
+    const bf16* sB1 = sA + C::A_ELEMS;
+    const bf16* sB2 = sB1 + C::B_ELEMS;
+    const int ch = kk * 2 + (lane >> 5);
+#pragma unroll
+    for (int t = 0; t < C::TM; t++) {
+      const int m = OFF0 + (wm * C::TM + t) * 32 + (lane & 31);
+      f.as[t] = *(const bf16x8*)(sA + swz<BK>(m, ch));
+      f.ap[t] = *(const bf16x8*)(sA + swz<BK>(m + DELTA, ch));
+    }
+#pragma unroll
+    for (int u = 0; u < C::TN; u++) {
+      const int nb = (wn * C::TN + u) * 32;
+      if constexpr (TRANS_B) {
+        f.b1[u] = tr_frag<RB>(sB1, kk * 16, nb, lane);
+        f.b2[u] = tr_frag<RB>(sB2, kk * 16, nb, lane);
+      } else {
+        f.b1[u] = *(const bf16x8*)(sB1 + swz<BK>(nb + (lane & 31), ch));
+        f.b2[u] = *(const bf16x8*)(sB2 + swz<BK>(nb + (lane & 31), ch));
+      }
+    }
+  };
+  // transposed products (weights as the MFMA A operand): lane l owns output
+  // row l % 32 of each block and 16 of its columns
+  auto mma = [&](const Frags& f) {
+    const bf16x8 zero = {};
+#pragma unroll
+    for (int t = 0; t < C::TM; t++)
+#pragma unroll
+      for (int u = 0; u < C::TN; u++) acc[t][u] = mfma32(f.b1[u], f.as[t], acc[t][u]);
+#pragma unroll
+    for (int t = 0; t < C::TM; t++) {
+      const bf16x8 ap = keep[t] ? f.ap[t] : zero;
+#pragma unroll
+      for (int u = 0; u < C::TN; u++) acc[t][u] = mfma32(f.b2[u], ap, acc[t][u]);
+    }
+  };
+
+  constexpr int KK = BK / 16;
+  constexpr int NMFMA = 2 * C::TM * C::TN;
+  constexpr int NDS = 2 * C::TM + 2 * C::TN * (TRANS_B ? 2 : 1);
+  const int nk = width / BK;
+  issue(0, 0);
+  Frags f[2];
+  for (int kt = 0; kt < nk; kt++) {
+    wait_dma();
+    __syncthreads();  // stage kt visible to all waves; buffer (kt-1) % 2 free
+    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+    const bf16* sA = smem + (kt & 1) * C::STAGE;
+    load_frags(f[0], sA, 0);
+#pragma unroll
+    for (int kk = 0; kk < KK; kk++) {
+      if (kk + 1 < KK) {
+        load_frags(f[(kk + 1) & 1], sA, kk + 1);
+        mma(f[kk & 1]);
+        interleave_front<NMFMA, NDS>();
+      } else {
+        mma(f[kk & 1]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __syncthreads();  // every wave done with the stage buffers
+
+  bf16* sO = smem;
+#pragma unroll
+  for (int t = 0; t < C::TM; t++)
+#pragma unroll
+    for (int u = 0; u < C::TN; u++) {
+      const int m = (wm * C::TM + t) * 32 + (lane & 31);
+      const int col = (wn * C::TN + u) * 32 + 4 * (lane >> 5);
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        const bf16x4 v = {to_bf16(acc[t][u][4 * g]), to_bf16(acc[t][u][4 * g + 1]),
+                          to_bf16(acc[t][u][4 * g + 2]), to_bf16(acc[t][u][4 * g + 3])};
+        *(bf16x4*)(sO + m * C::LDO + col + 8 * g) = v;
+      }
+    }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < C::O_IT; j++) {
+    const int idx = tid + C::NT * j;
+    const int m = idx / (BN / 8), ch = idx % (BN / 8);
+    if (r0 + m >= rows) continue;
+    *(u32x4*)(out + (size_t)(r0 + m) * width + n0 + ch * 8) =
+        *(const u32x4*)(sO + m * C::LDO + ch * 8);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradients, split over rows.  Block (tile, slot) computes the BO x BC
 // tile of dW_self and dW_off over the row pairs of its slot:
 //   dW_self += dY_L^T X_L + dY_U^T X_U
@@ -246,6 +445,8 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 // A K-step stages KP pairs = 2*KP rows of dY and X in LDS in their natural
 // layout (slots 0..KP-1 the lower rows, KP..2KP-1 their partners); both MFMA
 // operands are read transposed, the row (slot) index being the contraction.
+// The local layer (LINK_NEAR) uses the same machinery with pairs (r - 1, r):
+//   dW_self += dY_U^T X_U,  dW_off += dY_U^T X_L.
 //
 // A block is two groups of WO x WC waves (two waves per SIMD): the groups walk
 // the two halves of the block's row range side by side, each with its own
@@ -256,6 +457,15 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
 // ---------------------------------------------------------------------------
 constexpr int KP = 32;
 constexpr int SLOTS = 2 * KP;
+
+// Link of a weight-gradient launch.  Hypercube layers: K runs over row pairs
+// (lower row, upper row = lower + 2^d).  Local layer: K runs over rows r, the
+// "lower" slot holding row r - 1 (zero at a window's first row) and the "upper"
+// slot row r; only the upper slots' dY is used.
+constexpr int LINK_CAUSAL = 0, LINK_BIDIR = 1, LINK_NEAR = 2;
+
+// 16 zero bytes in global memory: the DMA source of masked slots.
+__device__ __attribute__((aligned(16))) bf16 g_zero16[8];
 
 template <int BO, int BC, int WO, int WC>
 struct DwCfg {
@@ -275,10 +485,11 @@ struct DwCfg {
   static_assert((size_t)NW * ACC * 64 * 4 <= LDS, "hand-over fits in the stage buffers");
 };
 
-template <int BO, int BC, int WO, int WC, bool BIDIR>
+template <int BO, int BC, int WO, int WC, int LINK>
 __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
     const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
-    int pairs, int width, int d, int pairs_per_group) {
+    int pairs, int width, int d, int n, int pairs_per_group) {
+  constexpr bool BIDIR = LINK == LINK_BIDIR, NEAR = LINK == LINK_NEAR;
   using C = DwCfg<BO, BC, WO, WC>;
   constexpr int RBG = BO * 2, RBX = BC * 2;
   extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
@@ -295,7 +506,7 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
   const int tile = lin % tiles;
   const int split = lin / tiles;
   const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
-  const int s = 1 << d;
+  const int s = NEAR ? 0 : 1 << d;
   const int pbeg = (2 * split + group) * pairs_per_group;
   const int pend = min(pairs, pbeg + pairs_per_group);   // may be <= pbeg: all zero-filled
 
@@ -307,18 +518,27 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
   for (int j = 0; j < C::X_DMA; j++) tr_dma_coord<RBX>(j * C::NW + wave, lane, &x_slot[j], &x_col[j]);
 
   auto row_of = [&](int p0, int slot) {
+    if constexpr (NEAR) return p0 + (slot % KP) - (slot < KP ? 1 : 0);
     return lower_row(p0 + (slot % KP), d) + (slot >= KP ? s : 0);
   };
+  // Local layer: a lower slot is zero when its row r = p0 + slot starts a
+  // window (no predecessor); dY's lower slots are never read.
+  auto x_zero = [&](int p0, int slot) {
+    return NEAR && slot < KP && ((p0 + slot) & (n - 1)) == 0;
+  };
+  auto g_zero = [&](int slot) { return NEAR && slot < KP; };
   // Whole K-step: every slot valid, straight DMA.
   auto issue = [&](int p0, int stage) {
     bf16* sG = smem + stage * C::STAGE;
     bf16* sX = sG + C::G_ELEMS;
 #pragma unroll
     for (int j = 0; j < C::G_DMA; j++)
-      dma16(dY + (size_t)row_of(p0, g_slot[j]) * width + o0 + g_col[j], sG + (j * C::NW + wave) * 512);
+      dma16(g_zero(g_slot[j]) ? g_zero16 : dY + (size_t)row_of(p0, g_slot[j]) * width + o0 + g_col[j],
+            sG + (j * C::NW + wave) * 512);
 #pragma unroll
     for (int j = 0; j < C::X_DMA; j++)
-      dma16(X + (size_t)row_of(p0, x_slot[j]) * width + c0 + x_col[j], sX + (j * C::NW + wave) * 512);
+      dma16(x_zero(p0, x_slot[j]) ? g_zero16 : X + (size_t)row_of(p0, x_slot[j]) * width + c0 + x_col[j],
+            sX + (j * C::NW + wave) * 512);
   };
   // Ragged last K-step: slots past the end of the split are zero-filled.
   auto fill_tail = [&](int p0, int stage) {
@@ -327,14 +547,14 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
 #pragma unroll
     for (int j = 0; j < C::G_DMA; j++) {
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (p0 + (g_slot[j] % KP) < pend)
+      if (p0 + (g_slot[j] % KP) < pend && !g_zero(g_slot[j]))
         v = *(const u32x4*)(dY + (size_t)row_of(p0, g_slot[j]) * width + o0 + g_col[j]);
       *(u32x4*)(sG + (j * C::NW + wave) * 512 + lane * 8) = v;
     }
 #pragma unroll
     for (int j = 0; j < C::X_DMA; j++) {
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (p0 + (x_slot[j] % KP) < pend)
+      if (p0 + (x_slot[j] % KP) < pend && !x_zero(p0, x_slot[j]))
         v = *(const u32x4*)(X + (size_t)row_of(p0, x_slot[j]) * width + c0 + x_col[j]);
       *(u32x4*)(sX + (j * C::NW + wave) * 512 + lane * 8) = v;
     }
@@ -358,7 +578,7 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
 #pragma unroll
     for (int a = 0; a < C::TO; a++) {
       const int ob = (wo * C::TO + a) * 32;
-      f.gL[a] = tr_frag<RBG>(sG, kk * 16, ob, lane);
+      if constexpr (!NEAR) f.gL[a] = tr_frag<RBG>(sG, kk * 16, ob, lane);
       f.gU[a] = tr_frag<RBG>(sG, KP + kk * 16, ob, lane);
     }
 #pragma unroll
@@ -369,6 +589,16 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
     }
   };
   auto mma = [&](const Frags& f) {
+    if constexpr (NEAR) {
+#pragma unroll
+      for (int a = 0; a < C::TO; a++)
+#pragma unroll
+        for (int b = 0; b < C::TC; b++) {
+          accS[a][b] = mfma32(f.gU[a], f.xU[b], accS[a][b]);
+          accO[a][b] = mfma32(f.gU[a], f.xL[b], accO[a][b]);
+        }
+      return;
+    }
 #pragma unroll
     for (int a = 0; a < C::TO; a++)
 #pragma unroll
@@ -385,8 +615,8 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
       }
   };
 
-  constexpr int NMFMA = C::TO * C::TC * (3 + (BIDIR ? 1 : 0));
-  constexpr int NDS = 4 * (C::TO + C::TC);   // two tr reads per fragment
+  constexpr int NMFMA = C::TO * C::TC * (NEAR ? 2 : 3 + (BIDIR ? 1 : 0));
+  constexpr int NDS = 2 * ((NEAR ? 1 : 2) * C::TO + 2 * C::TC);   // two tr reads per fragment
   // the same step count in both groups (their barriers are shared); steps past
   // a group's range are zero-filled
   const int nsteps = pairs_per_group / KP;
@@ -499,6 +729,29 @@ hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, 
   return hipGetLastError();
 }
 
+template <int BN, int WM, int WN, int DELTA, bool TRANS_B>
+hipError_t shift_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                        int width, int n, hipStream_t st) {
+  constexpr int BM = 256;
+  using C = ShiftCfg<BM, BN, WM, WN, MIX_BK>;
+  const int blocks = ((rows + BM - 1) / BM) * (width / BN);
+  const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
+  auto k = shift_bf16_kernel<BM, BN, WM, WN, MIX_BK, DELTA, TRANS_B>;
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return attr;
+  k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, rows, width, n);
+  return hipGetLastError();
+}
+
+template <int DELTA, bool TRANS_B>
+hipError_t shift_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                          int width, int n, hipStream_t st) {
+  if (width % 128 == 0)
+    return shift_launch<128, 2, 2, DELTA, TRANS_B>(A, B1, B2, out, rows, width, n, st);
+  return shift_launch<64, 4, 1, DELTA, TRANS_B>(A, B1, B2, out, rows, width, n, st);
+}
+
 template <bool TRANS_B>
 hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
                         int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
@@ -539,8 +792,7 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeArgs a) {
 // Split-K plan: about one block per CU, each block's row range two groups of
 // whole K-steps.  Returns the number of partial slots (blocks per tile);
 // *ppg gets the pairs per group.
-int dw_plan(int rows, int width, int* ppg) {
-  const int pairs = rows / 2;
+int dw_plan(int pairs, int width, int* ppg) {
   const int bo = width % DW_BO == 0 ? DW_BO : 64;
   const int tiles = (width / bo) * (width / bo);
   const int ksteps = (pairs + KP - 1) / KP;
@@ -553,20 +805,21 @@ int dw_plan(int rows, int width, int* ppg) {
 
 template <int BO, int BC, int WO, int WC>
 hipError_t dw_launch(const bf16* X, const bf16* dY, float* partial, int pairs, int width, int d,
-                     int bidir, int splits, int pps, hipStream_t st) {
+                     int n, int link, int splits, int pps, hipStream_t st) {
   using C = DwCfg<BO, BC, WO, WC>;
   const int blocks = (width / BO) * (width / BC) * splits;
   const size_t lds = C::LDS;
-#define HCMIX_DW(BIDIR)                                                                     \
+#define HCMIX_DW(LINK)                                                                      \
   {                                                                                         \
-    auto k = dw_bf16_kernel<BO, BC, WO, WC, BIDIR>;                                         \
+    auto k = dw_bf16_kernel<BO, BC, WO, WC, LINK>;                                          \
     static const hipError_t attr = hipFuncSetAttribute(                                     \
         (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
     if (attr != hipSuccess) return attr;                                                    \
-    k<<<blocks, C::NT, lds, st>>>(X, dY, partial, pairs, width, d, pps);                    \
+    k<<<blocks, C::NT, lds, st>>>(X, dY, partial, pairs, width, d, n, pps);                 \
   }
-  if (bidir) HCMIX_DW(true)
-  else HCMIX_DW(false)
+  if (link == LINK_NEAR) HCMIX_DW(LINK_NEAR)
+  else if (link == LINK_BIDIR) HCMIX_DW(LINK_BIDIR)
+  else HCMIX_DW(LINK_CAUSAL)
 #undef HCMIX_DW
   return hipGetLastError();
 }
@@ -587,22 +840,37 @@ hipError_t launch_transpose_bf16(const TransposeArgs& a, int count, hipStream_t 
   return hipGetLastError();
 }
 
+hipError_t launch_shift_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
+                             int width, int n, int delta, bool transpose_b, hipStream_t st) {
+  if (delta < 0)
+    return transpose_b ? shift_dispatch<-1, true>(A, B1, B2, out, rows, width, n, st)
+                       : shift_dispatch<-1, false>(A, B1, B2, out, rows, width, n, st);
+  return transpose_b ? shift_dispatch<1, true>(A, B1, B2, out, rows, width, n, st)
+                     : shift_dispatch<1, false>(A, B1, B2, out, rows, width, n, st);
+}
+
 int dw_bf16_splits(int rows, int width) {
-  int pps;
-  return dw_plan(rows, width, &pps);
+  // the partial slots of either kind of layer (pairs for hypercube layers,
+  // rows for the local layer), so one workspace size serves both
+  int ppg;
+  const int a = dw_plan(rows / 2, width, &ppg);
+  const int b = dw_plan(rows, width, &ppg);
+  return a > b ? a : b;
 }
 
 hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* dws, float* dwo,
-                          int rows, int width, int d, int bidir, int accumulate,
+                          int rows, int width, int d, int n, int bidir, int accumulate,
                           hipStream_t st) {
-  const int pairs = rows / 2;
-  int pps;
-  const int splits = dw_plan(rows, width, &pps);
+  const bool near = d < 0;
+  const int units = near ? rows : rows / 2;
+  const int link = near ? LINK_NEAR : bidir ? LINK_BIDIR : LINK_CAUSAL;
+  int ppg;
+  const int splits = dw_plan(units, width, &ppg);
   hipError_t e;
   if (width % DW_BO == 0)
-    e = dw_launch<DW_BO, DW_BC, 2, 2>(X, dY, partial, pairs, width, d, bidir, splits, pps, st);
+    e = dw_launch<DW_BO, DW_BC, 2, 2>(X, dY, partial, units, width, d, n, link, splits, ppg, st);
   else
-    e = dw_launch<64, 64, 2, 2>(X, dY, partial, pairs, width, d, bidir, splits, pps, st);
+    e = dw_launch<64, 64, 2, 2>(X, dY, partial, units, width, d, n, link, splits, ppg, st);
   if (e != hipSuccess) return e;
   const size_t ww = (size_t)width * width;
   int blocks = (int)((2 * ww / 4 + 255) / 256);

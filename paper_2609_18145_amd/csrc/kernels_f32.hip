@@ -12,11 +12,15 @@ constexpr int T = 64;    // output tile edge
 constexpr int KC = 16;   // contraction chunk
 constexpr int NT = 256;  // threads per block: 16 x 16, 4 x 4 outputs each
 
-// out[r][j] = sum_k A[r][k] W1(j,k) + m(r) sum_k A[r^s][k] W2(j,k)
+// out[r][j] = sum_k A[r][k] W1(j,k) + m(r) sum_k A[p(r)][k] W2(j,k)
+// Hypercube layer (d >= 0): p(r) = r ^ 2^d, m(r) = partner_upper / partner_lower
+// by bit d of r.  Local layer (d < 0): p(r) = r + shift with shift = -1
+// (forward; m = 0 at a window's first row) or +1 (dX; m = 0 at its last row).
 template <bool TRANSPOSE_W>
 __global__ __launch_bounds__(NT) void mix_f32_kernel(
     const float* __restrict__ A, const float* __restrict__ W1, const float* __restrict__ W2,
-    float* __restrict__ out, int rows, int width, int d, int partner_lower, int partner_upper) {
+    float* __restrict__ out, int rows, int width, int d, int partner_lower, int partner_upper,
+    int n, int shift) {
   __shared__ float sA[KC][T + 1];
   __shared__ float sP[KC][T + 1];
   __shared__ float sW1[KC][T + 1];
@@ -24,7 +28,7 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
   const int tid = threadIdx.x;
   const int tx = tid % 16, ty = tid / 16;
   const int r0 = blockIdx.x * T, j0 = blockIdx.y * T;
-  const int s = 1 << d;
+  const int s = d >= 0 ? 1 << d : 0;
   float acc[4][4] = {};
 
   for (int k0 = 0; k0 < width; k0 += KC) {
@@ -37,8 +41,16 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
         float a = 0.f, p = 0.f;
         if (r < rows && k < width) {
           a = A[(size_t)r * width + k];
-          const int take = ((r >> d) & 1) ? partner_upper : partner_lower;
-          if (take) p = A[(size_t)(r ^ s) * width + k];
+          int take, pr;
+          if (d >= 0) {
+            take = ((r >> d) & 1) ? partner_upper : partner_lower;
+            pr = r ^ s;
+          } else {
+            const int pos = r & (n - 1);
+            take = shift < 0 ? pos != 0 : pos != n - 1;
+            pr = r + shift;
+          }
+          if (take) p = A[(size_t)pr * width + k];
         }
         sA[kk][m] = a;
         sP[kk][m] = p;
@@ -89,18 +101,20 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
   }
 }
 
-// dws[o][c] (+)= sum_r dY[r][o] X[r][c];  dwo[o][c] (+)= sum_r m(r) dY[r][o] X[r^s][c]
-// One block per 64 x 64 output tile walks every row in a fixed order.
+// dws[o][c] (+)= sum_r dY[r][o] X[r][c];  dwo[o][c] (+)= sum_r m(r) dY[r][o] X[p(r)][c]
+// with p(r) = r ^ 2^d (hypercube layer) or r - 1 (local layer, d < 0; m = 0 at
+// a window's first row).  One block per 64 x 64 output tile walks every row in
+// a fixed order.
 __global__ __launch_bounds__(NT) void dw_f32_kernel(
     const float* __restrict__ X, const float* __restrict__ dY, float* __restrict__ dws,
-    float* __restrict__ dwo, int rows, int width, int d, int bidir, int accumulate) {
+    float* __restrict__ dwo, int rows, int width, int d, int n, int bidir, int accumulate) {
   __shared__ float sG[KC][T + 1];
   __shared__ float sX[KC][T + 1];
   __shared__ float sXP[KC][T + 1];
   const int tid = threadIdx.x;
   const int tx = tid % 16, ty = tid / 16;
   const int o0 = blockIdx.y * T, c0 = blockIdx.x * T;
-  const int s = 1 << d;
+  const int s = d >= 0 ? 1 << d : 0;
   float accS[4][4] = {}, accO[4][4] = {};
 
   for (int rb = 0; rb < rows; rb += KC) {
@@ -113,7 +127,11 @@ __global__ __launch_bounds__(NT) void dw_f32_kernel(
         if (o0 + j < width) g = dY[(size_t)r * width + o0 + j];
         if (c0 + j < width) {
           xv = X[(size_t)r * width + c0 + j];
-          if (bidir || ((r >> d) & 1)) xp = X[(size_t)(r ^ s) * width + c0 + j];
+          if (d < 0) {
+            if (r & (n - 1)) xp = X[(size_t)(r - 1) * width + c0 + j];
+          } else if (bidir || ((r >> d) & 1)) {
+            xp = X[(size_t)(r ^ s) * width + c0 + j];
+          }
         }
       }
       sG[kk][j] = g;
@@ -158,22 +176,22 @@ __global__ __launch_bounds__(NT) void dw_f32_kernel(
 }  // namespace
 
 hipError_t launch_mix_f32(const float* A, const float* W1, const float* W2, float* out, int rows,
-                          int width, int d, int partner_lower, int partner_upper,
-                          bool transpose_w, hipStream_t st) {
+                          int width, int d, int partner_lower, int partner_upper, int n,
+                          int shift, bool transpose_w, hipStream_t st) {
   dim3 grid((rows + T - 1) / T, (width + T - 1) / T);
   if (transpose_w)
     mix_f32_kernel<true><<<grid, NT, 0, st>>>(A, W1, W2, out, rows, width, d, partner_lower,
-                                              partner_upper);
+                                              partner_upper, n, shift);
   else
     mix_f32_kernel<false><<<grid, NT, 0, st>>>(A, W1, W2, out, rows, width, d, partner_lower,
-                                               partner_upper);
+                                               partner_upper, n, shift);
   return hipGetLastError();
 }
 
 hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo, int rows,
-                         int width, int d, int bidir, int accumulate, hipStream_t st) {
+                         int width, int d, int n, int bidir, int accumulate, hipStream_t st) {
   dim3 grid((width + T - 1) / T, (width + T - 1) / T);
-  dw_f32_kernel<<<grid, NT, 0, st>>>(X, dY, dws, dwo, rows, width, d, bidir, accumulate);
+  dw_f32_kernel<<<grid, NT, 0, st>>>(X, dY, dws, dwo, rows, width, d, n, bidir, accumulate);
   return hipGetLastError();
 }
 

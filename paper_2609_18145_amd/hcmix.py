@@ -20,6 +20,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhcmix.so
 HCMIX_OK, HCMIX_ERR_INVALID_VALUE, HCMIX_ERR_UNSUPPORTED, HCMIX_ERR_HIP = 0, 1, 2, 3
 HCMIX_F32, HCMIX_BF16 = 0, 1
 HCMIX_BIDIR, HCMIX_CAUSAL = 0, 1
+# layer code of the local layer (Eq. (1) with jump 1; causal only); codes >= 0
+# are hypercube layers
+LAYER_NEAR = -1
 
 # every symbol declared in include/hcmix.h
 EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_forward",

@@ -71,6 +71,9 @@ UNSUPPORTED = hcmix.HCMIX_ERR_UNSUPPORTED
     (dict(n=0), INVALID), (dict(n=1), INVALID), (dict(n=12), INVALID),
     (dict(batch=0), INVALID), (dict(batch=-3), INVALID), (dict(width=0), INVALID),
     (dict(layer=-1), INVALID), (dict(mode=2), INVALID), (dict(dtype=7), INVALID),
+    (dict(layer=-1, mode=0), INVALID),                # the local layer is causal only
+    (dict(layer=-2, mode=1), INVALID), (dict(layer=-1, mode=1, n=12), INVALID),
+    (dict(layer=-1, mode=1, width=96), UNSUPPORTED),  # a valid local layer, unsupported width
     (dict(x=None), INVALID), (dict(ws=None), INVALID), (dict(wo=None), INVALID),
     (dict(y=None), INVALID), (dict(y=P[0]), INVALID),                      # y aliases x
     (dict(batch=1 << 40), INVALID),                                       # too many rows
@@ -91,6 +94,7 @@ def test_forward_aliasing_checks_whole_extent():
 
 @pytest.mark.parametrize("kw,code", [
     (dict(n=3), INVALID), (dict(layer=-2), INVALID), (dict(dy=None), INVALID),
+    (dict(layer=-1, mode=0), INVALID), (dict(layer=-1, mode=1, dx=P[3]), INVALID),
     (dict(dx=None), INVALID), (dict(dws=None), INVALID), (dict(dwo=None), INVALID),
     (dict(dx=P[3]), INVALID),                         # dx aliases dy
     (dict(dws=FP[6]), INVALID),                       # dw_self aliases dw_off
