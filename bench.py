@@ -35,10 +35,16 @@ WORKLOADS = {
     "long4096": "window n=4096, width 1024, batch 8, 24 rotated causal layers, bf16, fwd+bwd",
     "hybrid": ("window n=256, width 512, batch 64, 16 rotated causal layers with 2 causal "
                "softmax attention layers (8 heads x 64) at slots 3 and 9 of 18, bf16, fwd+bwd"),
+    "hy256": ("window n=256, width 512, batch 64, the hybrid256 schedule: 8 local layers, 6 "
+              "causal jumps 128..1 and 2 causal softmax attention layers (8 heads x 64), 16 "
+              "layers, bf16, fwd+bwd"),
 }
 # hybrid: positions of the attention layers in the 18-layer list
 HYBRID_ATTN_SLOTS = (3, 9)
 HYBRID_LAYERS = 18
+# the paper's window-256 hybrid schedule string (Appendix A), by layer name
+HY256 = ("near jump128 near attn near jump32 near jump16 near attn near jump4 near jump2 "
+         "near jump1").split()
 
 
 def algorithmic_work(batch, n, width, layers, causal):
@@ -164,7 +170,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
-    if args.workload == "hybrid":
+    if args.workload in ("hybrid", "hy256"):
         return run_hybrid(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
     cfg = dict(inputs.PRESETS[args.workload], **over)
@@ -247,9 +253,12 @@ def main():
 
 
 def run_hybrid(args, torch, hcmix, inputs, dev):
-    """The lm256 stack with two causal softmax attention layers inserted (18
-    layers, attention at slots 3 and 9; the rotated layers keep d = their index
-    among the rotated layers mod 8).  Attention is harness code (PyTorch: QKV
+    """Sparse layers with two causal softmax attention layers among them:
+    "hybrid", the lm256 stack with attention inserted at slots 3 and 9 of 18
+    (the rotated layers keep d = their index among the rotated layers mod 8),
+    or "hy256", the paper's window-256 hybrid schedule string (local layers,
+    one causal jump per scale, attention at two of sixteen; weights are the
+    lm256 workload's first 14).  Attention is harness code (PyTorch: QKV
     projection, scaled-dot-product attention, output projection); the sparse
     segments are hcmix stack calls.  Forward and backward are chained by hand
     so that every segment is timed with HIP events on one stream; the line
@@ -259,7 +268,7 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     if args.batch > 0:
         cfg["batch"] = args.batch
     s = inputs.make_preset("lm256", **({"batch": args.batch} if args.batch > 0 else {}))
-    B, n, w, Ls = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"]
+    B, n, w = cfg["batch"], cfg["n"], cfg["width"]
     dt = torch.bfloat16
     heads, hd = 8, 64
     assert heads * hd == w
@@ -273,20 +282,39 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     gen = torch.Generator(device="cpu").manual_seed(1)
     attn_w = [((torch.randn(3 * w, w, generator=gen) / w ** 0.5).to(dt).to(dev),
                (torch.randn(w, w, generator=gen) / w ** 0.5).to(dt).to(dev))
-              for _ in HYBRID_ATTN_SLOTS]
-    # segments of consecutive rotated layers between the attention slots
-    segs, rot = [], 0
-    cur = []
-    for slot in range(HYBRID_LAYERS):
-        if slot in HYBRID_ATTN_SLOTS:
+              for _ in range(2)]
+    # the schedule as entries: a layer code, or "attn"
+    if args.workload == "hybrid":
+        sched, rot = [], 0
+        for slot in range(HYBRID_LAYERS):
+            if slot in HYBRID_ATTN_SLOTS:
+                sched.append("attn")
+            else:
+                sched.append(rot)   # rotated: dimension = index among rotated layers mod 8
+                rot += 1
+    else:
+        sched = []
+        for name in HY256:
+            if name == "attn":
+                sched.append("attn")
+            elif name == "near":
+                sched.append(hcmix.LAYER_NEAR)
+            else:
+                sched.append(int(name[len("jump"):]).bit_length() - 1)
+    # segments: runs of sparse layers (weight indices, layer codes) and attention layers
+    segs, cur, nsparse, nattn = [], [], 0, 0
+    for e in sched:
+        if e == "attn":
             segs.append(("sparse", cur))
-            segs.append(("attn", HYBRID_ATTN_SLOTS.index(slot)))
-            cur = []
+            segs.append(("attn", nattn))
+            cur, nattn = [], nattn + 1
         else:
-            cur.append(rot)
-            rot += 1
+            cur.append((nsparse, e))
+            nsparse += 1
     segs.append(("sparse", cur))
-    assert rot == Ls
+    segs = [sg for sg in segs if sg[0] == "attn" or sg[1]]
+    Ls = nsparse
+    assert Ls <= len(ws) and nattn == len(attn_w)
 
     from torch.nn.attention import SDPBackend, sdpa_kernel
     backend = {"name": None}
@@ -330,8 +358,8 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
             e0.record(stream)
             if kind == "sparse":
-                xs = hcmix.stack_forward(x, [ws[l] for l in arg], [wo[l] for l in arg],
-                                         [s.layers[l] for l in arg], True)
+                xs = hcmix.stack_forward(x, [ws[j] for j, _ in arg], [wo[j] for j, _ in arg],
+                                         [c for _, c in arg], True)
                 saved.append(xs)
                 x = xs[-1]
             else:
@@ -351,9 +379,9 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                 L = len(arg)
                 if L not in wsp:
                     wsp[L] = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
-                g, _, _ = hcmix.stack_backward(sv[:L], [ws[l] for l in arg], [wo[l] for l in arg],
-                                               [s.layers[l] for l in arg], g, True,
-                                               workspace=wsp[L])
+                g, _, _ = hcmix.stack_backward(sv[:L], [ws[j] for j, _ in arg],
+                                               [wo[j] for j, _ in arg], [c for _, c in arg], g,
+                                               True, workspace=wsp[L])
             else:
                 xin, out, params = sv
                 grads = torch.autograd.grad(out, [xin, *params], grad_outputs=g)
@@ -385,8 +413,8 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(total / args.steps * 1e3, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"hybrid: {WORKLOADS['hybrid']}", "batch": B, "n": n, "width": w,
-                   "layers": Ls, "attention_layers": len(HYBRID_ATTN_SLOTS), "mode": "causal",
+        "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}", "batch": B, "n": n,
+                   "width": w, "layers": Ls, "attention_layers": nattn, "mode": "causal",
                    "graph": False, "attention_backend": backend["name"]},
         "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
                    "sparse_ms": round(sparse / args.steps * 1e3, 4),
@@ -402,7 +430,7 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
 def cpu_baseline(s, n, w, L, causal, windows):
     """The CPU oracle (plain fp64 loops) on a bounded sample: `windows` windows
     of the same workload through every layer, forward and backward.  With
-    windows == 0 the sample is sized to about 15 s of CPU work from a timed
+    windows == 0 the sample is sized to 10-30 s of CPU work from a timed
     pilot of a few windows; when the whole workload takes less than that, it
     is run repeatedly (the sample then says how many passes)."""
     import oracle
@@ -417,11 +445,14 @@ def cpu_baseline(s, n, w, L, causal, windows):
 
     passes = 1
     if windows <= 0:
+        # a few-window pilot overstates the per-window cost (fewer rows to
+        # spread over the threads), so aim above the 10-30 s band's floor
+        target = 25.0
         pilot = min(B, 4)
         per_window = run(pilot) / pilot
-        windows = max(1, min(B, int(15.0 / max(per_window, 1e-4))))
+        windows = max(1, min(B, int(target / max(per_window, 1e-4))))
         if windows == B:
-            passes = max(1, min(200, int(round(15.0 / max(per_window * B, 1e-4)))))
+            passes = max(1, min(200, int(round(target / max(per_window * B, 1e-4)))))
     dt = sum(run(windows) for _ in range(passes))
     what = (f"{windows} of the workload's {B} windows" if windows < B
             else f"all {B} windows" + (f", {passes} passes" if passes > 1 else ""))
