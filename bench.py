@@ -35,6 +35,8 @@ WORKLOADS = {
     "long4096": "window n=4096, width 1024, batch 8, 24 rotated causal layers, bf16, fwd+bwd",
     "hybrid": ("window n=256, width 512, batch 64, 16 rotated causal layers with 2 causal "
                "softmax attention layers (8 heads x 64) at slots 3 and 9 of 18, bf16, fwd+bwd"),
+    "decode256": ("decode: window n=256, width 512, batch 64, 16 rotated causal layers, bf16; "
+                  "positions 0..255 one step each (all windows, every layer)"),
     "hy256": ("window n=256, width 512, batch 64, the hybrid256 schedule: 8 local layers, 6 "
               "causal jumps 128..1 and 2 causal softmax attention layers (8 heads x 64), 16 "
               "layers, bf16, fwd+bwd"),
@@ -172,6 +174,8 @@ def main():
 
     if args.workload in ("hybrid", "hy256"):
         return run_hybrid(args, torch, hcmix, inputs, dev)
+    if args.workload == "decode256":
+        return run_decode(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
     cfg = dict(inputs.PRESETS[args.workload], **over)
     s = inputs.make_preset(args.workload, **over)
@@ -422,6 +426,81 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                    "sparse_share_of_step": round(sparse / total, 4),
                    "note": "value = sparse positions*layers per second of sparse-layer time; "
                            "eager launches, each segment timed with HIP events"},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def run_decode(args, torch, hcmix, inputs, dev):
+    """Incremental decode at the lm256 shape: one hcmix_decode_step per
+    position, positions 0..n-1 of a window in order (every window of the batch
+    advances one position per step).  A step is one position of all windows
+    through all layers; value = windows * layers * steps / time."""
+    cfg = dict(inputs.PRESETS["lm256"])
+    if args.batch > 0:
+        cfg["batch"] = args.batch
+    s = inputs.make_preset("lm256", **({"batch": args.batch} if args.batch > 0 else {}))
+    B, n, w, L = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"]
+    dt = torch.bfloat16
+    x = torch.from_numpy(s.x).to(dt).to(dev)
+    cols = [x[:, p].contiguous() for p in range(n)]
+    ws = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_self]
+    wo = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_off]
+    cache = hcmix.alloc_decode_cache(B, n, w, L, dt, dev)
+    y = torch.empty(B, w, dtype=dt, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def window(npos):
+        for p in range(npos):
+            hcmix.decode_step(cols[p], ws, wo, s.layers, n, p, cache, out=y)
+
+    window(n)
+    torch.cuda.synchronize()
+    steps = max(args.steps, n)          # whole windows
+    steps = (steps + n - 1) // n * n
+
+    def timed(run):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps // n):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
+
+    t_eager = timed(lambda: window(n))
+    # one graph per position (the position is a launch argument), replayed in order
+    graphs = []
+    if args.graph:
+        side = torch.cuda.Stream(device=dev)
+        with torch.cuda.stream(side):
+            for p in range(n):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    hcmix.decode_step(cols[p], ws, wo, s.layers, n, p, cache, out=y)
+                graphs.append(g)
+        torch.cuda.synchronize()
+
+        def replay():
+            for g in graphs:
+                g.replay()
+        replay()
+        torch.cuda.synchronize()
+        t_graph = timed(replay)
+    t = t_graph if graphs else t_eager
+    out = {
+        "metric": METRIC, "value": round(B * L * steps / t, 1), "unit": UNIT, "n_gpus": 1,
+        "steps": steps, "warmup": n, "ms_per_step": round(t / steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"decode256: {WORKLOADS['decode256']}", "batch": B, "n": n,
+                   "width": w, "layers": L, "mode": "causal", "graph": bool(graphs)},
+        "decode": {"us_per_position": round(t / steps * 1e6, 2),
+                   "us_per_position_eager": round(t_eager / steps * 1e6, 2),
+                   "launches_per_position": L,
+                   "note": "value from one captured graph per position (the position is a "
+                           "launch argument), replayed in order; eager launches beside it"},
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -168,6 +168,38 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
                                   int32_t accumulate, void* workspace, size_t workspace_bytes,
                                   void* stream);
 
+/* ---- Decode: one new position of every window through the whole stack ----
+ *
+ * The causal stack evaluated incrementally (the one-position-at-a-time path
+ * of the paper's deployment paragraph, Section 8): at position `pos` layer l
+ * needs its own input there and, when the position receives, its input at the
+ * partner position (pos - 2^d for a hypercube layer whose bit d of pos is set,
+ * pos - 1 for the local layer), which an earlier step recorded in the cache.
+ *
+ * Cache: caller-owned device memory of hcmix_decode_cache_bytes() bytes,
+ * 256-byte aligned; it holds every layer's input at every position of the
+ * current window ([num_layers][batch][n][width] in dtype), so it is bounded by
+ * the window and never grows.  Positions of a window must be decoded in order
+ * 0, 1, 2, ... (a step reads what earlier steps recorded); starting a new
+ * window is starting again at pos = 0.  The cache's other contents are never
+ * read, so it needs no initialisation.
+ *
+ * x: [batch][width], the stack's input at `pos` for every window; y:
+ * [batch][width], the stack's output there.  layers: host array of layer codes
+ * as for the stacks (hypercube layers or HCMIX_LAYER_NEAR); the stack is
+ * causal.  bf16: width a multiple of 64, 16-byte aligned pointers; fp32: 4-byte
+ * aligned.  Results equal those of hcmix_stack_forward over the window at
+ * position pos, up to the order of floating-point summation.
+ * HCMIX_ERR_INVALID_VALUE also for pos outside [0, n), a short cache, or y or
+ * the cache overlapping an input. */
+size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                int32_t dtype);
+
+hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                               const int32_t* layers, int32_t dtype, int64_t pos, const void* x,
+                               const void* const* w_self, const void* const* w_off, void* cache,
+                               size_t cache_bytes, void* y, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

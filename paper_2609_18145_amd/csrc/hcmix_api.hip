@@ -424,3 +424,89 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
 }
 
 }  // extern "C"
+
+size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers) return 0;
+  if (check_shape(batch, n, width, 0, HCMIX_CAUSAL, dtype) != HCMIX_OK) return 0;
+  return align256((size_t)num_layers * batch * n * width * elem_size(dtype));
+}
+
+hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                               const int32_t* layers, int32_t dtype, int64_t pos, const void* x,
+                               const void* const* w_self, const void* const* w_off, void* cache,
+                               size_t cache_bytes, void* y, void* stream) {
+  if (!layers || !x || !w_self || !w_off || !cache || !y) return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], HCMIX_CAUSAL, dtype);
+    if (st != HCMIX_OK) return st;
+    if (!w_self[l] || !w_off[l]) return HCMIX_ERR_INVALID_VALUE;
+  }
+  if (pos < 0 || pos >= n) return HCMIX_ERR_INVALID_VALUE;
+  const size_t need = hcmix_decode_cache_bytes(batch, n, width, num_layers, dtype);
+  if (cache_bytes < need) return HCMIX_ERR_INVALID_VALUE;
+  const size_t es = elem_size(dtype);
+  const size_t row = (size_t)(batch * width) * es, wgt = (size_t)(width * width) * es;
+  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
+  // outputs: y and the cache; inputs: x and every weight
+  const Span outs[2] = {{y, row}, {cache, need}};
+  {
+    const Span ins[1] = {{x, row}};
+    hcmix_status st = check_spans(ins, 1, outs, 2, al);
+    if (st != HCMIX_OK) return st;
+  }
+  for (int l = 0; l < num_layers; l++) {
+    const Span ins[2] = {{w_self[l], wgt}, {w_off[l], wgt}};
+    hcmix_status st = check_spans(ins, 2, outs, 2, al);
+    if (st != HCMIX_OK) return st;
+  }
+  if (!aligned(cache, 256)) return HCMIX_ERR_UNSUPPORTED;
+
+  const int64_t w = width, win = n * width;   // a window's rows in one layer's cache
+  const size_t layer_elems = (size_t)batch * n * width;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  for (int l = 0; l < num_layers && e == hipSuccess; l++) {
+    // partner position of `pos` (causal): the earlier endpoint of the link
+    const int d = hcmix_dim(layers[l], n);
+    int64_t partner = -1;
+    if (d < 0) partner = pos >= 1 ? pos - 1 : -1;
+    else if ((pos >> d) & 1) partner = pos - ((int64_t)1 << d);
+    const bool last = l == num_layers - 1;
+    if (dtype == HCMIX_BF16) {
+      bf16* c = (bf16*)cache;
+      DecodeLayerArgs a = {};
+      a.x_in = l == 0 ? (const bf16*)x : c + l * layer_elems + pos * w;
+      a.in_stride = l == 0 ? w : win;
+      a.x_partner = partner >= 0 ? c + l * layer_elems + partner * w : nullptr;
+      a.partner_stride = win;
+      a.w_self = (const bf16*)w_self[l];
+      a.w_off = (const bf16*)w_off[l];
+      a.out = last ? (bf16*)y : c + (l + 1) * layer_elems + pos * w;
+      a.out_stride = last ? w : win;
+      a.record = l == 0 ? c + pos * w : nullptr;
+      a.rec_stride = win;
+      a.batch = (int)batch;
+      a.width = (int)width;
+      e = launch_decode_bf16(a, s);
+    } else {
+      float* c = (float*)cache;
+      DecodeLayerArgsF32 a = {};
+      a.x_in = l == 0 ? (const float*)x : c + l * layer_elems + pos * w;
+      a.in_stride = l == 0 ? w : win;
+      a.x_partner = partner >= 0 ? c + l * layer_elems + partner * w : nullptr;
+      a.partner_stride = win;
+      a.w_self = (const float*)w_self[l];
+      a.w_off = (const float*)w_off[l];
+      a.out = last ? (float*)y : c + (l + 1) * layer_elems + pos * w;
+      a.out_stride = last ? w : win;
+      a.record = l == 0 ? c + pos * w : nullptr;
+      a.rec_stride = win;
+      a.batch = (int)batch;
+      a.width = (int)width;
+      e = launch_decode_f32(a, s);
+    }
+  }
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}

@@ -107,4 +107,31 @@ hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hi
 hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
                                  bool bidir, hipStream_t st);
 
+// ---- decode step (one position of every window through one layer) ----
+// x_in / x_partner / record / out are row bases of window 0; window b is at
+// + b * stride elements.  x_partner null: the position takes no partner.
+// record (may be null): where the layer's input is written for later positions.
+struct DecodeLayerArgs {
+  const bf16* x_in;
+  const bf16* x_partner;
+  const bf16* w_self;
+  const bf16* w_off;
+  bf16* out;
+  bf16* record;
+  int64_t in_stride, partner_stride, out_stride, rec_stride;
+  int batch, width;
+};
+struct DecodeLayerArgsF32 {
+  const float* x_in;
+  const float* x_partner;
+  const float* w_self;
+  const float* w_off;
+  float* out;
+  float* record;
+  int64_t in_stride, partner_stride, out_stride, rec_stride;
+  int batch, width;
+};
+hipError_t launch_decode_bf16(const DecodeLayerArgs& a, hipStream_t st);   // width % 64 == 0
+hipError_t launch_decode_f32(const DecodeLayerArgsF32& a, hipStream_t st);
+
 }  // namespace hcmix

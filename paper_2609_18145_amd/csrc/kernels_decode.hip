@@ -1,0 +1,105 @@
+// Decode step: one new position `pos` of every window through every layer.
+// All windows are at the same position, so each layer is one small dense
+// product over the batch:
+//   y[b] = W_self x[b] + m(pos) W_off x_partner[b]
+// with the partner's layer input read from the cache.  The cache holds every
+// layer's input at every position of the current window,
+// cache[l][b][p][:] (l < L, p < n); the kernel of layer l reads its input at
+// `pos` (layer 0: from the caller's x, which it also records) and the
+// partner's, and writes its output to cache[l+1][b][pos] (or to y after the
+// last layer), so no launch overwrites anything another block of it reads.
+#include "device_common.h"
+#include "hcmix_internal.h"
+
+namespace hcmix {
+
+namespace {
+
+// bf16: one block per 32 output columns x 32 windows, 4 waves splitting the
+// contraction (self part then partner part) in 16-wide steps, their partial
+// products summed through LDS in wave order.
+__global__ __launch_bounds__(256) void decode_bf16_kernel(DecodeLayerArgs a) {
+  __shared__ f32x16 part[4][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int o0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
+  const int w = a.width;
+  const int b = min(b0 + (lane & 31), a.batch - 1);      // clamped; stores are masked
+  const int half = lane >> 5;
+  const bf16* xin = a.x_in + (size_t)b * a.in_stride;
+  const bf16* xp = a.x_partner ? a.x_partner + (size_t)b * a.partner_stride : nullptr;
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; e++) acc[e] = 0.f;
+  // this wave's 16-wide contraction steps k = wave, wave + 4, ...: the loads of
+  // CH steps are all issued before their MFMAs, so their latencies overlap
+  constexpr int CH = 8;
+  const int ksteps = w / 16;
+  auto part_product = [&](const bf16* W, const bf16* xr) {
+    for (int kb = wave; kb < ksteps; kb += 4 * CH) {
+      bf16x8 wf[CH], xf[CH];
+#pragma unroll
+      for (int j = 0; j < CH; j++) {
+        const int k = kb + 4 * j;
+        const int k0 = (k < ksteps ? k : 0) * 16 + 8 * half;
+        wf[j] = *(const bf16x8*)(W + (size_t)(o0 + (lane & 31)) * w + k0);
+        xf[j] = *(const bf16x8*)(xr + k0);
+      }
+#pragma unroll
+      for (int j = 0; j < CH; j++)
+        if (kb + 4 * j < ksteps) acc = mfma32(wf[j], xf[j], acc);
+    }
+  };
+  part_product(a.w_self, xin);
+  if (xp) part_product(a.w_off, xp);
+  part[wave][lane] = acc;
+  // layer 0 records its input for later positions: this block's 32 columns
+  if (a.record && wave == 0 && b0 + (lane & 31) < a.batch) {
+    const int c = o0 + 16 * half;
+    *(u32x4*)(a.record + (size_t)b * a.rec_stride + c) = *(const u32x4*)(xin + c);
+    *(u32x4*)(a.record + (size_t)b * a.rec_stride + c + 8) = *(const u32x4*)(xin + c + 8);
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  f32x16 s = part[0][lane];
+#pragma unroll
+  for (int v = 1; v < 4; v++) s += part[v][lane];
+  if (b0 + (lane & 31) >= a.batch) return;
+  // C[o][b]: lane l holds window b0 + l%32 and outputs o0 + 8 g + 4 (l/32) + 0..3
+  bf16* dst = a.out + (size_t)b * a.out_stride + o0 + 4 * half;
+#pragma unroll
+  for (int g = 0; g < 4; g++) {
+    const bf16x4 v = {to_bf16(s[4 * g]), to_bf16(s[4 * g + 1]), to_bf16(s[4 * g + 2]),
+                      to_bf16(s[4 * g + 3])};
+    *(bf16x4*)(dst + 8 * g) = v;
+  }
+}
+
+// fp32: one thread per output (window b, column o), plain FMAs.
+__global__ __launch_bounds__(256) void decode_f32_kernel(DecodeLayerArgsF32 a) {
+  const int o = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int b = blockIdx.y * 4 + (threadIdx.x >> 6);
+  if (o >= a.width || b >= a.batch) return;
+  const float* xin = a.x_in + (size_t)b * a.in_stride;
+  float acc = 0.f;
+  for (int c = 0; c < a.width; c++) acc = fmaf(a.w_self[(size_t)o * a.width + c], xin[c], acc);
+  if (a.x_partner) {
+    const float* xp = a.x_partner + (size_t)b * a.partner_stride;
+    for (int c = 0; c < a.width; c++) acc = fmaf(a.w_off[(size_t)o * a.width + c], xp[c], acc);
+  }
+  if (a.record) a.record[(size_t)b * a.rec_stride + o] = xin[o];
+  a.out[(size_t)b * a.out_stride + o] = acc;
+}
+
+}  // namespace
+
+hipError_t launch_decode_bf16(const DecodeLayerArgs& a, hipStream_t st) {
+  decode_bf16_kernel<<<dim3(a.width / 32, (a.batch + 31) / 32), 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_f32(const DecodeLayerArgsF32& a, hipStream_t st) {
+  decode_f32_kernel<<<dim3((a.width + 63) / 64, (a.batch + 3) / 4), 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace hcmix

@@ -27,7 +27,8 @@ LAYER_NEAR = -1
 # every symbol declared in include/hcmix.h
 EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_forward",
            "hcmix_backward_workspace_bytes", "hcmix_backward", "hcmix_stack_forward",
-           "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward")
+           "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward",
+           "hcmix_decode_cache_bytes", "hcmix_decode_step")
 
 _lib = None
 
@@ -71,6 +72,11 @@ def load():
         lib.hcmix_stack_backward.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp, vp, vp,
                                              pp, pp, i32, vp, sz, vp]
         lib.hcmix_stack_backward.restype = i32
+        lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
+        lib.hcmix_decode_cache_bytes.restype = sz
+        lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
+                                          vp]
+        lib.hcmix_decode_step.restype = i32
         _lib = lib
     return _lib
 
@@ -214,6 +220,35 @@ def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dx=None, dws=None, d
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_backward")
     return dx, dws, dwo
+
+
+def decode_cache_bytes(batch, n, width, num_layers, dtype) -> int:
+    code = HCMIX_BF16 if dtype == torch.bfloat16 else HCMIX_F32
+    return load().hcmix_decode_cache_bytes(batch, n, width, num_layers, code)
+
+
+def alloc_decode_cache(batch, n, width, num_layers, dtype, device):
+    """Device memory for hcmix_decode_step: every layer's input at every
+    position of the current window (no initialisation needed)."""
+    return torch.empty(decode_cache_bytes(batch, n, width, num_layers, dtype), dtype=torch.uint8,
+                       device=device)
+
+
+def decode_step(x, w_selfs, w_offs, layers, n, pos, cache, out=None):
+    """Position ``pos`` of every window through the causal stack: x and the
+    result are [batch, width]; positions of a window must come in order."""
+    L = len(layers)
+    _check(x, *w_selfs, *w_offs)
+    batch, width = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _check(x, out)
+    rc = load().hcmix_decode_step(batch, n, width, L, _layers(layers), _dtype_code(x), pos,
+                                  _ptr(x), _ptrs(w_selfs), _ptrs(w_offs), _ptr(cache),
+                                  cache.numel(), _ptr(out), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_decode_step")
+    return out
 
 
 class Stack(torch.autograd.Function):

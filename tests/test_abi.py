@@ -156,3 +156,36 @@ def test_stack_workspace_query():
     assert lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 1, hcmix.HCMIX_BF16) == layer
     assert lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 0, hcmix.HCMIX_BF16) == 0
     assert lib.hcmix_stack_backward_workspace_bytes(2, 16, 32, 1, hcmix.HCMIX_F32) == 0
+
+
+def dec(batch=2, n=16, width=64, L=4, layers=LP, dtype=1, pos=0, x=P[0], ws=None, wo=None,
+        cache=P[3], cb=None, y=P[4]):
+    lib = hcmix.load()
+    ws = ws if ws is not None else PP(P[1], P[1], P[1], P[1])
+    wo = wo if wo is not None else PP(P[2], P[2], P[2], P[2])
+    if cb is None:
+        cb = lib.hcmix_decode_cache_bytes(batch, n, width, L, dtype)
+    return lib.hcmix_decode_step(batch, n, width, L, layers, dtype, pos, x, ws, wo, cache, cb, y,
+                                 None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(pos=-1), INVALID), (dict(pos=16), INVALID), (dict(L=0), INVALID), (dict(n=12), INVALID),
+    (dict(layers=(ctypes.c_int32 * 4)(0, -2, 2, 3)), INVALID),
+    (dict(cb=16), INVALID), (dict(cache=None), INVALID), (dict(x=None), INVALID),
+    (dict(y=P[0]), INVALID),                          # y aliases x
+    (dict(y=P[3]), INVALID),                          # y aliases the cache
+    (dict(cache=P[1]), INVALID),                      # cache aliases a weight
+    (dict(cache=ctypes.c_void_p(0x400010)), UNSUPPORTED),   # cache not 256-aligned
+    (dict(width=96), UNSUPPORTED),
+])
+def test_decode_rejects_bad_arguments(kw, code):
+    assert dec(**kw) == code
+
+
+def test_decode_cache_query():
+    lib = hcmix.load()
+    assert lib.hcmix_decode_cache_bytes(2, 16, 64, 4, hcmix.HCMIX_BF16) == 4 * 2 * 16 * 64 * 2
+    assert lib.hcmix_decode_cache_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16) == 16 * 64 * 256 * 512 * 2
+    assert lib.hcmix_decode_cache_bytes(2, 12, 64, 4, hcmix.HCMIX_BF16) == 0
+    assert lib.hcmix_decode_cache_bytes(2, 16, 64, 0, hcmix.HCMIX_BF16) == 0

@@ -1,0 +1,70 @@
+"""Decode step (hcmix_decode_step): positions of a window decoded one at a
+time must give the causal stack's output at that position, as the oracle's
+full-window forward computes it."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_18145_amd import hcmix, inputs
+from tests.util import TOL, row_rel_err, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    hcmix.load()
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("batch,n,width,dtype,schedule", [
+    (3, 16, 64, "bf16", "rot"), (40, 16, 128, "bf16", "mixa"), (2, 64, 64, "bf16", "rot"),
+    (5, 8, 32, "f32", "rot"), (2, 16, 24, "f32", "mixa"), (33, 32, 512, "bf16", "mixa"),
+])
+def test_decode_every_position_matches_the_stack(batch, n, width, dtype, schedule):
+    layers = (list(range(2 * oracle.log2n(n))) if schedule == "rot"
+              else oracle.schedule_mixa(n))
+    L = len(layers)
+    log(f"decode {batch}x{n}x{width} {dtype} {schedule} L={L}")
+    s = inputs.make_stack(batch=batch, n=n, width=width, num_layers=L, causal=True, dtype=dtype,
+                          seed=41, layers=layers, with_dy=False)
+    want = oracle.stack_forward(s.x, s.w_self, s.w_off, layers, True)[-1]
+    x = to_dev(s.x, dtype)
+    ws = [to_dev(w, dtype) for w in s.w_self]
+    wo = [to_dev(w, dtype) for w in s.w_off]
+    cache = hcmix.alloc_decode_cache(batch, n, width, L, x.dtype, x.device)
+    cache.fill_(0xFF)                      # never-written contents must never be read
+    got = np.zeros_like(want)
+    for pos in range(n):
+        y = hcmix.decode_step(x[:, pos].contiguous(), ws, wo, layers, n, pos, cache)
+        got[:, pos] = to_host(y)
+    torch.cuda.synchronize()
+    err = row_rel_err(got, want)
+    log(f"  row err {err:.2e}")
+    assert err <= TOL[dtype]
+
+
+def test_decode_restarts_at_position_zero():
+    """A second window decoded into the same cache starts over at pos 0."""
+    batch, n, width = 4, 16, 64
+    layers = oracle.schedule_mixa(n)
+    L = len(layers)
+    s1 = inputs.make_stack(batch=batch, n=n, width=width, num_layers=L, causal=True, dtype="bf16",
+                           seed=42, layers=layers, with_dy=False)
+    s2 = inputs.make_stack(batch=batch, n=n, width=width, num_layers=L, causal=True, dtype="bf16",
+                           seed=43, layers=layers, with_dy=False)
+    ws = [to_dev(w, "bf16") for w in s1.w_self]
+    wo = [to_dev(w, "bf16") for w in s1.w_off]
+    cache = hcmix.alloc_decode_cache(batch, n, width, L, torch.bfloat16, "cuda")
+    for s in (s1, s2):
+        x = to_dev(s.x, "bf16")
+        got = np.stack([to_host(hcmix.decode_step(x[:, p].contiguous(), ws, wo, layers, n, p, cache))
+                        for p in range(n)], axis=1)
+        want = oracle.stack_forward(s.x, s1.w_self, s1.w_off, layers, True)[-1]
+        assert row_rel_err(got, want) <= TOL["bf16"]
