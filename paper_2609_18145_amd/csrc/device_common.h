@@ -19,13 +19,32 @@ __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
 }
 
-// 16-byte store through the global address space.  Pointers that were read
-// from memory (rather than taken from kernel arguments) are generic, and a
-// generic store becomes a FLAT instruction, which also counts on lgkmcnt and
-// so serialises with the LDS reads that feed it.
+// Pointers read from memory (rather than taken from kernel arguments) are
+// generic, and a generic store becomes a FLAT instruction, which also counts
+// on lgkmcnt and so serialises with the LDS reads that feed it; stores through
+// this type stay global.
 typedef __attribute__((address_space(1))) u32x4 global_u32x4;
-__device__ __forceinline__ void store_global16(void* dst, const u32x4& v) {
-  *(global_u32x4*)dst = v;
+
+// Stores that write through L2 to memory at device scope (the sc1 policy
+// bit).  A kernel's completion has to write the dirty L2 lines its ordinary
+// stores left behind back to memory before a dependent kernel may start;
+// lines written through are clean, so the tail of an output-heavy kernel is
+// shorter (about a microsecond per 16 MiB of output, measured).  Values and
+// ordering are those of an ordinary global store.
+//
+// store_wt16 is an asm statement, which the compiler does not know to be a
+// store: it inserts neither the wait states that must separate a store of
+// more than 8 bytes from a VALU write of its data registers (2 on
+// gfx94x/gfx950; the s_nop supplies them) nor those an MFMA result needs
+// before a memory instruction reads it.  So its data must come from LDS or
+// from VALU work, never straight from MFMA accumulators.  store_wt4 is a
+// relaxed device-scope atomic store, which compiles to the same sc1 store
+// with every hazard known to the compiler.
+__device__ __forceinline__ void store_wt16(void* dst, const u32x4& v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" ::"v"(dst), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_wt4(float* dst, float v) {
+  __hip_atomic_store(dst, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }

@@ -234,7 +234,7 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
     const int q = q0 + (m % BMP);
     if (q >= pairs) continue;
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
-    *(u32x4*)(out + (size_t)r * width + n0 + ch * 8) = *(const u32x4*)(sO + m * C::LDO + ch * 8);
+    store_wt16(out + (size_t)r * width + n0 + ch * 8, *(const u32x4*)(sO + m * C::LDO + ch * 8));
   }
 }
 
@@ -432,8 +432,7 @@ __global__ __launch_bounds__(64 * WM * WN) void shift_bf16_kernel(
     const int idx = tid + C::NT * j;
     const int m = idx / (BN / 8), ch = idx % (BN / 8);
     if (r0 + m >= rows) continue;
-    *(u32x4*)(out + (size_t)(r0 + m) * width + n0 + ch * 8) =
-        *(const u32x4*)(sO + m * C::LDO + ch * 8);
+    store_wt16(out + (size_t)(r0 + m) * width + n0 + ch * 8, *(const u32x4*)(sO + m * C::LDO + ch * 8));
   }
 }
 
@@ -677,8 +676,8 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
       for (int e = 0; e < 16; e++) {
         const int o = o0 + (wo * C::TO + a) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         const int c = c0 + (wc * C::TC + b) * 32 + (lane & 31);
-        outS[(size_t)o * width + c] = accS[a][b][e];
-        outO[(size_t)o * width + c] = accO[a][b][e];
+        store_wt4(outS + (size_t)o * width + c, accS[a][b][e]);
+        store_wt4(outO + (size_t)o * width + c, accO[a][b][e]);
       }
 }
 
@@ -697,7 +696,7 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
       acc += ((const f32x4*)(partial + ((size_t)sp * 2 + m) * ww))[j];
     f32x4* dst = (f32x4*)(m ? dwo : dws) + j;
     if (accumulate) acc += *dst;
-    *dst = acc;
+    store_wt16(dst, __builtin_bit_cast(u32x4, acc));
   }
 }
 
@@ -785,7 +784,7 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeArgs a) {
     bf16x8 v;
 #pragma unroll
     for (int j = 0; j < 8; j++) v[j] = t[c + j][r];
-    *(bf16x8*)(dst + (size_t)(tc * 64 + r) * a.width + tr * 64 + c) = v;
+    store_wt16(dst + (size_t)(tc * 64 + r) * a.width + tr * 64 + c, __builtin_bit_cast(u32x4, v));
   }
 }
 

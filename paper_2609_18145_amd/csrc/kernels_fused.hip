@@ -132,7 +132,9 @@ __device__ __forceinline__ void store_block(bf16* buf, const f32x16& accL, const
 
 // 16-byte pieces p0, p0 + stride, ... (K of them) of a window's activation
 // buffer -> their row-major places in global memory; all LDS reads first.
-template <int K>
+// WT writes through L2 (store_wt16), which pays for copies that overlap later
+// compute; a copy that ends the kernel is faster with ordinary stores.
+template <int K, bool WT>
 __device__ __forceinline__ void copy_out(const bf16* buf, bf16* dst, int p0, int stride) {
   u32x4 v[K];
 #pragma unroll
@@ -143,7 +145,11 @@ __device__ __forceinline__ void copy_out(const bf16* buf, bf16* dst, int p0, int
 #pragma unroll
   for (int i = 0; i < K; i++) {
     const int p = p0 + i * stride;
-    store_global16(dst + (size_t)(p / (FW / 8)) * FW + (p % (FW / 8)) * 8, v[i]);
+    bf16* q = dst + (size_t)(p / (FW / 8)) * FW + (p % (FW / 8)) * 8;
+    if (WT)
+      store_wt16(q, v[i]);
+    else
+      *(global_u32x4*)q = v[i];
   }
 }
 
@@ -223,7 +229,7 @@ __global__ __launch_bounds__(3 * N) void fused_fwd_kernel(FusedFwdArgs a) {
       wait_dma();  // this wave's share of the next weights
     } else if (l > 0) {
       bf16* dst = tab[l - 1].xs + win;
-      copy_out<SPT>(X, dst, tid - CT, N);
+      copy_out<SPT, true>(X, dst, tid - CT, N);
     }
     __syncthreads();  // Y complete, next weights landed, X and this layer's weights free
     bf16* t = X;
@@ -232,7 +238,7 @@ __global__ __launch_bounds__(3 * N) void fused_fwd_kernel(FusedFwdArgs a) {
   }
   if (compute) {
     bf16* dst = tab[L - 1].xs + win;
-    copy_out<CPT>(X, dst, tid, CT);
+    copy_out<CPT, false>(X, dst, tid, CT);
   }
 }
 
@@ -318,7 +324,10 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
           mma(fr[k & 1]);
         }
         // transposed accumulators: lane l holds output ob + l%32 and inputs
-        // cb + 8 g + 4 (l/32) + 0..3
+        // cb + 8 g + 4 (l/32) + 0..3.  Ordinary stores: the data comes
+        // straight from MFMA accumulators, and the split into 8-byte
+        // write-through stores left half-written sectors that doubled the
+        // HBM writes.
         float* rowS = part + (size_t)(ob + (lane & 31)) * FW + cb + 4 * (lane >> 5);
 #pragma unroll
         for (int g = 0; g < 4; g++) {
@@ -372,7 +381,7 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
     G = Gn;
     Gn = t;
   }
-  copy_out<PCS>(G, a.dx + win, tid, NT);
+  copy_out<PCS, false>(G, a.dx + win, tid, NT);
 }
 
 // dW_self[l] / dW_off[l] (+)= sum over windows of the partials.  Each block
@@ -401,7 +410,7 @@ __global__ __launch_bounds__(256) void fused_dw_reduce_kernel(FusedReduceArgs a)
     sum += part[3][o];
     f32x4* dst = (f32x4*)(m ? a.dwo[l] : a.dws[l]) + j;
     if (a.accumulate) sum += *dst;
-    *dst = sum;
+    store_wt16(dst, __builtin_bit_cast(u32x4, sum));
   }
 }
 
