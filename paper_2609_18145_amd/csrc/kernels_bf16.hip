@@ -755,8 +755,11 @@ template <bool TRANS_B>
 hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
                         int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
   const int pairs = rows / 2;
+  // Two waves per SIMD (8 per block, each 64 pairs x 32 columns): one wave's
+  // LDS reads and barrier waits hide under the other's MFMAs.  Measured at
+  // 16384 x 512: dX 18.1 -> 16.8 us, forward unchanged within noise.
   if (width % 128 == 0)
-    return mix_launch<MIX_BMP, 128, 2, 2, MIX_BK, MIX_NS, TRANS_B>(
+    return mix_launch<MIX_BMP, 128, 2, 4, MIX_BK, MIX_NS, TRANS_B>(
         A, B1, B2, out, pairs, width, d, partner_lower, partner_upper, st);
   return mix_launch<MIX_BMP, 64, 4, 1, MIX_BK, MIX_NS, TRANS_B>(
       A, B1, B2, out, pairs, width, d, partner_lower, partner_upper, st);
