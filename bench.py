@@ -106,30 +106,44 @@ def fused_path(n, w, L):
     return w == 64 and n in (64, 128, 256) and L <= 64
 
 
+def bwd_layer_path(n, w, L):
+    """Shapes whose stack backward runs one bwd_layer_kernel launch per layer
+    (dX, the layer's weight-gradient partials and the previous layer's
+    reduction), after a transpose of the weights and before a last reduction."""
+    return not fused_path(n, w, L) and L > 1 and w % 128 == 0
+
+
 def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo, workspace,
                     layers, B, n, w, L, causal):
-    """Roofline entry for the kernel that dominates the step, timed with HIP
-    events on the stream it runs on over back-to-back launches.
+    """Roofline entries, timed with HIP events on the stream the kernels run
+    on over back-to-back calls: (dominant, forward-launch entry or None).
 
-    Other shapes: the mix GEMM forward launch, against the bf16 MFMA peak
-    (flops per launch B n w^2 x 3 causal / x 4 bidirectional: 2 w^2 for the
-    self map of every position, 2 w^2 for the partner map of each receiver).
     Small width (the fused path): the backward stack call (fused_bwd_kernel
     plus its fixed-order partial reduction), against HBM bandwidth; its
     algorithmic bytes are dY, the L saved inputs and dX (bf16), the 2L weight
-    matrices (bf16) read and the 2L weight gradients (fp32) written."""
+    matrices (bf16) read and the 2L weight gradients (fp32) written.
+    Layer-by-layer backward on bwd_layer_kernel: that call dominates the step;
+    priced against the bf16 MFMA peak with flops B n L w^2 x 6 causal / x 8
+    bidirectional (dX and both weight gradients).  Beside it, the mix GEMM
+    forward launch (flops B n w^2 x 3 causal / x 4 bidirectional: 2 w^2 for
+    the self map of every position, 2 w^2 for the partner map of each
+    receiver), which is the dominant entry for the other shapes."""
     import torch
     reps = args.kernel_reps
     k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    if fused_path(n, w, L):
-        xs = [x0, *xs_out[:L - 1]]
+    xs = [x0, *xs_out[:L - 1]]
+
+    def time_backward():
         k0.record(stream)
         for _ in range(reps):
             hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0], dws=dws, dwo=dwo,
                                  workspace=workspace)
         k1.record(stream)
         torch.cuda.synchronize()
-        sec = k0.elapsed_time(k1) / 1e3 / reps
+        return k0.elapsed_time(k1) / 1e3 / reps
+
+    if fused_path(n, w, L):
+        sec = time_backward()
         act = B * n * w * 2
         nbytes = act * (L + 2) + 2 * L * w * w * 2 + 2 * L * w * w * 4
         gbs = nbytes / sec / 1e9
@@ -137,7 +151,7 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
                 "(one hcmix_stack_backward call)", "achieved": round(gbs, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                 "traffic": profiled_traffic(args.workload), "avg_launch_us": round(sec * 1e6, 2),
-                "algorithmic_bytes": nbytes}
+                "algorithmic_bytes": nbytes}, None
     k0.record(stream)
     for _ in range(reps):
         for l in range(L):
@@ -148,10 +162,21 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
     sec = k0.elapsed_time(k1) / 1e3 / (reps * L)
     flops = B * n * (3 if causal else 4) * w * w
     tflops = flops / sec / 1e12
-    return {"bound": "mfma", "kernel": "mix_bf16_kernel (forward launch)",
-            "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": profiled_traffic(args.workload),
-            "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops}
+    fwd = {"bound": "mfma", "kernel": "mix_bf16_kernel (forward launch)",
+           "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+           "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "avg_launch_us": round(sec * 1e6, 2),
+           "algorithmic_flops": flops}
+    if not bwd_layer_path(n, w, L):
+        fwd["traffic"] = profiled_traffic(args.workload)
+        return fwd, None
+    sec = time_backward()
+    flops = B * n * L * (6 if causal else 8) * w * w
+    tflops = flops / sec / 1e12
+    return {"bound": "mfma", "kernel": f"bwd_layer_kernel x{L} + weight transposes + last "
+            "reduction (one hcmix_stack_backward call)", "achieved": round(tflops, 2),
+            "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": profiled_traffic(args.workload), "avg_launch_us": round(sec * 1e6, 2),
+            "algorithmic_flops": flops}, fwd
 
 
 def main():
@@ -224,8 +249,9 @@ def main():
         gpu_s = e0.elapsed_time(e1) / 1e3
         t = max(wall, gpu_s)
 
-        roofline = dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo,
-                                   workspace, s.layers, B, n, w, L, causal)
+        roofline, roofline_fwd = dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out,
+                                                 dx_out, dws, dwo, workspace, s.layers, B, n, w,
+                                                 L, causal)
 
     if args.calib_copy_mb > 0:
         src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device=dev)
@@ -250,6 +276,8 @@ def main():
         "pct_hbm": round(nbytes / t * args.steps / 1e9 / PEAK_HBM_GBS * 100, 2),
         "roofline": roofline,
     }
+    if roofline_fwd is not None:
+        out["roofline_fwd"] = roofline_fwd
     if args.cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(s, n, w, L, causal, args.cpu_windows)
     print(json.dumps(out), flush=True)

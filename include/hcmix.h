@@ -148,9 +148,11 @@ hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_
 
 /* Bytes of device workspace hcmix_stack_backward needs (0 for invalid
  * arguments).  256-byte aligned.  Fused path: the per-window weight-gradient
- * partials.  Layer by layer: two gradient buffers, one layer's split-K
- * partials and (bf16, two or more layers) a transposed copy of every weight
- * matrix, so that dX runs the forward GEMM on W^T. */
+ * partials.  Layer by layer: two gradient buffers, the split-K partials of
+ * one layer, or of two (bf16, two or more layers, width a multiple of 128:
+ * a layer's partials are summed inside the next layer's backward launch),
+ * and (bf16, two or more layers) a transposed copy of every weight matrix,
+ * so that dX runs the forward GEMM on W^T. */
 size_t hcmix_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
                                             int32_t num_layers, int32_t dtype);
 

@@ -67,14 +67,23 @@ size_t transposed_weight_bytes(int64_t width, int32_t num_layers, int32_t dtype)
   return align256((size_t)2 * num_layers * width * width * sizeof(bf16));
 }
 
+// Partial-sum buffers of the layer-by-layer path: two when a layer's
+// weight-gradient reduction runs inside the next layer's backward launch
+// (bf16, two or more layers, a width that is a multiple of 128), so that one
+// layer's partials are read while the next layer's are written.
+int partial_buffers(int64_t width, int32_t num_layers, int32_t dtype) {
+  return dtype == HCMIX_BF16 && num_layers > 1 && width % 128 == 0 ? 2 : 1;
+}
+
 // Stack backward workspace: the per-window partials of the fused path, or two
-// gradient buffers, one layer's workspace and the transposed weights for the
-// layer-by-layer path.
+// gradient buffers, one or two layers' partials and the transposed weights
+// for the layer-by-layer path.
 size_t stack_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                              int32_t dtype) {
   const size_t act = align256((size_t)(batch * n * width) * elem_size(dtype));
   const size_t layered = (num_layers > 1 ? 2 * act : 0) +
-                         layer_workspace_bytes(batch, n, width, dtype) +
+                         partial_buffers(width, num_layers, dtype) *
+                             layer_workspace_bytes(batch, n, width, dtype) +
                          transposed_weight_bytes(width, num_layers, dtype);
   if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
     // the schedule is not known here: enough for the fused path and for the
@@ -386,7 +395,9 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
     void* layer_ws = ws + (num_layers > 1 ? 2 * act_al : 0);
     const void* g = dy;
     const size_t lws = layer_workspace_bytes(batch, n, width, dtype);
-    bf16* wt = (bf16*)((char*)layer_ws + lws);   // transposed weights (bf16, L >= 2)
+    const int nparts = partial_buffers(width, num_layers, dtype);
+    float* parts[2] = {(float*)layer_ws, (float*)((char*)layer_ws + (nparts - 1) * lws)};
+    bf16* wt = (bf16*)((char*)layer_ws + nparts * lws);   // transposed weights (bf16, L >= 2)
     const size_t ww = (size_t)w * w;
     if (transposed_weight_bytes(width, num_layers, dtype) > 0) {
       // wt[2l] = W_self[l]^T, wt[2l+1] = W_off[l]^T
@@ -403,9 +414,34 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
         e = launch_transpose_bf16(t, cnt, s);
       }
     }
+    // A layer's weight-gradient reduction waits for the next launch (the next
+    // fused backward layer takes it as a role, anything else flushes it first).
+    DwReduce pending = {};
     for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
       void* out = l == 0 ? dx : gbuf[l & 1];
       const int d = hcmix_dim(layers[l], n);
+      if (dtype == HCMIX_BF16 && num_layers > 1 && bwd_layer_fusable(w, d)) {
+        // dX (from the transposed copies), this layer's weight-gradient
+        // partials and the previous layer's reduction in one launch
+        float* part = parts[l & 1];
+        if (pending.partial == part) {   // cannot happen with ping-pong; keep it safe
+          e = launch_dw_reduce(pending, w, s);
+          pending = {};
+          if (e != hipSuccess) break;
+        }
+        int splits = 0;
+        e = launch_bwd_layer_bf16((const bf16*)xs_in[l], (const bf16*)g, wt + 2 * (size_t)l * ww,
+                                  wt + (2 * (size_t)l + 1) * ww, (bf16*)out, part, rows, w, d,
+                                  (int)n, bidir, pending, &splits, s);
+        pending = DwReduce{part, dw_self[l], dw_off[l], splits, accumulate != 0};
+        g = out;
+        continue;
+      }
+      if (pending.partial) {
+        e = launch_dw_reduce(pending, w, s);
+        pending = {};
+        if (e != hipSuccess) break;
+      }
       if (dtype == HCMIX_BF16 && num_layers > 1) {
         // dX = W_self^T dy (+ partner W_off^T dy): the forward kernels on W^T
         e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g, wt + 2 * (size_t)l * ww,
@@ -419,6 +455,7 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
       }
       g = out;
     }
+    if (e == hipSuccess && pending.partial) e = launch_dw_reduce(pending, w, s);
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }

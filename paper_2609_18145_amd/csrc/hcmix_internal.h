@@ -71,6 +71,33 @@ hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* 
                           int rows, int width, int d, int n, int bidir, int accumulate,
                           hipStream_t st);
 
+// A weight-gradient reduction whose split partials are complete:
+// dW_self/dW_off (+)= the sum of `splits` partial slots (each 2 x width^2
+// floats: the dW_self part, then the dW_off part), in slot order.
+struct DwReduce {
+  const float* partial;   // null: nothing to reduce
+  float* dws;
+  float* dwo;
+  int splits;
+  int accumulate;
+};
+hipError_t launch_dw_reduce(const DwReduce& r, int width, hipStream_t st);
+
+// Whether launch_bwd_layer_bf16 takes a layer: a hypercube layer (d >= 0) of a
+// width that is a multiple of 128.
+bool bwd_layer_fusable(int width, int d);
+// One hypercube layer's backward in one launch: dX = dY W_self + partner
+// dY W_off (partner rows per bidir), read from the transposed copies
+// wt_self = W_self^T and wt_off = W_off^T, and the split-K partials of the
+// layer's weight gradients into `partial` (dw_bf16_splits(rows, width) slots;
+// *splits gets the number written, for the caller's own reduction), plus, as
+// a third role, `prev`: another layer's reduction, whose partials must not be
+// `partial`.
+hipError_t launch_bwd_layer_bf16(const bf16* X, const bf16* dY, const bf16* wt_self,
+                                 const bf16* wt_off, bf16* dX, float* partial, int rows,
+                                 int width, int d, int n, int bidir, const DwReduce& prev,
+                                 int* splits, hipStream_t st);
+
 // ---- fused small-width stack (width 64, n in {64, 128, 256}) ----
 constexpr int kFusedMaxLayers = 64;
 

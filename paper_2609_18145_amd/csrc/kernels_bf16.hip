@@ -63,20 +63,21 @@ struct MixCfg {
   static_assert(NS >= 2 && (NS - 2) * DPS <= 63, "vmcnt range");
 };
 
+// One block's work: `block` indexes the (row tile, column tile) grid, dealt
+// to XCDs; `smem` is the block's dynamic LDS (MixCfg::LDS_ELEMS elements).
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool PL, bool PU, bool TRANS_B>
-__global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
+__device__ __forceinline__ void mix_bf16_block(
     const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
-    bf16* __restrict__ out, int pairs, int width, int d) {
+    bf16* __restrict__ out, int pairs, int width, int d, int block, bf16* smem) {
   using C = MixCfg<BMP, BN, WM, WN, BK, NS>;
   constexpr int RB = BN * 2;   // bytes per row of a transposed B tile
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
   const int s = 1 << d;
   const int tiles_n = width / BN;
   const int tiles_m = (pairs + BMP - 1) / BMP;
-  const int tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  const int tile = xcd_tile(block, tiles_m * tiles_n);
   const int q0 = (tile / tiles_n) * BMP;
   const int n0 = (tile % tiles_n) * BN;
 
@@ -236,6 +237,15 @@ __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
     store_wt16(out + (size_t)r * width + n0 + ch * 8, *(const u32x4*)(sO + m * C::LDO + ch * 8));
   }
+}
+
+template <int BMP, int BN, int WM, int WN, int BK, int NS, bool PL, bool PU, bool TRANS_B>
+__global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
+    const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
+    bf16* __restrict__ out, int pairs, int width, int d) {
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+  mix_bf16_block<BMP, BN, WM, WN, BK, NS, PL, PU, TRANS_B>(A, B1, B2, out, pairs, width, d,
+                                                           blockIdx.x, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -484,14 +494,16 @@ struct DwCfg {
   static_assert((size_t)NW * ACC * 64 * 4 <= LDS, "hand-over fits in the stage buffers");
 };
 
+// One block's work: `block` of `nblocks` indexes (split, tile), dealt to
+// XCDs; `smem_all` is the block's dynamic LDS (DwCfg::LDS bytes).
 template <int BO, int BC, int WO, int WC, int LINK>
-__global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
+__device__ __forceinline__ void dw_bf16_block(
     const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
-    int pairs, int width, int d, int n, int pairs_per_group) {
+    int pairs, int width, int d, int n, int pairs_per_group, int block, int nblocks,
+    bf16* smem_all) {
   constexpr bool BIDIR = LINK == LINK_BIDIR, NEAR = LINK == LINK_NEAR;
   using C = DwCfg<BO, BC, WO, WC>;
   constexpr int RBG = BO * 2, RBX = BC * 2;
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int group = (tid >> 6) / C::NW, wave = (tid >> 6) % C::NW;
@@ -501,7 +513,7 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
   const int tiles = (width / BO) * tiles_c;
   // split-major order through the XCD deal: every tile of one split (they all
   // read the same rows of X and dY) runs on one XCD and shares its L2
-  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int lin = xcd_tile(block, nblocks);
   const int tile = lin % tiles;
   const int split = lin / tiles;
   const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
@@ -681,14 +693,24 @@ __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
       }
 }
 
-// dW (+)= sum over splits, in split order.
-__global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict__ partial,
-                                                        float* __restrict__ dws,
-                                                        float* __restrict__ dwo, int splits,
-                                                        size_t ww, int accumulate) {
+template <int BO, int BC, int WO, int WC, int LINK>
+__global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
+    const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
+    int pairs, int width, int d, int n, int pairs_per_group) {
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
+  dw_bf16_block<BO, BC, WO, WC, LINK>(X, dY, partial, pairs, width, d, n, pairs_per_group,
+                                      blockIdx.x, gridDim.x, smem_all);
+}
+
+// dW (+)= sum over splits, in split order; `block` of `nblocks`, `nthreads`
+// threads each, striding over the float4 outputs of both matrices.
+__device__ __forceinline__ void dw_reduce_block(const float* __restrict__ partial,
+                                                float* __restrict__ dws, float* __restrict__ dwo,
+                                                int splits, size_t ww, int accumulate, int block,
+                                                int nblocks, int nthreads) {
   const size_t n4 = ww / 4;
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < 2 * n4;
-       i += (size_t)gridDim.x * blockDim.x) {
+  for (size_t i = block * (size_t)nthreads + threadIdx.x; i < 2 * n4;
+       i += (size_t)nblocks * nthreads) {
     const int m = i >= n4;
     const size_t j = i - m * n4;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -700,12 +722,73 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
   }
 }
 
+__global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict__ partial,
+                                                        float* __restrict__ dws,
+                                                        float* __restrict__ dwo, int splits,
+                                                        size_t ww, int accumulate) {
+  dw_reduce_block(partial, dws, dwo, splits, ww, accumulate, blockIdx.x, gridDim.x, blockDim.x);
+}
+
+// One backward layer of a hypercube layer in one launch, three roles:
+//  - red_blocks blocks finish another layer's weight gradients from its
+//    complete split partials (red_partial; none when red_blocks is 0);
+//  - dx_blocks blocks compute dX = dY W_self + partner dY W_off from
+//    transposed weight copies (the 8-wave mix configuration);
+//  - dw_blocks blocks write this layer's split-K weight-gradient partials.
+// No role reads what another writes, so they need no ordering; one launch
+// instead of three saves two kernel boundaries (dispatch ramp, drain and L2
+// writeback) per layer.  Launch order dW, dX, reduction: the dW blocks are
+// the longest, and interleaving roles slowed the dX blocks.  The dX and dW counts are
+// padded to multiples of 8 with idle blocks, so that role-local index and
+// launch index agree modulo 8 and every role keeps its XCD deal.
+constexpr int BWD_THREADS = 512;
+__host__ __device__ constexpr int round8(int v) { return (v + 7) / 8 * 8; }
+template <bool BIDIR>
+__global__ __launch_bounds__(BWD_THREADS) void bwd_layer_kernel(
+    const bf16* __restrict__ dY, const bf16* __restrict__ WtS, const bf16* __restrict__ WtO,
+    const bf16* __restrict__ X, bf16* __restrict__ dX, float* __restrict__ partial, int pairs,
+    int width, int d, int n, int pairs_per_group, int dx_blocks, int dw_blocks,
+    const float* __restrict__ red_partial, float* __restrict__ red_dws,
+    float* __restrict__ red_dwo, int red_splits, int red_accumulate, int red_blocks) {
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+  int b = blockIdx.x;
+  const int dx_slots = round8(dx_blocks);
+  const int tail = dx_slots + round8(dw_blocks);
+  if (b >= tail) {
+    b -= tail;
+    if (b < red_blocks)
+      dw_reduce_block(red_partial, red_dws, red_dwo, red_splits, (size_t)width * width,
+                      red_accumulate, b, red_blocks, BWD_THREADS);
+    return;
+  }
+  {  // dW blocks first: launch block b < dw_slots is dW block b
+    const int dw_slots = round8(dw_blocks);
+    b = b < dw_slots ? b + dx_slots : b - dw_slots;
+  }
+  if (b < dx_slots) {
+    if (b < dx_blocks)
+      mix_bf16_block<128, 128, 2, 4, 64, 2, true, BIDIR, false>(dY, WtS, WtO, dX, pairs, width,
+                                                                d, b, smem);
+  } else if (b - dx_slots < dw_blocks) {
+    dw_bf16_block<128, 128, 2, 2, BIDIR ? LINK_BIDIR : LINK_CAUSAL>(
+        X, dY, partial, pairs, width, d, n, pairs_per_group, b - dx_slots, dw_blocks, smem);
+  }
+}
+
+
 // ---- launch configurations ----
 constexpr int MIX_BMP = 128;          // 256 rows per block
 constexpr int MIX_BK = 64;            // contraction slice per pipeline stage
 constexpr int MIX_NS = 2;             // pipeline stages in LDS
 constexpr int DW_BO = 128, DW_BC = 128;
 constexpr int DW_TARGET_BLOCKS = 256;  // split-K blocks aimed for (8 waves each)
+// Beside the dX blocks of bwd_layer_kernel: dW blocks for about half the CUs,
+// started first (longest blocks first keeps the tail short), but no more than
+// BWD_DW_MAX_PAIRS row pairs per block, beyond which the dW blocks become the
+// tail.  Measured at 16384 x 512: 8 splits 39.3 us per launch against 43.3
+// with 16; at 32768 x 1024: 4 splits 235.9, 3 splits 235.5, 2 splits 241.8.
+constexpr int BWD_DW_TARGET_BLOCKS = 128;
+constexpr int BWD_DW_MAX_PAIRS = 4096;
 
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool TRANS_B>
 hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int pairs,
@@ -794,11 +877,11 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(TransposeArgs a) {
 // Split-K plan: about one block per CU, each block's row range two groups of
 // whole K-steps.  Returns the number of partial slots (blocks per tile);
 // *ppg gets the pairs per group.
-int dw_plan(int pairs, int width, int* ppg) {
+int dw_plan(int pairs, int width, int* ppg, int target_blocks = DW_TARGET_BLOCKS) {
   const int bo = width % DW_BO == 0 ? DW_BO : 64;
   const int tiles = (width / bo) * (width / bo);
   const int ksteps = (pairs + KP - 1) / KP;
-  int slots = (DW_TARGET_BLOCKS + tiles - 1) / tiles;
+  int slots = (target_blocks + tiles - 1) / tiles;
   if (slots > (ksteps + 1) / 2) slots = (ksteps + 1) / 2;
   if (slots < 1) slots = 1;
   *ppg = ((ksteps + 2 * slots - 1) / (2 * slots)) * KP;
@@ -851,6 +934,14 @@ hipError_t launch_shift_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16
                      : shift_dispatch<1, false>(A, B1, B2, out, rows, width, n, st);
 }
 
+hipError_t launch_dw_reduce(const DwReduce& r, int width, hipStream_t st) {
+  const size_t ww = (size_t)width * width;
+  int blocks = (int)((2 * ww / 4 + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  dw_reduce_kernel<<<blocks, 256, 0, st>>>(r.partial, r.dws, r.dwo, r.splits, ww, r.accumulate);
+  return hipGetLastError();
+}
+
 int dw_bf16_splits(int rows, int width) {
   // the partial slots of either kind of layer (pairs for hypercube layers,
   // rows for the local layer), so one workspace size serves both
@@ -874,10 +965,49 @@ hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* 
   else
     e = dw_launch<64, 64, 2, 2>(X, dY, partial, units, width, d, n, link, splits, ppg, st);
   if (e != hipSuccess) return e;
-  const size_t ww = (size_t)width * width;
-  int blocks = (int)((2 * ww / 4 + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
-  dw_reduce_kernel<<<blocks, 256, 0, st>>>(partial, dws, dwo, splits, ww, accumulate);
+  return launch_dw_reduce(DwReduce{partial, dws, dwo, splits, accumulate}, width, st);
+}
+
+bool bwd_layer_fusable(int width, int d) { return d >= 0 && width % 128 == 0; }
+
+hipError_t launch_bwd_layer_bf16(const bf16* X, const bf16* dY, const bf16* wt_self,
+                                 const bf16* wt_off, bf16* dX, float* partial, int rows,
+                                 int width, int d, int n, int bidir, const DwReduce& prev,
+                                 int* splits, hipStream_t st) {
+  using M = MixCfg<128, 128, 2, 4, 64, 2>;
+  using W = DwCfg<128, 128, 2, 2>;
+  static_assert(M::NT == BWD_THREADS && W::NT == BWD_THREADS, "one block size for every role");
+  const int pairs = rows / 2;
+  const int dx_blocks = ((pairs + 127) / 128) * (width / 128);
+  int ppg;
+  const int tiles = (width / 128) * (width / 128);
+  int target = (pairs + BWD_DW_MAX_PAIRS - 1) / BWD_DW_MAX_PAIRS * tiles;
+  if (target < BWD_DW_TARGET_BLOCKS) target = BWD_DW_TARGET_BLOCKS;
+  if (target > DW_TARGET_BLOCKS) target = DW_TARGET_BLOCKS;   // the workspace holds that many
+  *splits = dw_plan(pairs, width, &ppg, target);
+  const int dw_blocks = tiles * *splits;
+  // the reduction's float4 outputs, BWD_THREADS per block, at most one block per CU
+  int red_blocks = 0;
+  if (prev.partial) {
+    red_blocks = (int)((2 * (size_t)width * width / 4 + BWD_THREADS - 1) / BWD_THREADS);
+    if (red_blocks > 256) red_blocks = 256;
+  }
+  const size_t lds_m = (size_t)M::LDS_ELEMS * sizeof(bf16);
+  const size_t lds = lds_m > W::LDS ? lds_m : W::LDS;
+  const int grid = round8(dx_blocks) + round8(dw_blocks) + red_blocks;
+#define HCMIX_BWD(BIDIR)                                                                    \
+  {                                                                                         \
+    auto k = bwd_layer_kernel<BIDIR>;                                                       \
+    static const hipError_t attr = hipFuncSetAttribute(                                     \
+        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+    if (attr != hipSuccess) return attr;                                                    \
+    k<<<grid, BWD_THREADS, lds, st>>>(dY, wt_self, wt_off, X, dX, partial, pairs, width, d, n, \
+                                      ppg, dx_blocks, dw_blocks, prev.partial, prev.dws,    \
+                                      prev.dwo, prev.splits, prev.accumulate, red_blocks);  \
+  }
+  if (bidir) HCMIX_BWD(true)
+  else HCMIX_BWD(false)
+#undef HCMIX_BWD
   return hipGetLastError();
 }
 

@@ -151,8 +151,13 @@ def test_stack_workspace_query():
     assert fused == 64 * 8 * 2 * 64 * 64 * 4          # per-window partial weight gradients
     wide = lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16)
     layer = lib.hcmix_backward_workspace_bytes(64, 256, 512, hcmix.HCMIX_BF16)
-    # two gradient buffers, one layer's split-K partials, transposed weights of every layer
-    assert wide == 2 * 64 * 256 * 512 * 2 + layer + 2 * 16 * 512 * 512 * 2
+    # two gradient buffers, two layers' split-K partials (one layer's are summed
+    # inside the next layer's launch), transposed weights of every layer
+    assert wide == 2 * 64 * 256 * 512 * 2 + 2 * layer + 2 * 16 * 512 * 512 * 2
+    # a width that is not a multiple of 128: one layer's partials
+    w192 = lib.hcmix_stack_backward_workspace_bytes(64, 256, 192, 4, hcmix.HCMIX_BF16)
+    layer192 = lib.hcmix_backward_workspace_bytes(64, 256, 192, hcmix.HCMIX_BF16)
+    assert w192 == 2 * 64 * 256 * 192 * 2 + layer192 + 2 * 4 * 192 * 192 * 2
     assert lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 1, hcmix.HCMIX_BF16) == layer
     assert lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 0, hcmix.HCMIX_BF16) == 0
     assert lib.hcmix_stack_backward_workspace_bytes(2, 16, 32, 1, hcmix.HCMIX_F32) == 0

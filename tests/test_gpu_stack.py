@@ -216,3 +216,14 @@ def test_layer_by_layer_backward_matches_oracle_and_replays_in_a_graph():
         for a, b in zip(got, ref):
             assert torch.equal(a, b), f"replay {rep} differs from the eager call"
         log(f"  replay {rep} bitwise equal")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_layer_by_layer_backward_ragged_rows(causal):
+    """bf16 stack backward on the layer-by-layer path (width 256, 6 rotated
+    layers) with 3 windows of 64 positions: 96 row pairs, one partial 128-pair
+    tile, in both modes; every output and weight gradient against the oracle."""
+    s = inputs.make_stack(batch=3, n=64, width=256, num_layers=6, causal=causal, dtype="bf16",
+                          seed=12)
+    log(f"case: layer-by-layer bf16 backward, B=3 n=64 w=256 L=6 causal={causal}, seed 12")
+    check_stack(s, run_gpu_stack(s))
