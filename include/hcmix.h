@@ -147,12 +147,16 @@ hcmix_status hcmix_stack_forward(int64_t batch, int64_t n, int64_t width, int32_
                                  const void* const* w_off, void* const* xs, void* stream);
 
 /* Bytes of device workspace hcmix_stack_backward needs (0 for invalid
- * arguments).  256-byte aligned.  Fused path: the per-window weight-gradient
- * partials.  Layer by layer: two gradient buffers, the split-K partials of
- * one layer, or of two (bf16, two or more layers, width a multiple of 128:
- * a layer's partials are summed inside the next layer's backward launch),
- * and (bf16, two or more layers) a transposed copy of every weight matrix,
- * so that dX runs the forward GEMM on W^T. */
+ * arguments).  256-byte aligned.
+ *  - bf16, two or more layers, width a multiple of 128 (deferred weight
+ *    gradients): the gradient of every intermediate activation (L - 1 of
+ *    [batch][n][width], or a ring of 65 for stacks longer than 64 layers), a
+ *    transposed copy of every weight matrix, and the row-range partials of the
+ *    weight-gradient launch when the stack is too short to fill the chip
+ *    (hcmix_stack_weight_gradients_workspace_bytes).
+ *  - fused path: the per-window weight-gradient partials;
+ *  - otherwise, layer by layer: two gradient buffers, the split-K partials of
+ *    one layer and (bf16, two or more layers) the transposed weights. */
 size_t hcmix_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
                                             int32_t num_layers, int32_t dtype);
 
@@ -161,7 +165,10 @@ size_t hcmix_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t wi
  * (gradient of x_0, in dtype) and, for every layer, dw_self[l] and dw_off[l]
  * (host arrays of device pointers to fp32 [width][width]), overwritten when
  * accumulate == 0, added to otherwise.  Weight gradients are summed in a
- * fixed order (bitwise-repeatable). */
+ * fixed order (bitwise-repeatable).  On the deferred path (bf16, two or more
+ * layers, width a multiple of 128) the dX chain runs first, keeping every
+ * intermediate gradient in the workspace, and then
+ * hcmix_stack_weight_gradients forms all weight gradients at once. */
 hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                   const int32_t* layers, int32_t mode, int32_t dtype,
                                   const void* const* xs_in, const void* const* w_self,
@@ -169,6 +176,33 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
                                   float* const* dw_self, float* const* dw_off,
                                   int32_t accumulate, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/* Weight gradients of every layer of a stack from the layers' inputs and the
+ * gradients of their outputs (the weight-gradient half of the backward, e.g.
+ * for schedules that defer it):
+ *   dw_self[l] (+)= sum over (t, i) of dys[l][t][i] xs_in[l][t][i]^T
+ *   dw_off[l]  (+)= sum over (t, i) of m(i) dys[l][t][i] xs_in[l][t][partner(i)]^T
+ * with partner and m as in hcmix_backward for layer code layers[l].  xs_in and
+ * dys: host arrays of num_layers device pointers to [batch][n][width] in dtype;
+ * dw_self, dw_off: host arrays of device pointers to fp32 [width][width],
+ * overwritten when accumulate == 0, added to otherwise; no output may overlap
+ * any input or another output.  bf16 with width a multiple of 128: one launch
+ * per 64 layers whose blocks each own a 128 x 128 tile of both matrices over
+ * every row (or, when layers x tiles cannot fill the chip, over a row range,
+ * plus a fixed-order sum of the ranges); other shapes: the per-layer kernels
+ * of hcmix_backward.  Bitwise-repeatable.  The workspace (256-byte aligned,
+ * hcmix_stack_weight_gradients_workspace_bytes, possibly 0) holds those
+ * partial sums. */
+size_t hcmix_stack_weight_gradients_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                                     int32_t num_layers, int32_t dtype);
+
+hcmix_status hcmix_stack_weight_gradients(int64_t batch, int64_t n, int64_t width,
+                                          int32_t num_layers, const int32_t* layers, int32_t mode,
+                                          int32_t dtype, const void* const* xs_in,
+                                          const void* const* dys, float* const* dw_self,
+                                          float* const* dw_off, int32_t accumulate,
+                                          void* workspace, size_t workspace_bytes,
+                                          void* stream);
 
 /* ---- Decode: one new position of every window through the whole stack ----
  *

@@ -67,23 +67,63 @@ size_t transposed_weight_bytes(int64_t width, int32_t num_layers, int32_t dtype)
   return align256((size_t)2 * num_layers * width * width * sizeof(bf16));
 }
 
-// Partial-sum buffers of the layer-by-layer path: two when a layer's
-// weight-gradient reduction runs inside the next layer's backward launch
-// (bf16, two or more layers, a width that is a multiple of 128), so that one
-// layer's partials are read while the next layer's are written.
-int partial_buffers(int64_t width, int32_t num_layers, int32_t dtype) {
-  return dtype == HCMIX_BF16 && num_layers > 1 && width % 128 == 0 ? 2 : 1;
+// Deferred weight gradients (bf16, two or more layers, a width that is a
+// multiple of 128): the dX chain runs first and keeps every intermediate
+// gradient; then one launch per chunk of up to kBatchMaxLayers layers forms
+// all their weight gradients, each block owning its tiles over every row pair
+// of its layer (no split-K partials unless the stack is too short to fill the
+// chip).
+bool deferred_dw(int64_t width, int32_t num_layers, int32_t dtype) {
+  return dtype == HCMIX_BF16 && num_layers > 1 && width % 128 == 0;
 }
 
-// Stack backward workspace: the per-window partials of the fused path, or two
-// gradient buffers, one or two layers' partials and the transposed weights
-// for the layer-by-layer path.
+// Intermediate gradients kept by the deferred path: g_1 .. g_{L-1} (g_L is the
+// caller's dy, g_0 its dx), or a ring of kBatchMaxLayers + 1 for longer stacks
+// (a chunk's weight gradients read kBatchMaxLayers of them while the chain has
+// written one more).
+int grad_buffers(int32_t num_layers) {
+  return num_layers <= kBatchMaxLayers ? num_layers - 1 : kBatchMaxLayers + 1;
+}
+
+size_t batch_partial_bytes(int64_t rows, int64_t width, int32_t chunk) {
+  const int splits = dw_batch_splits((int)rows, (int)width, chunk);
+  return splits > 1 ? align256((size_t)chunk * splits * 2 * width * width * sizeof(float)) : 0;
+}
+
+// Workspace of hcmix_stack_weight_gradients: the batched launch's partials
+// (bf16, width a multiple of 128), else one layer's split-K partials.
+size_t weight_grad_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                                   int32_t dtype) {
+  if (dtype == HCMIX_BF16 && width % 128 == 0) {
+    const int32_t full = num_layers < kBatchMaxLayers ? num_layers : kBatchMaxLayers;
+    size_t part = batch_partial_bytes(batch * n, width, full);
+    if (num_layers > kBatchMaxLayers && num_layers % kBatchMaxLayers) {
+      const size_t last = batch_partial_bytes(batch * n, width, num_layers % kBatchMaxLayers);
+      if (last > part) part = last;
+    }
+    return part;
+  }
+  return layer_workspace_bytes(batch, n, width, dtype);
+}
+
+size_t deferred_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers) {
+  const size_t act = align256((size_t)(batch * n * width) * sizeof(bf16));
+  return (size_t)grad_buffers(num_layers) * act +
+         transposed_weight_bytes(width, num_layers, HCMIX_BF16) +
+         weight_grad_workspace_bytes(batch, n, width, num_layers, HCMIX_BF16);
+}
+
+// Stack backward workspace: the deferred path's gradients, transposed weights
+// and partials; the per-window partials of the fused path; or two gradient
+// buffers, one layer's partials and the transposed weights for the
+// layer-by-layer path.
 size_t stack_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                              int32_t dtype) {
+  if (deferred_dw(width, num_layers, dtype))
+    return deferred_workspace_bytes(batch, n, width, num_layers);
   const size_t act = align256((size_t)(batch * n * width) * elem_size(dtype));
   const size_t layered = (num_layers > 1 ? 2 * act : 0) +
-                         partial_buffers(width, num_layers, dtype) *
-                             layer_workspace_bytes(batch, n, width, dtype) +
+                         layer_workspace_bytes(batch, n, width, dtype) +
                          transposed_weight_bytes(width, num_layers, dtype);
   if (dtype == HCMIX_BF16 && fused_stack_eligible(n, width, num_layers)) {
     // the schedule is not known here: enough for the fused path and for the
@@ -176,6 +216,88 @@ hcmix_status check_spans(const Span* ins, int nin, const Span* outs, int nout, s
   for (int i = 0; i < nout; i++)
     if (outs[i].n && !aligned(outs[i].p, al)) return HCMIX_ERR_UNSUPPORTED;
   return HCMIX_OK;
+}
+
+// wt[2l] = W_self[l]^T, wt[2l+1] = W_off[l]^T for every layer (bf16).
+hipError_t transpose_weights(int w, int32_t num_layers, const void* const* w_self,
+                             const void* const* w_off, bf16* wt, hipStream_t s) {
+  const size_t ww = (size_t)w * w;
+  hipError_t e = hipSuccess;
+  for (int l0 = 0; l0 < num_layers && e == hipSuccess; l0 += kTransposeBatch / 2) {
+    TransposeArgs t = {};
+    t.width = w;
+    int cnt = 0;
+    for (int l = l0; l < num_layers && l < l0 + kTransposeBatch / 2; l++) {
+      t.src[cnt] = (const bf16*)w_self[l];
+      t.dst[cnt++] = wt + (2 * (size_t)l) * ww;
+      t.src[cnt] = (const bf16*)w_off[l];
+      t.dst[cnt++] = wt + (2 * (size_t)l + 1) * ww;
+    }
+    e = launch_transpose_bf16(t, cnt, s);
+  }
+  return e;
+}
+
+// Weight gradients of up to kBatchMaxLayers bf16 layers (width a multiple of
+// 128) in one launch; `partial` is the workspace for split row ranges.
+hipError_t launch_dw_chunk(int rows, int w, int n, int count, const int32_t* layers, int bidir,
+                           const void* const* xs_in, const void* const* gs,
+                           float* const* dw_self, float* const* dw_off, int accumulate,
+                           float* partial, hipStream_t s) {
+  DwBatchArgs a = {};
+  for (int l = 0; l < count; l++) {
+    a.x[l] = (const bf16*)xs_in[l];
+    a.dy[l] = (const bf16*)gs[l];
+    a.dws[l] = dw_self[l];
+    a.dwo[l] = dw_off[l];
+    a.dim[l] = hcmix_dim(layers[l], n);   // -1 for the local layer
+  }
+  a.partial = partial;
+  a.rows = rows;
+  a.width = w;
+  a.n = n;
+  a.num_layers = count;
+  a.splits = dw_batch_splits(rows, w, count);
+  a.bidir = bidir;
+  a.accumulate = accumulate;
+  return launch_dw_batch_bf16(a, s);
+}
+
+// The deferred path (arguments validated; workspace laid out as
+// deferred_workspace_bytes counts it): gradients, transposed weights, partials.
+hipError_t stack_backward_deferred(int rows, int w, int n, int32_t num_layers,
+                                   const int32_t* layers, int bidir, const void* const* xs_in,
+                                   const void* dy, void* dx, const void* const* w_self,
+                                   const void* const* w_off, float* const* dw_self,
+                                   float* const* dw_off, int accumulate, void* workspace,
+                                   hipStream_t s) {
+  const size_t act = align256((size_t)rows * w * sizeof(bf16));
+  const size_t ww = (size_t)w * w;
+  const int nb = grad_buffers(num_layers);
+  char* gbase = (char*)workspace;
+  bf16* wt = (bf16*)(gbase + (size_t)nb * act);
+  float* partial = (float*)((char*)wt + transposed_weight_bytes(w, num_layers, HCMIX_BF16));
+  // g_l: gradient of layer l's input (= layer l-1's output)
+  auto grad = [&](int l) -> void* {
+    if (l == num_layers) return (void*)dy;
+    if (l == 0) return dx;
+    return gbase + (size_t)(l % nb) * act;
+  };
+  hipError_t e = transpose_weights(w, num_layers, w_self, w_off, wt, s);
+  for (int l1 = num_layers; l1 > 0 && e == hipSuccess;) {
+    const int l0 = l1 > kBatchMaxLayers ? l1 - kBatchMaxLayers : 0;
+    for (int l = l1 - 1; l >= l0 && e == hipSuccess; l--)
+      e = run_dx_bf16(rows, w, hcmix_dim(layers[l], n), n, bidir, (const bf16*)grad(l + 1),
+                      wt + 2 * (size_t)l * ww, wt + (2 * (size_t)l + 1) * ww, (bf16*)grad(l),
+                      /*transpose_b=*/false, s);
+    if (e != hipSuccess) break;
+    const void* gs[kBatchMaxLayers];
+    for (int l = l0; l < l1; l++) gs[l - l0] = grad(l + 1);
+    e = launch_dw_chunk(rows, w, n, l1 - l0, layers + l0, bidir, xs_in + l0, gs, dw_self + l0,
+                        dw_off + l0, accumulate, partial, s);
+    l1 = l0;
+  }
+  return e;
 }
 
 }  // namespace
@@ -387,6 +509,9 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
     r.num_layers = num_layers;
     r.accumulate = accumulate != 0;
     e = launch_fused_backward(a, r, (int)batch, bidir, s);
+  } else if (deferred_dw(width, num_layers, dtype)) {
+    e = stack_backward_deferred(rows, w, (int)n, num_layers, layers, bidir, xs_in, dy, dx,
+                                w_self, w_off, dw_self, dw_off, accumulate != 0, workspace, s);
   } else {
     // layer by layer; intermediate gradients ping-pong in the workspace
     const size_t act_al = align256(act);
@@ -395,53 +520,13 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
     void* layer_ws = ws + (num_layers > 1 ? 2 * act_al : 0);
     const void* g = dy;
     const size_t lws = layer_workspace_bytes(batch, n, width, dtype);
-    const int nparts = partial_buffers(width, num_layers, dtype);
-    float* parts[2] = {(float*)layer_ws, (float*)((char*)layer_ws + (nparts - 1) * lws)};
-    bf16* wt = (bf16*)((char*)layer_ws + nparts * lws);   // transposed weights (bf16, L >= 2)
+    bf16* wt = (bf16*)((char*)layer_ws + lws);   // transposed weights (bf16, L >= 2)
+    if (transposed_weight_bytes(width, num_layers, dtype) > 0)
+      e = transpose_weights(w, num_layers, w_self, w_off, wt, s);
     const size_t ww = (size_t)w * w;
-    if (transposed_weight_bytes(width, num_layers, dtype) > 0) {
-      // wt[2l] = W_self[l]^T, wt[2l+1] = W_off[l]^T
-      for (int l0 = 0; l0 < num_layers && e == hipSuccess; l0 += kTransposeBatch / 2) {
-        TransposeArgs t = {};
-        t.width = w;
-        int cnt = 0;
-        for (int l = l0; l < num_layers && l < l0 + kTransposeBatch / 2; l++) {
-          t.src[cnt] = (const bf16*)w_self[l];
-          t.dst[cnt++] = wt + (2 * (size_t)l) * ww;
-          t.src[cnt] = (const bf16*)w_off[l];
-          t.dst[cnt++] = wt + (2 * (size_t)l + 1) * ww;
-        }
-        e = launch_transpose_bf16(t, cnt, s);
-      }
-    }
-    // A layer's weight-gradient reduction waits for the next launch (the next
-    // fused backward layer takes it as a role, anything else flushes it first).
-    DwReduce pending = {};
     for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
       void* out = l == 0 ? dx : gbuf[l & 1];
       const int d = hcmix_dim(layers[l], n);
-      if (dtype == HCMIX_BF16 && num_layers > 1 && bwd_layer_fusable(w, d)) {
-        // dX (from the transposed copies), this layer's weight-gradient
-        // partials and the previous layer's reduction in one launch
-        float* part = parts[l & 1];
-        if (pending.partial == part) {   // cannot happen with ping-pong; keep it safe
-          e = launch_dw_reduce(pending, w, s);
-          pending = {};
-          if (e != hipSuccess) break;
-        }
-        int splits = 0;
-        e = launch_bwd_layer_bf16((const bf16*)xs_in[l], (const bf16*)g, wt + 2 * (size_t)l * ww,
-                                  wt + (2 * (size_t)l + 1) * ww, (bf16*)out, part, rows, w, d,
-                                  (int)n, bidir, pending, &splits, s);
-        pending = DwReduce{part, dw_self[l], dw_off[l], splits, accumulate != 0};
-        g = out;
-        continue;
-      }
-      if (pending.partial) {
-        e = launch_dw_reduce(pending, w, s);
-        pending = {};
-        if (e != hipSuccess) break;
-      }
       if (dtype == HCMIX_BF16 && num_layers > 1) {
         // dX = W_self^T dy (+ partner W_off^T dy): the forward kernels on W^T
         e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g, wt + 2 * (size_t)l * ww,
@@ -455,12 +540,79 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
       }
       g = out;
     }
-    if (e == hipSuccess && pending.partial) e = launch_dw_reduce(pending, w, s);
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
 }  // extern "C"
+
+size_t hcmix_stack_weight_gradients_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                                     int32_t num_layers, int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers) return 0;
+  if (check_shape(batch, n, width, 0, HCMIX_BIDIR, dtype) != HCMIX_OK) return 0;
+  return weight_grad_workspace_bytes(batch, n, width, num_layers, dtype);
+}
+
+hcmix_status hcmix_stack_weight_gradients(int64_t batch, int64_t n, int64_t width,
+                                          int32_t num_layers, const int32_t* layers, int32_t mode,
+                                          int32_t dtype, const void* const* xs_in,
+                                          const void* const* dys, float* const* dw_self,
+                                          float* const* dw_off, int32_t accumulate,
+                                          void* workspace, size_t workspace_bytes,
+                                          void* stream) {
+  if (!layers || !xs_in || !dys || !dw_self || !dw_off) return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], mode, dtype);
+    if (st != HCMIX_OK) return st;
+    if (!xs_in[l] || !dys[l] || !dw_self[l] || !dw_off[l]) return HCMIX_ERR_INVALID_VALUE;
+  }
+  const size_t need = weight_grad_workspace_bytes(batch, n, width, num_layers, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
+  const size_t act = (size_t)(batch * n * width) * elem_size(dtype);
+  const size_t gw = (size_t)(width * width) * sizeof(float);
+  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
+  // Outputs: the workspace and every weight gradient; inputs: every xs_in[l]
+  // and dys[l].  No output may overlap any input or another output.
+  for (int l = 0; l < num_layers; l++) {
+    const Span ins[2] = {{xs_in[l], act}, {dys[l], act}};
+    const Span outs[3] = {{workspace, need}, {dw_self[l], gw}, {dw_off[l], gw}};
+    hcmix_status st = check_spans(ins, 2, outs, 3, al);
+    if (st != HCMIX_OK) return st;
+    for (int j = 0; j < num_layers; j++) {
+      if (j == l) continue;
+      const Span other[4] = {{xs_in[j], act}, {dys[j], act}, {dw_self[j], gw}, {dw_off[j], gw}};
+      for (int k = 1; k < 3; k++)
+        for (int m = 0; m < 4; m++)
+          if (overlaps(outs[k].p, outs[k].n, other[m].p, other[m].n))
+            return HCMIX_ERR_INVALID_VALUE;
+    }
+    if (!aligned(dw_self[l], 16) || !aligned(dw_off[l], 16)) return HCMIX_ERR_UNSUPPORTED;
+  }
+  if (need && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  const int rows = (int)(batch * n), w = (int)width;
+  const int bidir = mode == HCMIX_BIDIR;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  if (dtype == HCMIX_BF16 && width % 128 == 0) {
+    for (int l0 = 0; l0 < num_layers && e == hipSuccess; l0 += kBatchMaxLayers) {
+      const int count = num_layers - l0 < kBatchMaxLayers ? num_layers - l0 : kBatchMaxLayers;
+      e = launch_dw_chunk(rows, w, (int)n, count, layers + l0, bidir, xs_in + l0, dys + l0,
+                          dw_self + l0, dw_off + l0, accumulate != 0, (float*)workspace, s);
+    }
+  } else {
+    for (int l = 0; l < num_layers && e == hipSuccess; l++) {
+      const int d = hcmix_dim(layers[l], n);
+      if (dtype == HCMIX_BF16)
+        e = launch_dw_bf16((const bf16*)xs_in[l], (const bf16*)dys[l], (float*)workspace,
+                           dw_self[l], dw_off[l], rows, w, d, (int)n, bidir, accumulate != 0, s);
+      else
+        e = launch_dw_f32((const float*)xs_in[l], (const float*)dys[l], dw_self[l], dw_off[l],
+                          rows, w, d, (int)n, bidir, accumulate != 0, s);
+    }
+  }
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
 
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                 int32_t dtype) {

@@ -83,22 +83,25 @@ struct DwReduce {
 };
 hipError_t launch_dw_reduce(const DwReduce& r, int width, hipStream_t st);
 
-// Whether launch_bwd_layer_bf16 takes a layer: a hypercube layer (d >= 0) of a
-// width that is a multiple of 128.
-bool bwd_layer_fusable(int width, int d);
-// One hypercube layer's backward in one launch: dX = dY W_self + partner
-// dY W_off (partner rows per bidir), read from the transposed copies
-// wt_self = W_self^T and wt_off = W_off^T, and the split-K partials of the
-// layer's weight gradients into `partial` (dw_bf16_splits(rows, width) slots;
-// *splits gets the number written, for the caller's own reduction), plus, as
-// a third role, `prev`: another layer's reduction, whose partials must not be
-// `partial`.
-hipError_t launch_bwd_layer_bf16(const bf16* X, const bf16* dY, const bf16* wt_self,
-                                 const bf16* wt_off, bf16* dX, float* partial, int rows,
-                                 int width, int d, int n, int bidir, const DwReduce& prev,
-                                 int* splits, hipStream_t st);
+// Weight gradients of a whole stack (up to kBatchMaxLayers layers) in one
+// launch (bf16, width % 128 == 0), plus a fixed-order reduction when the
+// layers are split over row ranges.
+constexpr int kBatchMaxLayers = 64;
+struct DwBatchArgs {
+  const bf16* x[kBatchMaxLayers];    // input of each layer
+  const bf16* dy[kBatchMaxLayers];   // gradient of each layer's output
+  float* dws[kBatchMaxLayers];
+  float* dwo[kBatchMaxLayers];
+  int dim[kBatchMaxLayers];          // hypercube dimension, or -1 for the local layer
+  float* partial;                    // [L][splits][2][width][width] when splits > 1
+  int rows, width, n, num_layers, splits, bidir, accumulate;
+};
+// Splits per layer for num_layers layers of this shape (1: no partials).
+int dw_batch_splits(int rows, int width, int num_layers);
+hipError_t launch_dw_batch_bf16(const DwBatchArgs& a, hipStream_t st);
 
 // ---- fused small-width stack (width 64, n in {64, 128, 256}) ----
+
 constexpr int kFusedMaxLayers = 64;
 
 struct FusedFwdArgs {

@@ -494,13 +494,15 @@ struct DwCfg {
   static_assert((size_t)NW * ACC * 64 * 4 <= LDS, "hand-over fits in the stage buffers");
 };
 
-// One block's work: `block` of `nblocks` indexes (split, tile), dealt to
-// XCDs; `smem_all` is the block's dynamic LDS (DwCfg::LDS bytes).
+// One block's work: the BO x BC tile `tile` over the pairs of range `split`
+// (two groups of pairs_per_group each), written to out_s / out_o (row stride
+// width; added to what they hold when `accumulate`).  `smem_all` is the
+// block's dynamic LDS (DwCfg::LDS bytes).
 template <int BO, int BC, int WO, int WC, int LINK>
 __device__ __forceinline__ void dw_bf16_block(
-    const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
-    int pairs, int width, int d, int n, int pairs_per_group, int block, int nblocks,
-    bf16* smem_all) {
+    const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ out_s,
+    float* __restrict__ out_o, int accumulate, int pairs, int width, int d, int n,
+    int pairs_per_group, int tile, int split, bf16* smem_all) {
   constexpr bool BIDIR = LINK == LINK_BIDIR, NEAR = LINK == LINK_NEAR;
   using C = DwCfg<BO, BC, WO, WC>;
   constexpr int RBG = BO * 2, RBX = BC * 2;
@@ -510,12 +512,6 @@ __device__ __forceinline__ void dw_bf16_block(
   bf16* smem = smem_all + group * 2 * C::STAGE;
   const int wo = wave % WO, wc = wave / WO;
   const int tiles_c = width / BC;
-  const int tiles = (width / BO) * tiles_c;
-  // split-major order through the XCD deal: every tile of one split (they all
-  // read the same rows of X and dY) runs on one XCD and shares its L2
-  const int lin = xcd_tile(block, nblocks);
-  const int tile = lin % tiles;
-  const int split = lin / tiles;
   const int o0 = (tile / tiles_c) * BO, c0 = (tile % tiles_c) * BC;
   const int s = NEAR ? 0 : 1 << d;
   const int pbeg = (2 * split + group) * pairs_per_group;
@@ -677,9 +673,6 @@ __device__ __forceinline__ void dw_bf16_block(
         }
   }
 
-  const size_t ww = (size_t)width * width;
-  float* outS = partial + (size_t)split * 2 * ww;
-  float* outO = outS + ww;
 #pragma unroll
   for (int a = 0; a < C::TO; a++)
 #pragma unroll
@@ -688,18 +681,83 @@ __device__ __forceinline__ void dw_bf16_block(
       for (int e = 0; e < 16; e++) {
         const int o = o0 + (wo * C::TO + a) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         const int c = c0 + (wc * C::TC + b) * 32 + (lane & 31);
-        store_wt4(outS + (size_t)o * width + c, accS[a][b][e]);
-        store_wt4(outO + (size_t)o * width + c, accO[a][b][e]);
+        float* ps = out_s + (size_t)o * width + c;
+        float* po = out_o + (size_t)o * width + c;
+        store_wt4(ps, accumulate ? *ps + accS[a][b][e] : accS[a][b][e]);
+        store_wt4(po, accumulate ? *po + accO[a][b][e] : accO[a][b][e]);
       }
 }
 
+// Split-K launch: block -> (split, tile), split-major through the XCD deal, so
+// every tile of one split (they all read the same rows of X and dY) runs on
+// one XCD and shares its L2.  Split `sp` writes partial[sp] = [2][width][width].
 template <int BO, int BC, int WO, int WC, int LINK>
 __global__ __launch_bounds__(128 * WO * WC) void dw_bf16_kernel(
     const bf16* __restrict__ X, const bf16* __restrict__ dY, float* __restrict__ partial,
     int pairs, int width, int d, int n, int pairs_per_group) {
   extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
-  dw_bf16_block<BO, BC, WO, WC, LINK>(X, dY, partial, pairs, width, d, n, pairs_per_group,
-                                      blockIdx.x, gridDim.x, smem_all);
+  const int tiles = (width / BO) * (width / BC);
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const size_t ww = (size_t)width * width;
+  float* out = partial + (size_t)(lin / tiles) * 2 * ww;
+  dw_bf16_block<BO, BC, WO, WC, LINK>(X, dY, out, out + ww, 0, pairs, width, d, n,
+                                      pairs_per_group, lin % tiles, lin / tiles, smem_all);
+}
+
+// Weight gradients of every layer of a stack in one launch: block ->
+// (layer, split, tile), in that order through the XCD deal, so the tiles of
+// one layer and split (which read the same rows) share an L2.  With one split
+// each block owns its tiles over all row pairs and writes the layer's dW_self
+// and dW_off directly; otherwise split sp of layer l writes the partial
+// [l][sp][2][width][width] for dw_batch_reduce_kernel.
+template <int BO, int BC, int WO, int WC>
+__global__ __launch_bounds__(128 * WO * WC) void dw_batch_kernel(DwBatchArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem_all[];
+  const int tiles = (a.width / BO) * (a.width / BC);
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int layer = lin / (a.splits * tiles);
+  const int split = (lin / tiles) % a.splits;
+  const int tile = lin % tiles;
+  const int d = a.dim[layer];
+  const int units = d < 0 ? a.rows : a.rows / 2;   // rows (local layer) or row pairs
+  const int ppg = ((units + KP - 1) / KP + 2 * a.splits - 1) / (2 * a.splits) * KP;
+  const size_t ww = (size_t)a.width * a.width;
+  float *out_s, *out_o;
+  int acc = a.accumulate;
+  if (a.splits == 1) {
+    out_s = a.dws[layer];
+    out_o = a.dwo[layer];
+  } else {
+    out_s = a.partial + ((size_t)layer * a.splits + split) * 2 * ww;
+    out_o = out_s + ww;
+    acc = 0;
+  }
+  if (d < 0)
+    dw_bf16_block<BO, BC, WO, WC, LINK_NEAR>(a.x[layer], a.dy[layer], out_s, out_o, acc, units,
+                                             a.width, d, a.n, ppg, tile, split, smem_all);
+  else if (a.bidir)
+    dw_bf16_block<BO, BC, WO, WC, LINK_BIDIR>(a.x[layer], a.dy[layer], out_s, out_o, acc, units,
+                                              a.width, d, a.n, ppg, tile, split, smem_all);
+  else
+    dw_bf16_block<BO, BC, WO, WC, LINK_CAUSAL>(a.x[layer], a.dy[layer], out_s, out_o, acc, units,
+                                               a.width, d, a.n, ppg, tile, split, smem_all);
+}
+
+// dW[l] (+)= sum over splits of partial[l][sp], in split order: block (l, j)
+// strides over the float4 outputs of layer l's two matrices.
+__global__ __launch_bounds__(256) void dw_batch_reduce_kernel(DwBatchArgs a, int blocks_per_layer) {
+  const int l = blockIdx.x / blocks_per_layer, j0 = blockIdx.x % blocks_per_layer;
+  const size_t ww = (size_t)a.width * a.width, n4 = ww / 4;
+  const float* part = a.partial + (size_t)l * a.splits * 2 * ww;
+  for (size_t i = j0 * (size_t)256 + threadIdx.x; i < 2 * n4; i += (size_t)blocks_per_layer * 256) {
+    const int m = i >= n4;
+    const size_t j = i - m * n4;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.splits; sp++) acc += ((const f32x4*)(part + ((size_t)sp * 2 + m) * ww))[j];
+    f32x4* dst = (f32x4*)(m ? a.dwo[l] : a.dws[l]) + j;
+    if (a.accumulate) acc += *dst;
+    store_wt16(dst, __builtin_bit_cast(u32x4, acc));
+  }
 }
 
 // dW (+)= sum over splits, in split order; `block` of `nblocks`, `nthreads`
@@ -729,67 +787,12 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float* __restrict_
   dw_reduce_block(partial, dws, dwo, splits, ww, accumulate, blockIdx.x, gridDim.x, blockDim.x);
 }
 
-// One backward layer of a hypercube layer in one launch, three roles:
-//  - red_blocks blocks finish another layer's weight gradients from its
-//    complete split partials (red_partial; none when red_blocks is 0);
-//  - dx_blocks blocks compute dX = dY W_self + partner dY W_off from
-//    transposed weight copies (the 8-wave mix configuration);
-//  - dw_blocks blocks write this layer's split-K weight-gradient partials.
-// No role reads what another writes, so they need no ordering; one launch
-// instead of three saves two kernel boundaries (dispatch ramp, drain and L2
-// writeback) per layer.  Launch order dW, dX, reduction: the dW blocks are
-// the longest, and interleaving roles slowed the dX blocks.  The dX and dW counts are
-// padded to multiples of 8 with idle blocks, so that role-local index and
-// launch index agree modulo 8 and every role keeps its XCD deal.
-constexpr int BWD_THREADS = 512;
-__host__ __device__ constexpr int round8(int v) { return (v + 7) / 8 * 8; }
-template <bool BIDIR>
-__global__ __launch_bounds__(BWD_THREADS) void bwd_layer_kernel(
-    const bf16* __restrict__ dY, const bf16* __restrict__ WtS, const bf16* __restrict__ WtO,
-    const bf16* __restrict__ X, bf16* __restrict__ dX, float* __restrict__ partial, int pairs,
-    int width, int d, int n, int pairs_per_group, int dx_blocks, int dw_blocks,
-    const float* __restrict__ red_partial, float* __restrict__ red_dws,
-    float* __restrict__ red_dwo, int red_splits, int red_accumulate, int red_blocks) {
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
-  int b = blockIdx.x;
-  const int dx_slots = round8(dx_blocks);
-  const int tail = dx_slots + round8(dw_blocks);
-  if (b >= tail) {
-    b -= tail;
-    if (b < red_blocks)
-      dw_reduce_block(red_partial, red_dws, red_dwo, red_splits, (size_t)width * width,
-                      red_accumulate, b, red_blocks, BWD_THREADS);
-    return;
-  }
-  {  // dW blocks first: launch block b < dw_slots is dW block b
-    const int dw_slots = round8(dw_blocks);
-    b = b < dw_slots ? b + dx_slots : b - dw_slots;
-  }
-  if (b < dx_slots) {
-    if (b < dx_blocks)
-      mix_bf16_block<128, 128, 2, 4, 64, 2, true, BIDIR, false>(dY, WtS, WtO, dX, pairs, width,
-                                                                d, b, smem);
-  } else if (b - dx_slots < dw_blocks) {
-    dw_bf16_block<128, 128, 2, 2, BIDIR ? LINK_BIDIR : LINK_CAUSAL>(
-        X, dY, partial, pairs, width, d, n, pairs_per_group, b - dx_slots, dw_blocks, smem);
-  }
-}
-
-
 // ---- launch configurations ----
 constexpr int MIX_BMP = 128;          // 256 rows per block
 constexpr int MIX_BK = 64;            // contraction slice per pipeline stage
 constexpr int MIX_NS = 2;             // pipeline stages in LDS
 constexpr int DW_BO = 128, DW_BC = 128;
 constexpr int DW_TARGET_BLOCKS = 256;  // split-K blocks aimed for (8 waves each)
-// Beside the dX blocks of bwd_layer_kernel: dW blocks for about half the CUs,
-// started first (longest blocks first keeps the tail short), but no more than
-// BWD_DW_MAX_PAIRS row pairs per block, beyond which the dW blocks become the
-// tail.  Measured at 16384 x 512: 8 splits 39.3 us per launch against 43.3
-// with 16; at 32768 x 1024: 4 splits 235.9, 3 splits 235.5, 2 splits 241.8.
-constexpr int BWD_DW_TARGET_BLOCKS = 128;
-constexpr int BWD_DW_MAX_PAIRS = 4096;
-
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool TRANS_B>
 hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int pairs,
                       int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
@@ -968,46 +971,30 @@ hipError_t launch_dw_bf16(const bf16* X, const bf16* dY, float* partial, float* 
   return launch_dw_reduce(DwReduce{partial, dws, dwo, splits, accumulate}, width, st);
 }
 
-bool bwd_layer_fusable(int width, int d) { return d >= 0 && width % 128 == 0; }
+int dw_batch_splits(int rows, int width, int num_layers) {
+  const int tiles = (width / DW_BO) * (width / DW_BC);
+  const int per_split = num_layers * tiles;
+  int splits = (DW_TARGET_BLOCKS + per_split - 1) / per_split;
+  // at least two K-steps per group: rows / 2 pairs over 2 * splits groups
+  const int max_splits = (rows / 2) / (4 * KP);
+  if (splits > max_splits) splits = max_splits;
+  return splits < 1 ? 1 : splits;
+}
 
-hipError_t launch_bwd_layer_bf16(const bf16* X, const bf16* dY, const bf16* wt_self,
-                                 const bf16* wt_off, bf16* dX, float* partial, int rows,
-                                 int width, int d, int n, int bidir, const DwReduce& prev,
-                                 int* splits, hipStream_t st) {
-  using M = MixCfg<128, 128, 2, 4, 64, 2>;
-  using W = DwCfg<128, 128, 2, 2>;
-  static_assert(M::NT == BWD_THREADS && W::NT == BWD_THREADS, "one block size for every role");
-  const int pairs = rows / 2;
-  const int dx_blocks = ((pairs + 127) / 128) * (width / 128);
-  int ppg;
-  const int tiles = (width / 128) * (width / 128);
-  int target = (pairs + BWD_DW_MAX_PAIRS - 1) / BWD_DW_MAX_PAIRS * tiles;
-  if (target < BWD_DW_TARGET_BLOCKS) target = BWD_DW_TARGET_BLOCKS;
-  if (target > DW_TARGET_BLOCKS) target = DW_TARGET_BLOCKS;   // the workspace holds that many
-  *splits = dw_plan(pairs, width, &ppg, target);
-  const int dw_blocks = tiles * *splits;
-  // the reduction's float4 outputs, BWD_THREADS per block, at most one block per CU
-  int red_blocks = 0;
-  if (prev.partial) {
-    red_blocks = (int)((2 * (size_t)width * width / 4 + BWD_THREADS - 1) / BWD_THREADS);
-    if (red_blocks > 256) red_blocks = 256;
-  }
-  const size_t lds_m = (size_t)M::LDS_ELEMS * sizeof(bf16);
-  const size_t lds = lds_m > W::LDS ? lds_m : W::LDS;
-  const int grid = round8(dx_blocks) + round8(dw_blocks) + red_blocks;
-#define HCMIX_BWD(BIDIR)                                                                    \
-  {                                                                                         \
-    auto k = bwd_layer_kernel<BIDIR>;                                                       \
-    static const hipError_t attr = hipFuncSetAttribute(                                     \
-        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
-    if (attr != hipSuccess) return attr;                                                    \
-    k<<<grid, BWD_THREADS, lds, st>>>(dY, wt_self, wt_off, X, dX, partial, pairs, width, d, n, \
-                                      ppg, dx_blocks, dw_blocks, prev.partial, prev.dws,    \
-                                      prev.dwo, prev.splits, prev.accumulate, red_blocks);  \
-  }
-  if (bidir) HCMIX_BWD(true)
-  else HCMIX_BWD(false)
-#undef HCMIX_BWD
+hipError_t launch_dw_batch_bf16(const DwBatchArgs& a, hipStream_t st) {
+  using C = DwCfg<DW_BO, DW_BC, 2, 2>;
+  const int tiles = (a.width / DW_BO) * (a.width / DW_BC);
+  const int blocks = a.num_layers * a.splits * tiles;
+  auto k = dw_batch_kernel<DW_BO, DW_BC, 2, 2>;
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+  if (attr != hipSuccess) return attr;
+  k<<<blocks, C::NT, C::LDS, st>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  int per_layer = (int)((2 * (size_t)a.width * a.width / 4 + 255) / 256);
+  if (per_layer * a.num_layers > 2048) per_layer = (2048 + a.num_layers - 1) / a.num_layers;
+  dw_batch_reduce_kernel<<<per_layer * a.num_layers, 256, 0, st>>>(a, per_layer);
   return hipGetLastError();
 }
 

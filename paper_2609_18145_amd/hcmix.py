@@ -28,6 +28,7 @@ LAYER_NEAR = -1
 EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_forward",
            "hcmix_backward_workspace_bytes", "hcmix_backward", "hcmix_stack_forward",
            "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward",
+           "hcmix_stack_weight_gradients_workspace_bytes", "hcmix_stack_weight_gradients",
            "hcmix_decode_cache_bytes", "hcmix_decode_step")
 
 _lib = None
@@ -72,6 +73,11 @@ def load():
         lib.hcmix_stack_backward.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp, vp, vp,
                                              pp, pp, i32, vp, sz, vp]
         lib.hcmix_stack_backward.restype = i32
+        lib.hcmix_stack_weight_gradients_workspace_bytes.argtypes = [i64, i64, i64, i32, i32]
+        lib.hcmix_stack_weight_gradients_workspace_bytes.restype = sz
+        lib.hcmix_stack_weight_gradients.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp,
+                                                     pp, i32, vp, sz, vp]
+        lib.hcmix_stack_weight_gradients.restype = i32
         lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
@@ -220,6 +226,38 @@ def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dx=None, dws=None, d
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_backward")
     return dx, dws, dwo
+
+
+def weight_gradients_workspace_bytes(batch, n, width, num_layers, dtype) -> int:
+    code = HCMIX_BF16 if dtype == torch.bfloat16 else HCMIX_F32
+    return load().hcmix_stack_weight_gradients_workspace_bytes(batch, n, width, num_layers, code)
+
+
+def stack_weight_gradients(xs, dys, layers, causal, dws=None, dwo=None, accumulate=False,
+                           workspace=None):
+    """Weight gradients of every layer from its input xs[l] and the gradient of
+    its output dys[l], in one library call; returns ([dW_self], [dW_off])."""
+    L = len(layers)
+    x0 = xs[0]
+    _check(x0, *xs[:L], *dys[:L])
+    batch, n, width = x0.shape
+    if dws is None:
+        dws = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+    if dwo is None:
+        dwo = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+    if workspace is None:
+        nbytes = weight_gradients_workspace_bytes(batch, n, width, L, x0.dtype)
+        workspace = (torch.empty(nbytes, dtype=torch.uint8, device=x0.device) if nbytes
+                     else None)
+    ws_bytes = workspace.numel() if workspace is not None else 0
+    rc = load().hcmix_stack_weight_gradients(batch, n, width, L, _layers(layers),
+                                             int(bool(causal)), _dtype_code(x0), _ptrs(xs[:L]),
+                                             _ptrs(dys[:L]), _ptrs(dws), _ptrs(dwo),
+                                             int(bool(accumulate)), _ptr(workspace), ws_bytes,
+                                             _stream(x0))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_stack_weight_gradients")
+    return dws, dwo
 
 
 def decode_cache_bytes(batch, n, width, num_layers, dtype) -> int:

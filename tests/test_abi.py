@@ -145,15 +145,75 @@ def test_stack_forward_rejects_bad_arguments(kw, code):
     assert sfwd(**kw) == code
 
 
+def swg(batch=2, n=16, width=128, L=4, layers=LP, mode=0, dtype=1, xs=None, dys=None, dws=None,
+        dwo=None, wsp=P[7], wsb=1 << 20):
+    xs = xs if xs is not None else PP(P[0], P[0], P[0], P[0])
+    dys = dys if dys is not None else PP(P[1], P[1], P[1], P[1])
+    dws = dws if dws is not None else PP(*[ctypes.c_void_p(P[2].value + k * 0x10000) for k in range(4)])
+    dwo = dwo if dwo is not None else PP(*[ctypes.c_void_p(P[3].value + k * 0x10000) for k in range(4)])
+    return hcmix.load().hcmix_stack_weight_gradients(batch, n, width, L, layers, mode, dtype, xs,
+                                                     dys, dws, dwo, 0, wsp, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), INVALID), (dict(n=12), INVALID),
+    (dict(layers=(ctypes.c_int32 * 4)(0, -1, 2, 3)), INVALID),     # local layer needs causal mode
+    (dict(xs=ctypes.POINTER(ctypes.c_void_p)()), INVALID),        # null array
+    (dict(dys=(ctypes.c_void_p * 4)(P[1].value, P[1].value, None, P[1].value)), INVALID),
+    (dict(dws=PP(P[2], P[2], P[4], P[5])), INVALID),                # two gradients alias
+    (dict(dws=PP(P[0], P[2], P[4], P[5])), INVALID),                # a gradient aliases an input
+    (dict(dws=PP(ctypes.c_void_p(P[2].value + 4), P[4], P[5], P[6])), UNSUPPORTED),   # misaligned
+    (dict(width=96), UNSUPPORTED),
+])
+def test_weight_gradients_reject_bad_arguments(kw, code):
+    assert swg(**kw) == code
+
+
+def test_weight_gradients_check_the_workspace():
+    # 64 windows of 256 x 512, 2 layers: 32 MiB of row-range partials
+    V = lambda a: ctypes.c_void_p(a)  # noqa: E731
+    need = hcmix.load().hcmix_stack_weight_gradients_workspace_bytes(64, 256, 512, 2, 1)
+    assert need == 2 * 8 * 2 * 512 * 512 * 4
+    kw = dict(batch=64, n=256, width=512, L=2, layers=(ctypes.c_int32 * 2)(3, 4),
+              xs=PP(V(0x10000000), V(0x12000000)), dys=PP(V(0x20000000), V(0x22000000)),
+              dws=PP(V(0x30000000), V(0x30400000)), dwo=PP(V(0x31000000), V(0x31400000)),
+              wsp=V(0x40000000), wsb=need)
+    assert swg(**{**kw, "wsb": need - 1}) == INVALID                          # short workspace
+    assert swg(**{**kw, "dwo": PP(V(0x40000000 + 4096), V(0x31400000))}) == INVALID   # aliases it
+    assert swg(**{**kw, "wsp": V(0x40000010)}) == UNSUPPORTED                 # not 256-aligned
+
+
+def test_weight_gradients_workspace_query():
+    lib = hcmix.load()
+    q = lib.hcmix_stack_weight_gradients_workspace_bytes
+    # 16 layers x 16 tiles of 128 x 128 fill the chip: every block covers all rows, no partials
+    assert q(64, 256, 512, 16, hcmix.HCMIX_BF16) == 0
+    # 2 layers: 8 row ranges per layer, their partials
+    assert q(64, 256, 512, 2, hcmix.HCMIX_BF16) == 2 * 8 * 2 * 512 * 512 * 4
+    # width not a multiple of 128, and fp32: the per-layer kernels of hcmix_backward
+    assert q(64, 256, 192, 4, hcmix.HCMIX_BF16) == lib.hcmix_backward_workspace_bytes(
+        64, 256, 192, hcmix.HCMIX_BF16)
+    assert q(2, 16, 32, 4, hcmix.HCMIX_F32) == 0
+    assert q(64, 256, 512, 0, hcmix.HCMIX_BF16) == 0
+
+
 def test_stack_workspace_query():
     lib = hcmix.load()
     fused = lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 8, hcmix.HCMIX_BF16)
     assert fused == 64 * 8 * 2 * 64 * 64 * 4          # per-window partial weight gradients
     wide = lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16)
     layer = lib.hcmix_backward_workspace_bytes(64, 256, 512, hcmix.HCMIX_BF16)
-    # two gradient buffers, two layers' split-K partials (one layer's are summed
-    # inside the next layer's launch), transposed weights of every layer
-    assert wide == 2 * 64 * 256 * 512 * 2 + 2 * layer + 2 * 16 * 512 * 512 * 2
+    act = 64 * 256 * 512 * 2
+    # deferred weight gradients: the 15 intermediate gradients and the transposed
+    # weights of every layer; 16 layers x 16 tiles fill the chip, so no partials
+    assert wide == 15 * act + 2 * 16 * 512 * 512 * 2
+    # two layers: 32 tiles, so 8 row ranges per layer and their partials
+    two = lib.hcmix_stack_backward_workspace_bytes(64, 256, 512, 2, hcmix.HCMIX_BF16)
+    assert two == act + 2 * 2 * 512 * 512 * 2 + 2 * 8 * 2 * 512 * 512 * 4
+    # longer than one chunk of 64 layers: a ring of 65 gradients
+    long = lib.hcmix_stack_backward_workspace_bytes(4, 256, 512, 100, hcmix.HCMIX_BF16)
+    act4 = 4 * 256 * 512 * 2
+    assert long == 65 * act4 + 2 * 100 * 512 * 512 * 2
     # a width that is not a multiple of 128: one layer's partials
     w192 = lib.hcmix_stack_backward_workspace_bytes(64, 256, 192, 4, hcmix.HCMIX_BF16)
     layer192 = lib.hcmix_backward_workspace_bytes(64, 256, 192, hcmix.HCMIX_BF16)
