@@ -87,10 +87,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(workload: str):
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    summary (profiles/traffic_<workload>.json), or None if it was taken on
-    different kernel sources."""
+def profiled_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/traffic_<workload>.json), or None if it was taken on different
+    kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -98,7 +98,7 @@ def profiled_traffic(workload: str):
         rec = json.load(f)
     if rec.get("source_hash") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("bytes_per_launch", {}).get(kernel)
 
 
 def fused_path(n, w, L):
@@ -106,77 +106,92 @@ def fused_path(n, w, L):
     return w == 64 and n in (64, 128, 256) and L <= 64
 
 
-def bwd_layer_path(n, w, L):
-    """Shapes whose stack backward runs one bwd_layer_kernel launch per layer
-    (dX, the layer's weight-gradient partials and the previous layer's
-    reduction), after a transpose of the weights and before a last reduction."""
+def deferred_path(n, w, L):
+    """Shapes whose stack backward runs the dX chain (one mix launch per
+    layer) and then every layer's weight gradients in one dw_batch_kernel
+    launch (bf16, two or more layers, width a multiple of 128)."""
     return not fused_path(n, w, L) and L > 1 and w % 128 == 0
 
 
 def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo, workspace,
                     layers, B, n, w, L, causal):
     """Roofline entries, timed with HIP events on the stream the kernels run
-    on over back-to-back calls: (dominant, forward-launch entry or None).
+    on over back-to-back calls: {name: entry}, the dominant one under
+    "roofline".
 
     Small width (the fused path): the backward stack call (fused_bwd_kernel
     plus its fixed-order partial reduction), against HBM bandwidth; its
     algorithmic bytes are dY, the L saved inputs and dX (bf16), the 2L weight
     matrices (bf16) read and the 2L weight gradients (fp32) written.
-    Layer-by-layer backward on bwd_layer_kernel: that call dominates the step;
-    priced against the bf16 MFMA peak with flops B n L w^2 x 6 causal / x 8
-    bidirectional (dX and both weight gradients).  Beside it, the mix GEMM
-    forward launch (flops B n w^2 x 3 causal / x 4 bidirectional: 2 w^2 for
-    the self map of every position, 2 w^2 for the partner map of each
-    receiver), which is the dominant entry for the other shapes."""
+
+    Wider layers: the mix GEMM (mix_bf16_kernel), which runs every forward
+    layer and every dX and so holds most of the step, timed on its forward
+    instance (hcmix_forward launches of the stack's layers, the launch
+    configuration the stack uses): flops B n w^2 x 3 causal / x 4
+    bidirectional per launch (2 w^2 for the self map of every position, 2 w^2
+    for the partner map of each receiver).  Beside it ("roofline_dw", deferred
+    path only) the all-layer weight-gradient launch (hcmix_stack_weight_
+    gradients, dw_batch_kernel): flops B n L w^2 x 3 causal / x 4 bidirectional
+    (dW_self 2 w^2 per position, dW_off 2 w^2 per receiver)."""
     import torch
     reps = args.kernel_reps
     k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     xs = [x0, *xs_out[:L - 1]]
 
-    def time_backward():
+    def timed(fn, count):
         k0.record(stream)
-        for _ in range(reps):
-            hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0], dws=dws, dwo=dwo,
-                                 workspace=workspace)
+        for _ in range(count):
+            fn()
         k1.record(stream)
         torch.cuda.synchronize()
-        return k0.elapsed_time(k1) / 1e3 / reps
+        return k0.elapsed_time(k1) / 1e3 / count
 
     if fused_path(n, w, L):
-        sec = time_backward()
+        sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
+                                                 dws=dws, dwo=dwo, workspace=workspace), reps)
         act = B * n * w * 2
         nbytes = act * (L + 2) + 2 * L * w * w * 2 + 2 * L * w * w * 4
         gbs = nbytes / sec / 1e9
-        return {"bound": "hbm", "kernel": "fused_bwd_kernel + fused_dw_reduce_kernel "
-                "(one hcmix_stack_backward call)", "achieved": round(gbs, 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                "traffic": profiled_traffic(args.workload), "avg_launch_us": round(sec * 1e6, 2),
-                "algorithmic_bytes": nbytes}, None
-    k0.record(stream)
-    for _ in range(reps):
+        kname = "fused_bwd_kernel + fused_dw_reduce_kernel"
+        return {"roofline": {"bound": "hbm", "kernel": kname + " (one hcmix_stack_backward call)",
+                             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                             "frac": round(gbs / PEAK_HBM_GBS, 4),
+                             "traffic": profiled_traffic(args.workload, kname),
+                             "avg_launch_us": round(sec * 1e6, 2), "algorithmic_bytes": nbytes}}
+
+    def fwd_layers():
         for l in range(L):
             hcmix.forward(xs_out[l - 1] if l else x0, ws[l], wo[l], layers[l], causal,
                           out=xs_out[l])
-    k1.record(stream)
-    torch.cuda.synchronize()
-    sec = k0.elapsed_time(k1) / 1e3 / (reps * L)
+
+    sec = timed(fwd_layers, reps) / L
     flops = B * n * (3 if causal else 4) * w * w
     tflops = flops / sec / 1e12
-    fwd = {"bound": "mfma", "kernel": "mix_bf16_kernel (forward launch)",
-           "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-           "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "avg_launch_us": round(sec * 1e6, 2),
-           "algorithmic_flops": flops}
-    if not bwd_layer_path(n, w, L):
-        fwd["traffic"] = profiled_traffic(args.workload)
-        return fwd, None
-    sec = time_backward()
-    flops = B * n * L * (6 if causal else 8) * w * w
-    tflops = flops / sec / 1e12
-    return {"bound": "mfma", "kernel": f"bwd_layer_kernel x{L} + weight transposes + last "
-            "reduction (one hcmix_stack_backward call)", "achieved": round(tflops, 2),
-            "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": profiled_traffic(args.workload), "avg_launch_us": round(sec * 1e6, 2),
-            "algorithmic_flops": flops}, fwd
+    kname = "mix_bf16_kernel<forward>"
+    out = {"roofline": {"bound": "mfma", "kernel": kname + " (one forward layer launch)",
+                        "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                        "traffic": profiled_traffic(args.workload, kname),
+                        "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops}}
+    if deferred_path(n, w, L):
+        # the saved activations stand in for the output gradients: the same
+        # shapes and magnitudes, and the kernel's work does not depend on values
+        gs = [*xs_out[1:L], dy]
+        sec = timed(lambda: hcmix.stack_weight_gradients(xs, gs, layers, causal, dws=dws,
+                                                         dwo=dwo), reps)
+        flops = B * n * L * (3 if causal else 4) * w * w
+        tflops = flops / sec / 1e12
+        kname = "dw_batch_kernel"
+        out["roofline_dw"] = {"bound": "mfma", "kernel": kname + f" (weight gradients of all {L} "
+                              "layers, one launch)", "achieved": round(tflops, 2),
+                              "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                              "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                              "traffic": profiled_traffic(args.workload, kname),
+                              "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops}
+    sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
+                                             dws=dws, dwo=dwo, workspace=workspace), reps)
+    out["backward_call_us"] = round(sec * 1e6, 2)
+    return out
 
 
 def main():
@@ -249,9 +264,8 @@ def main():
         gpu_s = e0.elapsed_time(e1) / 1e3
         t = max(wall, gpu_s)
 
-        roofline, roofline_fwd = dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out,
-                                                 dx_out, dws, dwo, workspace, s.layers, B, n, w,
-                                                 L, causal)
+        kernels = dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo,
+                                  workspace, s.layers, B, n, w, L, causal)
 
     if args.calib_copy_mb > 0:
         src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device=dev)
@@ -274,10 +288,8 @@ def main():
                    "graph": bool(args.graph)},
         "pct_bf16_peak": round(flops / t * args.steps / 1e12 / PEAK_BF16_TFLOPS * 100, 2),
         "pct_hbm": round(nbytes / t * args.steps / 1e9 / PEAK_HBM_GBS * 100, 2),
-        "roofline": roofline,
     }
-    if roofline_fwd is not None:
-        out["roofline_fwd"] = roofline_fwd
+    out.update(kernels)
     if args.cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(s, n, w, L, causal, args.cpu_windows)
     print(json.dumps(out), flush=True)
