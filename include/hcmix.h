@@ -236,6 +236,37 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
                                const void* const* w_self, const void* const* w_off, void* cache,
                                size_t cache_bytes, void* y, void* stream);
 
+/* ---- Causal multi-head softmax attention (the hybrids' attention layers) ----
+ *
+ * The hybrid schedules (Section 3.3; the window-256 hybrid of Appendix A keeps
+ * two attention layers among sixteen) replace some sparse layers with standard
+ * multi-head attention.  These entry points are its core, per window and head:
+ *   S = Q K^T / sqrt(64), S[i][j] = -inf for j > i (a position sees itself and
+ *   the past), P = row softmax of S, out = P V,
+ * for windows of n positions (n a multiple of 32, at most 256), head dimension
+ * 64, bf16 in and out with fp32 accumulation.  The projections around it are
+ * plain GEMMs and stay with the caller.
+ *   qkv:  [batch][n][3][heads][64] bf16, Q, K, V of every position (the
+ *         [batch, n, 3 * heads * 64] output of a QKV projection).
+ *   out:  [batch][n][heads][64] bf16.
+ *   lse:  fp32 [batch][heads][n], the natural log of each query row's softmax
+ *         denominator, log sum_j exp(S[i][j]); written by the forward, read by
+ *         the backward.
+ * HCMIX_ERR_INVALID_VALUE: null pointers, batch, heads or n < 1, an output
+ * overlapping an input or another output.  HCMIX_ERR_UNSUPPORTED: head_dim !=
+ * 64, n not a multiple of 32 or above 256, bf16 pointers not 16-byte aligned,
+ * lse not 4-byte aligned. */
+hcmix_status hcmix_attention_forward(int64_t batch, int64_t n, int32_t heads, int32_t head_dim,
+                                     const void* qkv, void* out, float* lse, void* stream);
+
+/* Backward: dqkv [batch][n][3][heads][64] bf16, the gradients of Q, K and V,
+ * from qkv, the forward's out and lse, and dout = dL/dout:
+ *   dV = P^T dout, dS = P * (dout V^T - rowsum(dout * out)),
+ *   dQ = dS K / 8, dK = dS^T Q / 8. */
+hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, int32_t head_dim,
+                                      const void* qkv, const void* out, const float* lse,
+                                      const void* dout, void* dqkv, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

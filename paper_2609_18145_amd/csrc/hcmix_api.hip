@@ -614,6 +614,53 @@ hcmix_status hcmix_stack_weight_gradients(int64_t batch, int64_t n, int64_t widt
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
+// Shape checks of the attention entry points.
+hcmix_status check_attention(int64_t batch, int64_t n, int32_t heads, int32_t head_dim) {
+  if (batch < 1 || n < 1 || heads < 1) return HCMIX_ERR_INVALID_VALUE;
+  if (batch > kMaxRows / n || heads > 1024) return HCMIX_ERR_INVALID_VALUE;
+  if (head_dim != 64 || n % 32 != 0 || n > 256) return HCMIX_ERR_UNSUPPORTED;
+  return HCMIX_OK;
+}
+
+hcmix_status hcmix_attention_forward(int64_t batch, int64_t n, int32_t heads, int32_t head_dim,
+                                     const void* qkv, void* out, float* lse, void* stream) {
+  if (!qkv || !out || !lse) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_attention(batch, n, heads, head_dim);
+  if (st != HCMIX_OK) return st;
+  const size_t rows = (size_t)(batch * n);
+  const Span ins[1] = {{qkv, rows * 3 * heads * 64 * sizeof(bf16)}};
+  const Span outs[2] = {{out, rows * heads * 64 * sizeof(bf16)},
+                        {lse, rows * heads * sizeof(float)}};
+  st = check_spans(ins, 1, outs, 1, 16);
+  if (st != HCMIX_OK) return st;
+  st = check_spans(ins, 1, outs + 1, 1, 4);
+  if (st != HCMIX_OK) return st;
+  if (overlaps(out, outs[0].n, lse, outs[1].n)) return HCMIX_ERR_INVALID_VALUE;
+  hipError_t e = launch_attention_fwd_bf16((const bf16*)qkv, (bf16*)out, lse, (int)batch, (int)n,
+                                           heads, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, int32_t head_dim,
+                                      const void* qkv, const void* out, const float* lse,
+                                      const void* dout, void* dqkv, void* stream) {
+  if (!qkv || !out || !lse || !dout || !dqkv) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_attention(batch, n, heads, head_dim);
+  if (st != HCMIX_OK) return st;
+  const size_t rows = (size_t)(batch * n);
+  const size_t act = rows * heads * 64 * sizeof(bf16);
+  const Span ins[3] = {{qkv, 3 * act}, {out, act}, {dout, act}};
+  const Span outs[1] = {{dqkv, 3 * act}};
+  st = check_spans(ins, 3, outs, 1, 16);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(lse, 4)) return HCMIX_ERR_UNSUPPORTED;
+  if (overlaps(dqkv, 3 * act, lse, rows * heads * sizeof(float))) return HCMIX_ERR_INVALID_VALUE;
+  hipError_t e = launch_attention_bwd_bf16((const bf16*)qkv, (const bf16*)out, lse,
+                                           (const bf16*)dout, (bf16*)dqkv, (int)batch, (int)n,
+                                           heads, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                 int32_t dtype) {
   if (num_layers < 1 || num_layers > kMaxLayers) return 0;

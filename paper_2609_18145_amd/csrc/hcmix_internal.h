@@ -141,6 +141,15 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r
 // x_in / x_partner / record / out are row bases of window 0; window b is at
 // + b * stride elements.  x_partner null: the position takes no partner.
 // record (may be null): where the layer's input is written for later positions.
+// Causal multi-head attention, bf16, head dimension 64, n a multiple of 32
+// up to 256: qkv [batch][n][3][heads][64], out / dout [batch][n][heads][64],
+// lse [batch][heads][n] fp32.
+hipError_t launch_attention_fwd_bf16(const bf16* qkv, bf16* out, float* lse, int batch, int n,
+                                     int heads, hipStream_t st);
+hipError_t launch_attention_bwd_bf16(const bf16* qkv, const bf16* out, const float* lse,
+                                     const bf16* dout, bf16* dqkv, int batch, int n, int heads,
+                                     hipStream_t st);
+
 struct DecodeLayerArgs {
   const bf16* x_in;
   const bf16* x_partner;

@@ -29,7 +29,8 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_backward_workspace_bytes", "hcmix_backward", "hcmix_stack_forward",
            "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward",
            "hcmix_stack_weight_gradients_workspace_bytes", "hcmix_stack_weight_gradients",
-           "hcmix_decode_cache_bytes", "hcmix_decode_step")
+           "hcmix_decode_cache_bytes", "hcmix_decode_step", "hcmix_attention_forward",
+           "hcmix_attention_backward")
 
 _lib = None
 
@@ -78,6 +79,10 @@ def load():
         lib.hcmix_stack_weight_gradients.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp,
                                                      pp, i32, vp, sz, vp]
         lib.hcmix_stack_weight_gradients.restype = i32
+        lib.hcmix_attention_forward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp]
+        lib.hcmix_attention_forward.restype = i32
+        lib.hcmix_attention_backward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp, vp, vp]
+        lib.hcmix_attention_backward.restype = i32
         lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
@@ -258,6 +263,51 @@ def stack_weight_gradients(xs, dys, layers, causal, dws=None, dwo=None, accumula
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_weight_gradients")
     return dws, dwo
+
+
+def attention_forward(qkv, out=None, lse=None):
+    """Causal multi-head attention core: qkv [batch, n, 3, heads, 64] bf16 ->
+    (out [batch, n, heads, 64] bf16, lse [batch, heads, n] fp32)."""
+    _check(qkv)
+    batch, n, three, heads, hd = qkv.shape
+    assert three == 3
+    if out is None:
+        out = torch.empty((batch, n, heads, hd), dtype=qkv.dtype, device=qkv.device)
+    if lse is None:
+        lse = torch.empty((batch, heads, n), dtype=torch.float32, device=qkv.device)
+    rc = load().hcmix_attention_forward(batch, n, heads, hd, _ptr(qkv), _ptr(out), _fptr(lse),
+                                        _stream(qkv))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_attention_forward")
+    return out, lse
+
+
+def attention_backward(qkv, out, lse, dout, dqkv=None):
+    """Gradient of qkv ([batch, n, 3, heads, 64]) given dout = dL/dout."""
+    _check(qkv, out, dout)
+    batch, n, three, heads, hd = qkv.shape
+    if dqkv is None:
+        dqkv = torch.empty_like(qkv)
+    rc = load().hcmix_attention_backward(batch, n, heads, hd, _ptr(qkv), _ptr(out), _fptr(lse),
+                                         _ptr(dout), _ptr(dqkv), _stream(qkv))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_attention_backward")
+    return dqkv
+
+
+class Attention(torch.autograd.Function):
+    """The attention core as an autograd function over qkv."""
+
+    @staticmethod
+    def forward(ctx, qkv):
+        out, lse = attention_forward(qkv.contiguous())
+        ctx.save_for_backward(qkv, out, lse)
+        return out
+
+    @staticmethod
+    def backward(ctx, gout):
+        qkv, out, lse = ctx.saved_tensors
+        return attention_backward(qkv, out, lse, gout.contiguous())
 
 
 def decode_cache_bytes(batch, n, width, num_layers, dtype) -> int:

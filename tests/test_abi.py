@@ -197,6 +197,40 @@ def test_weight_gradients_workspace_query():
     assert q(64, 256, 512, 0, hcmix.HCMIX_BF16) == 0
 
 
+def att(batch=2, n=64, heads=2, hd=64, qkv=P[0], out=P[1], lse=P[2]):
+    fp = ctypes.cast(lse, ctypes.POINTER(ctypes.c_float)) if lse is not None else None
+    return hcmix.load().hcmix_attention_forward(batch, n, heads, hd, qkv, out, fp, None)
+
+
+def attb(batch=2, n=64, heads=2, hd=64, qkv=P[0], out=P[1], lse=P[2], dout=P[3], dqkv=P[4]):
+    fp = ctypes.cast(lse, ctypes.POINTER(ctypes.c_float)) if lse is not None else None
+    return hcmix.load().hcmix_attention_backward(batch, n, heads, hd, qkv, out, fp, dout, dqkv,
+                                                 None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=0), INVALID), (dict(n=0), INVALID), (dict(heads=0), INVALID),
+    (dict(qkv=None), INVALID), (dict(out=None), INVALID), (dict(lse=None), INVALID),
+    (dict(out=P[0]), INVALID),                                   # out aliases qkv
+    (dict(lse=ctypes.c_void_p(P[1].value + 64)), INVALID),       # lse inside out
+    (dict(hd=32), UNSUPPORTED), (dict(n=48), UNSUPPORTED), (dict(n=288), UNSUPPORTED),
+    (dict(out=ctypes.c_void_p(P[1].value + 8)), UNSUPPORTED),    # misaligned
+])
+def test_attention_forward_rejects_bad_arguments(kw, code):
+    assert att(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dout=None), INVALID), (dict(dqkv=None), INVALID),
+    (dict(dqkv=P[3]), INVALID),                                  # dqkv aliases dout
+    (dict(dqkv=ctypes.c_void_p(P[2].value - 4096)), INVALID),    # dqkv covers lse
+    (dict(hd=128), UNSUPPORTED), (dict(n=40), UNSUPPORTED),
+    (dict(lse=ctypes.c_void_p(P[2].value + 2)), UNSUPPORTED),
+])
+def test_attention_backward_rejects_bad_arguments(kw, code):
+    assert attb(**kw) == code
+
+
 def test_stack_workspace_query():
     lib = hcmix.load()
     fused = lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 8, hcmix.HCMIX_BF16)
