@@ -72,6 +72,8 @@ def parse():
     ap.add_argument("--cpu-windows", type=int, default=0,
                     help="windows in the oracle sample (0: sized for ~10-30 s)")
     ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--attention", default="native", choices=["native", "sdpa"],
+                    help="hybrid workloads: the library's attention core, or PyTorch SDPA")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -302,9 +304,11 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     (the rotated layers keep d = their index among the rotated layers mod 8),
     or "hy256", the paper's window-256 hybrid schedule string (local layers,
     one causal jump per scale, attention at two of sixteen; weights are the
-    lm256 workload's first 14).  Attention is harness code (PyTorch: QKV
-    projection, scaled-dot-product attention, output projection); the sparse
-    segments are hcmix stack calls.  Forward and backward are chained by hand
+    lm256 workload's first 14).  An attention layer is the QKV projection and
+    the output projection (PyTorch GEMMs) around the library's causal attention
+    core (hcmix_attention_forward / _backward; --attention sdpa swaps in
+    PyTorch's scaled-dot-product attention); the sparse segments are hcmix
+    stack calls.  Forward and backward are chained by hand
     so that every segment is timed with HIP events on one stream; the line
     reports the sparse layers' share of the step and their own throughput."""
     import torch.nn.functional as F
@@ -388,8 +392,11 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     def attention(x, i):
         wqkv, wout = attn_w[i]
         qkv = F.linear(x, wqkv).view(B, n, 3, heads, hd)
-        q, k, v = (qkv[:, :, j].transpose(1, 2).contiguous() for j in range(3))
-        o = sdpa(q, k, v).transpose(1, 2).reshape(B, n, w)
+        if args.attention == "native":
+            o = hcmix.Attention.apply(qkv).reshape(B, n, w)
+        else:
+            q, k, v = (qkv[:, :, j].transpose(1, 2).contiguous() for j in range(3))
+            o = sdpa(q, k, v).transpose(1, 2).reshape(B, n, w)
         return F.linear(o, wout)
 
     wsp = {}
@@ -452,6 +459,23 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     sparse = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "sparse") / 1e3
     attn = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "attn") / 1e3
     pl = B * n * Ls
+    core_us = None
+    if args.attention == "native":
+        # the attention core alone (forward + backward of one layer), back to back
+        gen_q = torch.Generator(device="cpu").manual_seed(2)
+        qkv = torch.randn(B, n, 3, heads, hd, generator=gen_q).to(dt).to(dev)
+        gout = torch.randn(B, n, heads, hd, generator=gen_q).to(dt).to(dev)
+        o_, l_ = hcmix.attention_forward(qkv)
+        hcmix.attention_backward(qkv, o_, l_, gout)
+        c2, c3 = ev(enable_timing=True), ev(enable_timing=True)
+        c2.record(stream)
+        for _ in range(args.kernel_reps):
+            o_, l_ = hcmix.attention_forward(qkv, out=o_, lse=l_)
+            hcmix.attention_backward(qkv, o_, l_, gout)
+        c3.record(stream)
+        torch.cuda.synchronize()
+        core_us = round(c2.elapsed_time(c3) * 1e3 / args.kernel_reps, 2)
+        backend["name"] = "hcmix_attention (library kernels)"
     out = {
         "metric": METRIC, "value": round(pl * args.steps / sparse, 1), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
@@ -463,6 +487,7 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
                    "sparse_ms": round(sparse / args.steps * 1e3, 4),
                    "attention_ms": round(attn / args.steps * 1e3, 4),
+                   "attention_core_fwd_bwd_us_per_layer": core_us,
                    "sparse_share_of_step": round(sparse / total, 4),
                    "note": "value = sparse positions*layers per second of sparse-layer time; "
                            "eager launches, each segment timed with HIP events"},
