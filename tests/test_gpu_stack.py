@@ -37,8 +37,8 @@ def run_gpu_stack(s, with_backward=True):
             for k, v in out.items()}
 
 
-def check_stack(s, got, windows=None, with_dw=True):
-    tol = TOL[s.dtype]
+def check_stack(s, got, windows=None, with_dw=True, tol=None):
+    tol = TOL[s.dtype] if tol is None else tol
     sel = slice(None) if windows is None else windows
     x = s.x[sel]
     xs = oracle.stack_forward(x, s.w_self, s.w_off, s.layers, s.causal)
@@ -226,4 +226,27 @@ def test_layer_by_layer_backward_ragged_rows(causal):
     s = inputs.make_stack(batch=3, n=64, width=256, num_layers=6, causal=causal, dtype="bf16",
                           seed=12)
     log(f"case: layer-by-layer bf16 backward, B=3 n=64 w=256 L=6 causal={causal}, seed 12")
+    check_stack(s, run_gpu_stack(s))
+
+
+def test_deferred_backward_longer_than_one_chunk():
+    """bf16 stack of 66 rotated causal layers (width 128): the deferred path
+    keeps a ring of 65 gradients and forms the weight gradients in two
+    launches (64 + 2 layers); every output against the oracle.  The bf16
+    storage of each layer's output is a rounding step, and over a stack these
+    compound like a random walk (about sqrt(L) 2^-9 per row), so the bound of
+    the 2e-2 workloads (at most 24 layers) is scaled by sqrt(L / 24) here."""
+    L = 66
+    s = inputs.make_stack(batch=1, n=64, width=128, num_layers=L, causal=True, dtype="bf16",
+                          seed=13)
+    log(f"case: deferred backward, B=1 n=64 w=128 L={L} causal, seed 13")
+    check_stack(s, run_gpu_stack(s), tol=TOL["bf16"] * (L / 24) ** 0.5)
+
+
+def test_deferred_backward_bidirectional_short_stack():
+    """Bidirectional deferred path on a two-layer stack (row ranges and the
+    fixed-order sum of the weight-gradient launch), against the oracle."""
+    s = inputs.make_stack(batch=8, n=256, width=256, num_layers=2, causal=False, dtype="bf16",
+                          seed=14)
+    log("case: deferred backward, B=8 n=256 w=256 L=2 bidirectional, seed 14")
     check_stack(s, run_gpu_stack(s))
