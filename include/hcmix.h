@@ -267,6 +267,41 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
                                       const void* qkv, const void* out, const float* lse,
                                       const void* dout, void* dqkv, void* stream);
 
+/* ---- Token embedding, output head and cross-entropy (language-model workloads) ----
+ *
+ * Section 5 trains character-level language models and reports bits per
+ * character, the mean next-symbol cross-entropy.  These entry points are the
+ * model's input and output ends around the sparse stack:
+ *   x[r] = table[tokens[r]],        dtable[v] (+)= sum of dx[r] over tokens[r] == v,
+ *   logits[r] = W x[r] + bias,      loss[r] = log sum_v exp(logits[r][v]) - logits[r][targets[r]],
+ *   dlogits[r] = scale (softmax(logits[r]) - onehot(targets[r]))   (scale = 1/rows: mean loss).
+ * rows = batch * n positions; table and W are [vocab][width] bf16, x and dx
+ * [rows][width] bf16, tokens and targets int32 [rows], bias, loss and dtable
+ * fp32, dlogits [rows][vocab] bf16 (the gradients of W, bias and x then are
+ * plain products with it: dlogits^T x, its column sums, dlogits W).
+ * bf16 only; width a multiple of 64; head: vocab a multiple of 32 up to 256.
+ * A token outside [0, vocab) embeds as a zero row and is skipped by the
+ * backward; a target outside it contributes log sum exp alone.  The embedding
+ * backward sums in a fixed order (bitwise-repeatable) through a workspace of
+ * hcmix_embedding_backward_workspace_bytes (256-byte aligned).
+ * HCMIX_ERR_INVALID_VALUE: null pointers, rows, width or vocab < 1, an output
+ * overlapping an input or another output, a short workspace.
+ * HCMIX_ERR_UNSUPPORTED: other shapes, bf16 pointers not 16-byte aligned, fp32
+ * and int32 pointers not 16-byte (bias) or 4-byte aligned. */
+hcmix_status hcmix_embedding_forward(int64_t rows, int64_t width, int32_t vocab, const void* table,
+                                     const int32_t* tokens, void* x, void* stream);
+
+size_t hcmix_embedding_backward_workspace_bytes(int64_t rows, int64_t width, int32_t vocab);
+
+hcmix_status hcmix_embedding_backward(int64_t rows, int64_t width, int32_t vocab,
+                                      const int32_t* tokens, const void* dx, float* dtable,
+                                      int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                      void* stream);
+
+hcmix_status hcmix_head_cross_entropy(int64_t rows, int64_t width, int32_t vocab, const void* x,
+                                      const void* w, const float* bias, const int32_t* targets,
+                                      float scale, float* loss, void* dlogits, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

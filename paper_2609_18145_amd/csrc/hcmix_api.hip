@@ -661,6 +661,79 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
+// Shape checks of the language-model entry points.
+hcmix_status check_lm(int64_t rows, int64_t width, int32_t vocab) {
+  if (rows < 1 || width < 1 || vocab < 1) return HCMIX_ERR_INVALID_VALUE;
+  if (rows > kMaxRows || vocab > (1 << 20) || width > (1 << 16)) return HCMIX_ERR_INVALID_VALUE;
+  if (width % 64 != 0) return HCMIX_ERR_UNSUPPORTED;
+  return HCMIX_OK;
+}
+
+hcmix_status hcmix_embedding_forward(int64_t rows, int64_t width, int32_t vocab, const void* table,
+                                     const int32_t* tokens, void* x, void* stream) {
+  if (!table || !tokens || !x) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_lm(rows, width, vocab);
+  if (st != HCMIX_OK) return st;
+  const Span ins[2] = {{table, (size_t)vocab * width * sizeof(bf16)},
+                       {tokens, (size_t)rows * sizeof(int32_t)}};
+  const Span outs[1] = {{x, (size_t)rows * width * sizeof(bf16)}};
+  st = check_spans(ins, 2, outs, 1, 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(table, 16) || !aligned(x, 16)) return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = launch_embedding_fwd((const bf16*)table, (const int*)tokens, (bf16*)x, (int)rows,
+                                      (int)width, vocab, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+size_t hcmix_embedding_backward_workspace_bytes(int64_t rows, int64_t width, int32_t vocab) {
+  if (check_lm(rows, width, vocab) != HCMIX_OK) return 0;
+  return align256(embedding_workspace_bytes((int)rows, (int)width, vocab));
+}
+
+hcmix_status hcmix_embedding_backward(int64_t rows, int64_t width, int32_t vocab,
+                                      const int32_t* tokens, const void* dx, float* dtable,
+                                      int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+  if (!tokens || !dx || !dtable || !workspace) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_lm(rows, width, vocab);
+  if (st != HCMIX_OK) return st;
+  const size_t need = embedding_workspace_bytes((int)rows, (int)width, vocab);
+  if (workspace_bytes < need) return HCMIX_ERR_INVALID_VALUE;
+  const Span ins[2] = {{tokens, (size_t)rows * sizeof(int32_t)},
+                       {dx, (size_t)rows * width * sizeof(bf16)}};
+  const Span outs[2] = {{dtable, (size_t)vocab * width * sizeof(float)}, {workspace, need}};
+  st = check_spans(ins, 2, outs, 2, 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(dx, 16) || !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = launch_embedding_bwd((const int*)tokens, (const bf16*)dx, dtable,
+                                      accumulate != 0, (float*)workspace, (int)rows, (int)width,
+                                      vocab, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+hcmix_status hcmix_head_cross_entropy(int64_t rows, int64_t width, int32_t vocab, const void* x,
+                                      const void* w, const float* bias, const int32_t* targets,
+                                      float scale, float* loss, void* dlogits, void* stream) {
+  if (!x || !w || !bias || !targets || !loss || !dlogits) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_lm(rows, width, vocab);
+  if (st != HCMIX_OK) return st;
+  if (vocab % 32 != 0 || vocab > 256) return HCMIX_ERR_UNSUPPORTED;
+  const Span ins[4] = {{x, (size_t)rows * width * sizeof(bf16)},
+                       {w, (size_t)vocab * width * sizeof(bf16)},
+                       {bias, (size_t)vocab * sizeof(float)},
+                       {targets, (size_t)rows * sizeof(int32_t)}};
+  const Span outs[2] = {{loss, (size_t)rows * sizeof(float)},
+                        {dlogits, (size_t)rows * vocab * sizeof(bf16)}};
+  st = check_spans(ins, 4, outs, 2, 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(bias, 16) || !aligned(dlogits, 16))
+    return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = launch_head_ce((const bf16*)x, (const bf16*)w, bias, (const int*)targets, scale,
+                                loss, (bf16*)dlogits, (int)rows, (int)width, vocab,
+                                (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                 int32_t dtype) {
   if (num_layers < 1 || num_layers > kMaxLayers) return 0;

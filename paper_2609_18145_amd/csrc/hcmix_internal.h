@@ -150,6 +150,18 @@ hipError_t launch_attention_bwd_bf16(const bf16* qkv, const bf16* out, const flo
                                      const bf16* dout, bf16* dqkv, int batch, int n, int heads,
                                      hipStream_t st);
 
+// Language-model harness kernels (bf16, width % 64 == 0): embedding gather and
+// its fixed-order scatter sum (workspace embedding_workspace_bytes), fused
+// output head + cross-entropy (vocab a multiple of 32 up to 256).
+size_t embedding_workspace_bytes(int rows, int width, int vocab);
+hipError_t launch_embedding_fwd(const bf16* table, const int* tokens, bf16* x, int rows,
+                                int width, int vocab, hipStream_t st);
+hipError_t launch_embedding_bwd(const int* tokens, const bf16* dx, float* dtable, int accumulate,
+                                float* workspace, int rows, int width, int vocab, hipStream_t st);
+hipError_t launch_head_ce(const bf16* x, const bf16* w, const float* bias, const int* targets,
+                          float scale, float* loss, bf16* dlogits, int rows, int width, int vocab,
+                          hipStream_t st);
+
 struct DecodeLayerArgs {
   const bf16* x_in;
   const bf16* x_partner;

@@ -30,7 +30,9 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward",
            "hcmix_stack_weight_gradients_workspace_bytes", "hcmix_stack_weight_gradients",
            "hcmix_decode_cache_bytes", "hcmix_decode_step", "hcmix_attention_forward",
-           "hcmix_attention_backward")
+           "hcmix_attention_backward", "hcmix_embedding_forward",
+           "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
+           "hcmix_head_cross_entropy")
 
 _lib = None
 
@@ -83,6 +85,15 @@ def load():
         lib.hcmix_attention_forward.restype = i32
         lib.hcmix_attention_backward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp, vp, vp]
         lib.hcmix_attention_backward.restype = i32
+        lib.hcmix_embedding_forward.argtypes = [i64, i64, i32, vp, vp, vp, vp]
+        lib.hcmix_embedding_forward.restype = i32
+        lib.hcmix_embedding_backward_workspace_bytes.argtypes = [i64, i64, i32]
+        lib.hcmix_embedding_backward_workspace_bytes.restype = sz
+        lib.hcmix_embedding_backward.argtypes = [i64, i64, i32, vp, vp, fp, i32, vp, sz, vp]
+        lib.hcmix_embedding_backward.restype = i32
+        lib.hcmix_head_cross_entropy.argtypes = [i64, i64, i32, vp, vp, fp, vp, ctypes.c_float,
+                                                 fp, vp, vp]
+        lib.hcmix_head_cross_entropy.restype = i32
         lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
@@ -293,6 +304,54 @@ def attention_backward(qkv, out, lse, dout, dqkv=None):
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_attention_backward")
     return dqkv
+
+
+def embedding_forward(table, tokens, out=None):
+    """x[r] = table[tokens[r]]: table [vocab, width] bf16, tokens int32 (any shape)."""
+    if tokens.dtype != torch.int32 or not tokens.is_contiguous() or not table.is_contiguous():
+        raise ValueError("tokens must be contiguous int32, table contiguous")
+    vocab, width = table.shape
+    rows = tokens.numel()
+    if out is None:
+        out = torch.empty((*tokens.shape, width), dtype=table.dtype, device=table.device)
+    rc = load().hcmix_embedding_forward(rows, width, vocab, _ptr(table), _ptr(tokens), _ptr(out),
+                                        _stream(table))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_embedding_forward")
+    return out
+
+
+def embedding_backward(tokens, dx, vocab, dtable=None, accumulate=False, workspace=None):
+    """dtable[v] (+)= sum of dx rows whose token is v (fp32 [vocab, width])."""
+    width = dx.shape[-1]
+    rows = tokens.numel()
+    if dtable is None:
+        dtable = torch.empty((vocab, width), dtype=torch.float32, device=dx.device)
+    nbytes = load().hcmix_embedding_backward_workspace_bytes(rows, width, vocab)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dx.device)
+    rc = load().hcmix_embedding_backward(rows, width, vocab, _ptr(tokens), _ptr(dx), _fptr(dtable),
+                                         int(bool(accumulate)), _ptr(workspace),
+                                         workspace.numel(), _stream(dx))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_embedding_backward")
+    return dtable
+
+
+def head_cross_entropy(x, w, bias, targets, scale, loss=None, dlogits=None):
+    """Per-row loss (fp32 [rows]) and scale * (softmax - onehot) (bf16 [rows, vocab])."""
+    vocab, width = w.shape
+    rows = targets.numel()
+    if loss is None:
+        loss = torch.empty(rows, dtype=torch.float32, device=x.device)
+    if dlogits is None:
+        dlogits = torch.empty((rows, vocab), dtype=x.dtype, device=x.device)
+    rc = load().hcmix_head_cross_entropy(rows, width, vocab, _ptr(x), _ptr(w), _fptr(bias),
+                                         _ptr(targets), float(scale), _fptr(loss), _ptr(dlogits),
+                                         _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_head_cross_entropy")
+    return loss, dlogits
 
 
 class Attention(torch.autograd.Function):

@@ -231,6 +231,34 @@ def test_attention_backward_rejects_bad_arguments(kw, code):
     assert attb(**kw) == code
 
 
+def test_lm_entry_points_reject_bad_arguments():
+    lib = hcmix.load()
+    fp = lambda p: ctypes.cast(p, ctypes.POINTER(ctypes.c_float))  # noqa: E731
+    ef = lib.hcmix_embedding_forward
+    assert ef(0, 64, 16, P[0], P[1], P[2], None) == INVALID
+    assert ef(10, 64, 16, None, P[1], P[2], None) == INVALID
+    assert ef(10, 64, 16, P[0], P[1], P[0], None) == INVALID          # x aliases the table
+    assert ef(10, 96, 16, P[0], P[1], P[2], None) == UNSUPPORTED      # width % 64
+    assert ef(10, 64, 16, P[0], P[1], ctypes.c_void_p(P[2].value + 4), None) == UNSUPPORTED
+    need = lib.hcmix_embedding_backward_workspace_bytes(1000, 64, 16)
+    assert need == 8 * 16 * 64 * 4
+    assert lib.hcmix_embedding_backward_workspace_bytes(100000, 64, 16) == 25 * 16 * 64 * 4
+    eb = lib.hcmix_embedding_backward
+    assert eb(1000, 64, 16, P[0], P[1], fp(P[2]), 0, P[3], need - 1, None) == INVALID
+    assert eb(1000, 64, 16, P[0], P[1], fp(P[1]), 0, P[3], need, None) == INVALID   # dtable = dx
+    assert eb(1000, 64, 16, P[0], P[1], fp(P[2]), 0, ctypes.c_void_p(P[3].value + 16), need,
+              None) == UNSUPPORTED
+    hc = lib.hcmix_head_cross_entropy
+    args = [P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[5], None]
+    assert hc(100, 64, 0, *args) == INVALID
+    assert hc(100, 64, 48, *args) == UNSUPPORTED                      # vocab % 32
+    assert hc(100, 64, 288, *args) == UNSUPPORTED                     # vocab > 256
+    assert hc(100, 64, 256, P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[4],
+              None) == INVALID                                        # dlogits over the loss
+    assert hc(100, 64, 256, P[0], P[1], fp(ctypes.c_void_p(P[2].value + 4)), P[3],
+              ctypes.c_float(0.5), fp(P[4]), P[5], None) == UNSUPPORTED   # bias alignment
+
+
 def test_stack_workspace_query():
     lib = hcmix.load()
     fused = lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 8, hcmix.HCMIX_BF16)
