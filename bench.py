@@ -37,6 +37,9 @@ WORKLOADS = {
                "softmax attention layers (8 heads x 64) at slots 3 and 9 of 18, bf16, fwd+bwd"),
     "decode256": ("decode: window n=256, width 512, batch 64, 16 rotated causal layers, bf16; "
                   "positions 0..255 one step each (all windows, every layer)"),
+    "lm256_step": ("window n=256, width 512, batch 64, 16 rotated causal layers, bf16: the whole "
+                   "language-model training step, Zipf byte-token embedding, the stack forward and "
+                   "backward, 256-way output head with bias and cross-entropy"),
     "hy256": ("window n=256, width 512, batch 64, the hybrid256 schedule: 8 local layers, 6 "
               "causal jumps 128..1 and 2 causal softmax attention layers (8 heads x 64), 16 "
               "layers, bf16, fwd+bwd"),
@@ -218,6 +221,8 @@ def main():
         return run_hybrid(args, torch, hcmix, inputs, dev)
     if args.workload == "decode256":
         return run_decode(args, torch, hcmix, inputs, dev)
+    if args.workload == "lm256_step":
+        return run_lm_step(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
     cfg = dict(inputs.PRESETS[args.workload], **over)
     s = inputs.make_preset(args.workload, **over)
@@ -491,6 +496,119 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                    "sparse_share_of_step": round(sparse / total, 4),
                    "note": "value = sparse positions*layers per second of sparse-layer time; "
                            "eager launches, each segment timed with HIP events"},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def run_lm_step(args, torch, hcmix, inputs, dev):
+    """The lm256 stack inside a whole training step of the byte-level language
+    model: embedding (library gather), the 16-layer stack forward, the 256-way
+    head with bias and cross-entropy (library kernel: logits, loss and
+    dlogits), the head's weight, bias and input gradients (PyTorch GEMMs on
+    dlogits), the stack backward and the embedding's scatter sum (library),
+    replayed as a HIP graph.  value = positions * sparse layers / step time;
+    the sparse stack's share of the step is reported beside it."""
+    over = {"batch": args.batch} if args.batch > 0 else {}
+    cfg = dict(inputs.PRESETS["lm256"], **over)
+    s = inputs.make_preset("lm256", **over)
+    B, n, w, L = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"]
+    V = 256
+    dt = torch.bfloat16
+    rows = B * n
+    gen = torch.Generator(device="cpu").manual_seed(3)
+    table = (torch.randn(V, w, generator=gen)).to(dt).to(dev)
+    head_w = (torch.randn(V, w, generator=gen) / w ** 0.5).to(dt).to(dev)
+    head_b = torch.zeros(V, dtype=torch.float32, device=dev)
+    tokens = torch.from_numpy(s.tokens.astype("int32")).to(dev)
+    targets = torch.from_numpy(s.targets.astype("int32")).to(dev)
+    ws = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_self]
+    wo = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_off]
+    x0 = torch.empty(B, n, w, dtype=dt, device=dev)
+    xs_out = [torch.empty_like(x0) for _ in range(L)]
+    dx0 = torch.empty_like(x0)
+    dws = [torch.empty((w, w), dtype=torch.float32, device=dev) for _ in range(L)]
+    dwo = [torch.empty((w, w), dtype=torch.float32, device=dev) for _ in range(L)]
+    loss = torch.empty(rows, dtype=torch.float32, device=dev)
+    dlogits = torch.empty(rows, V, dtype=dt, device=dev)
+    d_table = torch.empty(V, w, dtype=torch.float32, device=dev)
+    stack_ws = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
+    emb_ws = torch.empty(hcmix.load().hcmix_embedding_backward_workspace_bytes(rows, w, V),
+                         dtype=torch.uint8, device=dev)
+    grads = {}
+
+    def step(times=None):
+        ev = []
+
+        def mark():
+            if times is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                ev.append(e)
+        mark()
+        hcmix.embedding_forward(table, tokens, out=x0)
+        mark()
+        xs = hcmix.stack_forward(x0, ws, wo, s.layers, True, outs=xs_out)
+        mark()
+        xl = xs[-1].view(rows, w)
+        hcmix.head_cross_entropy(xl, head_w, head_b, targets, 1.0 / rows, loss=loss,
+                                 dlogits=dlogits)
+        # head gradients as plain GEMMs; the weight gradient's K = rows is split
+        # into 16 batched products (one GEMM over all rows leaves the chip idle)
+        kch = 16
+        grads["head_w"] = torch.bmm(xl.view(kch, rows // kch, w).transpose(1, 2),
+                                    dlogits.view(kch, rows // kch, V)).sum(0).t()
+        grads["head_b"] = torch.sum(dlogits, 0, dtype=torch.float32)
+        gx = torch.matmul(dlogits, head_w).view(B, n, w)
+        mark()
+        hcmix.stack_backward(xs, ws, wo, s.layers, gx, True, dx=dx0, dws=dws, dwo=dwo,
+                             workspace=stack_ws)
+        mark()
+        hcmix.embedding_backward(tokens, dx0, V, dtable=d_table, workspace=emb_ws)
+        mark()
+        if times is not None:
+            times.append(ev)
+
+    stream = torch.cuda.Stream(device=dev)
+    with torch.cuda.stream(stream):
+        step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
+        # phase split from eager steps with events between the phases
+        per = []
+        for _ in range(5):
+            step(per)
+        torch.cuda.synchronize()
+    names = ["embedding", "stack_forward", "head_and_cross_entropy", "stack_backward",
+             "embedding_backward"]
+    phase_ms = {nm: round(sum(ev[i].elapsed_time(ev[i + 1]) for ev in per) / len(per), 4)
+                for i, nm in enumerate(names)}
+    sparse = phase_ms["stack_forward"] + phase_ms["stack_backward"]
+    eager = sum(phase_ms.values())
+    out = {
+        "metric": METRIC, "value": round(rows * L * args.steps / t, 1), "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"lm256_step: {WORKLOADS['lm256_step']}", "batch": B, "n": n,
+                   "width": w, "layers": L, "vocab": V, "mode": "causal", "graph": True},
+        "lm_step": {"phase_ms_eager": phase_ms, "sparse_share_of_eager_step": round(sparse / eager, 4),
+                    "loss_mean": round(float(loss.mean()), 5),
+                    "note": "value counts the sparse layers' positions*layers per second of the "
+                            "whole training step (graph replay); phases timed on eager steps"},
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -38,12 +38,12 @@ __global__ __launch_bounds__(LM_THREADS) void embed_fwd_kernel(
 // Embedding backward, fixed summation order.  Block (v, c) sums, for vocabulary
 // entry v, the rows of chunk c (emb_chunks(rows) chunks of consecutive rows,
 // at most EMB_MAX_CHUNK each) whose token is v: wave 0 lists the matching rows
-// in row order, then wave k adds
-// matches k, k + 4, ... (8 columns per lane, 64 lanes: 512 columns per pass),
-// and the four wave sums are added in wave order into partial[c][v].
+// in row order, then wave k adds matches k, k + 4, ... in that order (8 columns
+// per lane, 64 lanes: 512 columns per pass), and the four wave sums are added
+// in wave order into partial[c][v].
 // A second kernel adds the chunks in chunk order.
 // ---------------------------------------------------------------------------
-constexpr int EMB_MIN_CHUNKS = 8;     // spreads a frequent token's rows over blocks
+constexpr int EMB_MIN_CHUNKS = 32;    // spreads a frequent token's rows over blocks
 constexpr int EMB_MAX_CHUNK = 4096;   // rows per chunk held in LDS as a match list
 int emb_chunks(int rows) {
   const int c = (rows + EMB_MAX_CHUNK - 1) / EMB_MAX_CHUNK;
@@ -77,7 +77,19 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_partial_kernel(
     const int col = c0 + 8 * lane;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (col < width) {
-      for (int k = wave; k < n; k += 4) {
+      // eight rows in flight per step (a frequent token has hundreds per chunk),
+      // added in row order
+      int k = wave;
+      for (; k + 28 < n; k += 32) {
+        bf16x8 g[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) g[u] = *(const bf16x8*)(dx + (size_t)list[k + 4 * u] * width + col);
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+#pragma unroll
+          for (int e = 0; e < 8; e++) acc[e] += (float)g[u][e];
+      }
+      for (; k < n; k += 4) {
         const bf16x8 g = *(const bf16x8*)(dx + (size_t)list[k] * width + col);
 #pragma unroll
         for (int e = 0; e < 8; e++) acc[e] += (float)g[e];
@@ -104,8 +116,9 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_reduce_kernel(
 
 // ---------------------------------------------------------------------------
 // Head + cross-entropy.  Block: 4 waves x 32 rows.  Wave: logits^T for its 32
-// rows and all NT * 32 vocabulary entries, operands straight from global
-// memory (the weights are L2-resident); register e of tile t holds entry
+// rows and all NT * 32 vocabulary entries; the weights pass through LDS in
+// 64-column slices shared by the four waves (two buffers), the wave's rows
+// come straight from global memory.  Register e of tile t holds entry
 // 32 t + 8 (e / 4) + 4 (lane / 32) + e % 4 of row lane % 32.
 // ---------------------------------------------------------------------------
 template <int NT>
@@ -114,21 +127,50 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
     const int* __restrict__ targets, float scale, float* __restrict__ loss,
     bf16* __restrict__ dlogits, int rows, int width) {
   constexpr int V = NT * 32;
+  constexpr int PIECES = V * 8 / LM_THREADS;        // 16-byte pieces of a slice per thread
+  __shared__ __attribute__((aligned(1024))) bf16 sw[2][V * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
   int r = (blockIdx.x * 4 + wave) * 32 + (lane & 31);
   const bool live = r < rows;
   if (!live) r = rows - 1;                     // load a valid row, store nothing
   const bf16* xr = x + (size_t)r * width + 8 * half;
+  u32x4 wreg[PIECES];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < PIECES; j++) {
+      const int pi = threadIdx.x + LM_THREADS * j, row = pi >> 3, p = pi & 7;
+      wreg[j] = *(const u32x4*)(w + (size_t)row * width + k0 + 8 * p);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < PIECES; j++) {
+      const int pi = threadIdx.x + LM_THREADS * j, row = pi >> 3, p = pi & 7;
+      *(u32x4*)(sw[buf] + swz<64>(row, p)) = wreg[j];
+    }
+  };
   f32x16 acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; t++) acc[t] = f32x16{};
-  for (int k = 0; k < width; k += 16) {
-    const bf16x8 b = *(const bf16x8*)(xr + k);
+  const int slices = width / 64;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int sl = 0; sl < slices; sl++) {
+    const int k0 = sl * 64;
+    bf16x8 b[4];
 #pragma unroll
-    for (int t = 0; t < NT; t++) {
-      const bf16x8 a = *(const bf16x8*)(w + (size_t)(32 * t + (lane & 31)) * width + k + 8 * half);
-      acc[t] = mfma32(a, b, acc[t]);
-    }
+    for (int kk = 0; kk < 4; kk++) b[kk] = *(const bf16x8*)(xr + k0 + 16 * kk);
+    if (sl + 1 < slices) fetch(k0 + 64);
+    const bf16* cur = sw[sl & 1];
+#pragma unroll
+    for (int kk = 0; kk < 4; kk++)
+#pragma unroll
+      for (int t = 0; t < NT; t++)
+        acc[t] = mfma32(*(const bf16x8*)(cur + swz<64>(32 * t + (lane & 31), 2 * kk + half)),
+                        b[kk], acc[t]);
+    if (sl + 1 < slices) stash((sl + 1) & 1);
+    __syncthreads();
   }
   const int tgt = targets[r];
   float mx = -INFINITY, tl = 0.f;

@@ -241,8 +241,8 @@ def test_lm_entry_points_reject_bad_arguments():
     assert ef(10, 96, 16, P[0], P[1], P[2], None) == UNSUPPORTED      # width % 64
     assert ef(10, 64, 16, P[0], P[1], ctypes.c_void_p(P[2].value + 4), None) == UNSUPPORTED
     need = lib.hcmix_embedding_backward_workspace_bytes(1000, 64, 16)
-    assert need == 8 * 16 * 64 * 4
-    assert lib.hcmix_embedding_backward_workspace_bytes(100000, 64, 16) == 25 * 16 * 64 * 4
+    assert need == 32 * 16 * 64 * 4        # 32 row chunks of partial sums
+    assert lib.hcmix_embedding_backward_workspace_bytes(200000, 64, 16) == 49 * 16 * 64 * 4
     eb = lib.hcmix_embedding_backward
     assert eb(1000, 64, 16, P[0], P[1], fp(P[2]), 0, P[3], need - 1, None) == INVALID
     assert eb(1000, 64, 16, P[0], P[1], fp(P[1]), 0, P[3], need, None) == INVALID   # dtable = dx
