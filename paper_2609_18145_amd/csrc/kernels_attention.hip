@@ -1,9 +1,9 @@
 // Causal multi-head softmax attention for the hybrid schedules' attention
 // layers (bf16 in, fp32 accumulation), windows of at most 256 positions, head
-// dimension 64.  One block per (window, head): the window's keys and values
-// (and for the backward its queries and output gradients) sit in LDS, so the
-// whole causal row of scores fits in registers and the softmax is exact (no
-// running rescale).
+// dimension 64.  One block per (window, head): two of the window's tiles sit in
+// LDS (keys and values; for the backward's two kernels queries and output
+// gradients, or keys and values), the whole causal row of scores fits in
+// registers and the softmax is exact (no running rescale).
 //
 // Layouts: qkv [batch][n][3][heads][64] (Q, K, V of every position), out and
 // dout [batch][n][heads][64], lse [batch][heads][n] fp32.
@@ -93,7 +93,7 @@ __device__ __forceinline__ bool att_masked(int e, int lane) {
 // Forward: O = softmax(s Q K^T, causal) V and lse, s = 1/8.
 // ---------------------------------------------------------------------------
 template <int NT>
-__global__ __launch_bounds__(ATT_THREADS) void attn_fwd_kernel(
+__global__ __launch_bounds__(ATT_THREADS, 2) void attn_fwd_kernel(
     const bf16* __restrict__ qkv, bf16* __restrict__ out, float* __restrict__ lse, int heads) {
   constexpr int n = NT * 32;
   __shared__ __attribute__((aligned(1024))) bf16 sK[n * HD], sV[n * HD];
@@ -174,33 +174,20 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_fwd_kernel(
 // ---------------------------------------------------------------------------
 // Backward.  With P = exp(s S - lse) and D = rowsum(dO * O):
 //   dV = P^T dO,  dS = P (dO V^T - D),  dK = s dS^T Q,  dQ = s dS K.
-// Phase 1 (waves own key tiles): S, P, dP with lanes = keys, accumulating
-// dK^T and dV^T; phase 2 (waves own query tiles): S^T, P^T, dP^T with lanes =
-// queries, accumulating dQ^T.  Both read LDS only and write disjoint outputs.
+// Two kernels, each with two of the window's four tiles in LDS (64 KB, two
+// blocks per CU), writing disjoint parts of dqkv:
+//   attn_bwd_kv_kernel: waves own key tiles; S and dP with lanes = keys,
+//     accumulating dK^T and dV^T (Q and dO in LDS, read both ways);
+//   attn_bwd_q_kernel: waves own query tiles; S^T and dP^T with lanes =
+//     queries, accumulating dQ^T (K and V in LDS).
+// P, S and dP are recomputed rather than stored; no atomics, deterministic.
 // ---------------------------------------------------------------------------
-template <int NT>
-__global__ __launch_bounds__(ATT_THREADS) void attn_bwd_kernel(
-    const bf16* __restrict__ qkv, const bf16* __restrict__ out, const float* __restrict__ lse,
-    const bf16* __restrict__ dout, bf16* __restrict__ dqkv, int heads) {
-  constexpr int n = NT * 32;
-  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
-  bf16* sQ = smem;
-  bf16* sK = sQ + n * HD;
-  bf16* sV = sK + n * HD;
-  bf16* sO = sV + n * HD;                 // output gradient dO
-  float* sL = (float*)(sO + n * HD);      // lse, log2 units
-  float* sD = sL + n;                     // rowsum(dO * O)
-  const int bh = blockIdx.x, b = bh / heads, h = bh % heads;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  const size_t rs = (size_t)3 * heads * HD, os = (size_t)heads * HD;
-  const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
-  const bf16* obase = out + (size_t)b * n * os + (size_t)h * HD;
-  const bf16* dobase = dout + (size_t)b * n * os + (size_t)h * HD;
-  bf16* gbase = dqkv + (size_t)b * n * rs + (size_t)h * HD;
-  att_load_tile(base, rs, n, sQ);
-  att_load_tile(base + os, rs, n, sK);
-  att_load_tile(base + 2 * os, rs, n, sV);
-  att_load_tile(dobase, os, n, sO);
+
+// lse in log2 units and D = rowsum(dO * O) of the window's rows into LDS.
+__device__ __forceinline__ void att_row_stats(const bf16* __restrict__ obase,
+                                              const bf16* __restrict__ dobase, size_t os,
+                                              const float* __restrict__ lse_row, int n, float* sL,
+                                              float* sD) {
   for (int i = threadIdx.x; i < n; i += ATT_THREADS) {
     float d = 0.f;
 #pragma unroll
@@ -211,21 +198,40 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_bwd_kernel(
       for (int e = 0; e < 8; e++) d += (float)a[e] * (float)g[e];
     }
     sD[i] = d;
-    sL[i] = lse[(size_t)bh * n + i] * LOG2E;
+    sL[i] = lse_row[i] * LOG2E;
   }
+}
+
+template <int NT>
+__global__ __launch_bounds__(ATT_THREADS, 2) void attn_bwd_kv_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ out, const float* __restrict__ lse,
+    const bf16* __restrict__ dout, bf16* __restrict__ dqkv, int heads) {
+  constexpr int n = NT * 32;
+  __shared__ __attribute__((aligned(1024))) bf16 sQ[n * HD], sO[n * HD];   // sO: dO
+  __shared__ __attribute__((aligned(16))) float sL[n], sD[n];
+  const int bh = blockIdx.x, b = bh / heads, h = bh % heads;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  const size_t rs = (size_t)3 * heads * HD, os = (size_t)heads * HD;
+  const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
+  const bf16* dobase = dout + (size_t)b * n * os + (size_t)h * HD;
+  bf16* gbase = dqkv + (size_t)b * n * rs + (size_t)h * HD;
+  att_load_tile(base, rs, n, sQ);
+  att_load_tile(dobase, os, n, sO);
+  att_row_stats(out + (size_t)b * n * os + (size_t)h * HD, dobase, os, lse + (size_t)bh * n, n,
+                sL, sD);
   __syncthreads();
   const float sc = 0.125f * LOG2E;
-
-  // ---- phase 1: key tiles; S[q][key] lanes = keys, registers = 16 queries ----
 #pragma unroll
   for (int which = 0; which < 2; which++) {
     const int kt = att_tile(wave, which);
     if (kt >= NT) continue;
-    bf16x8 kf[4], vf[4];                // K and V rows of this lane's key as B operands
+    // K and V rows of this lane's key as B operands, straight from global memory
+    const int key = kt * 32 + (lane & 31);
+    bf16x8 kf[4], vf[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ks++) {
-      kf[ks] = att_frag(sK, kt * 32, 16 * ks, lane);
-      vf[ks] = att_frag(sV, kt * 32, 16 * ks, lane);
+      kf[ks] = *(const bf16x8*)(base + (size_t)key * rs + os + 16 * ks + 8 * half);
+      vf[ks] = *(const bf16x8*)(base + (size_t)key * rs + 2 * os + 16 * ks + 8 * half);
     }
     f32x16 dk[2] = {}, dv[2] = {};
 #pragma unroll
@@ -264,7 +270,6 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_bwd_kernel(
       }
     }
     // dK^T / dV^T register e of lane l: key kt*32 + l%32, dim 32 dt + 8 (e/4) + 4 half + e%4
-    const int key = kt * 32 + (lane & 31);
     bf16* krow = gbase + (size_t)key * rs + os;
     bf16* vrow = gbase + (size_t)key * rs + 2 * os;
 #pragma unroll
@@ -280,19 +285,38 @@ __global__ __launch_bounds__(ATT_THREADS) void attn_bwd_kernel(
         *(bf16x4*)(vrow + c) = vv;
       }
   }
+}
 
-  // ---- phase 2: query tiles; S^T[key][q] lanes = queries, registers = 16 keys ----
+template <int NT>
+__global__ __launch_bounds__(ATT_THREADS, 2) void attn_bwd_q_kernel(
+    const bf16* __restrict__ qkv, const bf16* __restrict__ out, const float* __restrict__ lse,
+    const bf16* __restrict__ dout, bf16* __restrict__ dqkv, int heads) {
+  constexpr int n = NT * 32;
+  __shared__ __attribute__((aligned(1024))) bf16 sK[n * HD], sV[n * HD];
+  __shared__ __attribute__((aligned(16))) float sL[n], sD[n];
+  const int bh = blockIdx.x, b = bh / heads, h = bh % heads;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  const size_t rs = (size_t)3 * heads * HD, os = (size_t)heads * HD;
+  const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
+  const bf16* dobase = dout + (size_t)b * n * os + (size_t)h * HD;
+  bf16* gbase = dqkv + (size_t)b * n * rs + (size_t)h * HD;
+  att_load_tile(base + os, rs, n, sK);
+  att_load_tile(base + 2 * os, rs, n, sV);
+  att_row_stats(out + (size_t)b * n * os + (size_t)h * HD, dobase, os, lse + (size_t)bh * n, n,
+                sL, sD);
+  __syncthreads();
+  const float sc = 0.125f * LOG2E;
 #pragma unroll
   for (int which = 0; which < 2; which++) {
     const int qt = att_tile(wave, which);
     if (qt >= NT) continue;
-    bf16x8 qf[4], of[4];
+    const int q = qt * 32 + (lane & 31);
+    bf16x8 qf[4], of[4];            // this lane's query and output-gradient rows, from global
 #pragma unroll
     for (int ks = 0; ks < 4; ks++) {
-      qf[ks] = att_frag(sQ, qt * 32, 16 * ks, lane);
-      of[ks] = att_frag(sO, qt * 32, 16 * ks, lane);
+      qf[ks] = *(const bf16x8*)(base + (size_t)q * rs + 16 * ks + 8 * half);
+      of[ks] = *(const bf16x8*)(dobase + (size_t)q * os + 16 * ks + 8 * half);
     }
-    const int q = qt * 32 + (lane & 31);
     const float lq = sL[q], dq = sD[q];
     f32x16 gq[2] = {};
 #pragma unroll
@@ -341,12 +365,10 @@ hipError_t attn_fwd_launch(const bf16* qkv, bf16* out, float* lse, int batch, in
 template <int NT>
 hipError_t attn_bwd_launch(const bf16* qkv, const bf16* out, const float* lse, const bf16* dout,
                            bf16* dqkv, int batch, int heads, hipStream_t st) {
-  const size_t lds = (size_t)4 * NT * 32 * HD * sizeof(bf16) + 2 * NT * 32 * sizeof(float);
-  auto k = attn_bwd_kernel<NT>;
-  static const hipError_t attr =
-      hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr != hipSuccess) return attr;
-  k<<<batch * heads, ATT_THREADS, lds, st>>>(qkv, out, lse, dout, dqkv, heads);
+  attn_bwd_kv_kernel<NT><<<batch * heads, ATT_THREADS, 0, st>>>(qkv, out, lse, dout, dqkv, heads);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  attn_bwd_q_kernel<NT><<<batch * heads, ATT_THREADS, 0, st>>>(qkv, out, lse, dout, dqkv, heads);
   return hipGetLastError();
 }
 
