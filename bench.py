@@ -394,15 +394,34 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         with sdpa_kernel([backend["be"]]):
             return F.scaled_dot_product_attention(q, k, v, is_causal=True)
 
+    class Linear(torch.autograd.Function):
+        """y = x W^T with the weight gradient's K = rows split into 16 batched
+        products (a single GEMM with K = 16384 and a 512-wide output leaves
+        most of the chip idle in the library's kernel choice)."""
+
+        @staticmethod
+        def forward(ctx, x2, wt):
+            ctx.save_for_backward(x2, wt)
+            return torch.matmul(x2, wt.t())
+
+        @staticmethod
+        def backward(ctx, g):
+            x2, wt = ctx.saved_tensors
+            g = g.contiguous()
+            kch = 16
+            r = x2.shape[0] // kch
+            dw = torch.bmm(g.view(kch, r, -1).transpose(1, 2), x2.view(kch, r, -1)).sum(0)
+            return torch.matmul(g, wt), dw
+
     def attention(x, i):
         wqkv, wout = attn_w[i]
-        qkv = F.linear(x, wqkv).view(B, n, 3, heads, hd)
+        qkv = Linear.apply(x.reshape(B * n, w), wqkv).view(B, n, 3, heads, hd)
         if args.attention == "native":
-            o = hcmix.Attention.apply(qkv).reshape(B, n, w)
+            o = hcmix.Attention.apply(qkv).reshape(B * n, w)
         else:
             q, k, v = (qkv[:, :, j].transpose(1, 2).contiguous() for j in range(3))
-            o = sdpa(q, k, v).transpose(1, 2).reshape(B, n, w)
-        return F.linear(o, wout)
+            o = sdpa(q, k, v).transpose(1, 2).reshape(B * n, w)
+        return Linear.apply(o, wout).view(B, n, w)
 
     wsp = {}
     stream = torch.cuda.current_stream(dev)
