@@ -672,21 +672,20 @@ def run_decode(args, torch, hcmix, inputs, dev):
         return max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
 
     t_eager = timed(lambda: window(n))
-    # one graph per position (the position is a launch argument), replayed in order
+    # one graph holding a whole window: n positions x L layer launches in
+    # order (the position is a launch argument), replayed once per window
     graphs = []
     if args.graph:
         side = torch.cuda.Stream(device=dev)
         with torch.cuda.stream(side):
-            for p in range(n):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=side):
-                    hcmix.decode_step(cols[p], ws, wo, s.layers, n, p, cache, out=y)
-                graphs.append(g)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                window(n)
+            graphs.append(g)
         torch.cuda.synchronize()
 
         def replay():
-            for g in graphs:
-                g.replay()
+            graphs[0].replay()
         replay()
         torch.cuda.synchronize()
         t_graph = timed(replay)
@@ -701,8 +700,8 @@ def run_decode(args, torch, hcmix, inputs, dev):
         "decode": {"us_per_position": round(t / steps * 1e6, 2),
                    "us_per_position_eager": round(t_eager / steps * 1e6, 2),
                    "launches_per_position": L,
-                   "note": "value from one captured graph per position (the position is a "
-                           "launch argument), replayed in order; eager launches beside it"},
+                   "note": "value from one captured graph per window (n positions x layers "
+                           "launches, the position a launch argument); eager launches beside it"},
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -15,42 +15,54 @@ namespace hcmix {
 
 namespace {
 
-// bf16: one block per 32 output columns x 32 windows, 4 waves splitting the
-// contraction (self part then partner part) in 16-wide steps, their partial
-// products summed through LDS in wave order.
-__global__ __launch_bounds__(256) void decode_bf16_kernel(DecodeLayerArgs a) {
-  __shared__ f32x16 part[4][64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// bf16: one block per 32 output columns x 32 windows, 8 waves splitting the
+// contraction in 16-wide steps (wave w takes steps w, w + 8, ...), their
+// partial products summed through LDS in wave order.  The self and partner
+// operands of CH steps are loaded before any of their MFMAs, so at width 512
+// every load of the block is in flight at once: a layer costs one memory
+// latency rather than one per product.
+constexpr int DEC_WAVES = 8;
+__global__ __launch_bounds__(64 * DEC_WAVES) void decode_bf16_kernel(DecodeLayerArgs a) {
+  __shared__ f32x16 part[DEC_WAVES][64];
+  // `wave` and `has_partner` are wave-uniform and must be known so: an MFMA
+  // under a lane mask (EXEC) still writes its whole result, so every MFMA
+  // guard below has to be a scalar branch.
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool has_partner = a.x_partner != nullptr;
   const int o0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
   const int w = a.width;
   const int b = min(b0 + (lane & 31), a.batch - 1);      // clamped; stores are masked
   const int half = lane >> 5;
   const bf16* xin = a.x_in + (size_t)b * a.in_stride;
-  const bf16* xp = a.x_partner ? a.x_partner + (size_t)b * a.partner_stride : nullptr;
+  const bf16* xp = has_partner ? a.x_partner + (size_t)b * a.partner_stride : a.x_in;
   f32x16 acc;
 #pragma unroll
   for (int e = 0; e < 16; e++) acc[e] = 0.f;
-  // this wave's 16-wide contraction steps k = wave, wave + 4, ...: the loads of
-  // CH steps are all issued before their MFMAs, so their latencies overlap
-  constexpr int CH = 8;
+  constexpr int CH = 4;
   const int ksteps = w / 16;
-  auto part_product = [&](const bf16* W, const bf16* xr) {
-    for (int kb = wave; kb < ksteps; kb += 4 * CH) {
-      bf16x8 wf[CH], xf[CH];
+  const bf16* ws = a.w_self + (size_t)(o0 + (lane & 31)) * w;
+  const bf16* wo = a.w_off + (size_t)(o0 + (lane & 31)) * w;
+  for (int kb = wave; kb < ksteps; kb += DEC_WAVES * CH) {
+    bf16x8 sw[CH], sx[CH], pw[CH], px[CH];
 #pragma unroll
-      for (int j = 0; j < CH; j++) {
-        const int k = kb + 4 * j;
-        const int k0 = (k < ksteps ? k : 0) * 16 + 8 * half;
-        wf[j] = *(const bf16x8*)(W + (size_t)(o0 + (lane & 31)) * w + k0);
-        xf[j] = *(const bf16x8*)(xr + k0);
+    for (int j = 0; j < CH; j++) {
+      const int k = kb + DEC_WAVES * j;
+      const int k0 = (k < ksteps ? k : 0) * 16 + 8 * half;   // clamped; the MFMA is skipped
+      sw[j] = *(const bf16x8*)(ws + k0);
+      sx[j] = *(const bf16x8*)(xin + k0);
+      if (has_partner) {
+        pw[j] = *(const bf16x8*)(wo + k0);
+        px[j] = *(const bf16x8*)(xp + k0);
       }
-#pragma unroll
-      for (int j = 0; j < CH; j++)
-        if (kb + 4 * j < ksteps) acc = mfma32(wf[j], xf[j], acc);
     }
-  };
-  part_product(a.w_self, xin);
-  if (xp) part_product(a.w_off, xp);
+#pragma unroll
+    for (int j = 0; j < CH; j++) {
+      if (kb + DEC_WAVES * j >= ksteps) continue;
+      acc = mfma32(sw[j], sx[j], acc);
+      if (has_partner) acc = mfma32(pw[j], px[j], acc);
+    }
+  }
   part[wave][lane] = acc;
   // layer 0 records its input for later positions: this block's 32 columns
   if (a.record && wave == 0 && b0 + (lane & 31) < a.batch) {
@@ -62,7 +74,7 @@ __global__ __launch_bounds__(256) void decode_bf16_kernel(DecodeLayerArgs a) {
   if (wave != 0) return;
   f32x16 s = part[0][lane];
 #pragma unroll
-  for (int v = 1; v < 4; v++) s += part[v][lane];
+  for (int v = 1; v < DEC_WAVES; v++) s += part[v][lane];
   if (b0 + (lane & 31) >= a.batch) return;
   // C[o][b]: lane l holds window b0 + l%32 and outputs o0 + 8 g + 4 (l/32) + 0..3
   bf16* dst = a.out + (size_t)b * a.out_stride + o0 + 4 * half;
@@ -93,7 +105,7 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeLayerArgsF32 a) {
 }  // namespace
 
 hipError_t launch_decode_bf16(const DecodeLayerArgs& a, hipStream_t st) {
-  decode_bf16_kernel<<<dim3(a.width / 32, (a.batch + 31) / 32), 256, 0, st>>>(a);
+  decode_bf16_kernel<<<dim3(a.width / 32, (a.batch + 31) / 32), 64 * DEC_WAVES, 0, st>>>(a);
   return hipGetLastError();
 }
 
