@@ -428,10 +428,20 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     ev = torch.cuda.Event
 
     def step(times):
+        """One step; with `times` a list, every segment is bracketed by events
+        on the current stream (left out under graph capture, times=None)."""
+        cur = torch.cuda.current_stream(dev)
+
+        def bracket():
+            if times is None:
+                return None, None
+            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
+            e0.record(cur)
+            return e0, e1
+
         saved, x = [], x0
         for kind, arg in segs:                      # forward
-            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
-            e0.record(stream)
+            e0, e1 = bracket()
             if kind == "sparse":
                 xs = hcmix.stack_forward(x, [ws[j] for j, _ in arg], [wo[j] for j, _ in arg],
                                          [c for _, c in arg], True)
@@ -444,12 +454,12 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                     out = attention(xin, arg)
                 saved.append((xin, out, params))
                 x = out.detach()
-            e1.record(stream)
-            times.append((kind, "fwd", e0, e1))
+            if times is not None:
+                e1.record(cur)
+                times.append((kind, "fwd", e0, e1))
         g = dy
         for (kind, arg), sv in zip(reversed(segs), reversed(saved)):   # backward
-            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
-            e0.record(stream)
+            e0, e1 = bracket()
             if kind == "sparse":
                 L = len(arg)
                 if L not in wsp:
@@ -461,8 +471,9 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                 xin, out, params = sv
                 grads = torch.autograd.grad(out, [xin, *params], grad_outputs=g)
                 g = grads[0].contiguous()
-            e1.record(stream)
-            times.append((kind, "bwd", e0, e1))
+            if times is not None:
+                e1.record(cur)
+                times.append((kind, "bwd", e0, e1))
         return g
 
     for _ in range(args.warmup):
@@ -479,9 +490,32 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     c1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    total = max(wall, c0.elapsed_time(c1) / 1e3)
+    total_eager = max(wall, c0.elapsed_time(c1) / 1e3)
     sparse = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "sparse") / 1e3
     attn = sum(e0.elapsed_time(e1) for st in per_step for k, _, e0, e1 in st if k == "attn") / 1e3
+    total = total_eager
+    if args.graph:
+        # the same step (forward, attention autograd, library backward) captured
+        # once and replayed: the step time without host launch overhead
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            step(None)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                step(None)
+            for _ in range(args.warmup):
+                graph.replay()
+            torch.cuda.synchronize()
+            g0, g1 = ev(enable_timing=True), ev(enable_timing=True)
+            t0 = time.perf_counter()
+            g0.record(side)
+            for _ in range(args.steps):
+                graph.replay()
+            g1.record(side)
+            torch.cuda.synchronize()
+        total = max(time.perf_counter() - t0, g0.elapsed_time(g1) / 1e3)
     pl = B * n * Ls
     core_us = None
     if args.attention == "native":
@@ -507,14 +541,17 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}", "batch": B, "n": n,
                    "width": w, "layers": Ls, "attention_layers": nattn, "mode": "causal",
-                   "graph": False, "attention_backend": backend["name"]},
+                   "graph": bool(args.graph), "attention_backend": backend["name"]},
         "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
+                   "step_ms_eager": round(total_eager / args.steps * 1e3, 4),
                    "sparse_ms": round(sparse / args.steps * 1e3, 4),
                    "attention_ms": round(attn / args.steps * 1e3, 4),
                    "attention_core_fwd_bwd_us_per_layer": core_us,
-                   "sparse_share_of_step": round(sparse / total, 4),
-                   "note": "value = sparse positions*layers per second of sparse-layer time; "
-                           "eager launches, each segment timed with HIP events"},
+                   "sparse_share_of_step": round(sparse / total_eager, 4),
+                   "note": "step_ms from one captured graph of the whole step (when graph); "
+                           "value = sparse positions*layers per second of sparse-layer time and "
+                           "the segment split from eager steps, each segment timed with HIP "
+                           "events"},
     }
     print(json.dumps(out), flush=True)
     return 0
