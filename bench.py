@@ -313,7 +313,9 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     the output projection (PyTorch GEMMs) around the library's causal attention
     core (hcmix_attention_forward / _backward; --attention sdpa swaps in
     PyTorch's scaled-dot-product attention); the sparse segments are hcmix
-    stack calls.  Forward and backward are chained by hand
+    stack calls: forward per segment, the dX chain per segment
+    (hcmix_stack_backward_data), and the weight gradients of every sparse
+    layer in one hcmix_stack_weight_gradients call at the end.  Forward and backward are chained by hand
     so that every segment is timed with HIP events on one stream; the line
     reports the sparse layers' share of the step and their own throughput."""
     import torch.nn.functional as F
@@ -458,15 +460,20 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                 e1.record(cur)
                 times.append((kind, "fwd", e0, e1))
         g = dy
+        # the sparse segments run their dX chains only; the weight gradients of
+        # all sparse layers follow in one library call
+        dw_x, dw_g, dw_codes = [], [], []
         for (kind, arg), sv in zip(reversed(segs), reversed(saved)):   # backward
             e0, e1 = bracket()
             if kind == "sparse":
                 L = len(arg)
-                if L not in wsp:
-                    wsp[L] = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
-                g, _, _ = hcmix.stack_backward(sv[:L], [ws[j] for j, _ in arg],
-                                               [wo[j] for j, _ in arg], [c for _, c in arg], g,
-                                               True, workspace=wsp[L])
+                g_out = g
+                g, grads = hcmix.stack_backward_data([ws[j] for j, _ in arg],
+                                                     [wo[j] for j, _ in arg],
+                                                     [c for _, c in arg], g_out, True)
+                dw_x += sv[:L]
+                dw_g += [*grads, g_out]
+                dw_codes += [c for _, c in arg]
             else:
                 xin, out, params = sv
                 grads = torch.autograd.grad(out, [xin, *params], grad_outputs=g)
@@ -474,6 +481,15 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             if times is not None:
                 e1.record(cur)
                 times.append((kind, "bwd", e0, e1))
+        e0, e1 = bracket()
+        if "dw" not in wsp:
+            wsp["dw"] = ([torch.empty((w, w), dtype=torch.float32, device=dev) for _ in dw_x],
+                         [torch.empty((w, w), dtype=torch.float32, device=dev) for _ in dw_x])
+        hcmix.stack_weight_gradients(dw_x, dw_g, dw_codes, True, dws=wsp["dw"][0],
+                                     dwo=wsp["dw"][1])
+        if times is not None:
+            e1.record(cur)
+            times.append(("sparse", "dw", e0, e1))
         return g
 
     for _ in range(args.warmup):

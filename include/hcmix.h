@@ -204,6 +204,32 @@ hcmix_status hcmix_stack_weight_gradients(int64_t batch, int64_t n, int64_t widt
                                           void* workspace, size_t workspace_bytes,
                                           void* stream);
 
+/* The data half of the stack backward: the dX chain alone (the adjoint of
+ * Eq. (1) layer after layer, from the top), keeping every intermediate
+ * gradient in caller memory, so that a model whose sparse stacks alternate
+ * with other layers can form the weight gradients of all its sparse layers
+ * afterwards in one hcmix_stack_weight_gradients call.  dy: the gradient of
+ * the stack's output x_L; grads: host array of num_layers - 1 device pointers
+ * (ignored, may be NULL, when num_layers == 1), grads[l - 1] receiving g_l,
+ * the gradient of layer l's input, for l = 1 .. L-1; dx receives g_0.  Layer
+ * l's output gradient is then grads[l] (or dy for the last layer), which is
+ * what hcmix_stack_weight_gradients takes as dys[l].  The dX products are the
+ * ones hcmix_stack_backward runs, so dx and the grads equal its intermediate
+ * gradients bitwise on the layer-by-layer and deferred paths.  Layouts,
+ * layer codes, modes and alignment as for hcmix_stack_backward; no output
+ * (dx, grads, workspace) may overlap an input (dy, weights) or another
+ * output.  Workspace (256-byte aligned, possibly 0 bytes): bf16 stacks of two
+ * or more layers keep a transposed copy of every weight matrix there. */
+size_t hcmix_stack_backward_data_workspace_bytes(int64_t width, int32_t num_layers,
+                                                 int32_t dtype);
+
+hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
+                                       int32_t num_layers, const int32_t* layers, int32_t mode,
+                                       int32_t dtype, const void* const* w_self,
+                                       const void* const* w_off, const void* dy,
+                                       void* const* grads, void* dx, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+
 /* ---- Decode: one new position of every window through the whole stack ----
  *
  * The causal stack evaluated incrementally (the one-position-at-a-time path

@@ -546,6 +546,84 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
 
 }  // extern "C"
 
+size_t hcmix_stack_backward_data_workspace_bytes(int64_t width, int32_t num_layers,
+                                                 int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers || width < 1) return 0;
+  if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return 0;
+  return transposed_weight_bytes(width, num_layers, dtype);
+}
+
+hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
+                                       int32_t num_layers, const int32_t* layers, int32_t mode,
+                                       int32_t dtype, const void* const* w_self,
+                                       const void* const* w_off, const void* dy,
+                                       void* const* grads, void* dx, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  if (!layers || !w_self || !w_off || !dy || !dx) return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  if (num_layers > 1 && !grads) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], mode, dtype);
+    if (st != HCMIX_OK) return st;
+    if (!w_self[l] || !w_off[l] || (l > 0 && !grads[l - 1])) return HCMIX_ERR_INVALID_VALUE;
+  }
+  const size_t need = transposed_weight_bytes(width, num_layers, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
+  const size_t es = elem_size(dtype);
+  const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
+  const size_t al = dtype == HCMIX_BF16 ? 16 : 4;
+  // Outputs: dx, the workspace and every grads[l]; inputs: dy and every weight.
+  for (int k = 0; k < num_layers; k++) {
+    // output k: dx (k == 0) or grads[k - 1], checked with the two fixed
+    // outputs against dy and layer k's weights, then against every other
+    // layer's weights and grads
+    const Span ins[3] = {{dy, act}, {w_self[k], wgt}, {w_off[k], wgt}};
+    const Span outs[3] = {{dx, act}, {workspace, need}, {k ? grads[k - 1] : nullptr, k ? act : 0}};
+    hcmix_status st = check_spans(ins, 3, outs, 3, al);
+    if (st != HCMIX_OK) return st;
+    for (int j = 0; j < num_layers; j++) {
+      if (j == k) continue;
+      const Span other[3] = {{w_self[j], wgt}, {w_off[j], wgt}, {j ? grads[j - 1] : nullptr, j ? act : 0}};
+      for (int o = 0; o < 3; o++) {
+        if (!outs[o].n) continue;
+        for (int m = 0; m < 3; m++)
+          if (other[m].n && overlaps(outs[o].p, outs[o].n, other[m].p, other[m].n))
+            return HCMIX_ERR_INVALID_VALUE;
+      }
+    }
+  }
+  if (need && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+
+  const int rows = (int)(batch * n), w = (int)width;
+  const int bidir = mode == HCMIX_BIDIR;
+  hipStream_t s = (hipStream_t)stream;
+  const size_t ww = (size_t)w * w;
+  // g(l): gradient of layer l's input; g(L) = dy
+  auto g = [&](int l) -> void* {
+    if (l == num_layers) return (void*)dy;
+    return l == 0 ? dx : grads[l - 1];
+  };
+  hipError_t e = hipSuccess;
+  bf16* wt = (bf16*)workspace;
+  if (need > 0) e = transpose_weights(w, num_layers, w_self, w_off, wt, s);
+  for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
+    const int d = hcmix_dim(layers[l], n);
+    if (dtype == HCMIX_BF16) {
+      if (need > 0)
+        e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g(l + 1), wt + 2 * (size_t)l * ww,
+                        wt + (2 * (size_t)l + 1) * ww, (bf16*)g(l), /*transpose_b=*/false, s);
+      else
+        e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g(l + 1), (const bf16*)w_self[l],
+                        (const bf16*)w_off[l], (bf16*)g(l), /*transpose_b=*/true, s);
+    } else {
+      e = launch_mix_f32((const float*)g(l + 1), (const float*)w_self[l], (const float*)w_off[l],
+                         (float*)g(l), rows, w, d, 1, bidir, (int)n, /*shift=*/1,
+                         /*transpose_w=*/true, s);
+    }
+  }
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
 size_t hcmix_stack_weight_gradients_workspace_bytes(int64_t batch, int64_t n, int64_t width,
                                                      int32_t num_layers, int32_t dtype) {
   if (num_layers < 1 || num_layers > kMaxLayers) return 0;

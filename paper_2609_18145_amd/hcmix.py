@@ -29,6 +29,7 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_backward_workspace_bytes", "hcmix_backward", "hcmix_stack_forward",
            "hcmix_stack_backward_workspace_bytes", "hcmix_stack_backward",
            "hcmix_stack_weight_gradients_workspace_bytes", "hcmix_stack_weight_gradients",
+           "hcmix_stack_backward_data_workspace_bytes", "hcmix_stack_backward_data",
            "hcmix_decode_cache_bytes", "hcmix_decode_step", "hcmix_attention_forward",
            "hcmix_attention_backward", "hcmix_embedding_forward",
            "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
@@ -81,6 +82,11 @@ def load():
         lib.hcmix_stack_weight_gradients.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, pp,
                                                      pp, i32, vp, sz, vp]
         lib.hcmix_stack_weight_gradients.restype = i32
+        lib.hcmix_stack_backward_data_workspace_bytes.argtypes = [i64, i32, i32]
+        lib.hcmix_stack_backward_data_workspace_bytes.restype = sz
+        lib.hcmix_stack_backward_data.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, vp, pp,
+                                                  vp, vp, sz, vp]
+        lib.hcmix_stack_backward_data.restype = i32
         lib.hcmix_attention_forward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp]
         lib.hcmix_attention_forward.restype = i32
         lib.hcmix_attention_backward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp, vp, vp]
@@ -242,6 +248,32 @@ def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dx=None, dws=None, d
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_backward")
     return dx, dws, dwo
+
+
+def stack_backward_data(w_selfs, w_offs, layers, dy, causal, dx=None, grads=None,
+                        workspace=None):
+    """The dX chain of the stack alone (no weight gradients); returns
+    (dx_0, [g_1, ..., g_{L-1}]) with g_l the gradient of layer l's input, so
+    that layer l's output gradient is grads[l] (dy for the last layer)."""
+    L = len(layers)
+    _check(dy, *w_selfs, *w_offs)
+    batch, n, width = dy.shape
+    if dx is None:
+        dx = torch.empty_like(dy)
+    if grads is None:
+        grads = [torch.empty_like(dy) for _ in range(L - 1)]
+    _check(dy, dx, *grads)
+    nbytes = load().hcmix_stack_backward_data_workspace_bytes(width, L, _dtype_code(dy))
+    if workspace is None and nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dy.device)
+    ws_bytes = workspace.numel() if workspace is not None else 0
+    gp = _ptrs(grads) if grads else None
+    rc = load().hcmix_stack_backward_data(batch, n, width, L, _layers(layers), int(bool(causal)),
+                                          _dtype_code(dy), _ptrs(w_selfs), _ptrs(w_offs), _ptr(dy),
+                                          gp, _ptr(dx), _ptr(workspace), ws_bytes, _stream(dy))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_stack_backward_data")
+    return dx, grads
 
 
 def weight_gradients_workspace_bytes(batch, n, width, num_layers, dtype) -> int:

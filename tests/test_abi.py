@@ -316,3 +316,43 @@ def test_decode_cache_query():
     assert lib.hcmix_decode_cache_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16) == 16 * 64 * 256 * 512 * 2
     assert lib.hcmix_decode_cache_bytes(2, 12, 64, 4, hcmix.HCMIX_BF16) == 0
     assert lib.hcmix_decode_cache_bytes(2, 16, 64, 0, hcmix.HCMIX_BF16) == 0
+
+
+def sbd(batch=2, n=16, width=128, L=4, layers=LP, mode=1, dtype=1, ws=None, wo=None, dy=P[0],
+        grads=None, dx=P[4], wsp=P[7], wsb=1 << 20):
+    ws = ws if ws is not None else PP(P[1], P[1], P[1], P[1])
+    wo = wo if wo is not None else PP(P[2], P[2], P[2], P[2])
+    grads = grads if grads is not None else PP(P[3], P[5], P[6])
+    return hcmix.load().hcmix_stack_backward_data(batch, n, width, L, layers, mode, dtype, ws, wo,
+                                                  dy, grads, dx, wsp, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), INVALID), (dict(n=12), INVALID), (dict(dy=None), INVALID), (dict(dx=None), INVALID),
+    (dict(grads=ctypes.POINTER(ctypes.c_void_p)()), INVALID),       # null array, L > 1
+    (dict(grads=(ctypes.c_void_p * 3)(P[3].value, None, P[6].value)), INVALID),
+    (dict(grads=PP(P[0], P[5], P[6])), INVALID),                    # a gradient aliases dy
+    (dict(grads=PP(P[3], P[3], P[6])), INVALID),                    # two gradients alias
+    (dict(grads=PP(P[3], P[5], P[2])), INVALID),                    # a gradient aliases a weight
+    (dict(dx=P[1]), INVALID),                                       # dx aliases a weight
+    (dict(dx=P[5]), INVALID),                                       # dx aliases a gradient
+    (dict(grads=PP(P[7], P[5], P[6])), INVALID),                    # a gradient in the workspace
+    (dict(wsb=2 * 4 * 128 * 128 * 2 - 1), INVALID),                 # short workspace
+    (dict(wsp=None), INVALID),
+    (dict(wsp=ctypes.c_void_p(P[7].value + 16)), UNSUPPORTED),      # not 256-aligned
+    (dict(dy=ctypes.c_void_p(P[0].value + 2)), UNSUPPORTED),        # misaligned bf16 operand
+    (dict(width=96), UNSUPPORTED),
+    (dict(layers=(ctypes.c_int32 * 4)(0, -1, 2, 3), mode=0), INVALID),   # local layer, bidir
+])
+def test_stack_backward_data_rejects_bad_arguments(kw, code):
+    assert sbd(**kw) == code
+
+
+def test_stack_backward_data_workspace_query():
+    q = hcmix.load().hcmix_stack_backward_data_workspace_bytes
+    assert q(128, 4, hcmix.HCMIX_BF16) == 2 * 4 * 128 * 128 * 2     # transposed weights
+    assert q(512, 16, hcmix.HCMIX_BF16) == 2 * 16 * 512 * 512 * 2
+    assert q(128, 1, hcmix.HCMIX_BF16) == 0                         # one layer reads W transposed
+    assert q(32, 4, hcmix.HCMIX_F32) == 0
+    assert q(128, 0, hcmix.HCMIX_BF16) == 0
+    assert q(128, 4, 7) == 0
