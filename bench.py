@@ -1,17 +1,20 @@
 #!/usr/bin/env python3
 """Throughput of the rotating-hypercube mixing stack on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload lm256]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload lm256_step]
 
-One step = forward and backward of the whole stack over one batch of
-synthetic inputs already resident in HBM: one hcmix_stack_forward and one
-hcmix_stack_backward call, replayed as a HIP graph.  At width 512 and up
-those run every layer as the mix GEMM forward, then in reverse the dX GEMM
-and the split-K weight gradients; at width 64 each is one LDS-resident
-kernel over all layers (plus the weight-gradient reduction).
+The default workload is the language-model-shaped stack's whole training
+step (window 256, width 512, batch 64, 16 rotated causal layers, byte-token
+embedding, 256-way output head and cross-entropy): one step = the embedding
+gather, the stack forward, the head with its loss and dlogits, the head's
+gradients, the stack backward and the embedding's scatter sum over one batch
+of synthetic inputs already resident in HBM, replayed as a HIP graph.
+`--workload lm256` times the stack alone (one hcmix_stack_forward and one
+hcmix_stack_backward call); the other workloads are the other shapes of the
+survey (reach, long4096, hybrids, decode).
 Prints one JSON line: positions*layers per second, the roofline of the
-dominant kernel (timed live with HIP events on its own stream) and the CPU
-oracle timed on a bounded sample of the same workload.
+dominant kernel (timed live with HIP events on the stream it runs on) and the
+CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -67,7 +70,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="lm256", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="lm256_step", choices=sorted(WORKLOADS))
     ap.add_argument("--batch", type=int, default=0,
                     help="override the workload's batch (windows), e.g. for a batch sweep")
     ap.add_argument("--graph", type=int, default=1, help="replay the step as a HIP graph")
@@ -577,8 +580,8 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
     """The lm256 stack inside a whole training step of the byte-level language
     model: embedding (library gather), the 16-layer stack forward, the 256-way
     head with bias and cross-entropy (library kernel: logits, loss and
-    dlogits), the head's weight, bias and input gradients (PyTorch GEMMs on
-    dlogits), the stack backward and the embedding's scatter sum (library),
+    dlogits and the bias gradient), the head's weight and input gradients
+    (PyTorch GEMMs on dlogits), the stack backward and the embedding's scatter sum (library),
     replayed as a HIP graph.  value = positions * sparse layers / step time;
     the sparse stack's share of the step is reported beside it."""
     over = {"batch": args.batch} if args.batch > 0 else {}
@@ -604,6 +607,10 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
     loss = torch.empty(rows, dtype=torch.float32, device=dev)
     dlogits = torch.empty(rows, V, dtype=dt, device=dev)
     d_table = torch.empty(V, w, dtype=torch.float32, device=dev)
+    gx_buf = torch.empty(B, n, w, dtype=dt, device=dev)
+    d_bias = torch.empty(V, dtype=torch.float32, device=dev)
+    head_ws = torch.empty(hcmix.load().hcmix_head_cross_entropy_workspace_bytes(rows, V),
+                          dtype=torch.uint8, device=dev)
     stack_ws = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
     emb_ws = torch.empty(hcmix.load().hcmix_embedding_backward_workspace_bytes(rows, w, V),
                          dtype=torch.uint8, device=dev)
@@ -623,15 +630,16 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
         xs = hcmix.stack_forward(x0, ws, wo, s.layers, True, outs=xs_out)
         mark()
         xl = xs[-1].view(rows, w)
+        # logits, loss, dlogits and the bias gradient in the library's kernel
         hcmix.head_cross_entropy(xl, head_w, head_b, targets, 1.0 / rows, loss=loss,
-                                 dlogits=dlogits)
-        # head gradients as plain GEMMs; the weight gradient's K = rows is split
-        # into 16 batched products (one GEMM over all rows leaves the chip idle)
+                                 dlogits=dlogits, dbias=d_bias, workspace=head_ws)
+        # weight and input gradients as plain GEMMs; the weight gradient's
+        # K = rows is split into 16 batched products (one GEMM over all rows
+        # leaves the chip idle)
         kch = 16
         grads["head_w"] = torch.bmm(xl.view(kch, rows // kch, w).transpose(1, 2),
                                     dlogits.view(kch, rows // kch, V)).sum(0).t()
-        grads["head_b"] = torch.sum(dlogits, 0, dtype=torch.float32)
-        gx = torch.matmul(dlogits, head_w).view(B, n, w)
+        gx = torch.matmul(dlogits, head_w, out=gx_buf.view(rows, w)).view(B, n, w)
         mark()
         hcmix.stack_backward(xs, ws, wo, s.layers, gx, True, dx=dx0, dws=dws, dwo=dwo,
                              workspace=stack_ws)
@@ -664,24 +672,41 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
         for _ in range(5):
             step(per)
         torch.cuda.synchronize()
+        # the stack's dominant kernels, timed as in the stack-only workload
+        kernels = dominant_kernel(args, hcmix, stream, x0, ws, wo, gx_buf, xs_out, [dx0], dws,
+                                  dwo, stack_ws, s.layers, B, n, w, L, True)
     names = ["embedding", "stack_forward", "head_and_cross_entropy", "stack_backward",
              "embedding_backward"]
     phase_ms = {nm: round(sum(ev[i].elapsed_time(ev[i + 1]) for ev in per) / len(per), 4)
                 for i, nm in enumerate(names)}
     sparse = phase_ms["stack_forward"] + phase_ms["stack_backward"]
     eager = sum(phase_ms.values())
+    flops, nbytes = algorithmic_work(B, n, w, L, True)
+    # the two ends: head logits, dlogits x W and dW_head (2 V w flops each per
+    # position); bytes: embedding gather (read the row, write x0) and its
+    # backward (read dx), head (read x twice, write dlogits, read it twice,
+    # write the input gradient)
+    flops += rows * 3 * 2 * V * w
+    nbytes += rows * (3 * 2 * w + 4 * w + 2 * w + 3 * 2 * V)
     out = {
         "metric": METRIC, "value": round(rows * L * args.steps / t, 1), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t / args.steps * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"lm256_step: {WORKLOADS['lm256_step']}", "batch": B, "n": n,
-                   "width": w, "layers": L, "vocab": V, "mode": "causal", "graph": True},
-        "lm_step": {"phase_ms_eager": phase_ms, "sparse_share_of_eager_step": round(sparse / eager, 4),
-                    "loss_mean": round(float(loss.mean()), 5),
-                    "note": "value counts the sparse layers' positions*layers per second of the "
-                            "whole training step (graph replay); phases timed on eager steps"},
+        "config": {"workload": f"lm256_step: {WORKLOADS['lm256_step']}"
+                               + (f" (batch overridden to {B})" if over else ""), "batch": B,
+                   "n": n, "width": w, "layers": L, "vocab": V, "mode": "causal", "graph": True},
+        "pct_bf16_peak": round(flops / t * args.steps / 1e12 / PEAK_BF16_TFLOPS * 100, 2),
+        "pct_hbm": round(nbytes / t * args.steps / 1e9 / PEAK_HBM_GBS * 100, 2),
     }
+    out.update(kernels)
+    out["lm_step"] = {"phase_ms_eager": phase_ms,
+                      "sparse_share_of_eager_step": round(sparse / eager, 4),
+                      "loss_mean": round(float(loss.mean()), 5),
+                      "note": "value = positions * sparse layers per second of the whole training "
+                              "step (graph replay); phases timed on eager steps with HIP events"}
+    if args.cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_lm(s, table, head_w, n, w, L, V, args.cpu_windows)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -792,6 +817,49 @@ def cpu_baseline(s, n, w, L, causal, windows):
     return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{what}, all {L} layers, forward+backward, {dt:.1f} s"}
+
+
+def cpu_baseline_lm(s, table, head_w, n, w, L, V, windows):
+    """The CPU oracle on a bounded sample of the whole LM step: `windows`
+    windows through the embedding, every layer, the head and cross-entropy,
+    the head's gradients (plain products on dlogits), the stack backward and
+    the embedding's scatter sum; sized like cpu_baseline when windows == 0."""
+    import numpy as np
+
+    import oracle
+    from oracle import lm_head
+
+    tab = table.float().cpu().numpy().astype(np.float64)
+    hw = head_w.float().cpu().numpy().astype(np.float64)
+    B = s.tokens.shape[0]
+
+    def run(k):
+        t0 = time.perf_counter()
+        x = lm_head.embedding_forward(tab, s.tokens[:k])
+        xs = oracle.stack_forward(x, s.w_self, s.w_off, s.layers, True)
+        xl = xs[-1].reshape(-1, w)
+        _, dlog = lm_head.head_cross_entropy(xl, hw, np.zeros(V), s.targets[:k], 1.0 / (B * n))
+        _ = dlog.T @ xl, dlog.sum(axis=0)
+        gx = (dlog @ hw).reshape(k, n, w)
+        dx, _, _ = oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, gx, True)
+        lm_head.embedding_backward(s.tokens[:k], dx, V)
+        return time.perf_counter() - t0
+
+    passes = 1
+    if windows <= 0:
+        target = 25.0
+        pilot = min(B, 4)
+        per_window = run(pilot) / pilot
+        windows = max(1, min(B, int(target / max(per_window, 1e-4))))
+        if windows == B:
+            passes = max(1, min(200, int(round(target / max(per_window * B, 1e-4)))))
+    dt = sum(run(windows) for _ in range(passes))
+    what = (f"{windows} of the workload's {B} windows" if windows < B
+            else f"all {B} windows" + (f", {passes} passes" if passes > 1 else ""))
+    return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{what}: embedding, all {L} layers, head and cross-entropy, forward+"
+                      f"backward, {dt:.1f} s"}
 
 
 if __name__ == "__main__":

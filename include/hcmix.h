@@ -303,8 +303,9 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
  *   dlogits[r] = scale (softmax(logits[r]) - onehot(targets[r]))   (scale = 1/rows: mean loss).
  * rows = batch * n positions; table and W are [vocab][width] bf16, x and dx
  * [rows][width] bf16, tokens and targets int32 [rows], bias, loss and dtable
- * fp32, dlogits [rows][vocab] bf16 (the gradients of W, bias and x then are
- * plain products with it: dlogits^T x, its column sums, dlogits W).
+ * fp32, dlogits [rows][vocab] bf16 (the gradients of W and x then are plain
+ * products with it: dlogits^T x and dlogits W; the bias gradient, its column
+ * sums, comes with it).
  * bf16 only; width a multiple of 64; head: vocab a multiple of 32 up to 256.
  * A token outside [0, vocab) embeds as a zero row and is skipped by the
  * backward; a target outside it contributes log sum exp alone.  The embedding
@@ -324,9 +325,18 @@ hcmix_status hcmix_embedding_backward(int64_t rows, int64_t width, int32_t vocab
                                       int32_t accumulate, void* workspace, size_t workspace_bytes,
                                       void* stream);
 
+/* Output head and cross-entropy: loss and dlogits as above and, when dbias is
+ * not NULL, the bias gradient dbias[v] = sum over rows of dlogits[r][v]
+ * (overwritten; summed from the unrounded fp32 values in a fixed order,
+ * bitwise-repeatable) through a workspace of
+ * hcmix_head_cross_entropy_workspace_bytes (256-byte aligned; unused, may be
+ * NULL, without dbias). */
+size_t hcmix_head_cross_entropy_workspace_bytes(int64_t rows, int32_t vocab);
+
 hcmix_status hcmix_head_cross_entropy(int64_t rows, int64_t width, int32_t vocab, const void* x,
                                       const void* w, const float* bias, const int32_t* targets,
-                                      float scale, float* loss, void* dlogits, void* stream);
+                                      float scale, float* loss, void* dlogits, float* dbias,
+                                      void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

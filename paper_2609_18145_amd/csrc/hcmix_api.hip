@@ -789,26 +789,37 @@ hcmix_status hcmix_embedding_backward(int64_t rows, int64_t width, int32_t vocab
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
+size_t hcmix_head_cross_entropy_workspace_bytes(int64_t rows, int32_t vocab) {
+  if (rows < 1 || rows > kMaxRows || vocab < 32 || vocab > 256 || vocab % 32) return 0;
+  return align256(head_workspace_bytes((int)rows, vocab));
+}
+
 hcmix_status hcmix_head_cross_entropy(int64_t rows, int64_t width, int32_t vocab, const void* x,
                                       const void* w, const float* bias, const int32_t* targets,
-                                      float scale, float* loss, void* dlogits, void* stream) {
+                                      float scale, float* loss, void* dlogits, float* dbias,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
   if (!x || !w || !bias || !targets || !loss || !dlogits) return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_lm(rows, width, vocab);
   if (st != HCMIX_OK) return st;
   if (vocab % 32 != 0 || vocab > 256) return HCMIX_ERR_UNSUPPORTED;
+  const size_t need = dbias ? head_workspace_bytes((int)rows, vocab) : 0;
+  if (dbias && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
   const Span ins[4] = {{x, (size_t)rows * width * sizeof(bf16)},
                        {w, (size_t)vocab * width * sizeof(bf16)},
                        {bias, (size_t)vocab * sizeof(float)},
                        {targets, (size_t)rows * sizeof(int32_t)}};
-  const Span outs[2] = {{loss, (size_t)rows * sizeof(float)},
-                        {dlogits, (size_t)rows * vocab * sizeof(bf16)}};
-  st = check_spans(ins, 4, outs, 2, 4);
+  const Span outs[4] = {{loss, (size_t)rows * sizeof(float)},
+                        {dlogits, (size_t)rows * vocab * sizeof(bf16)},
+                        {dbias, dbias ? (size_t)vocab * sizeof(float) : 0},
+                        {workspace, need}};
+  st = check_spans(ins, 4, outs, 4, 4);
   if (st != HCMIX_OK) return st;
   if (!aligned(x, 16) || !aligned(w, 16) || !aligned(bias, 16) || !aligned(dlogits, 16))
     return HCMIX_ERR_UNSUPPORTED;
+  if (dbias && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
   hipError_t e = launch_head_ce((const bf16*)x, (const bf16*)w, bias, (const int*)targets, scale,
-                                loss, (bf16*)dlogits, (int)rows, (int)width, vocab,
-                                (hipStream_t)stream);
+                                loss, (bf16*)dlogits, dbias, (float*)workspace, (int)rows,
+                                (int)width, vocab, (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 

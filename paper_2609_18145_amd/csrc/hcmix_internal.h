@@ -158,9 +158,12 @@ hipError_t launch_embedding_fwd(const bf16* table, const int* tokens, bf16* x, i
                                 int width, int vocab, hipStream_t st);
 hipError_t launch_embedding_bwd(const int* tokens, const bf16* dx, float* dtable, int accumulate,
                                 float* workspace, int rows, int width, int vocab, hipStream_t st);
+// Head: with dbias, also the bias gradient (column sums of dlogits) through
+// head_workspace_bytes of per-block sums.
+size_t head_workspace_bytes(int rows, int vocab);
 hipError_t launch_head_ce(const bf16* x, const bf16* w, const float* bias, const int* targets,
-                          float scale, float* loss, bf16* dlogits, int rows, int width, int vocab,
-                          hipStream_t st);
+                          float scale, float* loss, bf16* dlogits, float* dbias, float* workspace,
+                          int rows, int width, int vocab, hipStream_t st);
 
 struct DecodeLayerArgs {
   const bf16* x_in;

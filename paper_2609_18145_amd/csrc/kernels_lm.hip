@@ -37,14 +37,17 @@ __global__ __launch_bounds__(LM_THREADS) void embed_fwd_kernel(
 // ---------------------------------------------------------------------------
 // Embedding backward, fixed summation order.  Block (v, c) sums, for vocabulary
 // entry v, the rows of chunk c (emb_chunks(rows) chunks of consecutive rows,
-// at most EMB_MAX_CHUNK each) whose token is v: wave 0 lists the matching rows
-// in row order, then wave k adds matches k, k + 4, ... in that order (8 columns
-// per lane, 64 lanes: 512 columns per pass), and the four wave sums are added
-// in wave order into partial[c][v].
+// at most EMB_MAX_CHUNK each) whose token is v.  Each of the four waves lists
+// the matching rows of its quarter of the chunk, in row order, with all its
+// token loads in flight at once; the four lists read back to back are the
+// chunk's matches in row order.  Wave k then adds matches k, k + 4, ... in
+// that order (8 columns per lane, 64 lanes: 512 columns per pass), and the
+// four wave sums are added in wave order into partial[c][v].
 // A second kernel adds the chunks in chunk order.
 // ---------------------------------------------------------------------------
 constexpr int EMB_MIN_CHUNKS = 32;    // spreads a frequent token's rows over blocks
 constexpr int EMB_MAX_CHUNK = 4096;   // rows per chunk held in LDS as a match list
+constexpr int EMB_SCAN_LOADS = 4;     // token loads in flight per lane while listing
 int emb_chunks(int rows) {
   const int c = (rows + EMB_MAX_CHUNK - 1) / EMB_MAX_CHUNK;
   return c > EMB_MIN_CHUNKS ? c : EMB_MIN_CHUNKS;
@@ -54,24 +57,42 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_partial_kernel(
     const int* __restrict__ tokens, const bf16* __restrict__ dx, float* __restrict__ partial,
     int rows, int width, int vocab, int chunk) {
   __shared__ int list[EMB_MAX_CHUNK];
-  __shared__ int count;
+  __shared__ int count[4];
   __shared__ float red[4][512];
   const int v = blockIdx.x % vocab, c = blockIdx.x / vocab;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r0 = c * chunk, r1 = min(rows, r0 + chunk);
-  if (wave == 0) {
+  // wave w lists rows [q0, q1) into list[w * span ...]
+  const int span = (chunk + 3) / 4;
+  const int q0 = min(r1, r0 + wave * span), q1 = min(r1, q0 + span);
+  {
+    int* wl = list + wave * span;
     int n = 0;
-    for (int base = r0; base < r1; base += 64) {
-      const int r = base + lane;
-      const bool hit = r < r1 && tokens[r] == v;
-      const unsigned long long m = __ballot(hit);
-      if (hit) list[n + __popcll(m & ((1ull << lane) - 1))] = r;
-      n += __popcll(m);
+    for (int base = q0; base < q1; base += 64 * EMB_SCAN_LOADS) {
+      int tk[EMB_SCAN_LOADS];
+#pragma unroll
+      for (int u = 0; u < EMB_SCAN_LOADS; u++) {
+        const int r = base + 64 * u + lane;
+        tk[u] = r < q1 ? tokens[r] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < EMB_SCAN_LOADS; u++) {
+        const bool hit = tk[u] == v;       // v >= 0, so rows past q1 never hit
+        const unsigned long long m = __ballot(hit);
+        if (hit) wl[n + __popcll(m & ((1ull << lane) - 1))] = base + 64 * u + lane;
+        n += __popcll(m);
+      }
     }
-    if (lane == 0) count = n;
+    if (lane == 0) count[wave] = n;
   }
   __syncthreads();
-  const int n = count;
+  const int o1 = count[0], o2 = o1 + count[1], o3 = o2 + count[2], n = o3 + count[3];
+  // match k of the chunk, in row order
+  auto match = [&](int k) {
+    const int w = (k >= o1) + (k >= o2) + (k >= o3);
+    const int o = w == 0 ? 0 : w == 1 ? o1 : w == 2 ? o2 : o3;
+    return list[w * span + k - o];
+  };
   float* out = partial + ((size_t)c * vocab + v) * width;
   for (int c0 = 0; c0 < width; c0 += 512) {
     const int col = c0 + 8 * lane;
@@ -83,14 +104,14 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_partial_kernel(
       for (; k + 28 < n; k += 32) {
         bf16x8 g[8];
 #pragma unroll
-        for (int u = 0; u < 8; u++) g[u] = *(const bf16x8*)(dx + (size_t)list[k + 4 * u] * width + col);
+        for (int u = 0; u < 8; u++) g[u] = *(const bf16x8*)(dx + (size_t)match(k + 4 * u) * width + col);
 #pragma unroll
         for (int u = 0; u < 8; u++)
 #pragma unroll
           for (int e = 0; e < 8; e++) acc[e] += (float)g[u][e];
       }
       for (; k < n; k += 4) {
-        const bf16x8 g = *(const bf16x8*)(dx + (size_t)list[k] * width + col);
+        const bf16x8 g = *(const bf16x8*)(dx + (size_t)match(k) * width + col);
 #pragma unroll
         for (int e = 0; e < 8; e++) acc[e] += (float)g[e];
       }
@@ -115,116 +136,216 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_reduce_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Head + cross-entropy.  Block: 4 waves x 32 rows.  Wave: logits^T for its 32
-// rows and all NT * 32 vocabulary entries; the weights pass through LDS in
-// 64-column slices shared by the four waves (two buffers), the wave's rows
-// come straight from global memory.  Register e of tile t holds entry
-// 32 t + 8 (e / 4) + 4 (lane / 32) + e % 4 of row lane % 32.
+// Head + cross-entropy.  Block: 64 rows, four waves; wave (g, h) = (wave % 2,
+// wave / 2) computes logits^T for rows 32 g .. 32 g + 31 of the block and the
+// vocabulary tiles of half h (tiles 0 .. TA-1 or TA .. NT-1, TA = ceil(NT/2)).
+// The weights pass through LDS in 64-column slices, three stages filled by LDS
+// DMA two slices ahead, each block starting at its own slice; each wave loads
+// the x fragments of eight slices at a time into registers.  Register e of tile t holds entry 32 t + 8 (e / 4) + 4 (lane / 32)
+// + e % 4 of row lane % 32, so a row's softmax is in-lane, one exchange with
+// lane ^ 32 and one exchange with the other half's wave through LDS.
+// With `dbp` the block also writes the column sums of its rows' dlogits (fp32,
+// rows in order) to dbp[block][V], which head_db_reduce_kernel adds up.
 // ---------------------------------------------------------------------------
+constexpr int HEAD_ROWS = 64;
+constexpr int HEAD_XS = 8;      // slices of x fragments held in registers at once
+
+template <int NT>
+struct HeadCfg {
+  static constexpr int V = NT * 32;
+  static constexpr int TA = (NT + 1) / 2;         // tiles of the first half
+  static constexpr int SLICE = V * 64;            // bf16 elements per weight slice
+  static constexpr int DMA = V / 32;              // 1 KB DMA blocks per wave per slice
+  static constexpr int DB_LD = V + 4;             // fp32 row stride of the dlogits staging
+  static constexpr size_t LDS = (size_t)3 * SLICE * sizeof(bf16);
+  static_assert((size_t)HEAD_ROWS * DB_LD * sizeof(float) <= LDS, "dlogits staging fits");
+};
+
 template <int NT>
 __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
     const bf16* __restrict__ x, const bf16* __restrict__ w, const float* __restrict__ bias,
     const int* __restrict__ targets, float scale, float* __restrict__ loss,
-    bf16* __restrict__ dlogits, int rows, int width) {
-  constexpr int V = NT * 32;
-  constexpr int PIECES = V * 8 / LM_THREADS;        // 16-byte pieces of a slice per thread
-  __shared__ __attribute__((aligned(1024))) bf16 sw[2][V * 64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  int r = (blockIdx.x * 4 + wave) * 32 + (lane & 31);
+    bf16* __restrict__ dlogits, float* __restrict__ dbp, int rows, int width) {
+  using C = HeadCfg<NT>;
+  constexpr int V = C::V, TA = C::TA;
+  extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
+  __shared__ float xmax[2][HEAD_ROWS], xsum[2][HEAD_ROWS], xtl[2][HEAD_ROWS];
+  const int lane = threadIdx.x & 63;
+  // wave-uniform as far as the compiler knows: every MFMA guard below is a
+  // scalar branch
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = wave & 1, hv = wave >> 1, half = lane >> 5;
+  const int t0 = hv ? TA : 0, nt = hv ? NT - TA : TA;
+  const int lrow = g * 32 + (lane & 31);               // row within the block
+  int r = blockIdx.x * HEAD_ROWS + lrow;
   const bool live = r < rows;
-  if (!live) r = rows - 1;                     // load a valid row, store nothing
+  if (!live) r = rows - 1;                              // load a valid row, store nothing
   const bf16* xr = x + (size_t)r * width + 8 * half;
-  u32x4 wreg[PIECES];
-  auto fetch = [&](int k0) {
-#pragma unroll
-    for (int j = 0; j < PIECES; j++) {
-      const int pi = threadIdx.x + LM_THREADS * j, row = pi >> 3, p = pi & 7;
-      wreg[j] = *(const u32x4*)(w + (size_t)row * width + k0 + 8 * p);
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < PIECES; j++) {
-      const int pi = threadIdx.x + LM_THREADS * j, row = pi >> 3, p = pi & 7;
-      *(u32x4*)(sw[buf] + swz<64>(row, p)) = wreg[j];
-    }
-  };
-  f32x16 acc[NT];
-#pragma unroll
-  for (int t = 0; t < NT; t++) acc[t] = f32x16{};
   const int slices = width / 64;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int sl = 0; sl < slices; sl++) {
-    const int k0 = sl * 64;
-    bf16x8 b[4];
+  // the blocks walk the weight slices from different starting points (the
+  // contraction's order is free), so that they do not all stream the same
+  // weight lines out of L2 at once
+  const int rot = blockIdx.x % slices;
+  auto col0 = [&](int sl) {                 // logical slice -> first column
+    const int p = min(sl, slices - 1) + rot;
+    return (p >= slices ? p - slices : p) * 64;
+  };
+
+  // weight slice sl (clamped: issues past the last slice repeat it into a
+  // stage nobody reads again) -> stage
+  auto dma = [&](int sl, int stage) {
+    const int k0 = col0(sl);
+    bf16* dst = smem + stage * C::SLICE;
 #pragma unroll
-    for (int kk = 0; kk < 4; kk++) b[kk] = *(const bf16x8*)(xr + k0 + 16 * kk);
-    if (sl + 1 < slices) fetch(k0 + 64);
-    const bf16* cur = sw[sl & 1];
+    for (int j = 0; j < C::DMA; j++) {
+      const int blk = j * 4 + wave, row = blk * 8 + (lane >> 3);
+      const int piece = (lane & 7) ^ ((row >> 1) & 7);
+      dma16(w + (size_t)row * width + k0 + 8 * piece, dst + blk * 512);
+    }
+  };
+  f32x16 acc[TA];
 #pragma unroll
-    for (int kk = 0; kk < 4; kk++)
+  for (int t = 0; t < TA; t++) acc[t] = f32x16{};
+  dma(0, 0);
+  dma(1, 1);
+  // x fragments of HEAD_XS slices at a time, all loaded at the chunk's start
+  // (one memory latency per chunk); the weights two slices ahead by DMA
+  for (int c0 = 0; c0 < slices; c0 += HEAD_XS) {
+    bf16x8 xf[HEAD_XS][4];
 #pragma unroll
-      for (int t = 0; t < NT; t++)
-        acc[t] = mfma32(*(const bf16x8*)(cur + swz<64>(32 * t + (lane & 31), 2 * kk + half)),
-                        b[kk], acc[t]);
-    if (sl + 1 < slices) stash((sl + 1) & 1);
-    __syncthreads();
+    for (int i = 0; i < HEAD_XS; i++) {
+      const int k0 = col0(c0 + i);
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) xf[i][kk] = *(const bf16x8*)(xr + k0 + 16 * kk);
+    }
+#pragma unroll
+    for (int i = 0; i < HEAD_XS; i++) {
+      const int sl = c0 + i;
+      if (sl >= slices) break;
+      // loads issued after DMA(sl): DMA(sl + 1), plus this chunk's x loads
+      // for the chunk's first two slices (their DMAs came before them)
+      if (i < 2)
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::DMA + 4 * HEAD_XS)
+                     : "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::DMA) : "memory");
+      dma(sl + 2, (sl + 2) % 3);
+      const bf16* cur = smem + (sl % 3) * C::SLICE;
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++)
+#pragma unroll
+        for (int t = 0; t < TA; t++)
+          if (t < nt)
+            acc[t] = mfma32(
+                *(const bf16x8*)(cur + swz<64>(32 * (t0 + t) + (lane & 31), 2 * kk + half)),
+                xf[i][kk], acc[t]);
+    }
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // softmax over the row: in-lane, lane ^ 32, then the other half's wave
   const int tgt = targets[r];
   float mx = -INFINITY, tl = 0.f;
 #pragma unroll
-  for (int t = 0; t < NT; t++)
+  for (int t = 0; t < TA; t++) {
+    if (t >= nt) continue;
 #pragma unroll
-    for (int g = 0; g < 4; g++) {
-      const int v0 = 32 * t + 8 * g + 4 * half;
+    for (int q = 0; q < 4; q++) {
+      const int v0 = 32 * (t0 + t) + 8 * q + 4 * half;
       const f32x4 b4 = *(const f32x4*)(bias + v0);
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const float l = acc[t][4 * g + j] + b4[j];
-        acc[t][4 * g + j] = l;
+        const float l = acc[t][4 * q + j] + b4[j];
+        acc[t][4 * q + j] = l;
         mx = fmaxf(mx, l);
         if (v0 + j == tgt) tl = l;
       }
     }
+  }
   mx = fmaxf(mx, __shfl_xor(mx, 32));
   tl += __shfl_xor(tl, 32);
+  if (half == 0) {
+    xmax[hv][lrow] = mx;
+    xtl[hv][lrow] = tl;
+  }
+  __syncthreads();
+  mx = fmaxf(xmax[0][lrow], xmax[1][lrow]);
+  tl = xtl[0][lrow] + xtl[1][lrow];
   const float LOG2E = 1.4426950408889634f;
   float sum = 0.f;
 #pragma unroll
-  for (int t = 0; t < NT; t++)
+  for (int t = 0; t < TA; t++) {
+    if (t >= nt) continue;
 #pragma unroll
     for (int e = 0; e < 16; e++) {
       const float p = __builtin_amdgcn_exp2f((acc[t][e] - mx) * LOG2E);
       acc[t][e] = p;
       sum += p;
     }
+  }
   sum += __shfl_xor(sum, 32);
+  if (half == 0) xsum[hv][lrow] = sum;
+  __syncthreads();
+  sum = xsum[0][lrow] + xsum[1][lrow];
   const float inv = 1.f / sum;
-  if (!live) return;
-  if (half == 0) loss[r] = mx + __builtin_amdgcn_logf(sum) * 0.6931471805599453f - tl;
+  if (live && hv == 0 && half == 0)
+    loss[r] = mx + __builtin_amdgcn_logf(sum) * 0.6931471805599453f - tl;
+  float* dbs = (float*)smem;                            // [HEAD_ROWS][DB_LD] fp32
   bf16* dr = dlogits + (size_t)r * V;
 #pragma unroll
-  for (int t = 0; t < NT; t++)
+  for (int t = 0; t < TA; t++) {
+    if (t >= nt) continue;
 #pragma unroll
-    for (int g = 0; g < 4; g++) {
-      const int v0 = 32 * t + 8 * g + 4 * half;
+    for (int q = 0; q < 4; q++) {
+      const int v0 = 32 * (t0 + t) + 8 * q + 4 * half;
+      f32x4 d;
       bf16x4 o;
 #pragma unroll
-      for (int j = 0; j < 4; j++)
-        o[j] = to_bf16(scale * (acc[t][4 * g + j] * inv - (v0 + j == tgt ? 1.f : 0.f)));
-      *(bf16x4*)(dr + v0) = o;
+      for (int j = 0; j < 4; j++) {
+        d[j] = live ? scale * (acc[t][4 * q + j] * inv - (v0 + j == tgt ? 1.f : 0.f)) : 0.f;
+        o[j] = to_bf16(d[j]);
+      }
+      if (live) *(bf16x4*)(dr + v0) = o;
+      if (dbp) *(f32x4*)(dbs + lrow * C::DB_LD + v0) = d;
     }
+  }
+  if (!dbp) return;
+  __syncthreads();
+  for (int v = threadIdx.x; v < V; v += LM_THREADS) {
+    float s = 0.f;
+    for (int k = 0; k < HEAD_ROWS; k++) s += dbs[k * C::DB_LD + v];
+    dbp[(size_t)blockIdx.x * V + v] = s;
+  }
+}
+
+// dbias[v] = sum over blocks b of dbp[b][v]: one wave per entry, lane j adding
+// blocks j, j + 64, ... in order, then a fixed butterfly over the lanes.
+__global__ __launch_bounds__(64) void head_db_reduce_kernel(const float* __restrict__ dbp,
+                                                             float* __restrict__ dbias, int blocks,
+                                                             int vocab) {
+  const int v = blockIdx.x, lane = threadIdx.x;
+  float s = 0.f;
+  for (int b = lane; b < blocks; b += 64) s += dbp[(size_t)b * vocab + v];
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) s += __shfl_xor(s, m);
+  if (lane == 0) dbias[v] = s;
 }
 
 template <int NT>
 hipError_t head_launch(const bf16* x, const bf16* w, const float* bias, const int* targets,
-                       float scale, float* loss, bf16* dlogits, int rows, int width,
-                       hipStream_t st) {
-  const int blocks = (rows + 127) / 128;
-  head_ce_kernel<NT><<<blocks, LM_THREADS, 0, st>>>(x, w, bias, targets, scale, loss, dlogits,
-                                                    rows, width);
+                       float scale, float* loss, bf16* dlogits, float* dbias, float* dbp,
+                       int rows, int width, hipStream_t st) {
+  using C = HeadCfg<NT>;
+  const int blocks = (rows + HEAD_ROWS - 1) / HEAD_ROWS;
+  auto k = head_ce_kernel<NT>;
+  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)C::LDS);
+  if (e != hipSuccess) return e;
+  k<<<blocks, LM_THREADS, C::LDS, st>>>(x, w, bias, targets, scale, loss, dlogits,
+                                         dbias ? dbp : nullptr, rows, width);
+  e = hipGetLastError();
+  if (e != hipSuccess || !dbias) return e;
+  head_db_reduce_kernel<<<C::V, 64, 0, st>>>(dbp, dbias, blocks, C::V);
   return hipGetLastError();
 }
 
@@ -257,20 +378,29 @@ hipError_t launch_embedding_bwd(const int* tokens, const bf16* dx, float* dtable
   return hipGetLastError();
 }
 
+size_t head_workspace_bytes(int rows, int vocab) {
+  return (size_t)((rows + HEAD_ROWS - 1) / HEAD_ROWS) * vocab * sizeof(float);
+}
+
 hipError_t launch_head_ce(const bf16* x, const bf16* w, const float* bias, const int* targets,
-                          float scale, float* loss, bf16* dlogits, int rows, int width, int vocab,
-                          hipStream_t st) {
+                          float scale, float* loss, bf16* dlogits, float* dbias, float* workspace,
+                          int rows, int width, int vocab, hipStream_t st) {
+#define HCMIX_HEAD_CASE(NT)                                                                    \
+  case NT:                                                                                     \
+    return head_launch<NT>(x, w, bias, targets, scale, loss, dlogits, dbias, workspace, rows, \
+                           width, st);
   switch (vocab / 32) {
-    case 1: return head_launch<1>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 2: return head_launch<2>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 3: return head_launch<3>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 4: return head_launch<4>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 5: return head_launch<5>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 6: return head_launch<6>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 7: return head_launch<7>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
-    case 8: return head_launch<8>(x, w, bias, targets, scale, loss, dlogits, rows, width, st);
+    HCMIX_HEAD_CASE(1)
+    HCMIX_HEAD_CASE(2)
+    HCMIX_HEAD_CASE(3)
+    HCMIX_HEAD_CASE(4)
+    HCMIX_HEAD_CASE(5)
+    HCMIX_HEAD_CASE(6)
+    HCMIX_HEAD_CASE(7)
+    HCMIX_HEAD_CASE(8)
     default: return hipErrorInvalidValue;
   }
+#undef HCMIX_HEAD_CASE
 }
 
 }  // namespace hcmix

@@ -33,7 +33,7 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_decode_cache_bytes", "hcmix_decode_step", "hcmix_attention_forward",
            "hcmix_attention_backward", "hcmix_embedding_forward",
            "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
-           "hcmix_head_cross_entropy")
+           "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy")
 
 _lib = None
 
@@ -97,8 +97,10 @@ def load():
         lib.hcmix_embedding_backward_workspace_bytes.restype = sz
         lib.hcmix_embedding_backward.argtypes = [i64, i64, i32, vp, vp, fp, i32, vp, sz, vp]
         lib.hcmix_embedding_backward.restype = i32
+        lib.hcmix_head_cross_entropy_workspace_bytes.argtypes = [i64, i32]
+        lib.hcmix_head_cross_entropy_workspace_bytes.restype = sz
         lib.hcmix_head_cross_entropy.argtypes = [i64, i64, i32, vp, vp, fp, vp, ctypes.c_float,
-                                                 fp, vp, vp]
+                                                 fp, vp, fp, vp, sz, vp]
         lib.hcmix_head_cross_entropy.restype = i32
         lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
@@ -370,20 +372,34 @@ def embedding_backward(tokens, dx, vocab, dtable=None, accumulate=False, workspa
     return dtable
 
 
-def head_cross_entropy(x, w, bias, targets, scale, loss=None, dlogits=None):
-    """Per-row loss (fp32 [rows]) and scale * (softmax - onehot) (bf16 [rows, vocab])."""
+def head_cross_entropy(x, w, bias, targets, scale, loss=None, dlogits=None, dbias=None,
+                       with_dbias=False, workspace=None):
+    """Per-row loss (fp32 [rows]) and scale * (softmax - onehot) (bf16 [rows, vocab]);
+    with with_dbias (or a dbias buffer), also the bias gradient (fp32 [vocab]):
+    returns (loss, dlogits) or (loss, dlogits, dbias)."""
     vocab, width = w.shape
     rows = targets.numel()
     if loss is None:
         loss = torch.empty(rows, dtype=torch.float32, device=x.device)
     if dlogits is None:
         dlogits = torch.empty((rows, vocab), dtype=x.dtype, device=x.device)
+    want_db = with_dbias or dbias is not None
+    ws_bytes = 0
+    if want_db:
+        if dbias is None:
+            dbias = torch.empty(vocab, dtype=torch.float32, device=x.device)
+        if workspace is None:
+            workspace = torch.empty(load().hcmix_head_cross_entropy_workspace_bytes(rows, vocab),
+                                    dtype=torch.uint8, device=x.device)
+        ws_bytes = workspace.numel()
     rc = load().hcmix_head_cross_entropy(rows, width, vocab, _ptr(x), _ptr(w), _fptr(bias),
                                          _ptr(targets), float(scale), _fptr(loss), _ptr(dlogits),
+                                         _fptr(dbias) if want_db else None,
+                                         _ptr(workspace) if want_db else None, ws_bytes,
                                          _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_cross_entropy")
-    return loss, dlogits
+    return (loss, dlogits, dbias) if want_db else (loss, dlogits)
 
 
 class Attention(torch.autograd.Function):

@@ -249,14 +249,28 @@ def test_lm_entry_points_reject_bad_arguments():
     assert eb(1000, 64, 16, P[0], P[1], fp(P[2]), 0, ctypes.c_void_p(P[3].value + 16), need,
               None) == UNSUPPORTED
     hc = lib.hcmix_head_cross_entropy
-    args = [P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[5], None]
+    nodb = [None, None, 0, None]                                      # no bias gradient
+    args = [P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[5], *nodb]
     assert hc(100, 64, 0, *args) == INVALID
     assert hc(100, 64, 48, *args) == UNSUPPORTED                      # vocab % 32
     assert hc(100, 64, 288, *args) == UNSUPPORTED                     # vocab > 256
     assert hc(100, 64, 256, P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[4],
-              None) == INVALID                                        # dlogits over the loss
+              *nodb) == INVALID                                       # dlogits over the loss
     assert hc(100, 64, 256, P[0], P[1], fp(ctypes.c_void_p(P[2].value + 4)), P[3],
-              ctypes.c_float(0.5), fp(P[4]), P[5], None) == UNSUPPORTED   # bias alignment
+              ctypes.c_float(0.5), fp(P[4]), P[5], *nodb) == UNSUPPORTED   # bias alignment
+    # the bias gradient: per-block column sums of 64 rows each
+    q = lib.hcmix_head_cross_entropy_workspace_bytes
+    assert q(16384, 256) == 256 * 256 * 4
+    assert q(100, 96) == 768                                          # 2 blocks x 96 x 4 bytes
+    assert q(100, 48) == 0 and q(0, 256) == 0
+    dneed = q(100, 256)
+    base = [P[0], P[1], fp(P[2]), P[3], ctypes.c_float(0.5), fp(P[4]), P[5]]
+    assert hc(100, 64, 256, *base, fp(P[6]), None, dneed, None) == INVALID       # no workspace
+    assert hc(100, 64, 256, *base, fp(P[6]), P[7], dneed - 1, None) == INVALID   # short
+    assert hc(100, 64, 256, *base, fp(P[1]), P[7], dneed, None) == INVALID       # dbias over w
+    assert hc(100, 64, 256, *base, fp(P[6]), P[5], dneed, None) == INVALID       # over dlogits
+    assert hc(100, 64, 256, *base, fp(P[6]), ctypes.c_void_p(P[7].value + 16), dneed,
+              None) == UNSUPPORTED                                    # workspace alignment
 
 
 def test_stack_workspace_query():

@@ -75,32 +75,44 @@ def test_head_cross_entropy_matches_oracle(rows, width, vocab):
     w = inputs.round_bf16((rng.standard_normal((vocab, width)) / np.sqrt(width)).astype(np.float32))
     bias = (rng.standard_normal(vocab) * 0.3).astype(np.float32)
     targets = rng.integers(0, vocab, rows)
-    loss, d = hcmix.head_cross_entropy(to_dev(x, "bf16"), to_dev(w, "bf16"),
-                                       torch.from_numpy(bias).cuda(), i32(targets), 1.0 / rows)
+    args = (to_dev(x, "bf16"), to_dev(w, "bf16"), torch.from_numpy(bias).cuda(), i32(targets),
+            1.0 / rows)
+    loss, d, db = hcmix.head_cross_entropy(*args, with_dbias=True)
+    loss2, d2 = hcmix.head_cross_entropy(*args)             # without the bias gradient
+    _, _, db2 = hcmix.head_cross_entropy(*args, with_dbias=True)
     torch.cuda.synchronize()
     r_loss, r_d = lm_head.head_cross_entropy(x, w, bias, targets, 1.0 / rows)
     e_loss = np.abs(to_host(loss) - r_loss).max()
     g, r = to_host(d), r_d
     e_d = (np.linalg.norm(g - r, axis=1) / np.linalg.norm(r, axis=1)).max()
-    print(f"  loss abs err {e_loss:.2e}  dlogits row err {e_d:.2e}", flush=True)
+    r_db = r_d.sum(axis=0)
+    e_db = np.linalg.norm(to_host(db) - r_db) / np.linalg.norm(r_db)
+    print(f"  loss abs err {e_loss:.2e}  dlogits row err {e_d:.2e}  dbias err {e_db:.2e}",
+          flush=True)
     assert e_loss <= 1e-4
     assert e_d <= 2e-2
+    assert e_db <= 1e-3
+    assert torch.equal(loss, loss2) and torch.equal(d, d2) and torch.equal(db, db2)
 
 
 def test_head_cross_entropy_full_lm_shape_sampled():
-    """16384 rows (64 windows of 256), width 512, 256-way head: every loss, and
-    the gradient rows of windows 0 and 63, against the oracle."""
+    """16384 rows (64 windows of 256), width 512, 256-way head: every loss, the
+    bias gradient, and the gradient rows of windows 0 and 63, against the
+    oracle."""
     rows, width, vocab = 16384, 512, 256
     rng = np.random.default_rng(9)
     x = inputs.round_bf16(rng.standard_normal((rows, width)).astype(np.float32))
     w = inputs.round_bf16((rng.standard_normal((vocab, width)) / np.sqrt(width)).astype(np.float32))
     bias = np.zeros(vocab, dtype=np.float32)
     targets = inputs.zipf_byte_tokens(rng, (rows,))
-    loss, d = hcmix.head_cross_entropy(to_dev(x, "bf16"), to_dev(w, "bf16"),
-                                       torch.from_numpy(bias).cuda(), i32(targets), 1.0 / rows)
+    loss, d, db = hcmix.head_cross_entropy(to_dev(x, "bf16"), to_dev(w, "bf16"),
+                                           torch.from_numpy(bias).cuda(), i32(targets),
+                                           1.0 / rows, with_dbias=True)
     torch.cuda.synchronize()
-    r_loss, _ = lm_head.head_cross_entropy(x, w, bias, targets, 1.0 / rows)
+    r_loss, r_all = lm_head.head_cross_entropy(x, w, bias, targets, 1.0 / rows)
     assert np.abs(to_host(loss) - r_loss).max() <= 1e-4
+    r_db = r_all.sum(axis=0)
+    assert np.linalg.norm(to_host(db) - r_db) / np.linalg.norm(r_db) <= 1e-3
     for sl in (slice(0, 256), slice(rows - 256, rows)):
         _, r_d = lm_head.head_cross_entropy(x[sl], w, bias, targets[sl], 1.0 / rows)
         g = to_host(d)[sl]
