@@ -117,3 +117,79 @@ def test_head_cross_entropy_full_lm_shape_sampled():
         _, r_d = lm_head.head_cross_entropy(x[sl], w, bias, targets[sl], 1.0 / rows)
         g = to_host(d)[sl]
         assert (np.linalg.norm(g - r_d, axis=1) / np.linalg.norm(r_d, axis=1)).max() <= 2e-2
+
+
+def test_whole_lm_step_replays_in_a_graph():
+    """The LM step the default benchmark replays (embedding gather, the stack
+    forward on the deferred path, head + cross-entropy with the bias gradient,
+    the input gradient as a plain product, the stack backward, the embedding's
+    scatter sum), captured from a side stream and replayed three times with
+    eager work and synchronisation in between: every output of every replay
+    bitwise equal to the eager step, and the loss against the oracle."""
+    import oracle
+    B, n, w, L, V = 4, 256, 256, 4, 256
+    rows = B * n
+    s = inputs.make_stack(batch=B, n=n, width=w, num_layers=L, causal=True, dtype="bf16", seed=71)
+    rng = np.random.default_rng(72)
+    table_np = inputs.round_bf16(rng.standard_normal((V, w)).astype(np.float32))
+    head_np = inputs.round_bf16((rng.standard_normal((V, w)) / np.sqrt(w)).astype(np.float32))
+    tokens_np = inputs.zipf_byte_tokens(rng, (rows,))
+    targets_np = inputs.zipf_byte_tokens(rng, (rows,))
+    print(f"case: LM step graph replay B={B} n={n} w={w} L={L} V={V}", flush=True)
+    table, head_w = to_dev(table_np, "bf16"), to_dev(head_np, "bf16")
+    head_b = torch.zeros(V, dtype=torch.float32, device="cuda")
+    tokens, targets = i32(tokens_np), i32(targets_np)
+    ws = [to_dev(a, "bf16") for a in s.w_self]
+    wo = [to_dev(a, "bf16") for a in s.w_off]
+    x0 = torch.empty(B, n, w, dtype=torch.bfloat16, device="cuda")
+    outs = [torch.empty_like(x0) for _ in range(L)]
+    dx0 = torch.empty_like(x0)
+    gx = torch.empty(rows, w, dtype=torch.bfloat16, device="cuda")
+    dws = [torch.empty((w, w), dtype=torch.float32, device="cuda") for _ in range(L)]
+    dwo = [torch.empty((w, w), dtype=torch.float32, device="cuda") for _ in range(L)]
+    loss = torch.empty(rows, dtype=torch.float32, device="cuda")
+    dlog = torch.empty(rows, V, dtype=torch.bfloat16, device="cuda")
+    dbias = torch.empty(V, dtype=torch.float32, device="cuda")
+    dtable = torch.empty(V, w, dtype=torch.float32, device="cuda")
+    stack_ws = hcmix.alloc_stack_workspace(B, n, w, L, torch.bfloat16, "cuda")
+    head_ws = torch.empty(hcmix.load().hcmix_head_cross_entropy_workspace_bytes(rows, V),
+                          dtype=torch.uint8, device="cuda")
+    emb_ws = torch.empty(hcmix.load().hcmix_embedding_backward_workspace_bytes(rows, w, V),
+                         dtype=torch.uint8, device="cuda")
+    results = [x0, *outs, loss, dlog, dbias, gx, dx0, *dws, *dwo, dtable]
+
+    def step():
+        hcmix.embedding_forward(table, tokens, out=x0)
+        xs = hcmix.stack_forward(x0, ws, wo, s.layers, True, outs=outs)
+        hcmix.head_cross_entropy(xs[-1].view(rows, w), head_w, head_b, targets, 1.0 / rows,
+                                 loss=loss, dlogits=dlog, dbias=dbias, workspace=head_ws)
+        torch.matmul(dlog, head_w, out=gx)
+        hcmix.stack_backward(xs, ws, wo, s.layers, gx.view(B, n, w), True, dx=dx0, dws=dws,
+                             dwo=dwo, workspace=stack_ws)
+        hcmix.embedding_backward(tokens, dx0, V, dtable=dtable, workspace=emb_ws)
+
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        step()
+        torch.cuda.synchronize()
+        ref = [t.clone() for t in results]
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            step()
+    # the eager step against the oracle's forward: the loss of every row
+    xs_ref = oracle.stack_forward(table_np[tokens_np].reshape(B, n, w), s.w_self, s.w_off,
+                                  s.layers, True)
+    r_loss, _ = lm_head.head_cross_entropy(to_host(ref[L]).reshape(rows, w), head_np,
+                                           np.zeros(V), targets_np, 1.0 / rows)
+    assert np.abs(to_host(ref[L + 1]) - r_loss).max() <= 1e-3
+    rel = (np.linalg.norm(to_host(ref[L]) - xs_ref[-1]) / np.linalg.norm(xs_ref[-1]))
+    assert rel <= 2e-2
+    for rep in range(3):
+        for t in results:
+            t.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, (a, b) in enumerate(zip(results, ref)):
+            assert torch.equal(a, b), f"replay {rep}: output {k} differs from the eager step"
+        print(f"  replay {rep} bitwise equal", flush=True)
