@@ -841,6 +841,15 @@ template <bool TRANS_B>
 hipError_t mix_dispatch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
                         int width, int d, int partner_lower, int partner_upper, hipStream_t st) {
   const int pairs = rows / 2;
+  // Wide layers (1024 and up): 256-column tiles, 96 flop -> 131 flop per byte
+  // moved into the CU, in 32-wide K-steps with three stages (the LDS holds
+  // 3 x 48 KB).  Measured at 32768 x 1024: 126-130 -> 119-124 us per forward
+  // launch.  Weights read transposed keep the 128-column tile.
+  if constexpr (!TRANS_B) {
+    if (width % 256 == 0 && width >= 1024)
+      return mix_launch<MIX_BMP, 256, 2, 4, 32, 3, TRANS_B>(A, B1, B2, out, pairs, width, d,
+                                                            partner_lower, partner_upper, st);
+  }
   // Two waves per SIMD (8 per block, each 64 pairs x 32 columns): one wave's
   // LDS reads and barrier waits hide under the other's MFMAs.  Measured at
   // 16384 x 512: dX 18.1 -> 16.8 us, forward unchanged within noise.

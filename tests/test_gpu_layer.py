@@ -30,6 +30,7 @@ SHAPES = [
     (2, 16, 32, "f32"), (3, 8, 40, "f32"), (1, 2, 8, "f32"), (1, 4096, 32, "f32"),
     (2, 16, 64, "bf16"), (3, 8, 64, "bf16"), (1, 2, 64, "bf16"), (5, 64, 192, "bf16"),
     (4, 256, 128, "bf16"), (1, 4096, 64, "bf16"), (2, 512, 256, "bf16"),
+    (1, 64, 1024, "bf16"), (3, 32, 1280, "bf16"),      # 256-column tiles, ragged row tiles
 ]
 
 

@@ -29,6 +29,8 @@ CASES = [
     (3, 32, 128, [2], True, "bf16", (True, False)),               # one layer: split-K dW there
     (4, 128, 64, list(range(7)), False, "bf16", (False, False)),  # stack backward is fused here
     (2, 16, 32, [0, 1, 2, 3], False, "f32", (True, True)),
+    (1, 512, 1024, [0, 8, 3], True, "bf16", (True, True)),       # 256-column mix tiles
+    (3, 32, 1280, [4, 1], False, "bf16", (True, True)),          # ragged, bidirectional
 ]
 
 
