@@ -109,6 +109,15 @@ def profiled_traffic(workload: str, kernel: str):
     return rec.get("bytes_per_launch", {}).get(kernel)
 
 
+def calibration_copy(torch, dev, mib):
+    """One plain device copy of `mib` MiB: the reference that scales the
+    profiler's FETCH_SIZE and WRITE_SIZE counters to bytes."""
+    src = torch.empty(mib << 20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def fused_path(n, w, L):
     """Shapes the library runs as one LDS-resident kernel per stack direction."""
     return w == 64 and n in (64, 128, 256) and L <= 64
@@ -278,10 +287,7 @@ def main():
                                   workspace, s.layers, B, n, w, L, causal)
 
     if args.calib_copy_mb > 0:
-        src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        calibration_copy(torch, dev, args.calib_copy_mb)
 
     flops, nbytes = algorithmic_work(B, n, w, L, causal)
     pl_per_step = B * n * L
@@ -675,6 +681,8 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
         # the stack's dominant kernels, timed as in the stack-only workload
         kernels = dominant_kernel(args, hcmix, stream, x0, ws, wo, gx_buf, xs_out, [dx0], dws,
                                   dwo, stack_ws, s.layers, B, n, w, L, True)
+    if args.calib_copy_mb > 0:
+        calibration_copy(torch, dev, args.calib_copy_mb)
     names = ["embedding", "stack_forward", "head_and_cross_entropy", "stack_backward",
              "embedding_backward"]
     phase_ms = {nm: round(sum(ev[i].elapsed_time(ev[i + 1]) for ev in per) / len(per), 4)
