@@ -68,14 +68,28 @@ __device__ __forceinline__ bf16x8 att_pack(const f32x16& s, int m) {
   return v;
 }
 
-// Copy rows [0, n) of one head's 64 columns (src: the first row's, row_stride
-// elements apart: 3 * heads * 64 in qkv, heads * 64 in out and dout) into a
-// swizzled LDS tile.
-__device__ __forceinline__ void att_load_tile(const bf16* __restrict__ src, size_t row_stride,
-                                              int n, bf16* tile) {
-  for (int pi = threadIdx.x; pi < n * 8; pi += ATT_THREADS) {
-    const int r = pi >> 3, p = pi & 7;
-    *(u32x4*)(tile + att_off(r, 8 * p)) = *(const u32x4*)(src + (size_t)r * row_stride + 8 * p);
+// Copy rows [0, NT * 32) of one head's 64 columns of two arrays (src: the
+// first row's, row_stride elements apart: 3 * heads * 64 in qkv, heads * 64
+// in out and dout) into two swizzled LDS tiles, every load in flight before
+// the first LDS write (one memory latency for both tiles).
+template <int NT>
+__device__ __forceinline__ void att_load_tiles(const bf16* __restrict__ src_a, size_t stride_a,
+                                               bf16* tile_a, const bf16* __restrict__ src_b,
+                                               size_t stride_b, bf16* tile_b) {
+  constexpr int PER = NT * 32 * 8 / ATT_THREADS;   // 16-byte pieces per thread and tile
+  static_assert(PER * ATT_THREADS == NT * 32 * 8, "");
+  u32x4 va[PER], vb[PER];
+#pragma unroll
+  for (int j = 0; j < PER; j++) {
+    const int pi = threadIdx.x + ATT_THREADS * j, r = pi >> 3, p = pi & 7;
+    va[j] = *(const u32x4*)(src_a + (size_t)r * stride_a + 8 * p);
+    vb[j] = *(const u32x4*)(src_b + (size_t)r * stride_b + 8 * p);
+  }
+#pragma unroll
+  for (int j = 0; j < PER; j++) {
+    const int pi = threadIdx.x + ATT_THREADS * j, r = pi >> 3, p = pi & 7;
+    *(u32x4*)(tile_a + att_off(r, 8 * p)) = va[j];
+    *(u32x4*)(tile_b + att_off(r, 8 * p)) = vb[j];
   }
 }
 
@@ -101,8 +115,7 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attn_fwd_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
   const size_t rs = (size_t)3 * heads * HD;                 // qkv row stride
   const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
-  att_load_tile(base + (size_t)heads * HD, rs, n, sK);
-  att_load_tile(base + (size_t)2 * heads * HD, rs, n, sV);
+  att_load_tiles<NT>(base + (size_t)heads * HD, rs, sK, base + (size_t)2 * heads * HD, rs, sV);
   __syncthreads();
   const float sc = 0.125f * LOG2E;     // scores in log2 units
 #pragma unroll
@@ -215,8 +228,7 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attn_bwd_kv_kernel(
   const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
   const bf16* dobase = dout + (size_t)b * n * os + (size_t)h * HD;
   bf16* gbase = dqkv + (size_t)b * n * rs + (size_t)h * HD;
-  att_load_tile(base, rs, n, sQ);
-  att_load_tile(dobase, os, n, sO);
+  att_load_tiles<NT>(base, rs, sQ, dobase, os, sO);
   att_row_stats(out + (size_t)b * n * os + (size_t)h * HD, dobase, os, lse + (size_t)bh * n, n,
                 sL, sD);
   __syncthreads();
@@ -300,8 +312,7 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attn_bwd_q_kernel(
   const bf16* base = qkv + (size_t)b * n * rs + (size_t)h * HD;
   const bf16* dobase = dout + (size_t)b * n * os + (size_t)h * HD;
   bf16* gbase = dqkv + (size_t)b * n * rs + (size_t)h * HD;
-  att_load_tile(base + os, rs, n, sK);
-  att_load_tile(base + 2 * os, rs, n, sV);
+  att_load_tiles<NT>(base + os, rs, sK, base + 2 * os, rs, sV);
   att_row_stats(out + (size_t)b * n * os + (size_t)h * HD, dobase, os, lse + (size_t)bh * n, n,
                 sL, sD);
   __syncthreads();
