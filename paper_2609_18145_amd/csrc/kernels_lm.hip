@@ -125,14 +125,29 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_partial_kernel(
   }
 }
 
+// Four consecutive entries per thread (elems is a multiple of 4: width % 64 ==
+// 0), eight chunks' loads in flight; each entry still adds the chunks in
+// order.  dtable is only 4-byte aligned, so it is written entry by entry.
 __global__ __launch_bounds__(LM_THREADS) void embed_bwd_reduce_kernel(
     const float* __restrict__ partial, float* __restrict__ dtable, size_t elems, int chunks,
     int accumulate) {
-  const size_t i = (size_t)blockIdx.x * LM_THREADS + threadIdx.x;
-  if (i >= elems) return;
-  float s = 0.f;
-  for (int c = 0; c < chunks; c++) s += partial[(size_t)c * elems + i];
-  dtable[i] = accumulate ? dtable[i] + s : s;
+  const size_t i4 = (size_t)blockIdx.x * LM_THREADS + threadIdx.x;
+  if (i4 * 4 >= elems) return;
+  const f32x4* p = (const f32x4*)partial + i4;
+  const size_t cs = elems / 4;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  int c = 0;
+  for (; c + 8 <= chunks; c += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; u++) v[u] = p[(size_t)(c + u) * cs];
+#pragma unroll
+    for (int u = 0; u < 8; u++) s += v[u];
+  }
+  for (; c < chunks; c++) s += p[(size_t)c * cs];
+  float* d = dtable + i4 * 4;
+#pragma unroll
+  for (int e = 0; e < 4; e++) d[e] = accumulate ? d[e] + s[e] : s[e];
 }
 
 // ---------------------------------------------------------------------------
@@ -373,8 +388,8 @@ hipError_t launch_embedding_bwd(const int* tokens, const bf16* dx, float* dtable
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t elems = (size_t)vocab * width;
-  embed_bwd_reduce_kernel<<<(unsigned)((elems + LM_THREADS - 1) / LM_THREADS), LM_THREADS, 0,
-                            st>>>(workspace, dtable, elems, chunks, accumulate);
+  embed_bwd_reduce_kernel<<<(unsigned)((elems / 4 + LM_THREADS - 1) / LM_THREADS), LM_THREADS,
+                            0, st>>>(workspace, dtable, elems, chunks, accumulate);
   return hipGetLastError();
 }
 
