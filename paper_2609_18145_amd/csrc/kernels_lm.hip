@@ -154,25 +154,26 @@ __global__ __launch_bounds__(LM_THREADS) void embed_bwd_reduce_kernel(
 // Head + cross-entropy.  Block: 64 rows, four waves; wave (g, h) = (wave % 2,
 // wave / 2) computes logits^T for rows 32 g .. 32 g + 31 of the block and the
 // vocabulary tiles of half h (tiles 0 .. TA-1 or TA .. NT-1, TA = ceil(NT/2)).
-// The weights pass through LDS in 64-column slices, three stages filled by LDS
-// DMA two slices ahead, each block starting at its own slice; each wave loads
-// the x fragments of eight slices at a time into registers.  Register e of tile t holds entry 32 t + 8 (e / 4) + 4 (lane / 32)
+// The weights and the block's x rows pass through LDS in 64-column slices,
+// three stages filled by LDS DMA two slices ahead, each block starting at its
+// own slice.  Register e of tile t holds entry 32 t + 8 (e / 4) + 4 (lane / 32)
 // + e % 4 of row lane % 32, so a row's softmax is in-lane, one exchange with
 // lane ^ 32 and one exchange with the other half's wave through LDS.
 // With `dbp` the block also writes the column sums of its rows' dlogits (fp32,
 // rows in order) to dbp[block][V], which head_db_reduce_kernel adds up.
 // ---------------------------------------------------------------------------
 constexpr int HEAD_ROWS = 64;
-constexpr int HEAD_XS = 8;      // slices of x fragments held in registers at once
 
 template <int NT>
 struct HeadCfg {
   static constexpr int V = NT * 32;
   static constexpr int TA = (NT + 1) / 2;         // tiles of the first half
   static constexpr int SLICE = V * 64;            // bf16 elements per weight slice
-  static constexpr int DMA = V / 32;              // 1 KB DMA blocks per wave per slice
+  static constexpr int XSLICE = HEAD_ROWS * 64;   // bf16 elements per x slice
+  static constexpr int STAGE = SLICE + XSLICE;
+  static constexpr int DMA = V / 32 + 2;          // 1 KB DMA blocks per wave per stage
   static constexpr int DB_LD = V + 4;             // fp32 row stride of the dlogits staging
-  static constexpr size_t LDS = (size_t)3 * SLICE * sizeof(bf16);
+  static constexpr size_t LDS = (size_t)3 * STAGE * sizeof(bf16);
   static_assert((size_t)HEAD_ROWS * DB_LD * sizeof(float) <= LDS, "dlogits staging fits");
 };
 
@@ -185,6 +186,7 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
   constexpr int V = C::V, TA = C::TA;
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
   __shared__ float xmax[2][HEAD_ROWS], xsum[2][HEAD_ROWS], xtl[2][HEAD_ROWS];
+  __shared__ __attribute__((aligned(16))) float sbias[V];
   const int lane = threadIdx.x & 63;
   // wave-uniform as far as the compiler knows: every MFMA guard below is a
   // scalar branch
@@ -195,8 +197,12 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
   int r = blockIdx.x * HEAD_ROWS + lrow;
   const bool live = r < rows;
   if (!live) r = rows - 1;                              // load a valid row, store nothing
-  const bf16* xr = x + (size_t)r * width + 8 * half;
   const int slices = width / 64;
+  // the row's target and the bias, fetched before the main loop (the bias
+  // goes to LDS after it)
+  static_assert(V <= LM_THREADS, "one bias entry per thread");
+  const int tgt = targets[r];
+  const float bias_v = threadIdx.x < V ? bias[threadIdx.x] : 0.f;
   // the blocks walk the weight slices from different starting points (the
   // contraction's order is free), so that they do not all stream the same
   // weight lines out of L2 at once
@@ -208,14 +214,24 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
 
   // weight slice sl (clamped: issues past the last slice repeat it into a
   // stage nobody reads again) -> stage
+  // stage = the weight slice [V][64] and the block's x slice [64 rows][64],
+  // both swizzled (16-byte piece p of row m at p ^ ((m / 2) % 8))
+  const int row0 = blockIdx.x * HEAD_ROWS;
   auto dma = [&](int sl, int stage) {
     const int k0 = col0(sl);
-    bf16* dst = smem + stage * C::SLICE;
+    bf16* dst = smem + stage * C::STAGE;
 #pragma unroll
-    for (int j = 0; j < C::DMA; j++) {
+    for (int j = 0; j < V / 32; j++) {
       const int blk = j * 4 + wave, row = blk * 8 + (lane >> 3);
       const int piece = (lane & 7) ^ ((row >> 1) & 7);
       dma16(w + (size_t)row * width + k0 + 8 * piece, dst + blk * 512);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int blk = j * 4 + wave, row = blk * 8 + (lane >> 3);
+      const int piece = (lane & 7) ^ ((row >> 1) & 7);
+      const int xr = min(row0 + row, rows - 1);       // rows past the end: a valid row
+      dma16(x + (size_t)xr * width + k0 + 8 * piece, dst + C::SLICE + blk * 512);
     }
   };
   f32x16 acc[TA];
@@ -223,43 +239,28 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
   for (int t = 0; t < TA; t++) acc[t] = f32x16{};
   dma(0, 0);
   dma(1, 1);
-  // x fragments of HEAD_XS slices at a time, all loaded at the chunk's start
-  // (one memory latency per chunk); the weights two slices ahead by DMA
-  for (int c0 = 0; c0 < slices; c0 += HEAD_XS) {
-    bf16x8 xf[HEAD_XS][4];
+  for (int sl = 0; sl < slices; sl++) {
+    // stage sl landed (only stage sl + 1's DMA may be outstanding), and every
+    // wave is done with stage sl - 1, which the next DMA overwrites
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::DMA) : "memory");
+    dma(sl + 2, (sl + 2) % 3);
+    const bf16* cur = smem + (sl % 3) * C::STAGE;
+    const bf16* xs = cur + C::SLICE;
 #pragma unroll
-    for (int i = 0; i < HEAD_XS; i++) {
-      const int k0 = col0(c0 + i);
+    for (int kk = 0; kk < 4; kk++) {
+      const bf16x8 xf = *(const bf16x8*)(xs + swz<64>(lrow, 2 * kk + half));
 #pragma unroll
-      for (int kk = 0; kk < 4; kk++) xf[i][kk] = *(const bf16x8*)(xr + k0 + 16 * kk);
-    }
-#pragma unroll
-    for (int i = 0; i < HEAD_XS; i++) {
-      const int sl = c0 + i;
-      if (sl >= slices) break;
-      // loads issued after DMA(sl): DMA(sl + 1), plus this chunk's x loads
-      // for the chunk's first two slices (their DMAs came before them)
-      if (i < 2)
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::DMA + 4 * HEAD_XS)
-                     : "memory");
-      else
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::DMA) : "memory");
-      dma(sl + 2, (sl + 2) % 3);
-      const bf16* cur = smem + (sl % 3) * C::SLICE;
-#pragma unroll
-      for (int kk = 0; kk < 4; kk++)
-#pragma unroll
-        for (int t = 0; t < TA; t++)
-          if (t < nt)
-            acc[t] = mfma32(
-                *(const bf16x8*)(cur + swz<64>(32 * (t0 + t) + (lane & 31), 2 * kk + half)),
-                xf[i][kk], acc[t]);
+      for (int t = 0; t < TA; t++)
+        if (t < nt)
+          acc[t] = mfma32(*(const bf16x8*)(cur + swz<64>(32 * (t0 + t) + (lane & 31), 2 * kk + half)),
+                          xf, acc[t]);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (threadIdx.x < V) sbias[threadIdx.x] = bias_v;
+  __syncthreads();
 
   // softmax over the row: in-lane, lane ^ 32, then the other half's wave
-  const int tgt = targets[r];
   float mx = -INFINITY, tl = 0.f;
 #pragma unroll
   for (int t = 0; t < TA; t++) {
@@ -267,7 +268,7 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
 #pragma unroll
     for (int q = 0; q < 4; q++) {
       const int v0 = 32 * (t0 + t) + 8 * q + 4 * half;
-      const f32x4 b4 = *(const f32x4*)(bias + v0);
+      const f32x4 b4 = *(const f32x4*)(sbias + v0);
 #pragma unroll
       for (int j = 0; j < 4; j++) {
         const float l = acc[t][4 * q + j] + b4[j];
@@ -305,8 +306,9 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
   const float inv = 1.f / sum;
   if (live && hv == 0 && half == 0)
     loss[r] = mx + __builtin_amdgcn_logf(sum) * 0.6931471805599453f - tl;
+  // the block's fp32 dlogits go through LDS: written back as bf16 in whole
+  // 16-byte pieces of rows, and summed per column for the bias gradient
   float* dbs = (float*)smem;                            // [HEAD_ROWS][DB_LD] fp32
-  bf16* dr = dlogits + (size_t)r * V;
 #pragma unroll
   for (int t = 0; t < TA; t++) {
     if (t >= nt) continue;
@@ -314,18 +316,23 @@ __global__ __launch_bounds__(LM_THREADS) void head_ce_kernel(
     for (int q = 0; q < 4; q++) {
       const int v0 = 32 * (t0 + t) + 8 * q + 4 * half;
       f32x4 d;
-      bf16x4 o;
 #pragma unroll
-      for (int j = 0; j < 4; j++) {
+      for (int j = 0; j < 4; j++)
         d[j] = live ? scale * (acc[t][4 * q + j] * inv - (v0 + j == tgt ? 1.f : 0.f)) : 0.f;
-        o[j] = to_bf16(d[j]);
-      }
-      if (live) *(bf16x4*)(dr + v0) = o;
-      if (dbp) *(f32x4*)(dbs + lrow * C::DB_LD + v0) = d;
+      *(f32x4*)(dbs + lrow * C::DB_LD + v0) = d;
     }
   }
-  if (!dbp) return;
   __syncthreads();
+  for (int pi = threadIdx.x; pi < HEAD_ROWS * (V / 8); pi += LM_THREADS) {
+    const int lr = pi / (V / 8), c8 = (pi % (V / 8)) * 8;
+    if (row0 + lr >= rows) continue;
+    const f32x4 a = *(const f32x4*)(dbs + lr * C::DB_LD + c8);
+    const f32x4 b = *(const f32x4*)(dbs + lr * C::DB_LD + c8 + 4);
+    const bf16x8 o = {to_bf16(a[0]), to_bf16(a[1]), to_bf16(a[2]), to_bf16(a[3]),
+                      to_bf16(b[0]), to_bf16(b[1]), to_bf16(b[2]), to_bf16(b[3])};
+    *(bf16x8*)(dlogits + (size_t)(row0 + lr) * V + c8) = o;
+  }
+  if (!dbp) return;
   for (int v = threadIdx.x; v < V; v += LM_THREADS) {
     float s = 0.f;
     for (int k = 0; k < HEAD_ROWS; k++) s += dbs[k * C::DB_LD + v];
