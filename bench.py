@@ -819,9 +819,13 @@ def cpu_baseline(s, n, w, L, causal, windows):
         windows = max(1, min(B, int(target / max(per_window, 1e-4))))
         if windows == B:
             passes = max(1, min(200, int(round(target / max(per_window * B, 1e-4)))))
-    dt = sum(run(windows) for _ in range(passes))
+    dt, done = 0.0, 0
+    while done < passes or (dt < 10.0 and done < 200):   # the pilot may overestimate
+        dt += run(windows)
+        done += 1
+    passes = done
     what = (f"{windows} of the workload's {B} windows" if windows < B
-            else f"all {B} windows" + (f", {passes} passes" if passes > 1 else ""))
+            else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
     return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{what}, all {L} layers, forward+backward, {dt:.1f} s"}
@@ -861,9 +865,13 @@ def cpu_baseline_lm(s, table, head_w, n, w, L, V, windows):
         windows = max(1, min(B, int(target / max(per_window, 1e-4))))
         if windows == B:
             passes = max(1, min(200, int(round(target / max(per_window * B, 1e-4)))))
-    dt = sum(run(windows) for _ in range(passes))
+    dt, done = 0.0, 0
+    while done < passes or (dt < 10.0 and done < 200):   # the pilot may overestimate
+        dt += run(windows)
+        done += 1
+    passes = done
     what = (f"{windows} of the workload's {B} windows" if windows < B
-            else f"all {B} windows" + (f", {passes} passes" if passes > 1 else ""))
+            else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
     return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
             "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{what}: embedding, all {L} layers, head and cross-entropy, forward+"
