@@ -14,6 +14,13 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// 16 x 16 x 32: lane l holds row (A) or column (B) l % 16, K elements
+// 8 (l / 16) .. 8 (l / 16) + 7; the result's lane l holds column l % 16, rows
+// 4 (l / 16) .. 4 (l / 16) + 3.
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 // 16 bytes global -> LDS; `lds` is the wave-uniform base, lane i lands at +16*i.
 __device__ __forceinline__ void dma16(const bf16* src, bf16* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);

@@ -26,6 +26,7 @@ def log(msg):
 @pytest.mark.parametrize("batch,n,width,dtype,schedule", [
     (3, 16, 64, "bf16", "rot"), (40, 16, 128, "bf16", "mixa"), (2, 64, 64, "bf16", "rot"),
     (5, 8, 32, "f32", "rot"), (2, 16, 24, "f32", "mixa"), (33, 32, 512, "bf16", "mixa"),
+    (17, 16, 1024, "bf16", "rot"), (3, 16, 192, "bf16", "mixa"),   # two rounds; a partial one
 ])
 def test_decode_every_position_matches_the_stack(batch, n, width, dtype, schedule):
     layers = (list(range(2 * oracle.log2n(n))) if schedule == "rot"
