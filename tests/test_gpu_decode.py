@@ -69,3 +69,26 @@ def test_decode_restarts_at_position_zero():
                         for p in range(n)], axis=1)
         want = oracle.stack_forward(s.x, s1.w_self, s1.w_off, layers, True)[-1]
         assert row_rel_err(got, want) <= TOL["bf16"]
+
+
+def test_decode_lm256_shape_sampled_windows():
+    """The benchmark's decode configuration: 64 windows of 256 positions,
+    width 512, 16 rotated causal layers, every position decoded in turn into
+    one cache; the oracle's full-window forward of three of the windows is
+    their exact reference (windows are independent)."""
+    s = inputs.make_preset("lm256", with_dy=False)
+    B, n = s.x.shape[0], s.x.shape[1]
+    log(f"decode lm256 shape B={B} n={n} w={s.x.shape[2]} L={len(s.layers)}")
+    x = to_dev(s.x, "bf16")
+    ws = [to_dev(w, "bf16") for w in s.w_self]
+    wo = [to_dev(w, "bf16") for w in s.w_off]
+    cache = hcmix.alloc_decode_cache(B, n, x.shape[2], len(s.layers), x.dtype, x.device)
+    cols = [x[:, p].contiguous() for p in range(n)]
+    ys = [hcmix.decode_step(cols[p], ws, wo, s.layers, n, p, cache) for p in range(n)]
+    got = to_host(torch.stack(ys, dim=1))
+    windows = [0, 31, 63]
+    want = oracle.stack_forward(s.x[windows], s.w_self, s.w_off, s.layers, True)[-1]
+    err = row_rel_err(got[windows], want)
+    log(f"  row err {err:.2e}")
+    assert err <= TOL["bf16"]
+    assert np.isfinite(got).all()
