@@ -80,6 +80,9 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--attention", default="native", choices=["native", "sdpa"],
                     help="hybrid workloads: the library's attention core, or PyTorch SDPA")
+    ap.add_argument("--head-grad", default="library", choices=["library", "torch"],
+                    help="lm256_step: the head's input and weight gradients in the library's "
+                         "kernels or as PyTorch GEMMs")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -620,7 +623,9 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
     stack_ws = hcmix.alloc_stack_workspace(B, n, w, L, dt, dev)
     emb_ws = torch.empty(hcmix.load().hcmix_embedding_backward_workspace_bytes(rows, w, V),
                          dtype=torch.uint8, device=dev)
-    grads = {}
+    d_head = torch.empty(V, w, dtype=torch.float32, device=dev)
+    head_bws = torch.empty(hcmix.load().hcmix_head_backward_workspace_bytes(rows, w, V),
+                           dtype=torch.uint8, device=dev)
 
     def step(times=None):
         ev = []
@@ -639,13 +644,18 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
         # logits, loss, dlogits and the bias gradient in the library's kernel
         hcmix.head_cross_entropy(xl, head_w, head_b, targets, 1.0 / rows, loss=loss,
                                  dlogits=dlogits, dbias=d_bias, workspace=head_ws)
-        # weight and input gradients as plain GEMMs; the weight gradient's
-        # K = rows is split into 16 batched products (one GEMM over all rows
-        # leaves the chip idle)
-        kch = 16
-        grads["head_w"] = torch.bmm(xl.view(kch, rows // kch, w).transpose(1, 2),
-                                    dlogits.view(kch, rows // kch, V)).sum(0).t()
-        gx = torch.matmul(dlogits, head_w, out=gx_buf.view(rows, w)).view(B, n, w)
+        if args.head_grad == "library":
+            # the head's input and weight gradients in the library's kernels
+            hcmix.head_backward(xl, head_w, dlogits, gx=gx_buf.view(rows, w), dw=d_head,
+                                workspace=head_bws)
+        else:
+            # the same as PyTorch GEMMs; the weight gradient's K = rows is split
+            # into 16 batched products (one GEMM over all rows leaves the chip idle)
+            kch = 16
+            torch.bmm(xl.view(kch, rows // kch, w).transpose(1, 2),
+                      dlogits.view(kch, rows // kch, V)).sum(0).t()
+            torch.matmul(dlogits, head_w, out=gx_buf.view(rows, w))
+        gx = gx_buf
         mark()
         hcmix.stack_backward(xs, ws, wo, s.layers, gx, True, dx=dx0, dws=dws, dwo=dwo,
                              workspace=stack_ws)

@@ -230,6 +230,23 @@ hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
                                        void* const* grads, void* dx, void* workspace,
                                        size_t workspace_bytes, void* stream);
 
+/* Output head backward: the gradients that the chain rule gives for
+ * logits = W x + bias from dlogits (the products named above):
+ *   gx[r][k] = sum over v of dlogits[r][v] W[v][k]              (bf16, [rows][width]),
+ *   dw[v][k] (+)= sum over rows r of dlogits[r][v] x[r][k]      (fp32, [vocab][width]).
+ * Either output may be NULL (not both).  dw is summed in a fixed order
+ * (row-range partials, then the ranges in order: bitwise-repeatable) through a
+ * workspace of hcmix_head_backward_workspace_bytes (256-byte aligned; unused,
+ * may be NULL, without dw); accumulate != 0 adds to dw instead of overwriting.
+ * vocab a multiple of 32, width a multiple of 64; x, w, dlogits and gx 16-byte
+ * aligned, dw 4-byte aligned.  Errors as for the entry points above. */
+size_t hcmix_head_backward_workspace_bytes(int64_t rows, int64_t width, int32_t vocab);
+
+hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, const void* x,
+                                 const void* w, const void* dlogits, void* gx, float* dw,
+                                 int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
 /* ---- Decode: one new position of every window through the whole stack ----
  *
  * The causal stack evaluated incrementally (the one-position-at-a-time path
@@ -304,8 +321,8 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
  * rows = batch * n positions; table and W are [vocab][width] bf16, x and dx
  * [rows][width] bf16, tokens and targets int32 [rows], bias, loss and dtable
  * fp32, dlogits [rows][vocab] bf16 (the gradients of W and x then are plain
- * products with it: dlogits^T x and dlogits W; the bias gradient, its column
- * sums, comes with it).
+ * products with it, dlogits^T x and dlogits W, which hcmix_head_backward
+ * computes; the bias gradient, its column sums, comes with dlogits).
  * bf16 only; width a multiple of 64; head: vocab a multiple of 32 up to 256.
  * A token outside [0, vocab) embeds as a zero row and is skipped by the
  * backward; a target outside it contributes log sum exp alone.  The embedding

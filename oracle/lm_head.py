@@ -49,3 +49,13 @@ def head_cross_entropy(x, w, bias, targets, scale):
     d = np.exp(logits - lse[:, None])
     d[rows, targets] -= 1.0
     return loss, scale * d
+
+
+def head_backward(x, w, dlogits):
+    """The head's input and weight gradients for logits = W x + bias, given
+    dlogits = d(loss)/d(logits): (dlogits W, dlogits^T x) (the chain rule
+    through the linear map; Section 5's language models end in this head)."""
+    x = np.asarray(x, dtype=np.float64).reshape(-1, np.shape(w)[1])
+    w = np.asarray(w, dtype=np.float64)
+    d = np.asarray(dlogits, dtype=np.float64).reshape(x.shape[0], -1)
+    return d @ w, d.T @ x

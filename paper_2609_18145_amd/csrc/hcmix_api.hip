@@ -823,6 +823,38 @@ hcmix_status hcmix_head_cross_entropy(int64_t rows, int64_t width, int32_t vocab
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
+size_t hcmix_head_backward_workspace_bytes(int64_t rows, int64_t width, int32_t vocab) {
+  if (check_lm(rows, width, vocab) != HCMIX_OK || vocab % 32) return 0;
+  return align256(head_backward_workspace_bytes((int)rows, (int)width, vocab));
+}
+
+hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, const void* x,
+                                 const void* w, const void* dlogits, void* gx, float* dw,
+                                 int32_t accumulate, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  if (!x || !w || !dlogits || (!gx && !dw)) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_lm(rows, width, vocab);
+  if (st != HCMIX_OK) return st;
+  if (vocab % 32 != 0) return HCMIX_ERR_UNSUPPORTED;
+  const size_t need = dw ? head_backward_workspace_bytes((int)rows, (int)width, vocab) : 0;
+  if (dw && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
+  const Span ins[3] = {{x, (size_t)rows * width * sizeof(bf16)},
+                       {w, (size_t)vocab * width * sizeof(bf16)},
+                       {dlogits, (size_t)rows * vocab * sizeof(bf16)}};
+  const Span outs[3] = {{gx, gx ? (size_t)rows * width * sizeof(bf16) : 0},
+                        {dw, dw ? (size_t)vocab * width * sizeof(float) : 0},
+                        {workspace, need}};
+  st = check_spans(ins, 3, outs, 3, 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(dlogits, 16) || (gx && !aligned(gx, 16)))
+    return HCMIX_ERR_UNSUPPORTED;
+  if (dw && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = launch_head_backward((const bf16*)x, (const bf16*)w, (const bf16*)dlogits,
+                                      (bf16*)gx, dw, accumulate != 0, (float*)workspace,
+                                      (int)rows, (int)width, vocab, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                 int32_t dtype) {
   if (num_layers < 1 || num_layers > kMaxLayers) return 0;

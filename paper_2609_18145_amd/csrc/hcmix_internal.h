@@ -164,6 +164,13 @@ size_t head_workspace_bytes(int rows, int vocab);
 hipError_t launch_head_ce(const bf16* x, const bf16* w, const float* bias, const int* targets,
                           float scale, float* loss, bf16* dlogits, float* dbias, float* workspace,
                           int rows, int width, int vocab, hipStream_t st);
+// Head backward: gx = dl W (bf16, optional) and dW (+)= dl^T x (fp32, optional)
+// through head_backward_workspace_bytes of row-range partials summed in order;
+// vocab a multiple of 32.
+size_t head_backward_workspace_bytes(int rows, int width, int vocab);
+hipError_t launch_head_backward(const bf16* x, const bf16* w, const bf16* dl, bf16* gx, float* dw,
+                                int accumulate, float* workspace, int rows, int width, int vocab,
+                                hipStream_t st);
 
 struct DecodeLayerArgs {
   const bf16* x_in;

@@ -371,6 +371,215 @@ hipError_t head_launch(const bf16* x, const bf16* w, const float* bias, const in
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Head backward: the output head's weight and input gradients from dlogits,
+// the two products the chain rule gives for logits = W x + bias:
+//   dW[v][k] = sum over rows r of dl[r][v] x[r][k]   (fp32)
+//   gx[r][k] = sum over v of dl[r][v] W[v][k]        (bf16)
+// Both kernels: 128 x 128 output tiles, four waves of 64 x 64 (2 x 2 MFMA
+// tiles of 32 x 32), 64-wide contraction steps staged in two LDS buffers; each
+// thread loads the next step's pieces into registers before the MFMAs of the
+// current one.  Pieces outside the rows, the vocabulary or the width are zero.
+// ---------------------------------------------------------------------------
+constexpr int HB_TILE = 128;
+constexpr int HB_KS = 64;
+constexpr int HB_TARGET_BLOCKS = 256;
+
+// Rows per split of the weight gradient (a multiple of HB_KS) and the number
+// of splits, so that about HB_TARGET_BLOCKS blocks work.
+void head_dw_split(int rows, int width, int vocab, int* range, int* splits) {
+  const int tiles = ((vocab + HB_TILE - 1) / HB_TILE) * ((width + HB_TILE - 1) / HB_TILE);
+  int s = (HB_TARGET_BLOCKS + tiles - 1) / tiles;
+  const int steps = (rows + HB_KS - 1) / HB_KS;
+  if (s > steps) s = steps;
+  if (s < 1) s = 1;
+  const int per = (steps + s - 1) / s;                 // steps per split
+  *range = per * HB_KS;
+  *splits = (rows + *range - 1) / *range;
+}
+
+// LDS element offset of column `col` (a multiple of 8) of row `row` in a
+// [rows][128] tile read with tr_frag<256>.
+__device__ __forceinline__ int hb_tr_off(int row, int col) {
+  return row * HB_TILE + trswz<256>(row, col >> 5) * 32 + (col & 31);
+}
+
+// Weight-gradient partials: block (vocabulary tile, width tile, split s) sums
+// rows [s * range, (s + 1) * range) into part[s][v][k].  Both operands are
+// row-major over the contraction (the rows), staged as [64 rows][128 columns]
+// tiles and read transposed.
+__global__ __launch_bounds__(256) void head_dw_kernel(const bf16* __restrict__ dl,
+                                                      const bf16* __restrict__ x,
+                                                      float* __restrict__ part, int rows,
+                                                      int width, int vocab, int range) {
+  __shared__ __attribute__((aligned(16))) bf16 ta[2][HB_KS * HB_TILE];
+  __shared__ __attribute__((aligned(16))) bf16 tb[2][HB_KS * HB_TILE];
+  const int tk_n = (width + HB_TILE - 1) / HB_TILE, tv_n = (vocab + HB_TILE - 1) / HB_TILE;
+  int b = blockIdx.x;
+  const int tk = b % tk_n;
+  b /= tk_n;
+  const int tv = b % tv_n, sp = b / tv_n;
+  const int v0 = tv * HB_TILE, k0 = tk * HB_TILE;
+  const int r0 = sp * range, r1 = min(rows, r0 + range);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int nsteps = r1 > r0 ? (r1 - r0 + HB_KS - 1) / HB_KS : 0;
+  u32x4 ga[4], gb[4];
+  auto load = [&](int t) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int p = tid + 256 * j, row = p >> 4, col = 8 * (p & 15);
+      const int r = r0 + t * HB_KS + row;
+      const bool rok = r < r1;
+      ga[j] = rok && v0 + col < vocab ? *(const u32x4*)(dl + (size_t)r * vocab + v0 + col)
+                                      : u32x4{0u, 0u, 0u, 0u};
+      gb[j] = rok && k0 + col < width ? *(const u32x4*)(x + (size_t)r * width + k0 + col)
+                                      : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int p = tid + 256 * j, row = p >> 4, col = 8 * (p & 15);
+      *(u32x4*)(ta[buf] + hb_tr_off(row, col)) = ga[j];
+      *(u32x4*)(tb[buf] + hb_tr_off(row, col)) = gb[j];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
+  if (nsteps > 0) {
+    load(0);
+    stash(0);
+  }
+  __syncthreads();
+  for (int t = 0; t < nsteps; t++) {
+    const int buf = t & 1;
+    if (t + 1 < nsteps) load(t + 1);
+#pragma unroll
+    for (int kk = 0; kk < HB_KS; kk += 16) {
+      bf16x8 a[2], bb[2];
+#pragma unroll
+      for (int i = 0; i < 2; i++) a[i] = tr_frag<256>(ta[buf], kk, 64 * wm + 32 * i, lane);
+#pragma unroll
+      for (int j = 0; j < 2; j++) bb[j] = tr_frag<256>(tb[buf], kk, 64 * wn + 32 * j, lane);
+#pragma unroll
+      for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) acc[i][j] = mfma32(a[i], bb[j], acc[i][j]);
+    }
+    if (t + 1 < nsteps) stash(buf ^ 1);
+    __syncthreads();
+  }
+  // C[m = v][n = k]: lane l holds column k = .. + l % 32 and rows
+  // v = .. + 8 (e / 4) + 4 (l / 32) + e % 4
+  float* out = part + (size_t)sp * vocab * width;
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int k = k0 + 64 * wn + 32 * j + (lane & 31);
+      if (k >= width) continue;
+#pragma unroll
+      for (int e = 0; e < 16; e++) {
+        const int v = v0 + 64 * wm + 32 * i + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (v < vocab) out[(size_t)v * width + k] = acc[i][j][e];
+      }
+    }
+}
+
+// Input gradient: block (row tile, width tile) computes the transposed tile
+// gx^T = W^T dl^T, so that a lane owns one row and four runs of four columns.
+// W is row-major over the contraction (the vocabulary): [64 v][128 k] tiles
+// read transposed; dl rows are contraction-contiguous: [128 r][64 v] tiles.
+__global__ __launch_bounds__(256) void head_gx_kernel(const bf16* __restrict__ dl,
+                                                      const bf16* __restrict__ w,
+                                                      bf16* __restrict__ gx, int rows, int width,
+                                                      int vocab) {
+  __shared__ __attribute__((aligned(16))) bf16 tw[2][HB_KS * HB_TILE];
+  __shared__ __attribute__((aligned(16))) bf16 td[2][HB_TILE * HB_KS];
+  const int tk_n = (width + HB_TILE - 1) / HB_TILE;
+  const int tk = blockIdx.x % tk_n, tr = blockIdx.x / tk_n;
+  const int k0 = tk * HB_TILE, rb = tr * HB_TILE;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;      // columns 64 wm.., rows 64 wn..
+  const int nsteps = (vocab + HB_KS - 1) / HB_KS;
+  u32x4 gw[4], gd[4];
+  auto load = [&](int t) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int p = tid + 256 * j;
+      const int v = t * HB_KS + (p >> 4), col = 8 * (p & 15);
+      gw[j] = v < vocab && k0 + col < width ? *(const u32x4*)(w + (size_t)v * width + k0 + col)
+                                            : u32x4{0u, 0u, 0u, 0u};
+      const int r = rb + (p >> 3), vc = t * HB_KS + 8 * (p & 7);
+      gd[j] = r < rows && vc < vocab ? *(const u32x4*)(dl + (size_t)r * vocab + vc)
+                                     : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int p = tid + 256 * j;
+      *(u32x4*)(tw[buf] + hb_tr_off(p >> 4, 8 * (p & 15))) = gw[j];
+      *(u32x4*)(td[buf] + swz<64>(p >> 3, p & 7)) = gd[j];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
+  load(0);
+  stash(0);
+  __syncthreads();
+  for (int t = 0; t < nsteps; t++) {
+    const int buf = t & 1;
+    if (t + 1 < nsteps) load(t + 1);
+#pragma unroll
+    for (int kk = 0; kk < HB_KS; kk += 16) {
+      bf16x8 a[2], bb[2];
+#pragma unroll
+      for (int i = 0; i < 2; i++) a[i] = tr_frag<256>(tw[buf], kk, 64 * wm + 32 * i, lane);
+#pragma unroll
+      for (int j = 0; j < 2; j++)
+        bb[j] = *(const bf16x8*)(td[buf] + swz<64>(64 * wn + 32 * j + (lane & 31),
+                                                   (kk >> 3) + (lane >> 5)));
+#pragma unroll
+      for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) acc[i][j] = mfma32(a[i], bb[j], acc[i][j]);
+    }
+    if (t + 1 < nsteps) stash(buf ^ 1);
+    __syncthreads();
+  }
+  // C[m = k][n = r]: lane l holds row r = .. + l % 32 and columns
+  // k = .. + 8 g + 4 (l / 32) + 0..3 for g = 0..3
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int r = rb + 64 * wn + 32 * j + (lane & 31);
+      if (r >= rows) continue;
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        const int k = k0 + 64 * wm + 32 * i + 8 * g + 4 * (lane >> 5);
+        if (k >= width) continue;
+        const bf16x4 v = {to_bf16(acc[i][j][4 * g]), to_bf16(acc[i][j][4 * g + 1]),
+                          to_bf16(acc[i][j][4 * g + 2]), to_bf16(acc[i][j][4 * g + 3])};
+        *(bf16x4*)(gx + (size_t)r * width + k) = v;
+      }
+    }
+}
+
 }  // namespace
 
 size_t embedding_workspace_bytes(int rows, int width, int vocab) {
@@ -402,6 +611,35 @@ hipError_t launch_embedding_bwd(const int* tokens, const bf16* dx, float* dtable
 
 size_t head_workspace_bytes(int rows, int vocab) {
   return (size_t)((rows + HEAD_ROWS - 1) / HEAD_ROWS) * vocab * sizeof(float);
+}
+
+size_t head_backward_workspace_bytes(int rows, int width, int vocab) {
+  int range, splits;
+  head_dw_split(rows, width, vocab, &range, &splits);
+  return (size_t)splits * vocab * width * sizeof(float);
+}
+
+hipError_t launch_head_backward(const bf16* x, const bf16* w, const bf16* dl, bf16* gx, float* dw,
+                                int accumulate, float* workspace, int rows, int width, int vocab,
+                                hipStream_t st) {
+  const int tk_n = (width + HB_TILE - 1) / HB_TILE;
+  if (gx) {
+    const int tr_n = (rows + HB_TILE - 1) / HB_TILE;
+    head_gx_kernel<<<tr_n * tk_n, 256, 0, st>>>(dl, w, gx, rows, width, vocab);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (!dw) return hipSuccess;
+  int range, splits;
+  head_dw_split(rows, width, vocab, &range, &splits);
+  const int tv_n = (vocab + HB_TILE - 1) / HB_TILE;
+  head_dw_kernel<<<tk_n * tv_n * splits, 256, 0, st>>>(dl, x, workspace, rows, width, vocab, range);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t elems = (size_t)vocab * width;
+  embed_bwd_reduce_kernel<<<(unsigned)((elems / 4 + LM_THREADS - 1) / LM_THREADS), LM_THREADS,
+                            0, st>>>(workspace, dw, elems, splits, accumulate);
+  return hipGetLastError();
 }
 
 hipError_t launch_head_ce(const bf16* x, const bf16* w, const float* bias, const int* targets,

@@ -33,7 +33,8 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_decode_cache_bytes", "hcmix_decode_step", "hcmix_attention_forward",
            "hcmix_attention_backward", "hcmix_embedding_forward",
            "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
-           "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy")
+           "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy",
+           "hcmix_head_backward_workspace_bytes", "hcmix_head_backward")
 
 _lib = None
 
@@ -102,6 +103,10 @@ def load():
         lib.hcmix_head_cross_entropy.argtypes = [i64, i64, i32, vp, vp, fp, vp, ctypes.c_float,
                                                  fp, vp, fp, vp, sz, vp]
         lib.hcmix_head_cross_entropy.restype = i32
+        lib.hcmix_head_backward_workspace_bytes.argtypes = [i64, i64, i32]
+        lib.hcmix_head_backward_workspace_bytes.restype = sz
+        lib.hcmix_head_backward.argtypes = [i64, i64, i32, vp, vp, vp, vp, fp, i32, vp, sz, vp]
+        lib.hcmix_head_backward.restype = i32
         lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
@@ -400,6 +405,34 @@ def head_cross_entropy(x, w, bias, targets, scale, loss=None, dlogits=None, dbia
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_cross_entropy")
     return (loss, dlogits, dbias) if want_db else (loss, dlogits)
+
+
+def head_backward(x, w, dlogits, gx=None, dw=None, with_gx=True, with_dw=True,
+                  accumulate=False, workspace=None):
+    """The head's input gradient dlogits W (bf16 [rows, width]) and weight
+    gradient dlogits^T x (fp32 [vocab, width], added to dw with accumulate):
+    returns (gx, dw), None for one not asked for."""
+    vocab, width = w.shape
+    rows = dlogits.shape[0]
+    want_gx = with_gx or gx is not None
+    want_dw = with_dw or dw is not None
+    if want_gx and gx is None:
+        gx = torch.empty((rows, width), dtype=x.dtype, device=x.device)
+    ws_bytes = 0
+    if want_dw:
+        if dw is None:
+            dw = torch.empty((vocab, width), dtype=torch.float32, device=x.device)
+        if workspace is None:
+            workspace = torch.empty(load().hcmix_head_backward_workspace_bytes(rows, width, vocab),
+                                    dtype=torch.uint8, device=x.device)
+        ws_bytes = workspace.numel()
+    rc = load().hcmix_head_backward(rows, width, vocab, _ptr(x), _ptr(w), _ptr(dlogits),
+                                    _ptr(gx) if want_gx else None,
+                                    _fptr(dw) if want_dw else None, int(bool(accumulate)),
+                                    _ptr(workspace) if want_dw else None, ws_bytes, _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_head_backward")
+    return (gx if want_gx else None), (dw if want_dw else None)
 
 
 class Attention(torch.autograd.Function):

@@ -273,6 +273,31 @@ def test_lm_entry_points_reject_bad_arguments():
               None) == UNSUPPORTED                                    # workspace alignment
 
 
+
+def test_head_backward_rejects_before_launch():
+    lib = hcmix.load()
+    fp = lambda p: ctypes.cast(p, ctypes.POINTER(ctypes.c_float))  # noqa: E731
+    q = lib.hcmix_head_backward_workspace_bytes
+    assert q(16384, 512, 256) == 32 * 256 * 512 * 4     # 32 row ranges of 512 rows
+    assert q(100, 64, 32) == 2 * 32 * 64 * 4            # 2 ranges of 64 rows
+    assert q(100, 64, 48) == 0 and q(0, 64, 32) == 0 and q(100, 96, 32) == 0
+    hb = lib.hcmix_head_backward
+    need = q(100, 64, 256)
+    ok = [P[0], P[1], P[2], P[3], fp(P[4]), 0, P[5], need, None]
+    assert hb(0, 64, 256, *ok) == INVALID
+    assert hb(100, 64, 256, None, *ok[1:]) == INVALID                         # no x
+    assert hb(100, 64, 256, P[0], P[1], P[2], None, None, 0, P[5], need, None) == INVALID
+    assert hb(100, 64, 48, *ok) == UNSUPPORTED                                # vocab % 32
+    assert hb(100, 96, 256, *ok) == UNSUPPORTED                               # width % 64
+    assert hb(100, 64, 256, P[0], P[1], P[2], P[3], fp(P[4]), 0, None, need, None) == INVALID
+    assert hb(100, 64, 256, P[0], P[1], P[2], P[3], fp(P[4]), 0, P[5], need - 1, None) == INVALID
+    assert hb(100, 64, 256, P[0], P[1], P[2], P[0], fp(P[4]), 0, P[5], need, None) == INVALID
+    assert hb(100, 64, 256, P[0], P[1], P[2], P[3], fp(P[2]), 0, P[5], need, None) == INVALID
+    assert hb(100, 64, 256, P[0], P[1], P[2], ctypes.c_void_p(P[3].value + 8), fp(P[4]), 0,
+              P[5], need, None) == UNSUPPORTED                                # gx alignment
+    assert hb(100, 64, 256, P[0], P[1], P[2], P[3], fp(P[4]), 0,
+              ctypes.c_void_p(P[5].value + 16), need, None) == UNSUPPORTED    # workspace
+
 def test_stack_workspace_query():
     lib = hcmix.load()
     fused = lib.hcmix_stack_backward_workspace_bytes(64, 256, 64, 8, hcmix.HCMIX_BF16)

@@ -7,7 +7,7 @@ import torch
 
 from oracle import lm_head
 from paper_2609_18145_amd import hcmix, inputs
-from tests.util import to_dev, to_host
+from tests.util import TOL, fro_rel_err, row_rel_err, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +40,8 @@ def test_embedding_forward_is_an_exact_gather(rows, width, vocab):
 
 
 @pytest.mark.parametrize("rows,width,vocab,zipf", [(300, 64, 16, False), (16384, 512, 256, True),
-                                                    (40000, 128, 37, False)])
+                                                    (40000, 128, 37, False), (3000, 1024, 6, False),
+                                                    (70000, 64, 256, True)])
 def test_embedding_backward_matches_oracle_and_repeats(rows, width, vocab, zipf):
     print(f"case: embedding backward rows={rows} width={width} vocab={vocab}", flush=True)
     rng = np.random.default_rng(rows + 1)
@@ -193,3 +194,36 @@ def test_whole_lm_step_replays_in_a_graph():
         for k, (a, b) in enumerate(zip(results, ref)):
             assert torch.equal(a, b), f"replay {rep}: output {k} differs from the eager step"
         print(f"  replay {rep} bitwise equal", flush=True)
+
+
+@pytest.mark.parametrize("rows,width,vocab", [(16384, 512, 256), (1000, 192, 96), (200, 64, 32),
+                                              (130, 1024, 288), (77, 128, 64)])
+def test_head_backward_matches_oracle_and_repeats(rows, width, vocab):
+    """gx = dlogits W and dW = dlogits^T x against the oracle on the same bf16
+    operands (one full LM shape, ragged rows, vocabulary and width tiles that
+    do not fill 128); dW bitwise-repeatable and accumulating; each output alone
+    equals the pair's."""
+    print(f"case: head backward rows={rows} width={width} vocab={vocab}", flush=True)
+    rng = np.random.default_rng(rows + vocab)
+    x = inputs.round_bf16(rng.standard_normal((rows, width)).astype(np.float32))
+    w = inputs.round_bf16((rng.standard_normal((vocab, width)) / np.sqrt(width)).astype(np.float32))
+    d = inputs.round_bf16((rng.standard_normal((rows, vocab)) / rows).astype(np.float32))
+    xg, wg, dg = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(d, "bf16")
+    gx, dw = hcmix.head_backward(xg, wg, dg)
+    gx2, dw2 = hcmix.head_backward(xg, wg, dg)
+    torch.cuda.synchronize()
+    want_gx, want_dw = lm_head.head_backward(x, w, d)
+    e_gx = row_rel_err(to_host(gx), want_gx)
+    e_dw = fro_rel_err(to_host(dw), want_dw)
+    print(f"  gx row err {e_gx:.2e}, dW err {e_dw:.2e}", flush=True)
+    assert e_gx <= TOL["bf16"]
+    assert e_dw <= 1e-4
+    assert torch.equal(gx, gx2) and torch.equal(dw, dw2)
+    only_gx, none_dw = hcmix.head_backward(xg, wg, dg, with_dw=False)
+    none_gx, only_dw = hcmix.head_backward(xg, wg, dg, with_gx=False)
+    base = dw.clone()
+    hcmix.head_backward(xg, wg, dg, dw=dw, with_gx=False, accumulate=True)
+    torch.cuda.synchronize()
+    assert none_dw is None and none_gx is None
+    assert torch.equal(only_gx, gx) and torch.equal(only_dw, base)
+    assert torch.equal(dw, base + base)

@@ -65,3 +65,33 @@ def test_against_torch_autograd():
     dx = d @ w
     assert np.allclose(lm_head.embedding_backward(tokens, dx, V), tt.grad.numpy(), rtol=1e-12,
                        atol=1e-14)
+
+
+def test_head_backward_is_the_loss_gradient():
+    """The head's input and weight gradients equal central differences of the
+    mean cross-entropy (the loss itself, not the products), on a tiny head."""
+    rng = np.random.default_rng(9)
+    rows, width, vocab = 5, 6, 4
+    x = rng.standard_normal((rows, width))
+    w = rng.standard_normal((vocab, width)) * 0.5
+    bias = rng.standard_normal(vocab) * 0.1
+    targets = rng.integers(0, vocab, rows)
+    scale = 1.0 / rows
+
+    def mean_loss(xx, ww):
+        return scale * lm_head.head_cross_entropy(xx, ww, bias, targets, scale)[0].sum()
+
+    _, dlog = lm_head.head_cross_entropy(x, w, bias, targets, scale)
+    gx, dw = lm_head.head_backward(x, w, dlog)
+    h = 1e-6
+    for arr, grad in ((x, gx), (w, dw)):
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + h
+            up = mean_loss(x, w)
+            arr[idx] = old - h
+            down = mean_loss(x, w)
+            arr[idx] = old
+            num[idx] = (up - down) / (2 * h)
+        assert np.abs(num - grad).max() <= 1e-8 * max(1.0, np.abs(num).max())
