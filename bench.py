@@ -10,8 +10,8 @@ gather, the stack forward, the head with its loss and dlogits, the head's
 gradients, the stack backward and the embedding's scatter sum over one batch
 of synthetic inputs already resident in HBM, replayed as a HIP graph.
 `--workload lm256` times the stack alone (one hcmix_stack_forward and one
-hcmix_stack_backward call); the other workloads are the other shapes of the
-survey (reach, long4096, hybrids, decode).
+hcmix_stack_backward call); the other workloads are the method's other
+shapes (reach, long4096, hybrids, decode).
 Prints one JSON line: positions*layers per second, the roofline of the
 dominant kernel (timed live with HIP events on the stream it runs on) and the
 CPU oracle timed on a bounded sample of the same workload.
