@@ -80,6 +80,9 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--attention", default="native", choices=["native", "sdpa"],
                     help="hybrid workloads: the library's attention core, or PyTorch SDPA")
+    ap.add_argument("--proj", default="torch", choices=["library", "torch"],
+                    help="hybrids: the attention layers' projections in the library's kernels "
+                         "or as PyTorch GEMMs")
     ap.add_argument("--head-grad", default="library", choices=["library", "torch"],
                     help="lm256_step: the head's input and weight gradients in the library's "
                          "kernels or as PyTorch GEMMs")
@@ -409,19 +412,28 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             return F.scaled_dot_product_attention(q, k, v, is_causal=True)
 
     class Linear(torch.autograd.Function):
-        """y = x W^T with the weight gradient's K = rows split into 16 batched
-        products (a single GEMM with K = 16384 and a 512-wide output leaves
-        most of the chip idle in the library's kernel choice)."""
+        """y = x W^T.  --proj library: the library's two products of a linear
+        map's backward (hcmix_head_backward: dx = g W, dW = g^T x in a fixed
+        order), and the forward as the first of them on W^T (transposed once
+        per call).  --proj torch: PyTorch GEMMs, the weight gradient's K = rows
+        split into 16 batched products (a single GEMM with K = 16384 and a
+        512-wide output leaves most of the chip idle in its kernel choice)."""
 
         @staticmethod
         def forward(ctx, x2, wt):
             ctx.save_for_backward(x2, wt)
+            if args.proj == "library":
+                y, _ = hcmix.head_backward(None, wt.t().contiguous(), x2, with_dw=False)
+                return y
             return torch.matmul(x2, wt.t())
 
         @staticmethod
         def backward(ctx, g):
             x2, wt = ctx.saved_tensors
             g = g.contiguous()
+            if args.proj == "library":
+                dx, dw = hcmix.head_backward(x2, wt, g)
+                return dx, dw.to(wt.dtype)
             kch = 16
             r = x2.shape[0] // kch
             dw = torch.bmm(g.view(kch, r, -1).transpose(1, 2), x2.view(kch, r, -1)).sum(0)

@@ -234,7 +234,9 @@ hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
  * logits = W x + bias from dlogits (the products named above):
  *   gx[r][k] = sum over v of dlogits[r][v] W[v][k]              (bf16, [rows][width]),
  *   dw[v][k] (+)= sum over rows r of dlogits[r][v] x[r][k]      (fp32, [vocab][width]).
- * Either output may be NULL (not both).  dw is summed in a fixed order
+ * Either output may be NULL (not both); x is read only for dw and may be NULL
+ * without it (gx alone is then a plain product of two bf16 matrices, which
+ * also serves a linear map's forward on the transposed weights).  dw is summed in a fixed order
  * (row-range partials, then the ranges in order: bitwise-repeatable) through a
  * workspace of hcmix_head_backward_workspace_bytes (256-byte aligned; unused,
  * may be NULL, without dw); accumulate != 0 adds to dw instead of overwriting.

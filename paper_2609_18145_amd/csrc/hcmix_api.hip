@@ -832,21 +832,23 @@ hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, con
                                  const void* w, const void* dlogits, void* gx, float* dw,
                                  int32_t accumulate, void* workspace, size_t workspace_bytes,
                                  void* stream) {
-  if (!x || !w || !dlogits || (!gx && !dw)) return HCMIX_ERR_INVALID_VALUE;
+  // x is read only for dw
+  if (!w || !dlogits || (!gx && !dw) || (dw && !x)) return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_lm(rows, width, vocab);
   if (st != HCMIX_OK) return st;
   if (vocab % 32 != 0) return HCMIX_ERR_UNSUPPORTED;
   const size_t need = dw ? head_backward_workspace_bytes((int)rows, (int)width, vocab) : 0;
   if (dw && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
-  const Span ins[3] = {{x, (size_t)rows * width * sizeof(bf16)},
-                       {w, (size_t)vocab * width * sizeof(bf16)},
-                       {dlogits, (size_t)rows * vocab * sizeof(bf16)}};
+  const Span ins[3] = {{w, (size_t)vocab * width * sizeof(bf16)},
+                       {dlogits, (size_t)rows * vocab * sizeof(bf16)},
+                       {dw ? x : w, dw ? (size_t)rows * width * sizeof(bf16) : 0}};
   const Span outs[3] = {{gx, gx ? (size_t)rows * width * sizeof(bf16) : 0},
                         {dw, dw ? (size_t)vocab * width * sizeof(float) : 0},
                         {workspace, need}};
   st = check_spans(ins, 3, outs, 3, 4);
   if (st != HCMIX_OK) return st;
-  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(dlogits, 16) || (gx && !aligned(gx, 16)))
+  if ((dw && !aligned(x, 16)) || !aligned(w, 16) || !aligned(dlogits, 16) ||
+      (gx && !aligned(gx, 16)))
     return HCMIX_ERR_UNSUPPORTED;
   if (dw && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
   hipError_t e = launch_head_backward((const bf16*)x, (const bf16*)w, (const bf16*)dlogits,

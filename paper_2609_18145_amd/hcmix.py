@@ -411,25 +411,28 @@ def head_backward(x, w, dlogits, gx=None, dw=None, with_gx=True, with_dw=True,
                   accumulate=False, workspace=None):
     """The head's input gradient dlogits W (bf16 [rows, width]) and weight
     gradient dlogits^T x (fp32 [vocab, width], added to dw with accumulate):
-    returns (gx, dw), None for one not asked for."""
+    returns (gx, dw), None for one not asked for.  x is only read for dw (it
+    may be None without it)."""
     vocab, width = w.shape
     rows = dlogits.shape[0]
     want_gx = with_gx or gx is not None
     want_dw = with_dw or dw is not None
+    dev = dlogits.device
     if want_gx and gx is None:
-        gx = torch.empty((rows, width), dtype=x.dtype, device=x.device)
+        gx = torch.empty((rows, width), dtype=dlogits.dtype, device=dev)
     ws_bytes = 0
     if want_dw:
         if dw is None:
-            dw = torch.empty((vocab, width), dtype=torch.float32, device=x.device)
+            dw = torch.empty((vocab, width), dtype=torch.float32, device=dev)
         if workspace is None:
             workspace = torch.empty(load().hcmix_head_backward_workspace_bytes(rows, width, vocab),
-                                    dtype=torch.uint8, device=x.device)
+                                    dtype=torch.uint8, device=dev)
         ws_bytes = workspace.numel()
-    rc = load().hcmix_head_backward(rows, width, vocab, _ptr(x), _ptr(w), _ptr(dlogits),
-                                    _ptr(gx) if want_gx else None,
+    rc = load().hcmix_head_backward(rows, width, vocab, _ptr(x) if want_dw else None, _ptr(w),
+                                    _ptr(dlogits), _ptr(gx) if want_gx else None,
                                     _fptr(dw) if want_dw else None, int(bool(accumulate)),
-                                    _ptr(workspace) if want_dw else None, ws_bytes, _stream(x))
+                                    _ptr(workspace) if want_dw else None, ws_bytes,
+                                    _stream(dlogits))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_backward")
     return (gx if want_gx else None), (dw if want_dw else None)

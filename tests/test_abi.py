@@ -285,7 +285,8 @@ def test_head_backward_rejects_before_launch():
     need = q(100, 64, 256)
     ok = [P[0], P[1], P[2], P[3], fp(P[4]), 0, P[5], need, None]
     assert hb(0, 64, 256, *ok) == INVALID
-    assert hb(100, 64, 256, None, *ok[1:]) == INVALID                         # no x
+    assert hb(100, 64, 256, None, *ok[1:]) == INVALID                         # no x for dw
+    assert hb(100, 64, 256, P[0], None, *ok[2:]) == INVALID                   # no w
     assert hb(100, 64, 256, P[0], P[1], P[2], None, None, 0, P[5], need, None) == INVALID
     assert hb(100, 64, 48, *ok) == UNSUPPORTED                                # vocab % 32
     assert hb(100, 96, 256, *ok) == UNSUPPORTED                               # width % 64

@@ -219,7 +219,7 @@ def test_head_backward_matches_oracle_and_repeats(rows, width, vocab):
     assert e_gx <= TOL["bf16"]
     assert e_dw <= 1e-4
     assert torch.equal(gx, gx2) and torch.equal(dw, dw2)
-    only_gx, none_dw = hcmix.head_backward(xg, wg, dg, with_dw=False)
+    only_gx, none_dw = hcmix.head_backward(None, wg, dg, with_dw=False)   # x unused
     none_gx, only_dw = hcmix.head_backward(xg, wg, dg, with_gx=False)
     base = dw.clone()
     hcmix.head_backward(xg, wg, dg, dw=dw, with_gx=False, accumulate=True)
