@@ -49,6 +49,7 @@ def _load():
         lib.oracle_receives.argtypes, lib.oracle_receives.restype = [i64, i32, i64, i32], i32
         lib.oracle_valid_layer.argtypes, lib.oracle_valid_layer.restype = [i32, i64, i32], i32
         lib.oracle_num_threads.argtypes, lib.oracle_num_threads.restype = [], i32
+        lib.oracle_set_num_threads.argtypes, lib.oracle_set_num_threads.restype = [i32], None
         lib.oracle_forward.argtypes = [i64, i64, i64, i32, i32, dp, dp, dp, dp]
         lib.oracle_forward.restype = i32
         lib.oracle_backward.argtypes = [i64, i64, i64, i32, i32, dp, dp, dp, dp, dp, dp, dp]
@@ -87,6 +88,11 @@ def receives(i: int, layer: int, n: int, causal: bool) -> int:
 
 def num_threads() -> int:
     return _load().oracle_num_threads()
+
+
+def set_num_threads(k: int) -> None:
+    """Threads the C loops use from now on (for timing; results do not change)."""
+    _load().oracle_set_num_threads(int(k))
 
 
 def forward(x, w_self, w_off, layer: int, causal: bool) -> np.ndarray:

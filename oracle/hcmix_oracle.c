@@ -95,6 +95,16 @@ int32_t oracle_num_threads(void) {
 #endif
 }
 
+/* Threads the loops below use from now on (timing only; results do not
+ * depend on it, every element being summed in a fixed order). */
+void oracle_set_num_threads(int32_t k) {
+#ifdef _OPENMP
+    if (k >= 1) omp_set_num_threads(k);
+#else
+    (void)k;
+#endif
+}
+
 /* Forward of one layer, Eq. (1):
  *   y[bt][i][o] = sum_c w_self[o][c] x[bt][i][c]
  *               + receives(i) * sum_c w_off[o][c] x[bt][partner(i)][c]. */
@@ -136,20 +146,30 @@ int32_t oracle_backward(int64_t batch, int64_t n, int64_t width, int32_t layer,
     if (!oracle_valid_layer(layer, n, causal) || batch < 1 || width < 1) return -1;
     int64_t rows = batch * n;
 
-    /* dx: windows are independent, so parallelise over windows only. */
+    /* dx: windows are independent, and so is every column c of dx; a thread
+     * owns one window and one range of columns (the work items are spread over
+     * both so that a single long window still uses every core).  Each element
+     * is summed in the same order whatever the split: receivers i ascending,
+     * then o ascending. */
+    const int64_t cchunk = 64;
+    const int64_t nchunks = (width + cchunk - 1) / cchunk;
 #pragma omp parallel for schedule(static)
-    for (int64_t bt = 0; bt < batch; bt++) {
-        for (int64_t k = 0; k < n * width; k++) dx[bt * n * width + k] = 0.0;
+    for (int64_t item = 0; item < batch * nchunks; item++) {
+        const int64_t bt = item / nchunks;
+        const int64_t c0 = (item % nchunks) * cchunk;
+        const int64_t c1 = c0 + cchunk < width ? c0 + cchunk : width;
+        for (int64_t i = 0; i < n; i++)
+            for (int64_t c = c0; c < c1; c++) dx[(bt * n + i) * width + c] = 0.0;
         for (int64_t i = 0; i < n; i++) {
             const double* gi = dy + (bt * n + i) * width;
             double* dxi = dx + (bt * n + i) * width;
             for (int64_t o = 0; o < width; o++)
-                for (int64_t c = 0; c < width; c++) dxi[c] += w_self[o * width + c] * gi[o];
+                for (int64_t c = c0; c < c1; c++) dxi[c] += w_self[o * width + c] * gi[o];
             if (oracle_receives(i, layer, n, causal)) {
                 int64_t p = oracle_partner(i, layer, n);
                 double* dxp = dx + (bt * n + p) * width;
                 for (int64_t o = 0; o < width; o++)
-                    for (int64_t c = 0; c < width; c++) dxp[c] += w_off[o * width + c] * gi[o];
+                    for (int64_t c = c0; c < c1; c++) dxp[c] += w_off[o * width + c] * gi[o];
             }
         }
     }
