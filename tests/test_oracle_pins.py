@@ -121,6 +121,35 @@ def test_link_counts_synthetic(golden):
     assert L * n * n == g["links"]["dense"]
 
 
+def jump_of_layer(n, layer):
+    """Distance a causal layer moves information, measured through the oracle's
+    forward pass: the impulse at position 0 (the earliest source of every
+    link) arrives at 0 itself and at exactly one later position, whose index
+    is the jump (W_self = W_off = 1, width 1)."""
+    x = np.zeros((1, n, 1))
+    x[0, 0, 0] = 1.0
+    one = np.ones((1, 1))
+    y = oracle.forward(x, one, one, layer, True)
+    hit = sorted(int(i) for i in np.flatnonzero(y[0, :, 0]))
+    assert len(hit) == 2 and hit[0] == 0, hit
+    return hit[1]
+
+
+def test_mixa_order_is_the_printed_scale_list(golden):
+    """Section 3.3: mixa alternates local layers with long jumps that visit
+    each scale once, 32, 16, 8, 4, 2, 1 for n = 64, in that order.  The
+    oracle's schedule is read back layer by layer through its forward pass: the
+    local layers must sit at the even slots (jump 1), the jumps at the odd
+    slots in the printed order (an ascending or shuffled schedule fails here,
+    though it has the same link total)."""
+    g = golden["window64_twelve_layers"]
+    n = g["n"]
+    jumps = [jump_of_layer(n, code) for code in oracle.schedule_mixa(n)]
+    assert jumps[0::2] == [1] * 6
+    assert [code for code in oracle.schedule_mixa(n)[0::2]] == [oracle.NEAR] * 6
+    assert jumps[1::2] == g["mixa_jumps"]
+
+
 def test_link_counts_window64(golden):
     g = golden["window64_twelve_layers"]
     n, L = g["n"], g["layers"]
