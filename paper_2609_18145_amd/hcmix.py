@@ -132,12 +132,44 @@ def _fptr(t):
     return ctypes.cast(ctypes.c_void_p(t.data_ptr()), ctypes.POINTER(ctypes.c_float))
 
 
-def _check(x, *others):
-    if not x.is_cuda:
-        raise ValueError("hcmix works on GPU tensors only")
-    for t in (x, *others):
-        if t.device != x.device or t.dtype != x.dtype or not t.is_contiguous():
-            raise ValueError("all operands must be contiguous, on one device, of one dtype")
+def _need(t, name, shape, dtype, device=None):
+    """Validate one operand before anything reaches the library: a tensor of
+    exactly `shape` (None entries match any extent), of `dtype`, contiguous,
+    and (once the device is known) on `device`.  Raises ValueError."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a tensor, got {type(t).__name__}")
+    if shape is not None:
+        got = tuple(t.shape)
+        if len(got) != len(shape) or any(e is not None and g != e for g, e in zip(got, shape)):
+            raise ValueError(f"{name}: shape {got}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, expected {device}")
+
+
+def _gpu(dev):
+    """Every operand shares `dev` (checked per operand); it must be a GPU.
+    Checked after the shapes and dtypes, before the library is touched."""
+    if dev.type != "cuda":
+        raise ValueError(f"hcmix works on GPU tensors only (got {dev})")
+
+
+def _act_dtype(x, name="x"):
+    if x.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError(f"{name}: dtype {x.dtype}, expected bfloat16 or float32")
+    return x.dtype
+
+
+def _bytes(t):
+    """Byte extent of a workspace or cache tensor (any dtype, contiguous)."""
+    if t is None:
+        return 0
+    if not isinstance(t, torch.Tensor) or not t.is_contiguous():
+        raise ValueError("workspace/cache: expected a contiguous tensor")
+    return t.numel() * t.element_size()
 
 
 def _stream(x):
@@ -148,13 +180,32 @@ def dim(layer: int, n: int) -> int:
     return load().hcmix_dim(layer, n)
 
 
+def _act_shape(x, name="x"):
+    """[batch, n, width] of an activation tensor (checked to be 3-D)."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise ValueError(f"{name}: expected a [batch, n, width] tensor")
+    return tuple(x.shape)
+
+
+def _weights(ws, name, width, dtype, dev, count=None):
+    if count is not None and len(ws) != count:
+        raise ValueError(f"{name}: {len(ws)} matrices, expected {count}")
+    for k, w in enumerate(ws):
+        _need(w, f"{name}[{k}]", (width, width), dtype, dev)
+
+
 def forward(x: torch.Tensor, w_self: torch.Tensor, w_off: torch.Tensor, layer: int,
             causal: bool, out: torch.Tensor | None = None) -> torch.Tensor:
     """y = W_self x_i + m(i) W_off x_(i xor 2^d) over x of shape [batch, n, width]."""
-    _check(x, w_self, w_off)
-    batch, n, width = x.shape
+    batch, n, width = _act_shape(x)
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _weights([w_self, w_off], "w_self/w_off", width, dt, dev)
     if out is None:
         out = torch.empty_like(x)
+    _need(out, "out", (batch, n, width), dt, dev)
+    _gpu(dev)
     rc = load().hcmix_forward(batch, n, width, layer, int(bool(causal)), _dtype_code(x),
                               _ptr(x), _ptr(w_self), _ptr(w_off), _ptr(out), _stream(x))
     if rc != HCMIX_OK:
@@ -174,24 +225,36 @@ def alloc_workspace(batch, n, width, dtype, device) -> torch.Tensor | None:
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
+def _grad_out(t, name, width, dev, shape=None):
+    """A caller-supplied fp32 weight-gradient buffer ([width, width] unless given)."""
+    _need(t, name, shape or (width, width), torch.float32, dev)
+
+
 def backward(x, w_self, w_off, dy, layer: int, causal: bool, dx=None, dw_self=None,
              dw_off=None, accumulate: bool = False, workspace=None):
     """Adjoint of ``forward``: returns (dx, dw_self, dw_off); dw_* are fp32."""
-    _check(x, w_self, w_off, dy)
-    batch, n, width = x.shape
+    batch, n, width = _act_shape(x)
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _weights([w_self, w_off], "w_self/w_off", width, dt, dev)
+    _need(dy, "dy", (batch, n, width), dt, dev)
     if dx is None:
         dx = torch.empty_like(x)
+    _need(dx, "dx", (batch, n, width), dt, dev)
     if dw_self is None:
-        dw_self = torch.empty((width, width), dtype=torch.float32, device=x.device)
+        dw_self = torch.empty((width, width), dtype=torch.float32, device=dev)
     if dw_off is None:
-        dw_off = torch.empty((width, width), dtype=torch.float32, device=x.device)
+        dw_off = torch.empty((width, width), dtype=torch.float32, device=dev)
+    _grad_out(dw_self, "dw_self", width, dev)
+    _grad_out(dw_off, "dw_off", width, dev)
+    _gpu(dev)
     if workspace is None:
-        workspace = alloc_workspace(batch, n, width, x.dtype, x.device)
-    ws_bytes = workspace.numel() if workspace is not None else 0
+        workspace = alloc_workspace(batch, n, width, x.dtype, dev)
     rc = load().hcmix_backward(batch, n, width, layer, int(bool(causal)), _dtype_code(x),
                                _ptr(x), _ptr(w_self), _ptr(w_off), _ptr(dy), _ptr(dx),
                                _fptr(dw_self), _fptr(dw_off), int(bool(accumulate)),
-                               _ptr(workspace), ws_bytes, _stream(x))
+                               _ptr(workspace), _bytes(workspace), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_backward")
     return dx, dw_self, dw_off
@@ -205,20 +268,33 @@ def _layers(layers):
     return (ctypes.c_int32 * len(layers))(*[int(v) for v in layers])
 
 
+def _acts(ts, name, shape, dt, dev, count):
+    if len(ts) < count:
+        raise ValueError(f"{name}: {len(ts)} tensors, expected {count}")
+    for k in range(count):
+        _need(ts[k], f"{name}[{k}]", shape, dt, dev)
+
+
 def stack_forward(x, w_selfs, w_offs, layers, causal, outs=None):
     """Run the layers in order in one library call; returns [x_0, x_1, ..., x_L]."""
     L = len(layers)
-    _check(x, *w_selfs, *w_offs)
+    shape = _act_shape(x)
+    batch, n, width = shape
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _weights(w_selfs, "w_selfs", width, dt, dev, L)
+    _weights(w_offs, "w_offs", width, dt, dev, L)
     if outs is None:
         outs = [torch.empty_like(x) for _ in range(L)]
-    _check(x, *outs)
-    batch, n, width = x.shape
+    _acts(outs, "outs", shape, dt, dev, L)
+    _gpu(dev)
     rc = load().hcmix_stack_forward(batch, n, width, L, _layers(layers), int(bool(causal)),
                                     _dtype_code(x), _ptr(x), _ptrs(w_selfs), _ptrs(w_offs),
-                                    _ptrs(outs), _stream(x))
+                                    _ptrs(outs[:L]), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_forward")
-    return [x, *outs]
+    return [x, *outs[:L]]
 
 
 def stack_workspace_bytes(batch, n, width, num_layers, dtype) -> int:
@@ -237,21 +313,31 @@ def stack_backward(xs, w_selfs, w_offs, layers, dy, causal, dx=None, dws=None, d
     inputs xs[0..L-1]; returns (dx_0, [dW_self], [dW_off])."""
     L = len(layers)
     x0 = xs[0]
-    _check(x0, *xs[:L], *w_selfs, *w_offs, dy)
-    batch, n, width = x0.shape
+    shape = _act_shape(x0, "xs[0]")
+    batch, n, width = shape
+    dt = _act_dtype(x0, "xs[0]")
+    dev = x0.device
+    _acts(xs, "xs", shape, dt, dev, L)
+    _weights(w_selfs, "w_selfs", width, dt, dev, L)
+    _weights(w_offs, "w_offs", width, dt, dev, L)
+    _need(dy, "dy", shape, dt, dev)
     if dx is None:
         dx = torch.empty_like(x0)
+    _need(dx, "dx", shape, dt, dev)
     if dws is None:
-        dws = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+        dws = [torch.empty((width, width), dtype=torch.float32, device=dev) for _ in range(L)]
     if dwo is None:
-        dwo = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+        dwo = [torch.empty((width, width), dtype=torch.float32, device=dev) for _ in range(L)]
+    _acts(dws, "dws", (width, width), torch.float32, dev, L)
+    _acts(dwo, "dwo", (width, width), torch.float32, dev, L)
+    _gpu(dev)
     if workspace is None:
-        workspace = alloc_stack_workspace(batch, n, width, L, x0.dtype, x0.device)
-    ws_bytes = workspace.numel() if workspace is not None else 0
+        workspace = alloc_stack_workspace(batch, n, width, L, x0.dtype, dev)
     rc = load().hcmix_stack_backward(batch, n, width, L, _layers(layers), int(bool(causal)),
                                      _dtype_code(x0), _ptrs(xs[:L]), _ptrs(w_selfs), _ptrs(w_offs),
-                                     _ptr(dy), _ptr(dx), _ptrs(dws), _ptrs(dwo),
-                                     int(bool(accumulate)), _ptr(workspace), ws_bytes, _stream(x0))
+                                     _ptr(dy), _ptr(dx), _ptrs(dws[:L]), _ptrs(dwo[:L]),
+                                     int(bool(accumulate)), _ptr(workspace), _bytes(workspace),
+                                     _stream(x0))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_backward")
     return dx, dws, dwo
@@ -263,21 +349,28 @@ def stack_backward_data(w_selfs, w_offs, layers, dy, causal, dx=None, grads=None
     (dx_0, [g_1, ..., g_{L-1}]) with g_l the gradient of layer l's input, so
     that layer l's output gradient is grads[l] (dy for the last layer)."""
     L = len(layers)
-    _check(dy, *w_selfs, *w_offs)
-    batch, n, width = dy.shape
+    shape = _act_shape(dy, "dy")
+    batch, n, width = shape
+    dt = _act_dtype(dy, "dy")
+    _need(dy, "dy", None, dt)
+    dev = dy.device
+    _weights(w_selfs, "w_selfs", width, dt, dev, L)
+    _weights(w_offs, "w_offs", width, dt, dev, L)
     if dx is None:
         dx = torch.empty_like(dy)
     if grads is None:
         grads = [torch.empty_like(dy) for _ in range(L - 1)]
-    _check(dy, dx, *grads)
+    _need(dx, "dx", shape, dt, dev)
+    _acts(grads, "grads", shape, dt, dev, L - 1)
+    _gpu(dev)
     nbytes = load().hcmix_stack_backward_data_workspace_bytes(width, L, _dtype_code(dy))
     if workspace is None and nbytes:
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dy.device)
-    ws_bytes = workspace.numel() if workspace is not None else 0
-    gp = _ptrs(grads) if grads else None
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    gp = _ptrs(grads[:L - 1]) if L > 1 else None
     rc = load().hcmix_stack_backward_data(batch, n, width, L, _layers(layers), int(bool(causal)),
                                           _dtype_code(dy), _ptrs(w_selfs), _ptrs(w_offs), _ptr(dy),
-                                          gp, _ptr(dx), _ptr(workspace), ws_bytes, _stream(dy))
+                                          gp, _ptr(dx), _ptr(workspace), _bytes(workspace),
+                                          _stream(dy))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_backward_data")
     return dx, grads
@@ -294,37 +387,53 @@ def stack_weight_gradients(xs, dys, layers, causal, dws=None, dwo=None, accumula
     its output dys[l], in one library call; returns ([dW_self], [dW_off])."""
     L = len(layers)
     x0 = xs[0]
-    _check(x0, *xs[:L], *dys[:L])
-    batch, n, width = x0.shape
+    shape = _act_shape(x0, "xs[0]")
+    batch, n, width = shape
+    dt = _act_dtype(x0, "xs[0]")
+    dev = x0.device
+    _acts(xs, "xs", shape, dt, dev, L)
+    _acts(dys, "dys", shape, dt, dev, L)
     if dws is None:
-        dws = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+        dws = [torch.empty((width, width), dtype=torch.float32, device=dev) for _ in range(L)]
     if dwo is None:
-        dwo = [torch.empty((width, width), dtype=torch.float32, device=x0.device) for _ in range(L)]
+        dwo = [torch.empty((width, width), dtype=torch.float32, device=dev) for _ in range(L)]
+    _acts(dws, "dws", (width, width), torch.float32, dev, L)
+    _acts(dwo, "dwo", (width, width), torch.float32, dev, L)
+    _gpu(dev)
     if workspace is None:
         nbytes = weight_gradients_workspace_bytes(batch, n, width, L, x0.dtype)
-        workspace = (torch.empty(nbytes, dtype=torch.uint8, device=x0.device) if nbytes
+        workspace = (torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes
                      else None)
-    ws_bytes = workspace.numel() if workspace is not None else 0
     rc = load().hcmix_stack_weight_gradients(batch, n, width, L, _layers(layers),
                                              int(bool(causal)), _dtype_code(x0), _ptrs(xs[:L]),
-                                             _ptrs(dys[:L]), _ptrs(dws), _ptrs(dwo),
-                                             int(bool(accumulate)), _ptr(workspace), ws_bytes,
-                                             _stream(x0))
+                                             _ptrs(dys[:L]), _ptrs(dws[:L]), _ptrs(dwo[:L]),
+                                             int(bool(accumulate)), _ptr(workspace),
+                                             _bytes(workspace), _stream(x0))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_stack_weight_gradients")
     return dws, dwo
 
 
+def _qkv_shape(qkv):
+    if not isinstance(qkv, torch.Tensor) or qkv.dim() != 5 or qkv.shape[2] != 3:
+        raise ValueError("qkv: expected a [batch, n, 3, heads, head_dim] tensor")
+    batch, n, _, heads, hd = qkv.shape
+    return batch, n, heads, hd
+
+
 def attention_forward(qkv, out=None, lse=None):
     """Causal multi-head attention core: qkv [batch, n, 3, heads, 64] bf16 ->
     (out [batch, n, heads, 64] bf16, lse [batch, heads, n] fp32)."""
-    _check(qkv)
-    batch, n, three, heads, hd = qkv.shape
-    assert three == 3
+    batch, n, heads, hd = _qkv_shape(qkv)
+    _need(qkv, "qkv", None, torch.bfloat16)
+    dev = qkv.device
     if out is None:
-        out = torch.empty((batch, n, heads, hd), dtype=qkv.dtype, device=qkv.device)
+        out = torch.empty((batch, n, heads, hd), dtype=qkv.dtype, device=dev)
     if lse is None:
-        lse = torch.empty((batch, heads, n), dtype=torch.float32, device=qkv.device)
+        lse = torch.empty((batch, heads, n), dtype=torch.float32, device=dev)
+    _need(out, "out", (batch, n, heads, hd), torch.bfloat16, dev)
+    _need(lse, "lse", (batch, heads, n), torch.float32, dev)
+    _gpu(dev)
     rc = load().hcmix_attention_forward(batch, n, heads, hd, _ptr(qkv), _ptr(out), _fptr(lse),
                                         _stream(qkv))
     if rc != HCMIX_OK:
@@ -334,10 +443,16 @@ def attention_forward(qkv, out=None, lse=None):
 
 def attention_backward(qkv, out, lse, dout, dqkv=None):
     """Gradient of qkv ([batch, n, 3, heads, 64]) given dout = dL/dout."""
-    _check(qkv, out, dout)
-    batch, n, three, heads, hd = qkv.shape
+    batch, n, heads, hd = _qkv_shape(qkv)
+    _need(qkv, "qkv", None, torch.bfloat16)
+    dev = qkv.device
+    _need(out, "out", (batch, n, heads, hd), torch.bfloat16, dev)
+    _need(lse, "lse", (batch, heads, n), torch.float32, dev)
+    _need(dout, "dout", (batch, n, heads, hd), torch.bfloat16, dev)
     if dqkv is None:
         dqkv = torch.empty_like(qkv)
+    _need(dqkv, "dqkv", tuple(qkv.shape), torch.bfloat16, dev)
+    _gpu(dev)
     rc = load().hcmix_attention_backward(batch, n, heads, hd, _ptr(qkv), _ptr(out), _fptr(lse),
                                          _ptr(dout), _ptr(dqkv), _stream(qkv))
     if rc != HCMIX_OK:
@@ -345,14 +460,28 @@ def attention_backward(qkv, out, lse, dout, dqkv=None):
     return dqkv
 
 
+def _rows_of(t, name, width, dtype, dev):
+    """A [..., width] tensor of `dtype`; returns its number of rows."""
+    if not isinstance(t, torch.Tensor) or t.dim() < 1 or t.shape[-1] != width:
+        raise ValueError(f"{name}: expected a [..., {width}] tensor")
+    _need(t, name, None, dtype, dev)
+    return t.numel() // width
+
+
 def embedding_forward(table, tokens, out=None):
     """x[r] = table[tokens[r]]: table [vocab, width] bf16, tokens int32 (any shape)."""
-    if tokens.dtype != torch.int32 or not tokens.is_contiguous() or not table.is_contiguous():
-        raise ValueError("tokens must be contiguous int32, table contiguous")
+    if not isinstance(table, torch.Tensor) or table.dim() != 2:
+        raise ValueError("table: expected a [vocab, width] tensor")
     vocab, width = table.shape
+    _need(table, "table", None, torch.bfloat16)
+    dev = table.device
+    _need(tokens, "tokens", None, torch.int32, dev)
     rows = tokens.numel()
     if out is None:
-        out = torch.empty((*tokens.shape, width), dtype=table.dtype, device=table.device)
+        out = torch.empty((*tokens.shape, width), dtype=table.dtype, device=dev)
+    if _rows_of(out, "out", width, torch.bfloat16, dev) != rows:
+        raise ValueError(f"out: {out.numel() // width} rows, expected {rows}")
+    _gpu(dev)
     rc = load().hcmix_embedding_forward(rows, width, vocab, _ptr(table), _ptr(tokens), _ptr(out),
                                         _stream(table))
     if rc != HCMIX_OK:
@@ -362,16 +491,25 @@ def embedding_forward(table, tokens, out=None):
 
 def embedding_backward(tokens, dx, vocab, dtable=None, accumulate=False, workspace=None):
     """dtable[v] (+)= sum of dx rows whose token is v (fp32 [vocab, width])."""
+    if not isinstance(dx, torch.Tensor) or dx.dim() < 1:
+        raise ValueError("dx: expected a [..., width] tensor")
     width = dx.shape[-1]
+    _need(dx, "dx", None, torch.bfloat16)
+    dev = dx.device
+    _need(tokens, "tokens", None, torch.int32, dev)
     rows = tokens.numel()
+    if _rows_of(dx, "dx", width, torch.bfloat16, dev) != rows:
+        raise ValueError(f"dx: {dx.numel() // width} rows, expected {rows} (one per token)")
     if dtable is None:
-        dtable = torch.empty((vocab, width), dtype=torch.float32, device=dx.device)
+        dtable = torch.empty((vocab, width), dtype=torch.float32, device=dev)
+    _need(dtable, "dtable", (vocab, width), torch.float32, dev)
+    _gpu(dev)
     nbytes = load().hcmix_embedding_backward_workspace_bytes(rows, width, vocab)
     if workspace is None:
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dx.device)
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     rc = load().hcmix_embedding_backward(rows, width, vocab, _ptr(tokens), _ptr(dx), _fptr(dtable),
                                          int(bool(accumulate)), _ptr(workspace),
-                                         workspace.numel(), _stream(dx))
+                                         _bytes(workspace), _stream(dx))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_embedding_backward")
     return dtable
@@ -382,26 +520,35 @@ def head_cross_entropy(x, w, bias, targets, scale, loss=None, dlogits=None, dbia
     """Per-row loss (fp32 [rows]) and scale * (softmax - onehot) (bf16 [rows, vocab]);
     with with_dbias (or a dbias buffer), also the bias gradient (fp32 [vocab]):
     returns (loss, dlogits) or (loss, dlogits, dbias)."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("w: expected a [vocab, width] tensor")
     vocab, width = w.shape
+    _need(w, "w", None, torch.bfloat16)
+    dev = w.device
+    _need(targets, "targets", None, torch.int32, dev)
     rows = targets.numel()
+    _need(x, "x", (rows, width), torch.bfloat16, dev)
+    _need(bias, "bias", (vocab,), torch.float32, dev)
     if loss is None:
-        loss = torch.empty(rows, dtype=torch.float32, device=x.device)
+        loss = torch.empty(rows, dtype=torch.float32, device=dev)
     if dlogits is None:
-        dlogits = torch.empty((rows, vocab), dtype=x.dtype, device=x.device)
+        dlogits = torch.empty((rows, vocab), dtype=x.dtype, device=dev)
+    _need(loss, "loss", (rows,), torch.float32, dev)
+    _need(dlogits, "dlogits", (rows, vocab), torch.bfloat16, dev)
     want_db = with_dbias or dbias is not None
-    ws_bytes = 0
     if want_db:
         if dbias is None:
-            dbias = torch.empty(vocab, dtype=torch.float32, device=x.device)
-        if workspace is None:
-            workspace = torch.empty(load().hcmix_head_cross_entropy_workspace_bytes(rows, vocab),
-                                    dtype=torch.uint8, device=x.device)
-        ws_bytes = workspace.numel()
+            dbias = torch.empty(vocab, dtype=torch.float32, device=dev)
+        _need(dbias, "dbias", (vocab,), torch.float32, dev)
+    _gpu(dev)
+    if want_db and workspace is None:
+        workspace = torch.empty(load().hcmix_head_cross_entropy_workspace_bytes(rows, vocab),
+                                dtype=torch.uint8, device=dev)
     rc = load().hcmix_head_cross_entropy(rows, width, vocab, _ptr(x), _ptr(w), _fptr(bias),
                                          _ptr(targets), float(scale), _fptr(loss), _ptr(dlogits),
                                          _fptr(dbias) if want_db else None,
-                                         _ptr(workspace) if want_db else None, ws_bytes,
-                                         _stream(x))
+                                         _ptr(workspace) if want_db else None,
+                                         _bytes(workspace) if want_db else 0, _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_cross_entropy")
     return (loss, dlogits, dbias) if want_db else (loss, dlogits)
@@ -413,26 +560,38 @@ def head_backward(x, w, dlogits, gx=None, dw=None, with_gx=True, with_dw=True,
     gradient dlogits^T x (fp32 [vocab, width], added to dw with accumulate):
     returns (gx, dw), None for one not asked for.  x is only read for dw (it
     may be None without it)."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("w: expected a [vocab, width] tensor")
     vocab, width = w.shape
+    _need(w, "w", None, torch.bfloat16)
+    dev = w.device
+    if not isinstance(dlogits, torch.Tensor) or dlogits.dim() != 2:
+        raise ValueError("dlogits: expected a [rows, vocab] tensor")
     rows = dlogits.shape[0]
+    _need(dlogits, "dlogits", (rows, vocab), torch.bfloat16, dev)
     want_gx = with_gx or gx is not None
     want_dw = with_dw or dw is not None
-    dev = dlogits.device
-    if want_gx and gx is None:
-        gx = torch.empty((rows, width), dtype=dlogits.dtype, device=dev)
-    ws_bytes = 0
+    if not want_gx and not want_dw:
+        raise ValueError("head_backward: neither gx nor dw asked for")
+    if want_dw:
+        _need(x, "x", (rows, width), torch.bfloat16, dev)
+    if want_gx:
+        if gx is None:
+            gx = torch.empty((rows, width), dtype=dlogits.dtype, device=dev)
+        _need(gx, "gx", (rows, width), torch.bfloat16, dev)
     if want_dw:
         if dw is None:
             dw = torch.empty((vocab, width), dtype=torch.float32, device=dev)
-        if workspace is None:
-            workspace = torch.empty(load().hcmix_head_backward_workspace_bytes(rows, width, vocab),
-                                    dtype=torch.uint8, device=dev)
-        ws_bytes = workspace.numel()
+        _need(dw, "dw", (vocab, width), torch.float32, dev)
+    _gpu(dev)
+    if want_dw and workspace is None:
+        workspace = torch.empty(load().hcmix_head_backward_workspace_bytes(rows, width, vocab),
+                                dtype=torch.uint8, device=dev)
     rc = load().hcmix_head_backward(rows, width, vocab, _ptr(x) if want_dw else None, _ptr(w),
                                     _ptr(dlogits), _ptr(gx) if want_gx else None,
                                     _fptr(dw) if want_dw else None, int(bool(accumulate)),
-                                    _ptr(workspace) if want_dw else None, ws_bytes,
-                                    _stream(dlogits))
+                                    _ptr(workspace) if want_dw else None,
+                                    _bytes(workspace) if want_dw else 0, _stream(dlogits))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_backward")
     return (gx if want_gx else None), (dw if want_dw else None)
@@ -469,14 +628,23 @@ def decode_step(x, w_selfs, w_offs, layers, n, pos, cache, out=None):
     """Position ``pos`` of every window through the causal stack: x and the
     result are [batch, width]; positions of a window must come in order."""
     L = len(layers)
-    _check(x, *w_selfs, *w_offs)
+    if not isinstance(x, torch.Tensor) or x.dim() != 2:
+        raise ValueError("x: expected a [batch, width] tensor")
     batch, width = x.shape
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _weights(w_selfs, "w_selfs", width, dt, dev, L)
+    _weights(w_offs, "w_offs", width, dt, dev, L)
     if out is None:
         out = torch.empty_like(x)
-    _check(x, out)
+    _need(out, "out", (batch, width), dt, dev)
+    if not isinstance(cache, torch.Tensor) or cache.device != dev:
+        raise ValueError(f"cache: expected a tensor on {dev}")
+    _gpu(dev)
     rc = load().hcmix_decode_step(batch, n, width, L, _layers(layers), _dtype_code(x), pos,
                                   _ptr(x), _ptrs(w_selfs), _ptrs(w_offs), _ptr(cache),
-                                  cache.numel(), _ptr(out), _stream(x))
+                                  _bytes(cache), _ptr(out), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_decode_step")
     return out
