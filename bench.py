@@ -602,8 +602,9 @@ def run_lm_step(args, torch, hcmix, inputs, dev):
     model: embedding (library gather), the 16-layer stack forward, the 256-way
     head with bias and cross-entropy (library kernel: logits, loss and
     dlogits and the bias gradient), the head's weight and input gradients
-    (PyTorch GEMMs on dlogits), the stack backward and the embedding's scatter sum (library),
-    replayed as a HIP graph.  value = positions * sparse layers / step time;
+    (the library's hcmix_head_backward; --head-grad torch runs them as
+    PyTorch GEMMs instead, for comparison), the stack backward and the
+    embedding's scatter sum (library), replayed as a HIP graph.  value = positions * sparse layers / step time;
     the sparse stack's share of the step is reported beside it."""
     over = {"batch": args.batch} if args.batch > 0 else {}
     cfg = dict(inputs.PRESETS["lm256"], **over)
@@ -815,21 +816,28 @@ def run_decode(args, torch, hcmix, inputs, dev):
     return 0
 
 
-def cpu_baseline(s, n, w, L, causal, windows):
-    """The CPU oracle (plain fp64 loops) on a bounded sample: `windows` windows
-    of the same workload through every layer, forward and backward.  With
-    windows == 0 the sample is sized to 10-30 s of CPU work from a timed
-    pilot of a few windows; when the whole workload takes less than that, it
-    is run repeatedly (the sample then says how many passes)."""
+def cpu_model() -> str:
+    """The host CPU's model name (as lscpu prints it, from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def timed_oracle_legs(run, B, n, L, windows, what):
+    """Time `run(k)` (the oracle over k windows, every layer, forward and
+    backward) on all host threads and on one thread.
+
+    All threads: with windows == 0 the sample is sized to 10-30 s of CPU work
+    from a timed pilot of a few windows; when the whole workload takes less
+    than that, it is run repeatedly (the sample then says how many passes).
+    One thread: one window, repeated until about 5 s have passed (at most
+    once more than needed), so the whole baseline stays within about 35 s."""
     import oracle
-
-    B = s.x.shape[0]
-
-    def run(k):
-        t0 = time.perf_counter()
-        xs = oracle.stack_forward(s.x[:k], s.w_self, s.w_off, s.layers, causal)
-        oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, s.dy[:k], causal)
-        return time.perf_counter() - t0
 
     passes = 1
     if windows <= 0:
@@ -846,18 +854,46 @@ def cpu_baseline(s, n, w, L, causal, windows):
         dt += run(windows)
         done += 1
     passes = done
-    what = (f"{windows} of the workload's {B} windows" if windows < B
-            else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
-    return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{what}, all {L} layers, forward+backward, {dt:.1f} s"}
+    threads = oracle.num_threads()
+    sample = (f"{windows} of the workload's {B} windows" if windows < B
+              else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
+    out = {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT, "cores": threads,
+           "kind": "oracle", "sample": f"{sample}{what}, {dt:.1f} s", "cpu_model": cpu_model(),
+           "host_cpus": os.cpu_count()}
+    oracle.set_num_threads(1)
+    try:
+        dt1, done1 = 0.0, 0
+        while dt1 < 5.0 and done1 < 200:
+            dt1 += run(1)
+            done1 += 1
+    finally:
+        oracle.set_num_threads(threads)
+    out["single_thread"] = {"value": round(done1 * n * L / dt1, 1), "unit": UNIT, "cores": 1,
+                            "sample": f"1 window, {done1} passes{what}, {dt1:.1f} s"}
+    return out
+
+
+def cpu_baseline(s, n, w, L, causal, windows):
+    """The CPU oracle (plain fp64 loops) on a bounded sample of the same
+    workload: windows through every layer, forward and backward, on all host
+    threads and on one."""
+    import oracle
+
+    def run(k):
+        t0 = time.perf_counter()
+        xs = oracle.stack_forward(s.x[:k], s.w_self, s.w_off, s.layers, causal)
+        oracle.stack_backward(xs, s.w_self, s.w_off, s.layers, s.dy[:k], causal)
+        return time.perf_counter() - t0
+
+    return timed_oracle_legs(run, s.x.shape[0], n, L, windows,
+                             f", all {L} layers, forward+backward")
 
 
 def cpu_baseline_lm(s, table, head_w, n, w, L, V, windows):
-    """The CPU oracle on a bounded sample of the whole LM step: `windows`
-    windows through the embedding, every layer, the head and cross-entropy,
-    the head's gradients (plain products on dlogits), the stack backward and
-    the embedding's scatter sum; sized like cpu_baseline when windows == 0."""
+    """The CPU oracle on a bounded sample of the whole LM step: windows
+    through the embedding, every layer, the head and cross-entropy, the head's
+    gradients (plain products on dlogits), the stack backward and the
+    embedding's scatter sum; all host threads and one thread, as cpu_baseline."""
     import numpy as np
 
     import oracle
@@ -879,25 +915,9 @@ def cpu_baseline_lm(s, table, head_w, n, w, L, V, windows):
         lm_head.embedding_backward(s.tokens[:k], dx, V)
         return time.perf_counter() - t0
 
-    passes = 1
-    if windows <= 0:
-        target = 25.0
-        pilot = min(B, 4)
-        per_window = run(pilot) / pilot
-        windows = max(1, min(B, int(target / max(per_window, 1e-4))))
-        if windows == B:
-            passes = max(1, min(200, int(round(target / max(per_window * B, 1e-4)))))
-    dt, done = 0.0, 0
-    while done < passes or (dt < 10.0 and done < 200):   # the pilot may overestimate
-        dt += run(windows)
-        done += 1
-    passes = done
-    what = (f"{windows} of the workload's {B} windows" if windows < B
-            else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
-    return {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT,
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{what}: embedding, all {L} layers, head and cross-entropy, forward+"
-                      f"backward, {dt:.1f} s"}
+    return timed_oracle_legs(run, B, n, L, windows,
+                             f": embedding, all {L} layers, head and cross-entropy, "
+                             "forward+backward")
 
 
 if __name__ == "__main__":
