@@ -117,6 +117,27 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
                             int32_t accumulate, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* hcmix_backward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same computation and kernels, hence bitwise the same results, with the
+ * split-K partial sums kept in a scratch array inside the library instead of a
+ * caller workspace.  The array is HCMIX_NO_ALLOC_SCRATCH_BYTES of device
+ * memory per GPU, held from the first call on that GPU until the process
+ * ends; the call allocates and frees nothing.  Shapes whose partials need
+ * more than that (bf16 widths above 2048) return HCMIX_ERR_UNSUPPORTED; fp32
+ * calls use no scratch.  Every call on one GPU shares that GPU's array, so
+ * calls that overlap in time on one GPU (other streams, other threads) race
+ * and give wrong weight gradients; serialise them.  The array's contents are
+ * overwritten by every call before they are read.  Other arguments and
+ * errors as for hcmix_backward. */
+#define HCMIX_NO_ALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+hcmix_status hcmix_backward_no_alloc(int64_t batch, int64_t n, int64_t width, int32_t layer,
+                                     int32_t mode, int32_t dtype, const void* x,
+                                     const void* w_self, const void* w_off, const void* dy,
+                                     void* dx, float* dw_self, float* dw_off,
+                                     int32_t accumulate, void* stream);
+
 /* ---- Whole stacks (Section 3.3: a schedule is a list of layer indices) ----
  *
  * layers:        host array of num_layers layer indices (layer l uses

@@ -4,6 +4,7 @@
 #include "hcmix.h"
 #include "hcmix_internal.h"
 
+#include <mutex>
 #include <string.h>
 
 using namespace hcmix;
@@ -300,6 +301,34 @@ hipError_t stack_backward_deferred(int rows, int w, int n, int32_t num_layers,
   return e;
 }
 
+// Scratch memory of hcmix_backward_no_alloc: a file-scope device array, one
+// copy per GPU the library runs on, held until the process ends.  Its name
+// is a host-side stand-in; the device address of each GPU's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[HCMIX_NO_ALLOC_SCRATCH_BYTES];
+void* g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// The current device's copy of `scratch` (null on failure, with *e set).
+void* device_scratch(hipError_t* e) {
+  int dev = 0;
+  *e = hipGetDevice(&dev);
+  if (*e != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) {
+    *e = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    *e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*e != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -369,6 +398,39 @@ hcmix_status hcmix_backward(int64_t batch, int64_t n, int64_t width, int32_t lay
   hipError_t e = run_backward((int)(batch * n), (int)width, hcmix_dim(layer, n), (int)n,
                               mode == HCMIX_BIDIR, dtype, x, w_self, w_off, dy, dx, dw_self,
                               dw_off, accumulate != 0, workspace, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+hcmix_status hcmix_backward_no_alloc(int64_t batch, int64_t n, int64_t width, int32_t layer,
+                                     int32_t mode, int32_t dtype, const void* x,
+                                     const void* w_self, const void* w_off, const void* dy,
+                                     void* dx, float* dw_self, float* dw_off,
+                                     int32_t accumulate, void* stream) {
+  if (!x || !w_self || !w_off || !dy || !dx || !dw_self || !dw_off)
+    return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_shape(batch, n, width, layer, mode, dtype);
+  if (st != HCMIX_OK) return st;
+  const size_t need = layer_workspace_bytes(batch, n, width, dtype);
+  if (need > HCMIX_NO_ALLOC_SCRATCH_BYTES) return HCMIX_ERR_UNSUPPORTED;
+  const size_t es = elem_size(dtype);
+  const size_t act = (size_t)(batch * n * width) * es, wgt = (size_t)(width * width) * es;
+  const size_t gw = (size_t)(width * width) * sizeof(float);
+  const Span ins[4] = {{x, act}, {w_self, wgt}, {w_off, wgt}, {dy, act}};
+  const Span outs[3] = {{dx, act}, {dw_self, gw}, {dw_off, gw}};
+  st = check_spans(ins, 4, outs, 3, dtype == HCMIX_BF16 ? 16 : 4);
+  if (st != HCMIX_OK) return st;
+  if (!aligned(dw_self, 16) || !aligned(dw_off, 16)) return HCMIX_ERR_UNSUPPORTED;
+  void* ws = nullptr;
+  if (need > 0) {
+    hipError_t e = hipSuccess;
+    ws = device_scratch(&e);
+    if (!ws) return hip_fail(e);
+  }
+  // the split-K partials are written in full before they are read, so the
+  // scratch needs no clearing
+  hipError_t e = run_backward((int)(batch * n), (int)width, hcmix_dim(layer, n), (int)n,
+                              mode == HCMIX_BIDIR, dtype, x, w_self, w_off, dy, dx, dw_self,
+                              dw_off, accumulate != 0, ws, (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 

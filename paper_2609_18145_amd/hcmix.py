@@ -34,7 +34,8 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_attention_backward", "hcmix_embedding_forward",
            "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
            "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy",
-           "hcmix_head_backward_workspace_bytes", "hcmix_head_backward")
+           "hcmix_head_backward_workspace_bytes", "hcmix_head_backward",
+           "hcmix_backward_no_alloc")
 
 _lib = None
 
@@ -69,6 +70,9 @@ def load():
         lib.hcmix_backward.argtypes = [i64, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp, fp, fp,
                                        i32, vp, sz, vp]
         lib.hcmix_backward.restype = i32
+        lib.hcmix_backward_no_alloc.argtypes = [i64, i64, i64, i32, i32, i32, vp, vp, vp, vp, vp,
+                                                fp, fp, i32, vp]
+        lib.hcmix_backward_no_alloc.restype = i32
         pp = ctypes.POINTER(ctypes.c_void_p)
         ip = ctypes.POINTER(ctypes.c_int32)
         lib.hcmix_stack_forward.argtypes = [i64, i64, i64, i32, ip, i32, i32, vp, pp, pp, pp, vp]
@@ -257,6 +261,30 @@ def backward(x, w_self, w_off, dy, layer: int, causal: bool, dx=None, dw_self=No
                                _ptr(workspace), _bytes(workspace), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_backward")
+    return dx, dw_self, dw_off
+
+
+def backward_no_alloc(x, w_self, w_off, dy, layer: int, causal: bool, dx, dw_self, dw_off,
+                      accumulate: bool = False):
+    """``backward`` for callers that cannot allocate: every output is the
+    caller's, and the split-K partials live in the library's own scratch array
+    (hcmix_backward_no_alloc); calls that overlap on one GPU race."""
+    batch, n, width = _act_shape(x)
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _weights([w_self, w_off], "w_self/w_off", width, dt, dev)
+    _need(dy, "dy", (batch, n, width), dt, dev)
+    _need(dx, "dx", (batch, n, width), dt, dev)
+    _grad_out(dw_self, "dw_self", width, dev)
+    _grad_out(dw_off, "dw_off", width, dev)
+    _gpu(dev)
+    rc = load().hcmix_backward_no_alloc(batch, n, width, layer, int(bool(causal)),
+                                        _dtype_code(x), _ptr(x), _ptr(w_self), _ptr(w_off),
+                                        _ptr(dy), _ptr(dx), _fptr(dw_self), _fptr(dw_off),
+                                        int(bool(accumulate)), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_backward_no_alloc")
     return dx, dw_self, dw_off
 
 
