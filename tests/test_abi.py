@@ -107,6 +107,22 @@ def test_backward_rejects_bad_arguments(kw, code):
     assert bwd(**kw) == code
 
 
+def bwd_no_alloc(batch=2, n=16, width=64, layer=0, mode=0, dtype=1, x=P[0], ws=P[1], wo=P[2],
+                 dy=P[3], dx=P[4], dws=FP[5], dwo=FP[6], acc=0):
+    return hcmix.load().hcmix_backward_no_alloc(batch, n, width, layer, mode, dtype, x, ws, wo, dy,
+                                                dx, dws, dwo, acc, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=3), INVALID), (dict(batch=0), INVALID), (dict(dy=None), INVALID),
+    (dict(dx=P[3]), INVALID), (dict(dws=FP[6]), INVALID), (dict(dx=P[0]), INVALID),
+    (dict(width=32), UNSUPPORTED),
+    (dict(width=2112, n=64, batch=1), UNSUPPORTED),   # needs more than the 32 MiB scratch
+])
+def test_backward_no_alloc_rejects_bad_arguments(kw, code):
+    assert bwd_no_alloc(**kw) == code
+
+
 def test_workspace_query():
     lib = hcmix.load()
     assert lib.hcmix_backward_workspace_bytes(2, 16, 64, hcmix.HCMIX_F32) == 0
