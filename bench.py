@@ -46,6 +46,9 @@ WORKLOADS = {
     "hy256": ("window n=256, width 512, batch 64, the hybrid256 schedule: 8 local layers, 6 "
               "causal jumps 128..1 and 2 causal softmax attention layers (8 heads x 64), 16 "
               "layers, bf16, fwd+bwd"),
+    "shared256": ("window n=256, width 512, batch 64, 16 rotated causal channel-shared layers "
+                  "(per-position scalar maps from one 256 x 256 table per layer), Zipf byte-token "
+                  "embedding inputs, bf16, fwd+bwd"),
 }
 # hybrid: positions of the attention layers in the 18-layer list
 HYBRID_ATTN_SLOTS = (3, 9)
@@ -241,6 +244,8 @@ def main():
         return run_decode(args, torch, hcmix, inputs, dev)
     if args.workload == "lm256_step":
         return run_lm_step(args, torch, hcmix, inputs, dev)
+    if args.workload == "shared256":
+        return run_shared(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
     cfg = dict(inputs.PRESETS[args.workload], **over)
     s = inputs.make_preset(args.workload, **over)
@@ -597,6 +602,99 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     return 0
 
 
+def run_shared(args, torch, hcmix, inputs, dev):
+    """The channel-shared stack at the LM shape: one hcmix_shared_stack_forward
+    and one hcmix_shared_stack_backward call per step, replayed as a graph.
+    HBM-bound, so its roofline is bytes: the forward kernel reads x_0 and
+    writes every layer's output, (L + 1) activations; the backward kernel
+    reads dy and every layer input and writes dx, (L + 2) activations, plus
+    the L fp32 table gradients (n^2 each).  Each is timed with HIP events
+    around its own launches on the stream they run on."""
+    B, n, w, L = 64, 256, 512, 16
+    if args.batch > 0:
+        B = args.batch
+    s = inputs.make_shared_stack(B, n, w, L, True, "bf16", kind="zipf_bytes", seed=0)
+    dt = torch.bfloat16
+    x0 = torch.from_numpy(s.x).to(dt).to(dev)
+    dy = torch.from_numpy(s.dy).to(dt).to(dev)
+    tabs = [torch.from_numpy(t).to(dev) for t in s.tables]
+    outs = [torch.empty_like(x0) for _ in range(L)]
+    dx = torch.empty_like(x0)
+    dts = [torch.empty((n, n), dtype=torch.float32, device=dev) for _ in range(L)]
+    nbytes = hcmix.load().hcmix_shared_stack_backward_workspace_bytes(B, n, w, L, hcmix.HCMIX_BF16)
+    wsp = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    xs = [x0, *outs]
+
+    def fwd():
+        hcmix.shared_stack_forward(x0, tabs, s.layers, True, outs=outs)
+
+    def bwd():
+        hcmix.shared_stack_backward(xs[:L], tabs, s.layers, dy, True, dx=dx, dtables=dts,
+                                    workspace=wsp)
+
+    def step():
+        fwd()
+        bwd()
+
+    stream = torch.cuda.Stream(device=dev)
+    with torch.cuda.stream(stream):
+        step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
+        per = {"forward": [], "backward": []}
+        for _ in range(args.kernel_reps):
+            for name, fn in (("forward", fwd), ("backward", bwd)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn()
+                b.record(stream)
+                per[name].append((a, b))
+        torch.cuda.synchronize()
+    act = B * n * w * 2
+    bytes_fwd = (L + 1) * act + L * n * 8
+    bytes_bwd = (L + 2) * act + L * n * 8 + L * n * n * 4
+    us = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) * 1e3 for k, v in per.items()}
+    entries = {}
+    for name, nb, kname in (("forward", bytes_fwd, "shared_fwd_kernel"),
+                            ("backward", bytes_bwd, "shared_bwd_kernel + shared_dt_reduce_kernel")):
+        gbs = nb / (us[name] * 1e-6) / 1e9
+        entries[name] = {"bound": "hbm", "kernel": f"{kname} (one {name} call, all {L} layers)",
+                         "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": profiled_traffic(args.workload, kname),
+                         "avg_launch_us": round(us[name], 2), "algorithmic_bytes": nb}
+    dom = "backward" if us["backward"] >= us["forward"] else "forward"
+    out = {
+        "metric": METRIC, "value": round(B * n * L * args.steps / t, 1), "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(t / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"shared256: {WORKLOADS['shared256']}", "batch": B, "n": n,
+                   "width": w, "layers": L, "mode": "causal", "graph": True},
+        "pct_hbm": round((bytes_fwd + bytes_bwd) / t * args.steps / 1e9 / PEAK_HBM_GBS * 100, 2),
+        "roofline": entries[dom],
+        "roofline_" + ("forward" if dom == "backward" else "backward"):
+            entries["forward" if dom == "backward" else "backward"],
+    }
+    if args.cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_shared(s, n, L, args.cpu_windows)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def run_lm_step(args, torch, hcmix, inputs, dev):
     """The lm256 stack inside a whole training step of the byte-level language
     model: embedding (library gather), the 16-layer stack forward, the 256-way
@@ -828,7 +926,7 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def timed_oracle_legs(run, B, n, L, windows, what):
+def timed_oracle_legs(run, B, n, L, windows, what, single_threaded=False):
     """Time `run(k)` (the oracle over k windows, every layer, forward and
     backward) on all host threads and on one thread.
 
@@ -836,7 +934,9 @@ def timed_oracle_legs(run, B, n, L, windows, what):
     from a timed pilot of a few windows; when the whole workload takes less
     than that, it is run repeatedly (the sample then says how many passes).
     One thread: one window, repeated until about 5 s have passed (at most
-    once more than needed), so the whole baseline stays within about 35 s."""
+    once more than needed), so the whole baseline stays within about 35 s.
+    An oracle that runs on one thread anyway (single_threaded) gets the first
+    leg only, reported with one core."""
     import oracle
 
     passes = 1
@@ -854,12 +954,14 @@ def timed_oracle_legs(run, B, n, L, windows, what):
         dt += run(windows)
         done += 1
     passes = done
-    threads = oracle.num_threads()
+    threads = 1 if single_threaded else oracle.num_threads()
     sample = (f"{windows} of the workload's {B} windows" if windows < B
               else f"all {B} windows") + (f", {passes} passes" if passes > 1 else "")
     out = {"value": round(passes * windows * n * L / dt, 1), "unit": UNIT, "cores": threads,
            "kind": "oracle", "sample": f"{sample}{what}, {dt:.1f} s", "cpu_model": cpu_model(),
            "host_cpus": os.cpu_count()}
+    if single_threaded:
+        return out
     oracle.set_num_threads(1)
     try:
         dt1, done1 = 0.0, 0
@@ -918,6 +1020,22 @@ def cpu_baseline_lm(s, table, head_w, n, w, L, V, windows):
     return timed_oracle_legs(run, B, n, L, windows,
                              f": embedding, all {L} layers, head and cross-entropy, "
                              "forward+backward")
+
+
+def cpu_baseline_shared(s, n, L, windows):
+    """The channel-shared oracle (oracle/shared_mix.py, float64) on a bounded
+    sample of the workload, all host threads and one thread."""
+    from oracle import shared_mix
+
+    def run(k):
+        t0 = time.perf_counter()
+        xs = shared_mix.stack_forward(s.x[:k], s.tables, s.layers, True)
+        shared_mix.stack_backward(xs, s.tables, s.layers, s.dy[:k], True)
+        return time.perf_counter() - t0
+
+    return timed_oracle_legs(run, s.x.shape[0], n, L, windows,
+                             f", all {L} layers, forward+backward (numpy, one thread)",
+                             single_threaded=True)
 
 
 if __name__ == "__main__":

@@ -302,6 +302,49 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
                                const void* const* w_self, const void* const* w_off, void* cache,
                                size_t cache_bytes, void* y, void* stream);
 
+/* ---- Channel-shared mixing: the two maps as per-position scalars ----
+ *
+ * The sparse layer of Eq. (1) with both linear maps reduced to scalars per
+ * position, shared by every channel and taken from an n x n table T_l per
+ * layer (the paper's parameter totals, Section 5's cost tables, count n^2
+ * mixing parameters per layer, and its dense schedule uses the whole table):
+ *   y[t][i][c] = T_l[i][i] x[t][i][c] + m(i) T_l[i][p(i)] x[t][p(i)][c]
+ * with partner p and mask m exactly as for hcmix_forward (hypercube layer of
+ * dimension hcmix_dim(layer, n), or HCMIX_LAYER_NEAR in causal mode).  Entries
+ * of T_l off the layer's links are never read.
+ *
+ * tables: host array of num_layers device pointers to fp32 [n][n] tables
+ * (row = receiving position).  x, xs[l], dy, dx: [batch][n][width] in dtype
+ * (bf16: fp32 arithmetic, every layer's output rounded once to bf16).  The
+ * whole stack runs in one launch per direction, each window's slice of
+ * channels staying on chip through every layer.  Shapes: n a power of two
+ * from 2 to 256, width a multiple of 64 (bf16) or 32 (fp32), at most 64
+ * layers (HCMIX_ERR_UNSUPPORTED otherwise); activations 16-byte aligned,
+ * tables 4-byte aligned.  Other errors as for the stacks above. */
+hcmix_status hcmix_shared_stack_forward(int64_t batch, int64_t n, int64_t width,
+                                        int32_t num_layers, const int32_t* layers, int32_t mode,
+                                        int32_t dtype, const void* x, const float* const* tables,
+                                        void* const* xs, void* stream);
+
+/* Backward: dx (gradient of x_0, in dtype) and the table gradients
+ *   dT_l[i][i]    = sum over (t, c) of g[t][i][c] x_l[t][i][c]
+ *   dT_l[i][p(i)] = m(i) sum over (t, c) of g[t][i][c] x_l[t][p(i)][c]
+ * (g the gradient of layer l's output), every other entry 0; dtables[l] fp32
+ * [n][n], overwritten (accumulate == 0) or added to on the link entries only.
+ * xs_in: the layer inputs x_0 .. x_{L-1} as hcmix_shared_stack_forward wrote
+ * them.  Sums run in a fixed order (bitwise-repeatable) through a workspace of
+ * hcmix_shared_stack_backward_workspace_bytes (256-byte aligned) holding
+ * per-block partial sums. */
+size_t hcmix_shared_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                                   int32_t num_layers, int32_t dtype);
+
+hcmix_status hcmix_shared_stack_backward(int64_t batch, int64_t n, int64_t width,
+                                         int32_t num_layers, const int32_t* layers, int32_t mode,
+                                         int32_t dtype, const void* const* xs_in,
+                                         const float* const* tables, const void* dy, void* dx,
+                                         float* const* dtables, int32_t accumulate,
+                                         void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- Causal multi-head softmax attention (the hybrids' attention layers) ----
  *
  * The hybrid schedules (Section 3.3; the window-256 hybrid of Appendix A keeps

@@ -1004,3 +1004,127 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
+
+// ---- channel-shared mixing stack ----
+
+// Shape checks of the channel-shared entry points (layer codes checked per
+// layer by the caller).
+hcmix_status check_shared(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                          const int32_t* layers, int32_t mode, int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers) return HCMIX_ERR_INVALID_VALUE;
+  for (int l = 0; l < num_layers; l++) {
+    hcmix_status st = check_shape(batch, n, width, layers[l], mode, HCMIX_F32);
+    if (st != HCMIX_OK) return st;
+  }
+  if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return HCMIX_ERR_INVALID_VALUE;
+  if (!shared_stack_eligible(n, width, num_layers, (int32_t)elem_size(dtype)))
+    return HCMIX_ERR_UNSUPPORTED;
+  return HCMIX_OK;
+}
+
+hcmix_status hcmix_shared_stack_forward(int64_t batch, int64_t n, int64_t width,
+                                        int32_t num_layers, const int32_t* layers, int32_t mode,
+                                        int32_t dtype, const void* x, const float* const* tables,
+                                        void* const* xs, void* stream) {
+  if (!x || !layers || !tables || !xs) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_shared(batch, n, width, num_layers, layers, mode, dtype);
+  if (st != HCMIX_OK) return st;
+  const size_t act = (size_t)(batch * n * width) * elem_size(dtype);
+  const size_t tab = (size_t)(n * n) * sizeof(float);
+  for (int l = 0; l < num_layers; l++) {
+    if (!tables[l] || !aligned(tables[l], 4)) return tables[l] ? HCMIX_ERR_UNSUPPORTED
+                                                               : HCMIX_ERR_INVALID_VALUE;
+    const Span ins[1] = {{x, act}};
+    const Span outs[1] = {{xs[l], act}};
+    st = check_spans(ins, 1, outs, 1, 16);
+    if (st != HCMIX_OK) return st;
+    for (int j = 0; j < num_layers; j++) {
+      if (j != l && overlaps(xs[l], act, xs[j], act)) return HCMIX_ERR_INVALID_VALUE;
+      if (overlaps(xs[l], act, tables[j], tab)) return HCMIX_ERR_INVALID_VALUE;
+    }
+  }
+  SharedFwdArgs a = {};
+  a.x0 = x;
+  for (int l = 0; l < num_layers; l++) {
+    a.xs[l] = xs[l];
+    a.tab[l] = tables[l];
+    a.dim[l] = hcmix_dim(layers[l], n);   // -1 for the local layer
+  }
+  a.n = (int)n;
+  a.width = (int)width;
+  a.num_layers = num_layers;
+  a.bidir = mode == HCMIX_BIDIR;
+  hipError_t e = launch_shared_forward(a, (int)batch, (int)elem_size(dtype), (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+size_t hcmix_shared_stack_backward_workspace_bytes(int64_t batch, int64_t n, int64_t width,
+                                                   int32_t num_layers, int32_t dtype) {
+  if (num_layers < 1 || num_layers > kMaxLayers) return 0;
+  if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return 0;
+  if (check_shape(batch, n, width, 0, HCMIX_BIDIR, HCMIX_F32) != HCMIX_OK) return 0;
+  if (!shared_stack_eligible(n, width, num_layers, (int32_t)elem_size(dtype))) return 0;
+  return align256(shared_partial_bytes(batch, n, width, num_layers, (int32_t)elem_size(dtype)));
+}
+
+hcmix_status hcmix_shared_stack_backward(int64_t batch, int64_t n, int64_t width,
+                                         int32_t num_layers, const int32_t* layers, int32_t mode,
+                                         int32_t dtype, const void* const* xs_in,
+                                         const float* const* tables, const void* dy, void* dx,
+                                         float* const* dtables, int32_t accumulate,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!layers || !xs_in || !tables || !dy || !dx || !dtables || !workspace)
+    return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_shared(batch, n, width, num_layers, layers, mode, dtype);
+  if (st != HCMIX_OK) return st;
+  const size_t need =
+      shared_partial_bytes(batch, n, width, num_layers, (int32_t)elem_size(dtype));
+  if (workspace_bytes < need) return HCMIX_ERR_INVALID_VALUE;
+  const size_t act = (size_t)(batch * n * width) * elem_size(dtype);
+  const size_t tab = (size_t)(n * n) * sizeof(float);
+  // outputs: dx, the workspace, every dtables[l]; inputs: dy, every xs_in[l]
+  // and tables[l]; no output may overlap an input or another output
+  const Span fixed_outs[2] = {{dx, act}, {workspace, need}};
+  {
+    const Span ins[1] = {{dy, act}};
+    st = check_spans(ins, 1, fixed_outs, 2, 16);
+    if (st != HCMIX_OK) return st;
+  }
+  for (int l = 0; l < num_layers; l++) {
+    if (!xs_in[l] || !tables[l] || !dtables[l]) return HCMIX_ERR_INVALID_VALUE;
+    const Span ins[2] = {{xs_in[l], act}, {tables[l], tab}};
+    const Span outs[3] = {fixed_outs[0], fixed_outs[1], {dtables[l], tab}};
+    st = check_spans(ins, 2, outs, 3, 4);
+    if (st != HCMIX_OK) return st;
+    if (!aligned(xs_in[l], 16)) return HCMIX_ERR_UNSUPPORTED;
+    for (int j = 0; j < num_layers; j++) {
+      if (j == l) continue;
+      if (overlaps(dtables[l], tab, dtables[j], tab) || overlaps(dtables[l], tab, tables[j], tab) ||
+          overlaps(dtables[l], tab, xs_in[j], act))
+        return HCMIX_ERR_INVALID_VALUE;
+      if (overlaps(dx, act, xs_in[j], act) || overlaps(dx, act, tables[j], tab))
+        return HCMIX_ERR_INVALID_VALUE;
+    }
+  }
+  if (!aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  SharedBwdArgs a = {};
+  SharedReduceArgs r = {};
+  for (int l = 0; l < num_layers; l++) {
+    a.xs[l] = xs_in[l];
+    a.tab[l] = tables[l];
+    a.dim[l] = r.dim[l] = hcmix_dim(layers[l], n);
+    r.dt[l] = dtables[l];
+  }
+  a.dy = dy;
+  a.dx = dx;
+  a.partial = (float*)workspace;
+  a.n = r.n = (int)n;
+  a.width = (int)width;
+  a.num_layers = r.num_layers = num_layers;
+  a.bidir = r.bidir = mode == HCMIX_BIDIR;
+  r.partial = (const float*)workspace;
+  r.accumulate = accumulate != 0;
+  hipError_t e = launch_shared_backward(a, r, (int)batch, (int)elem_size(dtype),
+                                        (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}

@@ -137,6 +137,47 @@ hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hi
 hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
                                  bool bidir, hipStream_t st);
 
+// ---- channel-shared mixing stack (per-position scalars from n x n tables) ----
+// y[t][i][c] = T[i][i] x[t][i][c] + m(i) T[i][p(i)] x[t][p(i)][c]; tables fp32
+// [n][n]; activations bf16 or fp32; n a power of two up to kSharedMaxN; width a
+// multiple of 64 (bf16) or 32 (fp32).  One block per window and slice of
+// channels, the tile resident in LDS through every layer.
+
+constexpr int kSharedMaxLayers = 64;
+constexpr int kSharedMaxN = 256;
+
+struct SharedFwdArgs {
+  const void* x0;
+  void* xs[kSharedMaxLayers];          // x_1 .. x_L
+  const float* tab[kSharedMaxLayers];
+  int dim[kSharedMaxLayers];           // hypercube dimension, or -1 for the local layer
+  int n, width, num_layers, bidir;
+};
+
+struct SharedBwdArgs {
+  const void* xs[kSharedMaxLayers];    // inputs x_0 .. x_{L-1}
+  const float* tab[kSharedMaxLayers];
+  int dim[kSharedMaxLayers];
+  const void* dy;
+  void* dx;
+  float* partial;                      // [L][blocks][n][2] per-block sums of the table gradient
+  int n, width, num_layers, bidir;
+};
+
+struct SharedReduceArgs {
+  const float* partial;
+  float* dt[kSharedMaxLayers];         // fp32 [n][n] table gradients
+  int dim[kSharedMaxLayers];
+  int n, blocks, num_layers, bidir, accumulate;
+};
+
+bool shared_stack_eligible(int64_t n, int64_t width, int32_t num_layers, int32_t elem_bytes);
+size_t shared_partial_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
+                            int32_t elem_bytes);
+hipError_t launch_shared_forward(const SharedFwdArgs& a, int batch, int elem_bytes, hipStream_t st);
+hipError_t launch_shared_backward(const SharedBwdArgs& a, const SharedReduceArgs& r, int batch,
+                                  int elem_bytes, hipStream_t st);
+
 // ---- decode step (one position of every window through one layer) ----
 // x_in / x_partner / record / out are row bases of window 0; window b is at
 // + b * stride elements.  x_partner null: the position takes no partner.

@@ -35,7 +35,8 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_embedding_backward_workspace_bytes", "hcmix_embedding_backward",
            "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy",
            "hcmix_head_backward_workspace_bytes", "hcmix_head_backward",
-           "hcmix_backward_no_alloc")
+           "hcmix_backward_no_alloc", "hcmix_shared_stack_forward",
+           "hcmix_shared_stack_backward_workspace_bytes", "hcmix_shared_stack_backward")
 
 _lib = None
 
@@ -116,6 +117,14 @@ def load():
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
                                           vp]
         lib.hcmix_decode_step.restype = i32
+        lib.hcmix_shared_stack_forward.argtypes = [i64, i64, i64, i32, ip, i32, i32, vp, pp, pp,
+                                                   vp]
+        lib.hcmix_shared_stack_forward.restype = i32
+        lib.hcmix_shared_stack_backward_workspace_bytes.argtypes = [i64, i64, i64, i32, i32]
+        lib.hcmix_shared_stack_backward_workspace_bytes.restype = sz
+        lib.hcmix_shared_stack_backward.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, vp,
+                                                    vp, pp, i32, vp, sz, vp]
+        lib.hcmix_shared_stack_backward.restype = i32
         _lib = lib
     return _lib
 
@@ -623,6 +632,69 @@ def head_backward(x, w, dlogits, gx=None, dw=None, with_gx=True, with_dw=True,
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_head_backward")
     return (gx if want_gx else None), (dw if want_dw else None)
+
+
+def _tables(ts, name, n, dev, count):
+    if len(ts) < count:
+        raise ValueError(f"{name}: {len(ts)} tables, expected {count}")
+    for k in range(count):
+        _need(ts[k], f"{name}[{k}]", (n, n), torch.float32, dev)
+
+
+def shared_stack_forward(x, tables, layers, causal, outs=None):
+    """Channel-shared stack: y_i = T[i][i] x_i + m(i) T[i][p(i)] x_p(i) per
+    layer, tables fp32 [n, n]; returns [x_0, x_1, ..., x_L]."""
+    L = len(layers)
+    shape = _act_shape(x)
+    batch, n, width = shape
+    dt = _act_dtype(x)
+    _need(x, "x", None, dt)
+    dev = x.device
+    _tables(tables, "tables", n, dev, L)
+    if outs is None:
+        outs = [torch.empty_like(x) for _ in range(L)]
+    _acts(outs, "outs", shape, dt, dev, L)
+    _gpu(dev)
+    rc = load().hcmix_shared_stack_forward(batch, n, width, L, _layers(layers), int(bool(causal)),
+                                           _dtype_code(x), _ptr(x), _ptrs(tables[:L]),
+                                           _ptrs(outs[:L]), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_shared_stack_forward")
+    return [x, *outs[:L]]
+
+
+def shared_stack_backward(xs, tables, layers, dy, causal, dx=None, dtables=None,
+                          accumulate=False, workspace=None):
+    """Backward of ``shared_stack_forward`` from the saved inputs xs[0..L-1]:
+    returns (dx, [dT_l]) with dT_l fp32 [n, n] (zero off the layer's links)."""
+    L = len(layers)
+    x0 = xs[0]
+    shape = _act_shape(x0, "xs[0]")
+    batch, n, width = shape
+    dt = _act_dtype(x0, "xs[0]")
+    dev = x0.device
+    _acts(xs, "xs", shape, dt, dev, L)
+    _tables(tables, "tables", n, dev, L)
+    _need(dy, "dy", shape, dt, dev)
+    if dx is None:
+        dx = torch.empty_like(x0)
+    _need(dx, "dx", shape, dt, dev)
+    if dtables is None:
+        dtables = [torch.empty((n, n), dtype=torch.float32, device=dev) for _ in range(L)]
+    _tables(dtables, "dtables", n, dev, L)
+    _gpu(dev)
+    if workspace is None:
+        nbytes = load().hcmix_shared_stack_backward_workspace_bytes(batch, n, width, L,
+                                                                    _dtype_code(x0))
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    rc = load().hcmix_shared_stack_backward(batch, n, width, L, _layers(layers),
+                                            int(bool(causal)), _dtype_code(x0), _ptrs(xs[:L]),
+                                            _ptrs(tables[:L]), _ptr(dy), _ptr(dx),
+                                            _ptrs(dtables[:L]), int(bool(accumulate)),
+                                            _ptr(workspace), _bytes(workspace), _stream(x0))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_shared_stack_backward")
+    return dx, dtables
 
 
 class Attention(torch.autograd.Function):

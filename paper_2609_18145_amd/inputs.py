@@ -17,6 +17,8 @@ Workloads (shapes and value distributions of the paper's experiments):
             frequencies over a shuffled byte ranking, embedded through an N(0,1) table
             (stand-in for the character-level corpora of Section 5, which are not used)
   long4096  n=4096, width 1024, batch 8,  24 layers, bf16, causal; N(0,1) inputs
+  shared256 n=256, width 512, batch 64, 16 layers, bf16, causal; the lm256 inputs with the
+            channel-shared layer: one n x n table per layer, entries N(0, 1/2)
 Weights are N(0, 1/width); the upstream gradient dY is N(0,1).
 """
 from __future__ import annotations
@@ -117,3 +119,37 @@ def make_layer(batch: int, n: int, width: int, dtype: str = "bf16", seed: int = 
     wo = _finish(rng.standard_normal((width, width)) * std, dtype)
     dy = _finish(rng.standard_normal((batch, n, width)), dtype)
     return x, ws, wo, dy
+
+
+@dataclass
+class SharedInputs:
+    x: np.ndarray                      # [batch, n, width] float32
+    tables: list = field(default_factory=list)   # per layer [n, n] float32
+    layers: list = field(default_factory=list)
+    dy: np.ndarray | None = None
+    causal: bool = True
+    dtype: str = "bf16"
+
+
+def make_shared_stack(batch: int, n: int, width: int, num_layers: int, causal: bool = True,
+                      dtype: str = "bf16", kind: str = "normal", seed: int = 0,
+                      layers=None) -> SharedInputs:
+    """Inputs of the channel-shared stack: x (drawn as in make_stack), then one
+    n x n table per layer with N(0, 1/2) entries (a position and its partner
+    then keep the activations' scale on average), then dY.  Tables stay fp32."""
+    rng = np.random.default_rng(seed)
+    if kind == "normal":
+        x = rng.standard_normal((batch, n, width))
+    elif kind == "zipf_bytes":
+        seq = zipf_byte_tokens(rng, (batch, n + 1))
+        table = rng.standard_normal((256, width))
+        x = table[seq[:, :n]]
+    else:
+        raise ValueError(kind)
+    tables = [(rng.standard_normal((n, n)) * np.sqrt(0.5)).astype(np.float32)
+              for _ in range(num_layers)]
+    dy = _finish(rng.standard_normal((batch, n, width)), dtype)
+    if layers is None:
+        layers = list(range(num_layers))
+    return SharedInputs(x=_finish(x, dtype), tables=tables, layers=list(layers), dy=dy,
+                        causal=causal, dtype=dtype)

@@ -412,3 +412,50 @@ def test_stack_backward_data_workspace_query():
     assert q(32, 4, hcmix.HCMIX_F32) == 0
     assert q(128, 0, hcmix.HCMIX_BF16) == 0
     assert q(128, 4, 7) == 0
+
+
+def shared_fwd(batch=2, n=16, width=64, L=2, layers=(0, 1), mode=1, dtype=1, x=P[0],
+               tables=(FP[1], FP[2]), xs=(P[3], P[4])):
+    lib = hcmix.load()
+    lay = (ctypes.c_int32 * len(layers))(*layers)
+    tp = (ctypes.c_void_p * len(tables))(*[ctypes.cast(t, ctypes.c_void_p) if t is not None
+                                           else None for t in tables])
+    op = (ctypes.c_void_p * len(xs))(*[p.value if p is not None else None for p in xs])
+    return lib.hcmix_shared_stack_forward(batch, n, width, L, lay, mode, dtype, x, tp, op, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=12), INVALID), (dict(batch=0), INVALID), (dict(L=0), INVALID),
+    (dict(x=None), INVALID), (dict(tables=(FP[1], None)), INVALID),
+    (dict(xs=(P[3], P[0])), INVALID),                 # an output aliases x
+    (dict(xs=(P[3], P[3])), INVALID),                 # two outputs alias
+    (dict(layers=(-1, 0), mode=0), INVALID),          # the local layer is causal only
+    (dict(n=512), UNSUPPORTED),                       # windows above 256
+    (dict(width=96), UNSUPPORTED),                    # bf16 slices of 64 channels
+    (dict(dtype=0, width=48), UNSUPPORTED),           # fp32 slices of 32 channels
+    (dict(x=ctypes.c_void_p(0x100008)), UNSUPPORTED),
+])
+def test_shared_forward_rejects_bad_arguments(kw, code):
+    assert shared_fwd(**kw) == code
+
+
+def test_shared_backward_workspace_and_rejections():
+    lib = hcmix.load()
+    nb = lib.hcmix_shared_stack_backward_workspace_bytes(64, 256, 512, 16, 1)
+    # one fp32 pair per (layer, block, position): 16 layers x (64 windows x 8 slices) x 256 x 2
+    assert nb == 16 * 64 * 8 * 256 * 2 * 4
+    assert lib.hcmix_shared_stack_backward_workspace_bytes(64, 512, 512, 16, 1) == 0
+    assert lib.hcmix_shared_stack_backward_workspace_bytes(64, 256, 96, 16, 1) == 0
+    lay = (ctypes.c_int32 * 2)(0, 1)
+    vp = lambda *ps: (ctypes.c_void_p * len(ps))(*[p.value for p in ps])   # noqa: E731
+    nb = lib.hcmix_shared_stack_backward_workspace_bytes(2, 16, 64, 2, 1)
+    ws = ctypes.c_void_p(0x4000000)
+    call = lambda **k: lib.hcmix_shared_stack_backward(   # noqa: E731
+        2, 16, 64, 2, lay, 1, 1, k.get("xs", vp(P[0], P[1])), vp(P[2], P[3]),
+        k.get("dy", P[4]), k.get("dx", P[5]), k.get("dts", vp(P[6], P[7])), 0,
+        k.get("ws", ws), k.get("wsb", nb), None)
+    assert call(dx=P[4]) == INVALID                   # dx aliases dy
+    assert call(dts=vp(P[6], P[6])) == INVALID        # two table gradients alias
+    assert call(dts=vp(P[6], P[2])) == INVALID        # a table gradient aliases a table
+    assert call(wsb=nb - 4) == INVALID
+    assert call(ws=ctypes.c_void_p(0x4000010)) == UNSUPPORTED

@@ -138,3 +138,20 @@ def test_decode_checks():
     refused(hcmix.decode_step, x, [w] * L, [w] * L, [0, 1], N, 0, cache, out=z(B, W + 64),
             match="out")
     refused(hcmix.decode_step, x, [w] * L, [w] * L, [0, 1], N, 0, cache, match="GPU")
+
+
+def test_shared_stack_checks():
+    L, n = 2, N
+    x = z(B, n, W)
+    t = z(n, n, dtype=f32)
+    refused(hcmix.shared_stack_forward, x, [t], [0, 1], True, match="tables")
+    refused(hcmix.shared_stack_forward, x, [t, z(n, n)], [0, 1], True, match="tables")   # bf16
+    refused(hcmix.shared_stack_forward, x, [t, z(n, n + 1, dtype=f32)], [0, 1], True,
+            match="tables")
+    refused(hcmix.shared_stack_forward, x, [t, t], [0, 1], True, outs=[x], match="outs")
+    refused(hcmix.shared_stack_forward, x, [t, t], [0, 1], True, match="GPU")
+    refused(hcmix.shared_stack_backward, [x, x], [t, t], [0, 1], z(B, n, W + 64), True,
+            match="dy")
+    refused(hcmix.shared_stack_backward, [x, x], [t, t], [0, 1], x, True,
+            dtables=[t, z(n, n)], match="dtables")
+    refused(hcmix.shared_stack_backward, [x, x], [t, t], [0, 1], x, True, match="GPU")
