@@ -83,9 +83,9 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--attention", default="native", choices=["native", "sdpa"],
                     help="hybrid workloads: the library's attention core, or PyTorch SDPA")
-    ap.add_argument("--proj", default="torch", choices=["library", "torch"],
+    ap.add_argument("--proj", default="library", choices=["library", "torch"],
                     help="hybrids: the attention layers' projections in the library's kernels "
-                         "or as PyTorch GEMMs")
+                         "(the whole step in library calls) or as PyTorch GEMMs under autograd")
     ap.add_argument("--head-grad", default="library", choices=["library", "torch"],
                     help="lm256_step: the head's input and weight gradients in the library's "
                          "kernels or as PyTorch GEMMs")
@@ -330,12 +330,15 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     or "hy256", the paper's window-256 hybrid schedule string (local layers,
     one causal jump per scale, attention at two of sixteen; weights are the
     lm256 workload's first 14).  An attention layer is the QKV projection and
-    the output projection (PyTorch GEMMs) around the library's causal attention
-    core (hcmix_attention_forward / _backward; --attention sdpa swaps in
-    PyTorch's scaled-dot-product attention); the sparse segments are hcmix
-    stack calls: forward per segment, the dX chain per segment
-    (hcmix_stack_backward_data), and the weight gradients of every sparse
-    layer in one hcmix_stack_weight_gradients call at the end.  Forward and backward are chained by hand
+    the output projection (the library's linear maps, hcmix_linear_forward /
+    _backward) around the library's causal attention core
+    (hcmix_attention_forward / _backward): by default the whole step is
+    library calls (paper_2609_18145_amd.hybrid); --proj torch runs the
+    projections as PyTorch GEMMs and --attention sdpa swaps in PyTorch's
+    scaled-dot-product attention, both under torch autograd, for comparison.
+    The sparse segments are hcmix stack calls: forward per segment, the dX
+    chain per segment (hcmix_stack_backward_data), and the weight gradients of
+    every sparse layer in one hcmix_stack_weight_gradients call at the end.  Forward and backward are chained by hand
     so that every segment is timed with HIP events on one stream; the line
     reports the sparse layers' share of the step and their own throughput."""
     import torch.nn.functional as F
@@ -417,19 +420,18 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             return F.scaled_dot_product_attention(q, k, v, is_causal=True)
 
     class Linear(torch.autograd.Function):
-        """y = x W^T.  --proj library: the library's two products of a linear
-        map's backward (hcmix_head_backward: dx = g W, dW = g^T x in a fixed
-        order), and the forward as the first of them on W^T (transposed once
-        per call).  --proj torch: PyTorch GEMMs, the weight gradient's K = rows
-        split into 16 batched products (a single GEMM with K = 16384 and a
-        512-wide output leaves most of the chip idle in its kernel choice)."""
+        """y = x W^T under autograd (the comparison paths: --proj torch or
+        --attention sdpa).  --proj library: the library's linear map
+        (hcmix_linear_forward / _backward); --proj torch: PyTorch GEMMs, the
+        weight gradient's K = rows split into 16 batched products (a single GEMM
+        with K = 16384 and a 512-wide output leaves most of the chip idle in its
+        kernel choice)."""
 
         @staticmethod
         def forward(ctx, x2, wt):
             ctx.save_for_backward(x2, wt)
             if args.proj == "library":
-                y, _ = hcmix.head_backward(None, wt.t().contiguous(), x2, with_dw=False)
-                return y
+                return hcmix.linear_forward(x2.contiguous(), wt)
             return torch.matmul(x2, wt.t())
 
         @staticmethod
@@ -437,7 +439,7 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             x2, wt = ctx.saved_tensors
             g = g.contiguous()
             if args.proj == "library":
-                dx, dw = hcmix.head_backward(x2, wt, g)
+                dx, dw = hcmix.linear_backward(x2, wt, g)
                 return dx, dw.to(wt.dtype)
             kch = 16
             r = x2.shape[0] // kch
@@ -458,9 +460,44 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     stream = torch.cuda.current_stream(dev)
     ev = torch.cuda.Event
 
+    native = args.proj == "library" and args.attention == "native"
+    from paper_2609_18145_amd.hybrid import HybridStack
+    hstack = HybridStack(sched, ws[:Ls], wo[:Ls], attn_w[:nattn], heads)
+
+    def step_native(times):
+        """One step, every part a library call (paper_2609_18145_amd.hybrid):
+        sparse stacks, linear maps and attention cores forward, the reverse
+        backward (sparse dX chains, attention backward products), then all
+        sparse weight gradients in one call."""
+        cur = torch.cuda.current_stream(dev)
+
+        def timed(kind, phase, fn):
+            if times is None:
+                return fn()
+            e0, e1 = ev(enable_timing=True), ev(enable_timing=True)
+            e0.record(cur)
+            out = fn()
+            e1.record(cur)
+            times.append((kind, phase, e0, e1))
+            return out
+
+        hstack._saved = []
+        x = x0
+        for k, (kind, _) in enumerate(hstack.segments):
+            x = timed(kind, "fwd", lambda: hstack.forward_segment(k, x))
+        hstack._dw_in = []
+        hstack.dw_attn = [None] * nattn
+        g = dy
+        for k in reversed(range(len(hstack.segments))):
+            g = timed(hstack.segments[k][0], "bwd", lambda: hstack.backward_segment(k, g))
+        timed("sparse", "dw", hstack.sparse_weight_gradients)
+        return g
+
     def step(times):
         """One step; with `times` a list, every segment is bracketed by events
         on the current stream (left out under graph capture, times=None)."""
+        if native:
+            return step_native(times)
         cur = torch.cuda.current_stream(dev)
 
         def bracket():
@@ -586,7 +623,9 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}", "batch": B, "n": n,
                    "width": w, "layers": Ls, "attention_layers": nattn, "mode": "causal",
-                   "graph": bool(args.graph), "attention_backend": backend["name"]},
+                   "graph": bool(args.graph), "attention_backend": backend["name"],
+                   "projections": "hcmix_linear (library kernels)" if args.proj == "library"
+                   else "PyTorch GEMMs"},
         "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
                    "step_ms_eager": round(total_eager / args.steps * 1e3, 4),
                    "sparse_ms": round(sparse / args.steps * 1e3, 4),

@@ -376,6 +376,29 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
                                       const void* qkv, const void* out, const float* lse,
                                       const void* dout, void* dqkv, void* stream);
 
+/* ---- Linear maps: the attention layers' projections in the hybrids ----
+ *
+ * The hybrid schedules' attention layers (Section 3.3) project each position
+ * to queries, keys and values and back: plain linear maps y = x W^T around the
+ * attention core above.  bf16 in and out, fp32 accumulation.
+ *   x [rows][in_width], W [out_width][in_width], y [rows][out_width].
+ * rows even; in_width and out_width multiples of 64 (HCMIX_ERR_UNSUPPORTED
+ * otherwise); bf16 pointers 16-byte aligned.  Errors as above. */
+hcmix_status hcmix_linear_forward(int64_t rows, int64_t in_width, int64_t out_width,
+                                  const void* x, const void* w, void* y, void* stream);
+
+/* Backward of the linear map: dx = dy W (bf16 [rows][in_width]) and
+ * dw (+)= dy^T x (fp32 [out_width][in_width], row ranges summed in a fixed
+ * order through a workspace of hcmix_linear_backward_workspace_bytes, 256-byte
+ * aligned; bitwise-repeatable).  Either output may be NULL (not both); x is
+ * read only for dw.  accumulate != 0 adds to dw. */
+size_t hcmix_linear_backward_workspace_bytes(int64_t rows, int64_t in_width, int64_t out_width);
+
+hcmix_status hcmix_linear_backward(int64_t rows, int64_t in_width, int64_t out_width,
+                                   const void* x, const void* w, const void* dy, void* dx,
+                                   float* dw, int32_t accumulate, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
 /* ---- Token embedding, output head and cross-entropy (language-model workloads) ----
  *
  * Section 5 trains character-level language models and reports bits per

@@ -1128,3 +1128,70 @@ hcmix_status hcmix_shared_stack_backward(int64_t batch, int64_t n, int64_t width
                                         (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
+
+// ---- linear maps (the hybrids' attention projections) ----
+
+hcmix_status check_linear(int64_t rows, int64_t in_width, int64_t out_width) {
+  if (rows < 1 || in_width < 1 || out_width < 1) return HCMIX_ERR_INVALID_VALUE;
+  if (rows > kMaxRows || in_width > (1 << 16) || out_width > (1 << 16))
+    return HCMIX_ERR_INVALID_VALUE;
+  if (rows % 2 || in_width % 64 || out_width % 64) return HCMIX_ERR_UNSUPPORTED;
+  return HCMIX_OK;
+}
+
+hcmix_status hcmix_linear_forward(int64_t rows, int64_t in_width, int64_t out_width,
+                                  const void* x, const void* w, void* y, void* stream) {
+  if (!x || !w || !y) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_linear(rows, in_width, out_width);
+  if (st != HCMIX_OK) return st;
+  const Span ins[2] = {{x, (size_t)rows * in_width * sizeof(bf16)},
+                       {w, (size_t)out_width * in_width * sizeof(bf16)}};
+  const Span outs[1] = {{y, (size_t)rows * out_width * sizeof(bf16)}};
+  st = check_spans(ins, 2, outs, 1, 16);
+  if (st != HCMIX_OK) return st;
+  // y = x W^T: W's rows are the output columns, contiguous over the input
+  hipError_t e = launch_gemm_bf16((const bf16*)x, (const bf16*)w, (bf16*)y, (int)rows,
+                                  (int)in_width, (int)out_width, (int)in_width, (int)out_width,
+                                  /*transpose_b=*/false, (hipStream_t)stream);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}
+
+size_t hcmix_linear_backward_workspace_bytes(int64_t rows, int64_t in_width, int64_t out_width) {
+  if (check_linear(rows, in_width, out_width) != HCMIX_OK) return 0;
+  return align256(head_backward_workspace_bytes((int)rows, (int)in_width, (int)out_width));
+}
+
+hcmix_status hcmix_linear_backward(int64_t rows, int64_t in_width, int64_t out_width,
+                                   const void* x, const void* w, const void* dy, void* dx,
+                                   float* dw, int32_t accumulate, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  if (!w || !dy || (!dx && !dw) || (dw && !x)) return HCMIX_ERR_INVALID_VALUE;
+  hcmix_status st = check_linear(rows, in_width, out_width);
+  if (st != HCMIX_OK) return st;
+  const size_t need =
+      dw ? head_backward_workspace_bytes((int)rows, (int)in_width, (int)out_width) : 0;
+  if (dw && (!workspace || workspace_bytes < need)) return HCMIX_ERR_INVALID_VALUE;
+  const Span ins[3] = {{w, (size_t)out_width * in_width * sizeof(bf16)},
+                       {dy, (size_t)rows * out_width * sizeof(bf16)},
+                       {dw ? x : w, dw ? (size_t)rows * in_width * sizeof(bf16) : 0}};
+  const Span outs[3] = {{dx, dx ? (size_t)rows * in_width * sizeof(bf16) : 0},
+                        {dw, dw ? (size_t)out_width * in_width * sizeof(float) : 0},
+                        {workspace, need}};
+  st = check_spans(ins, 3, outs, 3, 4);
+  if (st != HCMIX_OK) return st;
+  if ((dw && !aligned(x, 16)) || !aligned(w, 16) || !aligned(dy, 16) || (dx && !aligned(dx, 16)))
+    return HCMIX_ERR_UNSUPPORTED;
+  if (dw && !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  // dx = dy W: W read as [out][in], rows k, so transposed into the tiles
+  if (dx)
+    e = launch_gemm_bf16((const bf16*)dy, (const bf16*)w, (bf16*)dx, (int)rows, (int)out_width,
+                         (int)in_width, (int)in_width, (int)in_width, /*transpose_b=*/true, s);
+  // dW = dy^T x, row ranges summed in a fixed order
+  if (e == hipSuccess && dw)
+    e = launch_head_backward((const bf16*)x, (const bf16*)w, (const bf16*)dy, nullptr, dw,
+                             accumulate != 0, (float*)workspace, (int)rows, (int)in_width,
+                             (int)out_width, s);
+  return e == hipSuccess ? HCMIX_OK : hip_fail(e);
+}

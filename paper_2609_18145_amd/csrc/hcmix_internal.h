@@ -49,6 +49,13 @@ hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* 
                            int rows, int width, int d, int partner_lower, int partner_upper,
                            bool transpose_b, hipStream_t st);
 
+// Plain bf16 product with the mix kernel's pipeline: out [rows][N] (row stride
+// ldo) = A [rows][K] B^T, B [N][ldb] (k contiguous), or = A B with B [K][ldb]
+// when transpose_b.  rows even, K % 64 == 0, N % 64 == 0; fp32 accumulation,
+// bf16 output.
+hipError_t launch_gemm_bf16(const bf16* A, const bf16* B, bf16* out, int rows, int K, int N,
+                            int ldb, int ldo, bool transpose_b, hipStream_t st);
+
 // Split-K weight gradients into `partial` ([splits][2][width][width] fp32),
 // then a fixed-order reduction into dws / dwo.
 // Local layer (jump 1), bf16: out_r = A_r B1^T + m(r) A_(r+delta) B2^T over

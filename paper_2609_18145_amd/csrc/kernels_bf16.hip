@@ -65,17 +65,26 @@ struct MixCfg {
 
 // One block's work: `block` indexes the (row tile, column tile) grid, dealt
 // to XCDs; `smem` is the block's dynamic LDS (MixCfg::LDS_ELEMS elements).
+//
+// The same block with no partner terms (PL = PU = false) is a plain product
+// out = A B1^T (or A B1 with TRANS_B) over any row count: the linear maps of
+// the hybrids' attention layers.  K is the contraction length and A's row
+// stride, N the output columns, ldb the row stride of B (k-contiguous B: its
+// rows are n; TRANS_B: its rows are k), ldo the output's row stride; the
+// mixing layer has K = N = ldb = ldo = width.
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool PL, bool PU, bool TRANS_B>
 __device__ __forceinline__ void mix_bf16_block(
     const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
-    bf16* __restrict__ out, int pairs, int width, int d, int block, bf16* smem) {
+    bf16* __restrict__ out, int pairs, int K, int N, int ldb, int ldo, int d, int block,
+    bf16* smem) {
   using C = MixCfg<BMP, BN, WM, WN, BK, NS>;
   constexpr int RB = BN * 2;   // bytes per row of a transposed B tile
+  constexpr bool HAS_B2 = PL || PU;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WM, wn = wave / WM;
   const int s = 1 << d;
-  const int tiles_n = width / BN;
+  const int tiles_n = N / BN;
   const int tiles_m = (pairs + BMP - 1) / BMP;
   const int tile = xcd_tile(block, tiles_m * tiles_n);
   const int q0 = (tile / tiles_n) * BMP;
@@ -92,7 +101,7 @@ __device__ __forceinline__ void mix_bf16_block(
     int q = q0 + (m % BMP);
     if (q >= pairs) q = pairs - 1;  // ragged last block: load a valid row, never store it
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
-    a_src[j] = A + (size_t)r * width + ch * 8;
+    a_src[j] = A + (size_t)r * K + ch * 8;
   }
   size_t b_src[C::B_DMA];
 #pragma unroll
@@ -101,15 +110,15 @@ __device__ __forceinline__ void mix_bf16_block(
     if constexpr (TRANS_B) {  // tile rows are k, columns n
       int kr, col;
       tr_dma_coord<RB>(b, lane, &kr, &col);
-      b_src[j] = (size_t)kr * width + n0 + col;
+      b_src[j] = (size_t)kr * ldb + n0 + col;
     } else {                  // tile rows are n, columns k
       const int o = b * 1024 + 16 * lane;
       const int nr = o / (2 * BK);
       const int ch = (swz<BK>(nr, (o % (2 * BK)) / 16) - nr * BK) / 8;
-      b_src[j] = (size_t)(n0 + nr) * width + ch * 8;
+      b_src[j] = (size_t)(n0 + nr) * ldb + ch * 8;
     }
   }
-  const size_t b_step = TRANS_B ? (size_t)BK * width : BK;
+  const size_t b_step = TRANS_B ? (size_t)BK * ldb : BK;
 
   auto issue = [&](int kt, int stage) {
     bf16* sA = smem + stage * C::STAGE;
@@ -120,7 +129,7 @@ __device__ __forceinline__ void mix_bf16_block(
 #pragma unroll
     for (int j = 0; j < C::B_DMA; j++) {
       dma16(B1 + b_src[j] + kt * b_step, sB1 + (j * C::NW + wave) * 512);
-      dma16(B2 + b_src[j] + kt * b_step, sB2 + (j * C::NW + wave) * 512);
+      if constexpr (HAS_B2) dma16(B2 + b_src[j] + kt * b_step, sB2 + (j * C::NW + wave) * 512);
     }
   };
 
@@ -148,10 +157,10 @@ __device__ __forceinline__ void mix_bf16_block(
       const int nb = (wn * C::TN + t) * 32;
       if constexpr (TRANS_B) {
         f.b1[t] = tr_frag<RB>(sB1, kk * 16, nb, lane);
-        f.b2[t] = tr_frag<RB>(sB2, kk * 16, nb, lane);
+        if constexpr (HAS_B2) f.b2[t] = tr_frag<RB>(sB2, kk * 16, nb, lane);
       } else {
         f.b1[t] = *(const bf16x8*)(sB1 + swz<BK>(nb + (lane & 31), ch));
-        f.b2[t] = *(const bf16x8*)(sB2 + swz<BK>(nb + (lane & 31), ch));
+        if constexpr (HAS_B2) f.b2[t] = *(const bf16x8*)(sB2 + swz<BK>(nb + (lane & 31), ch));
       }
     }
   };
@@ -178,8 +187,8 @@ __device__ __forceinline__ void mix_bf16_block(
 
   constexpr int KK = BK / 16;
   constexpr int NMFMA = C::TMP * C::TN * (2 + (PL ? 1 : 0) + (PU ? 1 : 0));
-  constexpr int NDS = 2 * C::TMP + 2 * C::TN * (TRANS_B ? 2 : 1);
-  const int nk = width / BK;
+  constexpr int NDS = 2 * C::TMP + (HAS_B2 ? 2 : 1) * C::TN * (TRANS_B ? 2 : 1);
+  const int nk = K / BK;
   // NS-stage ring: stage kt lives in buffer kt % NS; while stage kt is being
   // multiplied, stages kt+1 .. kt+NS-1 are in flight.
 #pragma unroll
@@ -235,17 +244,17 @@ __device__ __forceinline__ void mix_bf16_block(
     const int q = q0 + (m % BMP);
     if (q >= pairs) continue;
     const int r = lower_row(q, d) + (m >= BMP ? s : 0);
-    store_wt16(out + (size_t)r * width + n0 + ch * 8, *(const u32x4*)(sO + m * C::LDO + ch * 8));
+    store_wt16(out + (size_t)r * ldo + n0 + ch * 8, *(const u32x4*)(sO + m * C::LDO + ch * 8));
   }
 }
 
 template <int BMP, int BN, int WM, int WN, int BK, int NS, bool PL, bool PU, bool TRANS_B>
 __global__ __launch_bounds__(64 * WM * WN) void mix_bf16_kernel(
     const bf16* __restrict__ A, const bf16* __restrict__ B1, const bf16* __restrict__ B2,
-    bf16* __restrict__ out, int pairs, int width, int d) {
+    bf16* __restrict__ out, int pairs, int K, int N, int ldb, int ldo, int d) {
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
-  mix_bf16_block<BMP, BN, WM, WN, BK, NS, PL, PU, TRANS_B>(A, B1, B2, out, pairs, width, d,
-                                                           blockIdx.x, smem);
+  mix_bf16_block<BMP, BN, WM, WN, BK, NS, PL, PU, TRANS_B>(A, B1, B2, out, pairs, K, N, ldb, ldo,
+                                                           d, blockIdx.x, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -805,12 +814,30 @@ hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, 
     static const hipError_t attr = hipFuncSetAttribute(                                     \
         (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
     if (attr != hipSuccess) return attr;                                                    \
-    k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, pairs, width, d);                         \
+    k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, pairs, width, width, width, width, d);     \
   }
   if (partner_lower && partner_upper) HCMIX_MIX(true, true)
   else if (partner_upper) HCMIX_MIX(false, true)
   else HCMIX_MIX(true, false)
 #undef HCMIX_MIX
+  return hipGetLastError();
+}
+
+// The plain product instance (no partner terms): out [rows][N] (row stride
+// ldo) = A [rows][K] B^T with B [N][ldb] k-contiguous, or A B with B [K][ldb]
+// (TRANS_B).  Rows in consecutive pairs (dimension 0).
+template <int BN, int WM, int WN, bool TRANS_B>
+hipError_t gemm_launch(const bf16* A, const bf16* B, bf16* out, int rows, int K, int N, int ldb,
+                       int ldo, hipStream_t st) {
+  using C = MixCfg<MIX_BMP, BN, WM, WN, MIX_BK, MIX_NS>;
+  const int pairs = rows / 2;
+  const int blocks = ((pairs + MIX_BMP - 1) / MIX_BMP) * (N / BN);
+  const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
+  auto k = mix_bf16_kernel<MIX_BMP, BN, WM, WN, MIX_BK, MIX_NS, false, false, TRANS_B>;
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return attr;
+  k<<<blocks, C::NT, lds, st>>>(A, B, B, out, pairs, K, N, ldb, ldo, 0);
   return hipGetLastError();
 }
 
@@ -922,6 +949,15 @@ hipError_t dw_launch(const bf16* X, const bf16* dY, float* partial, int pairs, i
 }
 
 }  // namespace
+
+hipError_t launch_gemm_bf16(const bf16* A, const bf16* B, bf16* out, int rows, int K, int N,
+                            int ldb, int ldo, bool transpose_b, hipStream_t st) {
+  if (N % 128 == 0)
+    return transpose_b ? gemm_launch<128, 2, 4, true>(A, B, out, rows, K, N, ldb, ldo, st)
+                       : gemm_launch<128, 2, 4, false>(A, B, out, rows, K, N, ldb, ldo, st);
+  return transpose_b ? gemm_launch<64, 4, 1, true>(A, B, out, rows, K, N, ldb, ldo, st)
+                     : gemm_launch<64, 4, 1, false>(A, B, out, rows, K, N, ldb, ldo, st);
+}
 
 hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, int rows,
                            int width, int d, int partner_lower, int partner_upper,

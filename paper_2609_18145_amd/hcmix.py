@@ -36,7 +36,9 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_head_cross_entropy_workspace_bytes", "hcmix_head_cross_entropy",
            "hcmix_head_backward_workspace_bytes", "hcmix_head_backward",
            "hcmix_backward_no_alloc", "hcmix_shared_stack_forward",
-           "hcmix_shared_stack_backward_workspace_bytes", "hcmix_shared_stack_backward")
+           "hcmix_shared_stack_backward_workspace_bytes", "hcmix_shared_stack_backward",
+           "hcmix_linear_forward", "hcmix_linear_backward_workspace_bytes",
+           "hcmix_linear_backward")
 
 _lib = None
 
@@ -125,6 +127,12 @@ def load():
         lib.hcmix_shared_stack_backward.argtypes = [i64, i64, i64, i32, ip, i32, i32, pp, pp, vp,
                                                     vp, pp, i32, vp, sz, vp]
         lib.hcmix_shared_stack_backward.restype = i32
+        lib.hcmix_linear_forward.argtypes = [i64, i64, i64, vp, vp, vp, vp]
+        lib.hcmix_linear_forward.restype = i32
+        lib.hcmix_linear_backward_workspace_bytes.argtypes = [i64, i64, i64]
+        lib.hcmix_linear_backward_workspace_bytes.restype = sz
+        lib.hcmix_linear_backward.argtypes = [i64, i64, i64, vp, vp, vp, vp, fp, i32, vp, sz, vp]
+        lib.hcmix_linear_backward.restype = i32
         _lib = lib
     return _lib
 
@@ -695,6 +703,64 @@ def shared_stack_backward(xs, tables, layers, dy, causal, dx=None, dtables=None,
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_shared_stack_backward")
     return dx, dtables
+
+
+def linear_forward(x, w, out=None):
+    """y = x W^T: x [rows, in] bf16, W [out, in] bf16 -> y [rows, out] bf16."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("w: expected an [out, in] tensor")
+    n_out, n_in = w.shape
+    _need(w, "w", None, torch.bfloat16)
+    dev = w.device
+    _need(x, "x", (None, n_in), torch.bfloat16, dev)
+    rows = x.shape[0]
+    if out is None:
+        out = torch.empty((rows, n_out), dtype=torch.bfloat16, device=dev)
+    _need(out, "out", (rows, n_out), torch.bfloat16, dev)
+    _gpu(dev)
+    rc = load().hcmix_linear_forward(rows, n_in, n_out, _ptr(x), _ptr(w), _ptr(out), _stream(w))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_linear_forward")
+    return out
+
+
+def linear_backward(x, w, dy, dx=None, dw=None, with_dx=True, with_dw=True, accumulate=False,
+                    workspace=None):
+    """dx = dy W (bf16 [rows, in]) and dW (+)= dy^T x (fp32 [out, in]); returns
+    (dx, dw), None for one not asked for.  x is read only for dW."""
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise ValueError("w: expected an [out, in] tensor")
+    n_out, n_in = w.shape
+    _need(w, "w", None, torch.bfloat16)
+    dev = w.device
+    _need(dy, "dy", (None, n_out), torch.bfloat16, dev)
+    rows = dy.shape[0]
+    want_dx = with_dx or dx is not None
+    want_dw = with_dw or dw is not None
+    if not want_dx and not want_dw:
+        raise ValueError("linear_backward: neither dx nor dw asked for")
+    if want_dw:
+        _need(x, "x", (rows, n_in), torch.bfloat16, dev)
+    if want_dx:
+        if dx is None:
+            dx = torch.empty((rows, n_in), dtype=torch.bfloat16, device=dev)
+        _need(dx, "dx", (rows, n_in), torch.bfloat16, dev)
+    if want_dw:
+        if dw is None:
+            dw = torch.empty((n_out, n_in), dtype=torch.float32, device=dev)
+        _need(dw, "dw", (n_out, n_in), torch.float32, dev)
+    _gpu(dev)
+    if want_dw and workspace is None:
+        workspace = torch.empty(load().hcmix_linear_backward_workspace_bytes(rows, n_in, n_out),
+                                dtype=torch.uint8, device=dev)
+    rc = load().hcmix_linear_backward(rows, n_in, n_out, _ptr(x) if want_dw else None, _ptr(w),
+                                      _ptr(dy), _ptr(dx) if want_dx else None,
+                                      _fptr(dw) if want_dw else None, int(bool(accumulate)),
+                                      _ptr(workspace) if want_dw else None,
+                                      _bytes(workspace) if want_dw else 0, _stream(w))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_linear_backward")
+    return (dx if want_dx else None), (dw if want_dw else None)
 
 
 class Attention(torch.autograd.Function):
