@@ -894,7 +894,7 @@ def run_decode(args, torch, hcmix, inputs, dev):
     cols = [x[:, p].contiguous() for p in range(n)]
     ws = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_self]
     wo = [torch.from_numpy(a).to(dt).to(dev) for a in s.w_off]
-    cache = hcmix.alloc_decode_cache(B, n, w, L, dt, dev)
+    cache = hcmix.alloc_decode_cache(B, n, w, s.layers, dt, dev)
     y = torch.empty(B, w, dtype=dt, device=dev)
     stream = torch.cuda.current_stream(dev)
 

@@ -279,12 +279,17 @@ hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, con
  * pos - 1 for the local layer), which an earlier step recorded in the cache.
  *
  * Cache: caller-owned device memory of hcmix_decode_cache_bytes() bytes,
- * 256-byte aligned; it holds every layer's input at every position of the
- * current window ([num_layers][batch][n][width] in dtype), so it is bounded by
- * the window and never grows.  Positions of a window must be decoded in order
- * 0, 1, 2, ... (a step reads what earlier steps recorded); starting a new
- * window is starting again at pos = 0.  The cache's other contents are never
- * read, so it needs no initialisation.
+ * 256-byte aligned, sized by the schedule as the deployment paragraph bounds
+ * it: a hypercube layer of dimension d keeps the inputs of the last 2^d
+ * positions (a ring of 2^d [batch][width] slots: a position with bit d clear
+ * records its input, the position 2^d later reads it), the local layer the
+ * last two, plus two [batch][width] buffers that pass each layer's output to
+ * the next.  So it never grows with the position, and for the window-256
+ * rotated stack (dimensions 0..7 twice) it holds 512 slots instead of 16 x
+ * 256.  Positions of a window must be decoded in order 0, 1, 2, ... (a step
+ * reads what earlier steps recorded); starting a new window is starting
+ * again at pos = 0.  Only slots that earlier steps of the window wrote are
+ * ever read, so the cache needs no initialisation.
  *
  * x: [batch][width], the stack's input at `pos` for every window; y:
  * [batch][width], the stack's output there.  layers: host array of layer codes
@@ -295,7 +300,7 @@ hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, con
  * HCMIX_ERR_INVALID_VALUE also for pos outside [0, n), a short cache, or y or
  * the cache overlapping an input. */
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
-                                int32_t dtype);
+                                const int32_t* layers, int32_t dtype);
 
 hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
                                const int32_t* layers, int32_t dtype, int64_t pos, const void* x,

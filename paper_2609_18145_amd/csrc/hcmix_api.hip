@@ -919,11 +919,25 @@ hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, con
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }
 
+// Decode cache: two [batch][width] buffers that pass each layer's output to
+// the next, then per layer a ring of the inputs that a later position takes as
+// its partner: a hypercube layer of dimension d needs the input at pos - 2^d,
+// recorded at a position with bit d clear and read 2^d positions later, so
+// 2^d slots indexed by pos mod 2^d; the local layer reads pos - 1 and records
+// pos in the same step, so 2 slots indexed by pos mod 2.
+int64_t ring_slots(int32_t code, int64_t n) {
+  return code == HCMIX_LAYER_NEAR ? 2 : (int64_t)1 << hcmix_dim(code, n);
+}
+
 size_t hcmix_decode_cache_bytes(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
-                                int32_t dtype) {
-  if (num_layers < 1 || num_layers > kMaxLayers) return 0;
-  if (check_shape(batch, n, width, 0, HCMIX_CAUSAL, dtype) != HCMIX_OK) return 0;
-  return align256((size_t)num_layers * batch * n * width * elem_size(dtype));
+                                const int32_t* layers, int32_t dtype) {
+  if (!layers || num_layers < 1 || num_layers > kMaxLayers) return 0;
+  int64_t slots = 2;
+  for (int l = 0; l < num_layers; l++) {
+    if (check_shape(batch, n, width, layers[l], HCMIX_CAUSAL, dtype) != HCMIX_OK) return 0;
+    slots += ring_slots(layers[l], n);
+  }
+  return align256((size_t)slots * batch * width * elem_size(dtype));
 }
 
 hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t num_layers,
@@ -938,7 +952,7 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
     if (!w_self[l] || !w_off[l]) return HCMIX_ERR_INVALID_VALUE;
   }
   if (pos < 0 || pos >= n) return HCMIX_ERR_INVALID_VALUE;
-  const size_t need = hcmix_decode_cache_bytes(batch, n, width, num_layers, dtype);
+  const size_t need = hcmix_decode_cache_bytes(batch, n, width, num_layers, layers, dtype);
   if (cache_bytes < need) return HCMIX_ERR_INVALID_VALUE;
   const size_t es = elem_size(dtype);
   const size_t row = (size_t)(batch * width) * es, wgt = (size_t)(width * width) * es;
@@ -957,50 +971,55 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
   }
   if (!aligned(cache, 256)) return HCMIX_ERR_UNSUPPORTED;
 
-  const int64_t w = width, win = n * width;   // a window's rows in one layer's cache
-  const size_t layer_elems = (size_t)batch * n * width;
+  // slot k of the cache: [batch][width] elements at offset k * batch * width
+  const int64_t slot = batch * width;
+  char* c = (char*)cache;
+  auto at = [&](int64_t k) { return c + (size_t)(k * slot) * es; };
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = hipSuccess;
+  int64_t ring = 2;   // first slot of layer l's ring (after the two pass-on buffers)
   for (int l = 0; l < num_layers && e == hipSuccess; l++) {
-    // partner position of `pos` (causal): the earlier endpoint of the link
-    const int d = hcmix_dim(layers[l], n);
-    int64_t partner = -1;
-    if (d < 0) partner = pos >= 1 ? pos - 1 : -1;
-    else if ((pos >> d) & 1) partner = pos - ((int64_t)1 << d);
-    const bool last = l == num_layers - 1;
+    const int32_t code = layers[l];
+    const int64_t slots = ring_slots(code, n);
+    const int d = hcmix_dim(code, n);
+    const void* partner = nullptr;
+    void* record = nullptr;
+    if (code == HCMIX_LAYER_NEAR) {
+      if (pos >= 1) partner = at(ring + (pos - 1) % 2);
+      record = at(ring + pos % 2);
+    } else if ((pos >> d) & 1) {
+      partner = at(ring + pos % slots);   // recorded at pos - 2^d
+    } else {
+      record = at(ring + pos % slots);    // read at pos + 2^d
+    }
+    const void* in = l == 0 ? x : at(l & 1);
+    void* out = l == num_layers - 1 ? y : at((l + 1) & 1);
     if (dtype == HCMIX_BF16) {
-      bf16* c = (bf16*)cache;
       DecodeLayerArgs a = {};
-      a.x_in = l == 0 ? (const bf16*)x : c + l * layer_elems + pos * w;
-      a.in_stride = l == 0 ? w : win;
-      a.x_partner = partner >= 0 ? c + l * layer_elems + partner * w : nullptr;
-      a.partner_stride = win;
+      a.x_in = (const bf16*)in;
+      a.x_partner = (const bf16*)partner;
       a.w_self = (const bf16*)w_self[l];
       a.w_off = (const bf16*)w_off[l];
-      a.out = last ? (bf16*)y : c + (l + 1) * layer_elems + pos * w;
-      a.out_stride = last ? w : win;
-      a.record = l == 0 ? c + pos * w : nullptr;
-      a.rec_stride = win;
+      a.out = (bf16*)out;
+      a.record = (bf16*)record;
+      a.in_stride = a.partner_stride = a.out_stride = a.rec_stride = width;
       a.batch = (int)batch;
       a.width = (int)width;
       e = launch_decode_bf16(a, s);
     } else {
-      float* c = (float*)cache;
       DecodeLayerArgsF32 a = {};
-      a.x_in = l == 0 ? (const float*)x : c + l * layer_elems + pos * w;
-      a.in_stride = l == 0 ? w : win;
-      a.x_partner = partner >= 0 ? c + l * layer_elems + partner * w : nullptr;
-      a.partner_stride = win;
+      a.x_in = (const float*)in;
+      a.x_partner = (const float*)partner;
       a.w_self = (const float*)w_self[l];
       a.w_off = (const float*)w_off[l];
-      a.out = last ? (float*)y : c + (l + 1) * layer_elems + pos * w;
-      a.out_stride = last ? w : win;
-      a.record = l == 0 ? c + pos * w : nullptr;
-      a.rec_stride = win;
+      a.out = (float*)out;
+      a.record = (float*)record;
+      a.in_stride = a.partner_stride = a.out_stride = a.rec_stride = width;
       a.batch = (int)batch;
       a.width = (int)width;
       e = launch_decode_f32(a, s);
     }
+    ring += slots;
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }

@@ -2,12 +2,12 @@
 // All windows are at the same position, so each layer is one small dense
 // product over the batch:
 //   y[b] = W_self x[b] + m(pos) W_off x_partner[b]
-// with the partner's layer input read from the cache.  The cache holds every
-// layer's input at every position of the current window,
-// cache[l][b][p][:] (l < L, p < n); the kernel of layer l reads its input at
-// `pos` (layer 0: from the caller's x, which it also records) and the
-// partner's, and writes its output to cache[l+1][b][pos] (or to y after the
-// last layer), so no launch overwrites anything another block of it reads.
+// with the partner's layer input read from the cache.  The kernel of layer l
+// reads its input at `pos` (from the caller's x or the buffer the previous
+// layer wrote), the partner's from that layer's ring of earlier inputs, may
+// record its own input into the ring for a later position, and writes its
+// output to the other pass-on buffer (or to y after the last layer); the
+// buffers a launch writes are never ones it reads.
 #include "device_common.h"
 #include "hcmix_internal.h"
 
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_bf16_kernel(DecodeLayer
     }
   }
   part[wave][lane] = acc;
-  // layer 0 records its input for later positions: this block's 16 columns
+  // the layer records its input for a later position: this block's 16 columns
   if (a.record && wave == 0 && b0 + (lane & 15) < a.batch) {
     const int c = o0 + 4 * q;
     *(bf16x4*)(a.record + (size_t)b * a.rec_stride + c) = *(const bf16x4*)(xin + c);

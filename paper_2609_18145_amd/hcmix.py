@@ -114,7 +114,7 @@ def load():
         lib.hcmix_head_backward_workspace_bytes.restype = sz
         lib.hcmix_head_backward.argtypes = [i64, i64, i32, vp, vp, vp, vp, fp, i32, vp, sz, vp]
         lib.hcmix_head_backward.restype = i32
-        lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, i32]
+        lib.hcmix_decode_cache_bytes.argtypes = [i64, i64, i64, i32, ip, i32]
         lib.hcmix_decode_cache_bytes.restype = sz
         lib.hcmix_decode_step.argtypes = [i64, i64, i64, i32, ip, i32, i64, vp, pp, pp, vp, sz, vp,
                                           vp]
@@ -778,15 +778,16 @@ class Attention(torch.autograd.Function):
         return attention_backward(qkv, out, lse, gout.contiguous())
 
 
-def decode_cache_bytes(batch, n, width, num_layers, dtype) -> int:
+def decode_cache_bytes(batch, n, width, layers, dtype) -> int:
     code = HCMIX_BF16 if dtype == torch.bfloat16 else HCMIX_F32
-    return load().hcmix_decode_cache_bytes(batch, n, width, num_layers, code)
+    return load().hcmix_decode_cache_bytes(batch, n, width, len(layers), _layers(layers), code)
 
 
-def alloc_decode_cache(batch, n, width, num_layers, dtype, device):
-    """Device memory for hcmix_decode_step: every layer's input at every
-    position of the current window (no initialisation needed)."""
-    return torch.empty(decode_cache_bytes(batch, n, width, num_layers, dtype), dtype=torch.uint8,
+def alloc_decode_cache(batch, n, width, layers, dtype, device):
+    """Device memory for hcmix_decode_step with this schedule: per layer a ring
+    of the inputs later positions take as partners (2^d slots for dimension d,
+    two for the local layer) and two pass-on buffers (no initialisation)."""
+    return torch.empty(decode_cache_bytes(batch, n, width, layers, dtype), dtype=torch.uint8,
                        device=device)
 
 

@@ -347,7 +347,7 @@ def dec(batch=2, n=16, width=64, L=4, layers=LP, dtype=1, pos=0, x=P[0], ws=None
     ws = ws if ws is not None else PP(P[1], P[1], P[1], P[1])
     wo = wo if wo is not None else PP(P[2], P[2], P[2], P[2])
     if cb is None:
-        cb = lib.hcmix_decode_cache_bytes(batch, n, width, L, dtype)
+        cb = lib.hcmix_decode_cache_bytes(batch, n, width, L, layers, dtype)
     return lib.hcmix_decode_step(batch, n, width, L, layers, dtype, pos, x, ws, wo, cache, cb, y,
                                  None)
 
@@ -367,11 +367,23 @@ def test_decode_rejects_bad_arguments(kw, code):
 
 
 def test_decode_cache_query():
+    """Two pass-on buffers plus, per layer, 2^d ring slots (dimension d) or two
+    (the local layer), each [batch][width]: bounded by the schedule, not by
+    the window."""
     lib = hcmix.load()
-    assert lib.hcmix_decode_cache_bytes(2, 16, 64, 4, hcmix.HCMIX_BF16) == 4 * 2 * 16 * 64 * 2
-    assert lib.hcmix_decode_cache_bytes(64, 256, 512, 16, hcmix.HCMIX_BF16) == 16 * 64 * 256 * 512 * 2
-    assert lib.hcmix_decode_cache_bytes(2, 12, 64, 4, hcmix.HCMIX_BF16) == 0
-    assert lib.hcmix_decode_cache_bytes(2, 16, 64, 0, hcmix.HCMIX_BF16) == 0
+    q = lib.hcmix_decode_cache_bytes
+    lay = lambda *c: (ctypes.c_int32 * len(c))(*c)   # noqa: E731
+    # rotated n = 16: dimensions 0, 1, 2, 3 -> 1 + 2 + 4 + 8 slots
+    assert q(2, 16, 64, 4, lay(0, 1, 2, 3), hcmix.HCMIX_BF16) == (2 + 15) * 2 * 64 * 2
+    # the window-256 rotated stack: dimensions 0..7 twice, 510 ring slots + 2
+    rot = lay(*range(16))
+    assert q(64, 256, 512, 16, rot, hcmix.HCMIX_BF16) == 512 * 64 * 512 * 2
+    assert q(64, 256, 512, 16, rot, hcmix.HCMIX_BF16) <= 40 << 20
+    # the local layer: two slots
+    assert q(4, 64, 128, 2, lay(-1, -1), hcmix.HCMIX_BF16) == (2 + 4) * 4 * 128 * 2
+    assert q(2, 12, 64, 4, LP, hcmix.HCMIX_BF16) == 0
+    assert q(2, 16, 64, 0, LP, hcmix.HCMIX_BF16) == 0
+    assert q(2, 16, 64, 4, None, hcmix.HCMIX_BF16) == 0
 
 
 def sbd(batch=2, n=16, width=128, L=4, layers=LP, mode=1, dtype=1, ws=None, wo=None, dy=P[0],

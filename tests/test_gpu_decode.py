@@ -39,7 +39,7 @@ def test_decode_every_position_matches_the_stack(batch, n, width, dtype, schedul
     x = to_dev(s.x, dtype)
     ws = [to_dev(w, dtype) for w in s.w_self]
     wo = [to_dev(w, dtype) for w in s.w_off]
-    cache = hcmix.alloc_decode_cache(batch, n, width, L, x.dtype, x.device)
+    cache = hcmix.alloc_decode_cache(batch, n, width, layers, x.dtype, x.device)
     cache.fill_(0xFF)                      # never-written contents must never be read
     got = np.zeros_like(want)
     for pos in range(n):
@@ -62,7 +62,7 @@ def test_decode_restarts_at_position_zero():
                            seed=43, layers=layers, with_dy=False)
     ws = [to_dev(w, "bf16") for w in s1.w_self]
     wo = [to_dev(w, "bf16") for w in s1.w_off]
-    cache = hcmix.alloc_decode_cache(batch, n, width, L, torch.bfloat16, "cuda")
+    cache = hcmix.alloc_decode_cache(batch, n, width, layers, torch.bfloat16, "cuda")
     for s in (s1, s2):
         x = to_dev(s.x, "bf16")
         got = np.stack([to_host(hcmix.decode_step(x[:, p].contiguous(), ws, wo, layers, n, p, cache))
@@ -82,7 +82,7 @@ def test_decode_lm256_shape_sampled_windows():
     x = to_dev(s.x, "bf16")
     ws = [to_dev(w, "bf16") for w in s.w_self]
     wo = [to_dev(w, "bf16") for w in s.w_off]
-    cache = hcmix.alloc_decode_cache(B, n, x.shape[2], len(s.layers), x.dtype, x.device)
+    cache = hcmix.alloc_decode_cache(B, n, x.shape[2], s.layers, x.dtype, x.device)
     cols = [x[:, p].contiguous() for p in range(n)]
     ys = [hcmix.decode_step(cols[p], ws, wo, s.layers, n, p, cache) for p in range(n)]
     got = to_host(torch.stack(ys, dim=1))
