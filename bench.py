@@ -139,11 +139,57 @@ def deferred_path(n, w, L):
     return not fused_path(n, w, L) and L > 1 and w % 128 == 0
 
 
+def profiled_mfma(workload: str, kernel: str, sec: float, flops: int):
+    """MFMA counter evidence for `kernel` from the committed counter summary
+    (profiles/mfma_<workload>.json; the LM step's stack kernels run at the
+    lm256 launch configuration and use its file): the flops the MFMA units
+    issued per launch (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) against the
+    algorithmic count, and MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES over the 1024
+    SIMDs x 2.4 GHz x this launch's measured duration.  None if the counters
+    were taken on different kernel sources."""
+    wl = "lm256" if workload == "lm256_step" else workload
+    path = os.path.join(ROOT, "profiles", f"mfma_{wl}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    k = rec.get("kernels", {}).get(kernel)
+    if rec.get("source_hash") != kernel_source_hash() or k is None:
+        return None
+    return {"issued_flops": k["mops_bf16_x512"], "issued_equals_algorithmic":
+            k["mops_bf16_x512"] == flops,
+            "mfma_busy": round(k["mfma_busy_cycles"] / (sec * 2.4e9 * 1024), 4),
+            "source": f"profiles/mfma_{wl}.json"}
+
+
+def graph_timed(torch, stream, fn, count):
+    """Seconds per call of fn, from HIP events on `stream` around `count`
+    back-to-back replays of one captured graph of the call: the host-side
+    operand checks of the binding stay out of the timed region, so the GPU is
+    never idle between calls and the figure is the kernels' own time plus the
+    dependent-launch gaps inside the call."""
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        fn()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=stream):
+            fn()
+        graph.replay()
+        torch.cuda.synchronize()
+        k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        k0.record(stream)
+        for _ in range(count):
+            graph.replay()
+        k1.record(stream)
+        torch.cuda.synchronize()
+    return k0.elapsed_time(k1) / 1e3 / count
+
+
 def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo, workspace,
                     layers, B, n, w, L, causal):
     """Roofline entries, timed with HIP events on the stream the kernels run
-    on over back-to-back calls: {name: entry}, the dominant one under
-    "roofline".
+    on over back-to-back graph replays of the call (graph_timed): {name:
+    entry}, the dominant one under "roofline".
 
     Small width (the fused path): the backward stack call (fused_bwd_kernel
     plus its fixed-order partial reduction), against HBM bandwidth; its
@@ -161,16 +207,10 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
     (dW_self 2 w^2 per position, dW_off 2 w^2 per receiver)."""
     import torch
     reps = args.kernel_reps
-    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     xs = [x0, *xs_out[:L - 1]]
 
     def timed(fn, count):
-        k0.record(stream)
-        for _ in range(count):
-            fn()
-        k1.record(stream)
-        torch.cuda.synchronize()
-        return k0.elapsed_time(k1) / 1e3 / count
+        return graph_timed(torch, stream, fn, count)
 
     if fused_path(n, w, L):
         sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
@@ -198,7 +238,8 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
                         "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                         "traffic": profiled_traffic(args.workload, kname),
-                        "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops}}
+                        "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops,
+                        "counters": profiled_mfma(args.workload, kname, sec, flops)}}
     if deferred_path(n, w, L):
         # the saved activations stand in for the output gradients: the same
         # shapes and magnitudes, and the kernel's work does not depend on values
@@ -213,7 +254,8 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
                               "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                               "traffic": profiled_traffic(args.workload, kname),
-                              "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops}
+                              "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops,
+                              "counters": profiled_mfma(args.workload, kname, sec, flops)}
     sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
                                              dws=dws, dwo=dwo, workspace=workspace), reps)
     out["backward_call_us"] = round(sec * 1e6, 2)
@@ -601,20 +643,17 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     pl = B * n * Ls
     core_us = None
     if args.attention == "native":
-        # the attention core alone (forward + backward of one layer), back to back
+        # the attention core alone (forward + backward of one layer), graph replays back to back
         gen_q = torch.Generator(device="cpu").manual_seed(2)
         qkv = torch.randn(B, n, 3, heads, hd, generator=gen_q).to(dt).to(dev)
         gout = torch.randn(B, n, heads, hd, generator=gen_q).to(dt).to(dev)
         o_, l_ = hcmix.attention_forward(qkv)
-        hcmix.attention_backward(qkv, o_, l_, gout)
-        c2, c3 = ev(enable_timing=True), ev(enable_timing=True)
-        c2.record(stream)
-        for _ in range(args.kernel_reps):
-            o_, l_ = hcmix.attention_forward(qkv, out=o_, lse=l_)
-            hcmix.attention_backward(qkv, o_, l_, gout)
-        c3.record(stream)
-        torch.cuda.synchronize()
-        core_us = round(c2.elapsed_time(c3) * 1e3 / args.kernel_reps, 2)
+        dq_ = hcmix.attention_backward(qkv, o_, l_, gout)
+
+        def core():
+            hcmix.attention_forward(qkv, out=o_, lse=l_)
+            hcmix.attention_backward(qkv, o_, l_, gout, dqkv=dq_)
+        core_us = round(graph_timed(torch, stream, core, args.kernel_reps) * 1e6, 2)
         backend["name"] = "hcmix_attention (library kernels)"
     out = {
         "metric": METRIC, "value": round(pl * args.steps / sparse, 1), "unit": UNIT, "n_gpus": 1,
@@ -647,8 +686,9 @@ def run_shared(args, torch, hcmix, inputs, dev):
     HBM-bound, so its roofline is bytes: the forward kernel reads x_0 and
     writes every layer's output, (L + 1) activations; the backward kernel
     reads dy and every layer input and writes dx, (L + 2) activations, plus
-    the L fp32 table gradients (n^2 each).  Each is timed with HIP events
-    around its own launches on the stream they run on."""
+    the L fp32 table gradients (n^2 each).  Each call is timed on its own
+    with HIP events around graph replays of it (graph_timed), on the stream
+    it runs on."""
     B, n, w, L = 64, 256, 512, 16
     if args.batch > 0:
         B = args.batch
@@ -693,19 +733,13 @@ def run_shared(args, torch, hcmix, inputs, dev):
         e1.record(stream)
         torch.cuda.synchronize()
         t = max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
-        per = {"forward": [], "backward": []}
-        for _ in range(args.kernel_reps):
-            for name, fn in (("forward", fwd), ("backward", bwd)):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
-                fn()
-                b.record(stream)
-                per[name].append((a, b))
-        torch.cuda.synchronize()
+    us = {name: graph_timed(torch, stream, fn, args.kernel_reps) * 1e6
+          for name, fn in (("forward", fwd), ("backward", bwd))}
+    if args.calib_copy_mb > 0:
+        calibration_copy(torch, dev, args.calib_copy_mb)
     act = B * n * w * 2
     bytes_fwd = (L + 1) * act + L * n * 8
     bytes_bwd = (L + 2) * act + L * n * 8 + L * n * n * 4
-    us = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) * 1e3 for k, v in per.items()}
     entries = {}
     for name, nb, kname in (("forward", bytes_fwd, "shared_fwd_kernel"),
                             ("backward", bytes_bwd, "shared_bwd_kernel + shared_dt_reduce_kernel")):
