@@ -162,33 +162,40 @@ def profiled_mfma(workload: str, kernel: str, sec: float, flops: int):
             "source": f"profiles/mfma_{wl}.json"}
 
 
-def graph_timed(torch, stream, fn, count):
-    """Seconds per call of fn, from HIP events on `stream` around `count`
-    back-to-back replays of one captured graph of the call: the host-side
-    operand checks of the binding stay out of the timed region, so the GPU is
-    never idle between calls and the figure is the kernels' own time plus the
-    dependent-launch gaps inside the call."""
+def graph_timed(torch, fn, count, replays=3):
+    """Seconds per call of fn: `count` calls captured back to back in one
+    graph, replayed `replays` times between HIP events on the stream the
+    kernels run on (a stream of its own that first waits for the caller's).
+    Graph replay is how the timed steps run: the binding's host-side operand
+    checks stay out of the timed region, consecutive kernels start within
+    about 0.3 us of each other (kernel traces), and one graph launch is
+    spread over `count` calls, so the figure is the kernels' own time plus the
+    dependent-launch gaps of the step itself."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
     graph = torch.cuda.CUDAGraph()
-    with torch.cuda.stream(stream):
+    with torch.cuda.stream(side):
         fn()
         torch.cuda.synchronize()
-        with torch.cuda.graph(graph, stream=stream):
-            fn()
+        with torch.cuda.graph(graph, stream=side):
+            for _ in range(count):
+                fn()
         graph.replay()
         torch.cuda.synchronize()
         k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        k0.record(stream)
-        for _ in range(count):
+        k0.record(side)
+        for _ in range(replays):
             graph.replay()
-        k1.record(stream)
+        k1.record(side)
         torch.cuda.synchronize()
-    return k0.elapsed_time(k1) / 1e3 / count
+    del graph
+    return k0.elapsed_time(k1) / 1e3 / (count * replays)
 
 
 def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dwo, workspace,
                     layers, B, n, w, L, causal):
     """Roofline entries, timed with HIP events on the stream the kernels run
-    on over back-to-back graph replays of the call (graph_timed): {name:
+    on over calls captured back to back in one graph (graph_timed): {name:
     entry}, the dominant one under "roofline".
 
     Small width (the fused path): the backward stack call (fused_bwd_kernel
@@ -210,7 +217,7 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
     xs = [x0, *xs_out[:L - 1]]
 
     def timed(fn, count):
-        return graph_timed(torch, stream, fn, count)
+        return graph_timed(torch, fn, count)
 
     if fused_path(n, w, L):
         sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
@@ -365,6 +372,47 @@ def main():
     return 0
 
 
+def native_segment_split(torch, hstack, x0, dy, nattn, reps):
+    """Seconds per step of the sparse and the attention segments of a
+    library-only hybrid step (HybridStack): one eager step records every
+    segment's input and output gradient, then each segment's forward call and
+    backward call, and the closing all-layer weight-gradient call, is timed on
+    its own over calls captured back to back in a graph with those inputs
+    (graph_timed; the kernels' work does not depend on the values).  The
+    stack's saved state is restored around each timing, since a segment call
+    appends to it."""
+    hstack._saved = []
+    xin, x = [], x0
+    for k in range(len(hstack.segments)):
+        xin.append(x)
+        x = hstack.forward_segment(k, x)
+    saved = list(hstack._saved)
+    hstack._dw_in = []
+    hstack.dw_attn = [None] * nattn
+    gin, g = {}, dy
+    for k in reversed(range(len(hstack.segments))):
+        gin[k] = g
+        g = hstack.backward_segment(k, g)
+    dw_in = list(hstack._dw_in)
+    torch.cuda.synchronize()
+    res = {"sparse": 0.0, "attn": 0.0}
+    for k, (kind, _) in enumerate(hstack.segments):
+        def fwd(k=k):
+            hstack._saved = list(saved[:k])
+            hstack.forward_segment(k, xin[k])
+        t_f = graph_timed(torch, fwd, reps)
+        hstack._saved = saved
+
+        def bwd(k=k):
+            hstack._dw_in = []
+            hstack.backward_segment(k, gin[k])
+        t_b = graph_timed(torch, bwd, reps)
+        res[kind] += t_f + t_b
+    hstack._dw_in = dw_in
+    res["sparse"] += graph_timed(torch, hstack.sparse_weight_gradients, reps)
+    return res
+
+
 def run_hybrid(args, torch, hcmix, inputs, dev):
     """Sparse layers with two causal softmax attention layers among them:
     "hybrid", the lm256 stack with attention inserted at slots 3 and 9 of 18
@@ -381,8 +429,9 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
     The sparse segments are hcmix stack calls: forward per segment, the dX
     chain per segment (hcmix_stack_backward_data), and the weight gradients of
     every sparse layer in one hcmix_stack_weight_gradients call at the end.  Forward and backward are chained by hand
-    so that every segment is timed with HIP events on one stream; the line
-    reports the sparse layers' share of the step and their own throughput."""
+    so that every segment can be timed on its own.  value = positions x
+    (sparse + attention) layers per second of the whole step; beside it the
+    sparse and attention segments' times (native_segment_split)."""
     import torch.nn.functional as F
     cfg = dict(inputs.PRESETS["lm256"])
     if args.batch > 0:
@@ -640,10 +689,13 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
             g1.record(side)
             torch.cuda.synchronize()
         total = max(time.perf_counter() - t0, g0.elapsed_time(g1) / 1e3)
-    pl = B * n * Ls
+    seg_split = None
+    if native:
+        seg_split = native_segment_split(torch, hstack, x0, dy, nattn, args.kernel_reps)
+    pl = B * n * (Ls + nattn)
     core_us = None
     if args.attention == "native":
-        # the attention core alone (forward + backward of one layer), graph replays back to back
+        # the attention core alone (forward + backward of one layer), back to back
         gen_q = torch.Generator(device="cpu").manual_seed(2)
         qkv = torch.randn(B, n, 3, heads, hd, generator=gen_q).to(dt).to(dev)
         gout = torch.randn(B, n, heads, hd, generator=gen_q).to(dt).to(dev)
@@ -653,10 +705,10 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
         def core():
             hcmix.attention_forward(qkv, out=o_, lse=l_)
             hcmix.attention_backward(qkv, o_, l_, gout, dqkv=dq_)
-        core_us = round(graph_timed(torch, stream, core, args.kernel_reps) * 1e6, 2)
+        core_us = round(graph_timed(torch, core, args.kernel_reps) * 1e6, 2)
         backend["name"] = "hcmix_attention (library kernels)"
     out = {
-        "metric": METRIC, "value": round(pl * args.steps / sparse, 1), "unit": UNIT, "n_gpus": 1,
+        "metric": METRIC, "value": round(pl * args.steps / total, 1), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(total / args.steps * 1e3, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
@@ -667,15 +719,25 @@ def run_hybrid(args, torch, hcmix, inputs, dev):
                    else "PyTorch GEMMs"},
         "hybrid": {"step_ms": round(total / args.steps * 1e3, 4),
                    "step_ms_eager": round(total_eager / args.steps * 1e3, 4),
-                   "sparse_ms": round(sparse / args.steps * 1e3, 4),
-                   "attention_ms": round(attn / args.steps * 1e3, 4),
-                   "attention_core_fwd_bwd_us_per_layer": core_us,
-                   "sparse_share_of_step": round(sparse / total_eager, 4),
-                   "note": "step_ms from one captured graph of the whole step (when graph); "
-                           "value = sparse positions*layers per second of sparse-layer time and "
-                           "the segment split from eager steps, each segment timed with HIP "
-                           "events"},
+                   "attention_core_fwd_bwd_us_per_layer": core_us},
     }
+    if seg_split is not None:
+        out["hybrid"].update({
+            "sparse_ms": round(seg_split["sparse"] * 1e3, 4),
+            "attention_ms": round(seg_split["attn"] * 1e3, 4),
+            "sparse_share": round(seg_split["sparse"] / (seg_split["sparse"] + seg_split["attn"]), 4),
+            "sparse_positions_layers_per_s": round(B * n * Ls / seg_split["sparse"], 1),
+            "note": "value = positions * (sparse + attention) layers per second of the whole step "
+                    "(one captured graph, when graph); the split times every segment's forward and "
+                    "backward call and the sparse weight-gradient call on its own, each over "
+                    "calls captured back to back in one graph (graph_timed)"})
+    else:
+        out["hybrid"].update({
+            "sparse_ms_eager": round(sparse / args.steps * 1e3, 4),
+            "attention_ms_eager": round(attn / args.steps * 1e3, 4),
+            "note": "value = positions * (sparse + attention) layers per second of the whole step; "
+                    "the split from eager steps with HIP events around every segment (host "
+                    "overhead included)"})
     print(json.dumps(out), flush=True)
     return 0
 
@@ -687,7 +749,7 @@ def run_shared(args, torch, hcmix, inputs, dev):
     writes every layer's output, (L + 1) activations; the backward kernel
     reads dy and every layer input and writes dx, (L + 2) activations, plus
     the L fp32 table gradients (n^2 each).  Each call is timed on its own
-    with HIP events around graph replays of it (graph_timed), on the stream
+    with HIP events around graph replays of calls of it (graph_timed), on the stream
     it runs on."""
     B, n, w, L = 64, 256, 512, 16
     if args.batch > 0:
@@ -733,7 +795,7 @@ def run_shared(args, torch, hcmix, inputs, dev):
         e1.record(stream)
         torch.cuda.synchronize()
         t = max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
-    us = {name: graph_timed(torch, stream, fn, args.kernel_reps) * 1e6
+    us = {name: graph_timed(torch, fn, args.kernel_reps) * 1e6
           for name, fn in (("forward", fwd), ("backward", bwd))}
     if args.calib_copy_mb > 0:
         calibration_copy(torch, dev, args.calib_copy_mb)
