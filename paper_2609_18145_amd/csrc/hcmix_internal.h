@@ -120,6 +120,8 @@ struct FusedFwdArgs {
   int n, num_layers;
 };
 
+constexpr int kFusedMaxSplit = 4;    // blocks sharing one window's backward
+
 struct FusedBwdArgs {
   const bf16* xs[kFusedMaxLayers];  // input of each layer, x_0 .. x_{L-1}
   const bf16* ws[kFusedMaxLayers];
@@ -129,6 +131,11 @@ struct FusedBwdArgs {
   bf16* dx;                         // gradient of x_0
   float* partial;                   // [batch][L][2][64][64] per-window weight gradients
   int n, num_layers;
+  // Set by launch_fused_backward: `split` blocks per window; block j of a
+  // window forms the weight gradients of layers lo[j] .. hi[j] (a partition
+  // of 0 .. L-1, block 0 lowest) and block 0 also writes dx.
+  int split;
+  int lo[kFusedMaxSplit], hi[kFusedMaxSplit];
 };
 
 struct FusedReduceArgs {
@@ -141,6 +148,11 @@ struct FusedReduceArgs {
 bool fused_stack_eligible(int64_t n, int64_t width, int32_t num_layers);
 size_t fused_partial_bytes(int64_t batch, int32_t num_layers);
 hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hipStream_t st);
+// Blocks per window of the fused backward and their layer ranges (see
+// FusedBwdArgs), for `cus` compute units: up to kFusedMaxSplit when the
+// batch alone would leave compute units idle.
+void fused_backward_split(int batch, int num_layers, int cus, int* split, int* lo, int* hi);
+
 hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
                                  bool bidir, hipStream_t st);
 

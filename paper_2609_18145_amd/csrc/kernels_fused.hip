@@ -245,9 +245,18 @@ __global__ __launch_bounds__(3 * N) void fused_fwd_kernel(FusedFwdArgs a) {
 // ---------------------------------------------------------------------------
 // Backward: walks the layers in reverse with the gradient resident in LDS.
 //
-// 2 n / 64 waves in two roles that run side by side within a layer (one wave
-// of each role per SIMD at n = 256); they share only the gradient G, which
-// both read:
+// A window's backward may be shared by `split` blocks (small batches, so that
+// the grid fills the chip): every block runs the dX chain from the top layer
+// down, which needs only dY and the weights, and forms the weight gradients
+// of its own layers lo .. hi only, so it reads only those layers' inputs;
+// block 0 owns the lowest layers and also writes dx.  Each (window, layer)
+// partial is still written by exactly one block, and every value is formed
+// by the same sequence of operations whatever the split, so the results do
+// not depend on it (bitwise).
+//
+// Per layer, 2 n / 64 waves in two roles that run side by side (one wave of
+// each role per SIMD at n = 256); they share only the gradient G, which both
+// read:
 //  * weight-gradient waves: block c (0..3) is the 32 x 32 piece (outputs ob,
 //    inputs cb) of both dW_self and dW_off; one pass over the row pairs reads
 //    the fragments dY_L, dY_U (outputs) and X_L, X_U (inputs) and feeds
@@ -255,10 +264,13 @@ __global__ __launch_bounds__(3 * N) void fused_fwd_kernel(FusedFwdArgs a) {
 //    then stores the window's partial;
 //  * dX waves: 32 row pairs each, in two 32-column halves (the second half's
 //    MFMAs carry the first half's rounding and LDS writes).
-// The layer inputs are double-buffered, so the next layer's input and weights
-// are fetched from the start of the layer.  The per-layer arguments are read
-// from the kernel-argument block (the four activation buffers and two weight
-// sets fill the 160 KB of LDS at n = 256).
+// A layer above the block's own takes the dX alone, and then every wave
+// takes one 32-column half of 32 row pairs; the block's lowest layer (blocks
+// other than 0) takes the weight gradients alone.  The first two layer inputs
+// the block needs are fetched at the start, the others one layer ahead
+// (double-buffered), the weights one layer ahead.  The per-layer arguments
+// are read from the kernel-argument block (the four activation buffers and
+// two weight sets fill the 160 KB of LDS at n = 256).
 // ---------------------------------------------------------------------------
 template <int N, bool BIDIR>
 __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
@@ -267,33 +279,42 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
   extern __shared__ __attribute__((aligned(1024))) bf16 smem[];
   const int L = a.num_layers;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t win = (size_t)blockIdx.x * N * FW;
+  const int part = (int)(blockIdx.x % (unsigned)a.split);
+  const size_t win = (size_t)(blockIdx.x / (unsigned)a.split) * N * FW;
+  const int lo = a.lo[part], hi = a.hi[part];
+  const int last = part == 0 ? 0 : lo;   // the lowest layer this block visits
   bf16* G = smem;            // gradient of the current layer's output
   bf16* Gn = G + N * FW;     // gradient of its input (being built)
   bf16* Xs = Gn + N * FW;    // two layer-input buffers: x_l in buffer l % 2
   bf16* Wb = Xs + 2 * N * FW;  // two sets of [W_self | W_off], transposed-read layout
 
   dma_act<N, NW>(a.dy + win, G, wave, lane);
-  dma_act<N, NW>(a.xs[L - 1] + win, Xs + ((L - 1) & 1) * N * FW, wave, lane);
   dma_w_tr<NW>(a.ws[L - 1], Wb + ((L - 1) & 1) * 2 * WW, wave, lane);
   dma_w_tr<NW>(a.wo[L - 1], Wb + ((L - 1) & 1) * 2 * WW + WW, wave, lane);
+  dma_act<N, NW>(a.xs[hi] + win, Xs + (hi & 1) * N * FW, wave, lane);
+  if (hi - 1 >= lo) dma_act<N, NW>(a.xs[hi - 1] + win, Xs + ((hi - 1) & 1) * N * FW, wave, lane);
   wait_dma();
   __syncthreads();
 
-  for (int l = L - 1; l >= 0; l--) {
+  for (int l = L - 1; l >= last; l--) {
     const int d = a.dim[l], s = 1 << d;
+    const bool do_dw = l >= lo && l <= hi;
+    const bool do_dx = l > lo || part == 0;
     const bf16* Ws = Wb + (l & 1) * 2 * WW;
     const bf16* Wo = Ws + WW;
     const bf16* Xb = Xs + (l & 1) * N * FW;
-    if (l > 0) {
-      bf16* Wn = Wb + ((l - 1) & 1) * 2 * WW;
-      dma_w_tr<NW>(a.ws[l - 1], Wn, wave, lane);
-      dma_w_tr<NW>(a.wo[l - 1], Wn + WW, wave, lane);
-      dma_act<N, NW>(a.xs[l - 1] + win, Xs + ((l - 1) & 1) * N * FW, wave, lane);
+    if (l > last) {
+      if (l - 1 > lo || part == 0) {
+        bf16* Wn = Wb + ((l - 1) & 1) * 2 * WW;
+        dma_w_tr<NW>(a.ws[l - 1], Wn, wave, lane);
+        dma_w_tr<NW>(a.wo[l - 1], Wn + WW, wave, lane);
+      }
+      if (l < hi && l - 1 >= lo)
+        dma_act<N, NW>(a.xs[l - 1] + win, Xs + ((l - 1) & 1) * N * FW, wave, lane);
     }
-    if (wave < HW) {
+    if (do_dw && wave < HW) {
       // weight-gradient partials of this window
-      float* part = a.partial + ((size_t)blockIdx.x * L + l) * 2 * WW;
+      float* prt = a.partial + ((size_t)(blockIdx.x / (unsigned)a.split) * L + l) * 2 * WW;
 #pragma unroll
       for (int c = wave; c < 4; c += HW) {
         const int ob = (c >> 1) * 32, cb = (c & 1) * 32;
@@ -328,16 +349,17 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
         // straight from MFMA accumulators, and the split into 8-byte
         // write-through stores left half-written sectors that doubled the
         // HBM writes.
-        float* rowS = part + (size_t)(ob + (lane & 31)) * FW + cb + 4 * (lane >> 5);
+        float* rowS = prt + (size_t)(ob + (lane & 31)) * FW + cb + 4 * (lane >> 5);
 #pragma unroll
         for (int g = 0; g < 4; g++) {
           *(f32x4*)(rowS + 8 * g) = f32x4{accS[4 * g], accS[4 * g + 1], accS[4 * g + 2], accS[4 * g + 3]};
           *(f32x4*)(rowS + WW + 8 * g) = f32x4{accO[4 * g], accO[4 * g + 1], accO[4 * g + 2], accO[4 * g + 3]};
         }
       }
-    } else {
-      // dX: lower rows always take their partner's gradient through W_off^T
-      // (causal: the lower row is the sender), upper rows only when bidirectional.
+    } else if (do_dx && wave >= HW && do_dw) {
+      // dX beside the weight gradients: lower rows always take their
+      // partner's gradient through W_off^T (causal: the lower row is the
+      // sender), upper rows only when bidirectional.
       const int rL = lower_row(32 * (wave - HW) + (lane & 31), d), rU = rL + s;
       bf16x8 gL[4], gU[4], b1[2][4], b2[2][4];
 #pragma unroll
@@ -374,14 +396,40 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
       store_block(Gn, accL[0], accU[0], rL, rU, 0, lane);
       __builtin_amdgcn_sched_barrier(0);
       store_block(Gn, accL[1], accU[1], rL, rU, 1, lane);
+    } else if (do_dx && !do_dw) {
+      // dX alone: every wave takes one 32-column half of 32 row pairs, with
+      // the same operations per output as above.
+      const int t = wave / HW;
+      const int rL = lower_row(32 * (wave % HW) + (lane & 31), d), rU = rL + s;
+      bf16x8 gL[4], gU[4], b1[4], b2[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        const int ch = kk * 2 + (lane >> 5);
+        gL[kk] = *(const bf16x8*)(G + swz<FW>(rL, ch));
+        gU[kk] = *(const bf16x8*)(G + swz<FW>(rU, ch));
+        b1[kk] = tr_frag<FRB>(Ws, kk * 16, 32 * t, lane);
+        b2[kk] = tr_frag<FRB>(Wo, kk * 16, 32 * t, lane);
+      }
+      f32x16 accL, accU;
+#pragma unroll
+      for (int e = 0; e < 16; e++) { accL[e] = 0.f; accU[e] = 0.f; }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < 4; kk++) {
+        accL = mfma32(b1[kk], gL[kk], accL);
+        accU = mfma32(b1[kk], gU[kk], accU);
+        accL = mfma32(b2[kk], gU[kk], accL);
+        if (BIDIR) accU = mfma32(b2[kk], gL[kk], accU);
+      }
+      store_block(Gn, accL, accU, rL, rU, t, lane);
     }
     wait_dma();
     __syncthreads();  // Gn complete, partial stored; next input and weights landed
-    bf16* t = G;
+    bf16* tmp = G;
     G = Gn;
-    Gn = t;
+    Gn = tmp;
   }
-  copy_out<PCS, false>(G, a.dx + win, tid, NT);
+  if (part == 0) copy_out<PCS, false>(G, a.dx + win, tid, NT);
 }
 
 // dW_self[l] / dW_off[l] (+)= sum over windows of the partials.  Each block
@@ -431,7 +479,7 @@ hipError_t bwd_launch(const FusedBwdArgs& a, int batch, hipStream_t st) {
       (const void*)fused_bwd_kernel<N, BIDIR>, hipFuncAttributeMaxDynamicSharedMemorySize,
       (int)bwd_lds<N>());
   if (attr != hipSuccess) return attr;
-  fused_bwd_kernel<N, BIDIR><<<batch, 2 * N, bwd_lds<N>(), st>>>(a);
+  fused_bwd_kernel<N, BIDIR><<<batch * a.split, 2 * N, bwd_lds<N>(), st>>>(a);
   return hipGetLastError();
 }
 
@@ -470,8 +518,77 @@ hipError_t launch_fused_forward(const FusedFwdArgs& a, int batch, bool bidir, hi
   return bidir ? fwd_dispatch<true>(a, batch, st) : fwd_dispatch<false>(a, batch, st);
 }
 
-hipError_t launch_fused_backward(const FusedBwdArgs& a, const FusedReduceArgs& r, int batch,
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int c = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c <= 0)
+      c = 256;
+    cached[dev] = c;
+  }
+  return cached[dev];
+}
+
+// Relative time of a block of a split backward, in units of a layer that
+// runs the dX alone: a layer with both roles counts 2, the lowest layer of a
+// block other than 0 (weight gradients alone) 1, and every own layer after
+// the first two one more (its input is fetched one layer ahead rather than at
+// the start).
+static int split_cost(int L, int lo, int hi, bool first) {
+  const int own = hi - lo + 1;
+  const int late = own > 2 ? own - 2 : 0;
+  if (first) return (L - 1 - hi) + 2 * own + late;
+  return (L - 1 - hi) + 2 * (own - 1) + 1 + late;
+}
+
+void fused_backward_split(int batch, int num_layers, int cus, int* split, int* lo, int* hi) {
+  const int L = num_layers;
+  int S = batch > 0 ? cus / batch : 1;
+  S = S < 1 ? 1 : S;
+  S = S > kFusedMaxSplit ? kFusedMaxSplit : S;
+  S = S > L ? L : S;
+  *split = S;
+  if (S == 1) {
+    lo[0] = 0;
+    hi[0] = L - 1;
+    return;
+  }
+  // smallest bound T on every block's cost that a top-down greedy partition
+  // meets: each block from the top takes the longest range within T
+  for (int T = 1;; T++) {
+    int top = L - 1;
+    bool ok = true;
+    for (int j = S - 1; j >= 1 && ok; j--) {
+      int best = -1;
+      for (int c = j; c <= top; c++)
+        if (split_cost(L, c, top, false) <= T) {
+          best = c;
+          break;
+        }
+      if (best < 0) {
+        ok = false;
+      } else {
+        lo[j] = best;
+        hi[j] = top;
+        top = best - 1;
+      }
+    }
+    if (ok && split_cost(L, 0, top, true) <= T) {
+      lo[0] = 0;
+      hi[0] = top;
+      return;
+    }
+  }
+}
+
+hipError_t launch_fused_backward(const FusedBwdArgs& a0, const FusedReduceArgs& r, int batch,
                                  bool bidir, hipStream_t st) {
+  FusedBwdArgs a = a0;
+  fused_backward_split(batch, a.num_layers, device_cus(), &a.split, a.lo, a.hi);
   hipError_t e = bidir ? bwd_dispatch<true>(a, batch, st) : bwd_dispatch<false>(a, batch, st);
   if (e != hipSuccess) return e;
   const int blocks = r.num_layers * 2 * (WW / 4) / RED_OUT;   // exact: WW/4 = 1024

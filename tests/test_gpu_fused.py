@@ -114,6 +114,41 @@ def test_fused_accumulate_and_determinism():
         np.testing.assert_allclose(to_host(a), to_host(b) - 1.0, rtol=0, atol=1e-4)
 
 
+@pytest.mark.parametrize("causal", [False, True])
+def test_fused_backward_split_invariance_and_unsplit_path(causal):
+    """Small batches share each window's backward among up to four blocks
+    (every block replays the dX chain and forms the weight gradients of its
+    own layers); large batches run one block per window.  The same windows
+    inside batches of 256, 128 and 64 (one, two and four blocks per window
+    on 256 compute units) give bitwise the same dx, since the windows are
+    independent; at batch 256, dx and the weight gradients against the
+    oracle (the unsplit path)."""
+    s = inputs.make_preset("reach", batch=256)
+    if causal:
+        s = inputs.make_stack(batch=256, n=256, width=64, num_layers=8, causal=True,
+                              dtype="bf16", seed=11)
+    log(f"case: fused backward split invariance B=256/128/64 n=256 w=64 L=8 causal={causal}")
+    x = to_dev(s.x, "bf16")
+    ws = [to_dev(w, "bf16") for w in s.w_self]
+    wo = [to_dev(w, "bf16") for w in s.w_off]
+    dy = to_dev(s.dy, "bf16")
+    dxs = {}
+    for b in (256, 128, 64):
+        xs = hcmix.stack_forward(x[:b].contiguous(), ws, wo, s.layers, s.causal)
+        dx, dws, dwo = hcmix.stack_backward(xs, ws, wo, s.layers, dy[:b].contiguous(), s.causal)
+        torch.cuda.synchronize()
+        dxs[b] = dx
+        if b == 256:
+            ref = oracle.stack_forward(s.x, s.w_self, s.w_off, s.layers, s.causal)
+            rdx, rws, rwo = oracle.stack_backward(ref, s.w_self, s.w_off, s.layers, s.dy, s.causal)
+            assert row_rel_err(to_host(dx), rdx) <= TOL["bf16"]
+            e_w = max(fro_rel_err(to_host(g), r) for g, r in zip(dws + dwo, rws + rwo))
+            log(f"  B=256 dW err {e_w:.2e}")
+            assert e_w <= TOL["bf16"]
+    assert torch.equal(dxs[128], dxs[256][:128])
+    assert torch.equal(dxs[64], dxs[256][:64])
+
+
 def test_layer_by_layer_stack_path_fp32_and_wide_bf16():
     """Shapes outside the fused path go layer by layer inside the library."""
     for (batch, n, width, dtype, causal) in [(2, 16, 32, "f32", False), (2, 64, 128, "bf16", True)]:
