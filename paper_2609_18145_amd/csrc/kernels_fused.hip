@@ -292,8 +292,19 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
   dma_w_tr<NW>(a.ws[L - 1], Wb + ((L - 1) & 1) * 2 * WW, wave, lane);
   dma_w_tr<NW>(a.wo[L - 1], Wb + ((L - 1) & 1) * 2 * WW + WW, wave, lane);
   dma_act<N, NW>(a.xs[hi] + win, Xs + (hi & 1) * N * FW, wave, lane);
-  if (hi - 1 >= lo) dma_act<N, NW>(a.xs[hi - 1] + win, Xs + ((hi - 1) & 1) * N * FW, wave, lane);
-  wait_dma();
+  const bool two = hi - 1 >= lo;
+  if (two) dma_act<N, NW>(a.xs[hi - 1] + win, Xs + ((hi - 1) & 1) * N * FW, wave, lane);
+  // the top layer needs dY, its weights and (if it is the block's own) its
+  // input; the other inputs may still be in flight (loads complete in issue
+  // order, XI per activation buffer and wave) until the layer's closing wait
+  constexpr int XI = N / 8 / NW;
+  const int pending = (two ? 2 : 1) - (hi == L - 1 ? 1 : 0);
+  if (pending == 2)
+    wait_vmcnt<2 * XI>();
+  else if (pending == 1)
+    wait_vmcnt<XI>();
+  else
+    wait_dma();
   __syncthreads();
 
   for (int l = L - 1; l >= last; l--) {
@@ -433,29 +444,29 @@ __global__ __launch_bounds__(2 * N) void fused_bwd_kernel(FusedBwdArgs a) {
 }
 
 // dW_self[l] / dW_off[l] (+)= sum over windows of the partials.  Each block
-// handles 64 float4 outputs; its 4 thread groups sum consecutive quarters of
-// the windows in window order, and the quarters are then added in order, so
-// the result is the same on every run.
-constexpr int RED_OUT = 64;   // float4 outputs per block
-__global__ __launch_bounds__(256) void fused_dw_reduce_kernel(FusedReduceArgs a) {
-  __shared__ f32x4 part[4][RED_OUT];
+// handles 64 float4 outputs with 1024 threads: its 16 thread groups sum
+// consecutive sixteenths of the windows in window order (every wave reads
+// 1 KB contiguous per window), and the 16 group sums are then added in
+// order, so the result is the same on every run.
+constexpr int RED_OUT = 64;    // float4 outputs per block
+constexpr int RED_GROUPS = 16;
+__global__ __launch_bounds__(RED_OUT * RED_GROUPS) void fused_dw_reduce_kernel(FusedReduceArgs a) {
+  __shared__ f32x4 part[RED_GROUPS][RED_OUT];
   const int per = WW / 4;                           // float4 per matrix
-  const int idx = blockIdx.x * RED_OUT + (threadIdx.x % RED_OUT);
-  const int quarter = threadIdx.x / RED_OUT;
+  const int o = threadIdx.x % RED_OUT, grp = threadIdx.x / RED_OUT;
+  const int idx = blockIdx.x * RED_OUT + o;
   const int l = idx / (2 * per), m = (idx / per) % 2, j = idx % per;
-  const int q_len = (a.batch + 3) / 4;
-  const int b0 = quarter * q_len, b1 = min(a.batch, b0 + q_len);
+  const int q_len = (a.batch + RED_GROUPS - 1) / RED_GROUPS;
+  const int b0 = grp * q_len, b1 = min(a.batch, b0 + q_len);
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int b = b0; b < b1; b++)
     acc += ((const f32x4*)(a.partial + (((size_t)b * a.num_layers + l) * 2 + m) * WW))[j];
-  part[quarter][threadIdx.x % RED_OUT] = acc;
+  part[grp][o] = acc;
   __syncthreads();
-  if (quarter == 0) {
-    const int o = threadIdx.x;
+  if (grp == 0) {
     f32x4 sum = part[0][o];
-    sum += part[1][o];
-    sum += part[2][o];
-    sum += part[3][o];
+#pragma unroll
+    for (int g = 1; g < RED_GROUPS; g++) sum += part[g][o];
     f32x4* dst = (f32x4*)(m ? a.dwo[l] : a.dws[l]) + j;
     if (a.accumulate) sum += *dst;
     store_wt16(dst, __builtin_bit_cast(u32x4, sum));
@@ -533,16 +544,16 @@ static int device_cus() {
   return cached[dev];
 }
 
-// Relative time of a block of a split backward, in units of a layer that
-// runs the dX alone: a layer with both roles counts 2, the lowest layer of a
-// block other than 0 (weight gradients alone) 1, and every own layer after
-// the first two one more (its input is fetched one layer ahead rather than at
-// the start).
+// Relative time of a block of a split backward, from per-layer timings at
+// n = 256 (in units of about 0.5 us): a layer that runs the dX alone 3, one
+// with both roles 6, the lowest layer of a block other than 0 (weight
+// gradients alone) 4, and every own layer after the first two one more (its
+// input is fetched one layer ahead rather than at the start).
 static int split_cost(int L, int lo, int hi, bool first) {
   const int own = hi - lo + 1;
   const int late = own > 2 ? own - 2 : 0;
-  if (first) return (L - 1 - hi) + 2 * own + late;
-  return (L - 1 - hi) + 2 * (own - 1) + 1 + late;
+  if (first) return 3 * (L - 1 - hi) + 6 * own + late;
+  return 3 * (L - 1 - hi) + 6 * (own - 1) + 4 + late;
 }
 
 void fused_backward_split(int batch, int num_layers, int cus, int* split, int* lo, int* hi) {
@@ -592,7 +603,7 @@ hipError_t launch_fused_backward(const FusedBwdArgs& a0, const FusedReduceArgs& 
   hipError_t e = bidir ? bwd_dispatch<true>(a, batch, st) : bwd_dispatch<false>(a, batch, st);
   if (e != hipSuccess) return e;
   const int blocks = r.num_layers * 2 * (WW / 4) / RED_OUT;   // exact: WW/4 = 1024
-  fused_dw_reduce_kernel<<<blocks, 256, 0, st>>>(r);
+  fused_dw_reduce_kernel<<<blocks, RED_OUT * RED_GROUPS, 0, st>>>(r);
   return hipGetLastError();
 }
 
