@@ -272,8 +272,8 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the sharded path is described in DESIGN.md but not built.", file=sys.stderr)
+        print(f"bench.py: the hot path runs on one GPU only (asked for --gpus {args.gpus}); "
+              "sharding across GPUs is not implemented.", file=sys.stderr)
         return 2
 
     import numpy as np

@@ -28,13 +28,13 @@
  *
  * Errors: arguments are validated before anything is enqueued; a rejected
  * call has no effect.  HCMIX_ERR_INVALID_VALUE: null pointer, batch < 1, n not
- * a power of two >= 2, width < 1, layer < 0, unknown mode or dtype, an output
- * that overlaps an input, workspace smaller than the query, sizes beyond
- * 2^31 rows.  HCMIX_ERR_UNSUPPORTED: a shape or alignment this build has no
- * kernel for (bf16 needs width a multiple of 64 and 16-byte aligned
- * pointers; fp32 needs 4-byte aligned pointers).  HCMIX_ERR_HIP: a HIP call
- * or kernel launch failed; the message is available from
- * hcmix_last_hip_error().
+ * a power of two >= 2, width < 1 or above 65536, layer < 0, unknown mode or
+ * dtype, an output that overlaps an input, workspace smaller than the query,
+ * more than 2^30 rows (batch * n) or 2^40 elements.  HCMIX_ERR_UNSUPPORTED: a
+ * shape or alignment the library has no kernel for (bf16 needs width a
+ * multiple of 64 and 16-byte aligned pointers; fp32 needs 4-byte aligned
+ * pointers).  HCMIX_ERR_HIP: a HIP call or kernel launch failed; the message
+ * is available from hcmix_last_hip_error().
  */
 #ifndef HCMIX_H
 #define HCMIX_H

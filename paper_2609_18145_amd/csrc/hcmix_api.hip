@@ -21,6 +21,7 @@ hcmix_status hip_fail(hipError_t e) {
 
 constexpr int64_t kMaxRows = (int64_t)1 << 30;      // row indices stay in int32
 constexpr int64_t kMaxElems = (int64_t)1 << 40;     // element offsets in size_t
+constexpr int64_t kMaxWidth = (int64_t)1 << 16;     // widths stay in int32 products
 constexpr int32_t kMaxLayers = 1 << 16;
 
 size_t elem_size(int32_t dtype) { return dtype == HCMIX_BF16 ? 2 : 4; }
@@ -43,7 +44,7 @@ hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer,
   } else if (hcmix_dim(layer, n) < 0) {
     return HCMIX_ERR_INVALID_VALUE;
   }
-  if (batch < 1 || width < 1) return HCMIX_ERR_INVALID_VALUE;
+  if (batch < 1 || width < 1 || width > kMaxWidth) return HCMIX_ERR_INVALID_VALUE;
   if (mode != HCMIX_BIDIR && mode != HCMIX_CAUSAL) return HCMIX_ERR_INVALID_VALUE;
   if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return HCMIX_ERR_INVALID_VALUE;
   if (batch > kMaxRows / n) return HCMIX_ERR_INVALID_VALUE;

@@ -70,6 +70,7 @@ UNSUPPORTED = hcmix.HCMIX_ERR_UNSUPPORTED
 @pytest.mark.parametrize("kw,code", [
     (dict(n=0), INVALID), (dict(n=1), INVALID), (dict(n=12), INVALID),
     (dict(batch=0), INVALID), (dict(batch=-3), INVALID), (dict(width=0), INVALID),
+    (dict(width=1 << 17), INVALID),
     (dict(layer=-1), INVALID), (dict(mode=2), INVALID), (dict(dtype=7), INVALID),
     (dict(layer=-1, mode=0), INVALID),                # the local layer is causal only
     (dict(layer=-2, mode=1), INVALID), (dict(layer=-1, mode=1, n=12), INVALID),
