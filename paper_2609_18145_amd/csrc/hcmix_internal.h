@@ -5,7 +5,26 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace hcmix {
+
+// Raises kernel `fn`'s dynamic LDS limit to `bytes` on the current device,
+// once per device and call site: `done` is the call site's record of the
+// devices already set (bit = device index; devices past 63 are set on every
+// call).  The attribute is per device, so a process that drives several GPUs
+// needs it on each.
+inline hipError_t lds_limit_once(std::atomic<unsigned long long>& done, const void* fn,
+                                 int bytes) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const unsigned long long bit = (dev >= 0 && dev < 64) ? 1ull << dev : 0ull;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

@@ -811,8 +811,8 @@ hipError_t mix_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out, 
 #define HCMIX_MIX(PL, PU)                                                                   \
   {                                                                                         \
     auto k = mix_bf16_kernel<BMP, BN, WM, WN, BK, NS, PL, PU, TRANS_B>;                     \
-    static const hipError_t attr = hipFuncSetAttribute(                                     \
-        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+    static std::atomic<unsigned long long> lds_set{0};                                      \
+    const hipError_t attr = lds_limit_once(lds_set, (const void*)k, (int)lds);             \
     if (attr != hipSuccess) return attr;                                                    \
     k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, pairs, width, width, width, width, d);     \
   }
@@ -834,8 +834,8 @@ hipError_t gemm_launch(const bf16* A, const bf16* B, bf16* out, int rows, int K,
   const int blocks = ((pairs + MIX_BMP - 1) / MIX_BMP) * (N / BN);
   const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
   auto k = mix_bf16_kernel<MIX_BMP, BN, WM, WN, MIX_BK, MIX_NS, false, false, TRANS_B>;
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = lds_limit_once(lds_set, (const void*)k, (int)lds);
   if (attr != hipSuccess) return attr;
   k<<<blocks, C::NT, lds, st>>>(A, B, B, out, pairs, K, N, ldb, ldo, 0);
   return hipGetLastError();
@@ -849,8 +849,8 @@ hipError_t shift_launch(const bf16* A, const bf16* B1, const bf16* B2, bf16* out
   const int blocks = ((rows + BM - 1) / BM) * (width / BN);
   const size_t lds = (size_t)C::LDS_ELEMS * sizeof(bf16);
   auto k = shift_bf16_kernel<BM, BN, WM, WN, MIX_BK, DELTA, TRANS_B>;
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = lds_limit_once(lds_set, (const void*)k, (int)lds);
   if (attr != hipSuccess) return attr;
   k<<<blocks, C::NT, lds, st>>>(A, B1, B2, out, rows, width, n);
   return hipGetLastError();
@@ -936,8 +936,8 @@ hipError_t dw_launch(const bf16* X, const bf16* dY, float* partial, int pairs, i
 #define HCMIX_DW(LINK)                                                                      \
   {                                                                                         \
     auto k = dw_bf16_kernel<BO, BC, WO, WC, LINK>;                                          \
-    static const hipError_t attr = hipFuncSetAttribute(                                     \
-        (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+    static std::atomic<unsigned long long> lds_set{0};                                      \
+    const hipError_t attr = lds_limit_once(lds_set, (const void*)k, (int)lds);             \
     if (attr != hipSuccess) return attr;                                                    \
     k<<<blocks, C::NT, lds, st>>>(X, dY, partial, pairs, width, d, n, pps);                 \
   }
@@ -1031,8 +1031,8 @@ hipError_t launch_dw_batch_bf16(const DwBatchArgs& a, hipStream_t st) {
   const int tiles = (a.width / DW_BO) * (a.width / DW_BC);
   const int blocks = a.num_layers * a.splits * tiles;
   auto k = dw_batch_kernel<DW_BO, DW_BC, 2, 2>;
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr = lds_limit_once(lds_set, (const void*)k, (int)C::LDS);
   if (attr != hipSuccess) return attr;
   k<<<blocks, C::NT, C::LDS, st>>>(a);
   hipError_t e = hipGetLastError();

@@ -476,9 +476,9 @@ __global__ __launch_bounds__(RED_OUT * RED_GROUPS) void fused_dw_reduce_kernel(F
 
 template <int N, bool BIDIR>
 hipError_t fwd_launch(const FusedFwdArgs& a, int batch, hipStream_t st) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)fused_fwd_kernel<N, BIDIR>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)fwd_lds<N>());
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr =
+      lds_limit_once(lds_set, (const void*)fused_fwd_kernel<N, BIDIR>, (int)fwd_lds<N>());
   if (attr != hipSuccess) return attr;
   fused_fwd_kernel<N, BIDIR><<<batch, 3 * N, fwd_lds<N>(), st>>>(a);
   return hipGetLastError();
@@ -486,9 +486,9 @@ hipError_t fwd_launch(const FusedFwdArgs& a, int batch, hipStream_t st) {
 
 template <int N, bool BIDIR>
 hipError_t bwd_launch(const FusedBwdArgs& a, int batch, hipStream_t st) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)fused_bwd_kernel<N, BIDIR>, hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)bwd_lds<N>());
+  static std::atomic<unsigned long long> lds_set{0};
+  const hipError_t attr =
+      lds_limit_once(lds_set, (const void*)fused_bwd_kernel<N, BIDIR>, (int)bwd_lds<N>());
   if (attr != hipSuccess) return attr;
   fused_bwd_kernel<N, BIDIR><<<batch * a.split, 2 * N, bwd_lds<N>(), st>>>(a);
   return hipGetLastError();

@@ -360,8 +360,8 @@ hipError_t head_launch(const bf16* x, const bf16* w, const float* bias, const in
   using C = HeadCfg<NT>;
   const int blocks = (rows + HEAD_ROWS - 1) / HEAD_ROWS;
   auto k = head_ce_kernel<NT>;
-  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)C::LDS);
+  static std::atomic<unsigned long long> lds_set{0};
+  hipError_t e = lds_limit_once(lds_set, (const void*)k, (int)C::LDS);
   if (e != hipSuccess) return e;
   k<<<blocks, LM_THREADS, C::LDS, st>>>(x, w, bias, targets, scale, loss, dlogits,
                                          dbias ? dbp : nullptr, rows, width);

@@ -397,15 +397,15 @@ hipError_t launch_shared_forward(const SharedFwdArgs& a, int batch, int elem_byt
   const int blocks = shared_blocks(batch, a.width, elem_bytes);
   const size_t lds = shared_lds_bytes(a.n, elem_bytes);
   if (elem_bytes == 2) {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)shared_fwd_kernel<bf16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-        (int)shared_lds_bytes(kSharedMaxN, 2));
+    static std::atomic<unsigned long long> lds_set{0};
+    const hipError_t attr =
+        lds_limit_once(lds_set, (const void*)shared_fwd_kernel<bf16>, (int)shared_lds_bytes(kSharedMaxN, 2));
     if (attr != hipSuccess) return attr;
     shared_fwd_kernel<bf16><<<blocks, SH_THREADS, lds, st>>>(a);
   } else {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)shared_fwd_kernel<float>, hipFuncAttributeMaxDynamicSharedMemorySize,
-        (int)shared_lds_bytes(kSharedMaxN, 2));
+    static std::atomic<unsigned long long> lds_set{0};
+    const hipError_t attr =
+        lds_limit_once(lds_set, (const void*)shared_fwd_kernel<float>, (int)shared_lds_bytes(kSharedMaxN, 2));
     if (attr != hipSuccess) return attr;
     shared_fwd_kernel<float><<<blocks, SH_THREADS, lds, st>>>(a);
   }
@@ -417,15 +417,15 @@ hipError_t launch_shared_backward(const SharedBwdArgs& a, const SharedReduceArgs
   const int blocks = shared_blocks(batch, a.width, elem_bytes);
   const size_t lds = shared_lds_bytes(a.n, elem_bytes);
   if (elem_bytes == 2) {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)shared_bwd_kernel<bf16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-        (int)shared_lds_bytes(kSharedMaxN, 2));
+    static std::atomic<unsigned long long> lds_set{0};
+    const hipError_t attr =
+        lds_limit_once(lds_set, (const void*)shared_bwd_kernel<bf16>, (int)shared_lds_bytes(kSharedMaxN, 2));
     if (attr != hipSuccess) return attr;
     shared_bwd_kernel<bf16><<<blocks, SH_THREADS, lds, st>>>(a);
   } else {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)shared_bwd_kernel<float>, hipFuncAttributeMaxDynamicSharedMemorySize,
-        (int)shared_lds_bytes(kSharedMaxN, 2));
+    static std::atomic<unsigned long long> lds_set{0};
+    const hipError_t attr =
+        lds_limit_once(lds_set, (const void*)shared_bwd_kernel<float>, (int)shared_lds_bytes(kSharedMaxN, 2));
     if (attr != hipSuccess) return attr;
     shared_bwd_kernel<float><<<blocks, SH_THREADS, lds, st>>>(a);
   }
