@@ -32,9 +32,14 @@
  * dtype, an output that overlaps an input, workspace smaller than the query,
  * more than 2^30 rows (batch * n) or 2^40 elements.  HCMIX_ERR_UNSUPPORTED: a
  * shape or alignment the library has no kernel for (bf16 needs width a
- * multiple of 64 and 16-byte aligned pointers; fp32 needs 4-byte aligned
+ * multiple of 8 and 16-byte aligned pointers; fp32 needs 4-byte aligned
  * pointers).  HCMIX_ERR_HIP: a HIP call or kernel launch failed; the message
  * is available from hcmix_last_hip_error().
+ *
+ * Kernels of the mixing layer: bf16 widths that are a multiple of 64 run on
+ * matrix-core (MFMA) kernels; fp32 and the other bf16 widths (multiples of 8)
+ * run on fp32 FMA kernels.  Both accumulate in fp32 and round each bf16
+ * output once, so they agree up to the order of summation.
  */
 #ifndef HCMIX_H
 #define HCMIX_H
@@ -294,7 +299,7 @@ hcmix_status hcmix_head_backward(int64_t rows, int64_t width, int32_t vocab, con
  * x: [batch][width], the stack's input at `pos` for every window; y:
  * [batch][width], the stack's output there.  layers: host array of layer codes
  * as for the stacks (hypercube layers or HCMIX_LAYER_NEAR); the stack is
- * causal.  bf16: width a multiple of 64, 16-byte aligned pointers; fp32: 4-byte
+ * causal.  bf16: width a multiple of 8, 16-byte aligned pointers; fp32: 4-byte
  * aligned.  Results equal those of hcmix_stack_forward over the window at
  * position pos, up to the order of floating-point summation.
  * HCMIX_ERR_INVALID_VALUE also for pos outside [0, n), a short cache, or y or

@@ -49,14 +49,18 @@ hcmix_status check_shape(int64_t batch, int64_t n, int64_t width, int32_t layer,
   if (dtype != HCMIX_F32 && dtype != HCMIX_BF16) return HCMIX_ERR_INVALID_VALUE;
   if (batch > kMaxRows / n) return HCMIX_ERR_INVALID_VALUE;
   if (batch * n > kMaxElems / width) return HCMIX_ERR_INVALID_VALUE;
-  if (dtype == HCMIX_BF16 && width % 64 != 0) return HCMIX_ERR_UNSUPPORTED;
+  if (dtype == HCMIX_BF16 && width % 8 != 0) return HCMIX_ERR_UNSUPPORTED;
   return HCMIX_OK;
 }
+
+// bf16 widths that are a multiple of 64 run on the MFMA kernels; fp32, and
+// bf16 widths that are only a multiple of 8, on the FMA kernels.
+bool mfma_path(int32_t dtype, int64_t width) { return dtype == HCMIX_BF16 && width % 64 == 0; }
 
 // Backward workspace (bf16): the split-K partial sums of the weight
 // gradients, [splits][2][width][width] fp32.
 size_t layer_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t dtype) {
-  if (dtype != HCMIX_BF16) return 0;
+  if (!mfma_path(dtype, width)) return 0;
   const int splits = dw_bf16_splits((int)(batch * n), (int)width);
   return align256((size_t)splits * 2 * width * width * sizeof(float));
 }
@@ -65,7 +69,7 @@ size_t layer_workspace_bytes(int64_t batch, int64_t n, int64_t width, int32_t dt
 // or more layers on the layer-by-layer path): dX then multiplies by W^T with
 // the same kernel and the same 128-bit fragment reads as the forward.
 size_t transposed_weight_bytes(int64_t width, int32_t num_layers, int32_t dtype) {
-  if (dtype != HCMIX_BF16 || num_layers < 2) return 0;
+  if (!mfma_path(dtype, width) || num_layers < 2) return 0;
   return align256((size_t)2 * num_layers * width * width * sizeof(bf16));
 }
 
@@ -148,7 +152,7 @@ bool any_local_layer(const int32_t* layers, int32_t num_layers) {
 // d >= 0: hypercube layer of dimension d; d < 0: the local layer (jump 1).
 hipError_t run_forward(int rows, int w, int d, int n, int bidir, int32_t dtype, const void* x,
                        const void* w_self, const void* w_off, void* y, hipStream_t s) {
-  if (dtype == HCMIX_BF16) {
+  if (mfma_path(dtype, w)) {
     if (d < 0)
       return launch_shift_bf16((const bf16*)x, (const bf16*)w_self, (const bf16*)w_off, (bf16*)y,
                                rows, w, n, /*delta=*/-1, /*transpose_b=*/false, s);
@@ -156,8 +160,8 @@ hipError_t run_forward(int rows, int w, int d, int n, int bidir, int32_t dtype, 
                            rows, w, d, /*partner_lower=*/bidir, /*partner_upper=*/1,
                            /*transpose_b=*/false, s);
   }
-  return launch_mix_f32((const float*)x, (const float*)w_self, (const float*)w_off, (float*)y,
-                        rows, w, d, bidir, 1, n, /*shift=*/-1, /*transpose_w=*/false, s);
+  return launch_mix_fma(x, w_self, w_off, y, rows, w, d, bidir, 1, n, /*shift=*/-1,
+                        /*transpose_w=*/false, dtype == HCMIX_BF16, s);
 }
 
 // dX of one bf16 layer with the weights read as given (transpose_b) or from
@@ -176,18 +180,18 @@ hipError_t run_backward(int rows, int w, int d, int n, int bidir, int32_t dtype,
                         float* dw_self, float* dw_off, int accumulate, void* workspace,
                         hipStream_t s) {
   hipError_t e;
-  if (dtype == HCMIX_BF16) {
+  if (mfma_path(dtype, w)) {
     e = run_dx_bf16(rows, w, d, n, bidir, (const bf16*)dy, (const bf16*)w_self,
                     (const bf16*)w_off, (bf16*)dx, /*transpose_b=*/true, s);
     if (e == hipSuccess)
       e = launch_dw_bf16((const bf16*)x, (const bf16*)dy, (float*)workspace, dw_self, dw_off,
                          rows, w, d, n, bidir, accumulate, s);
   } else {
-    e = launch_mix_f32((const float*)dy, (const float*)w_self, (const float*)w_off, (float*)dx,
-                       rows, w, d, 1, bidir, n, /*shift=*/1, /*transpose_w=*/true, s);
+    const bool b16 = dtype == HCMIX_BF16;
+    e = launch_mix_fma(dy, w_self, w_off, dx, rows, w, d, 1, bidir, n, /*shift=*/1,
+                       /*transpose_w=*/true, b16, s);
     if (e == hipSuccess)
-      e = launch_dw_f32((const float*)x, (const float*)dy, dw_self, dw_off, rows, w, d, n, bidir,
-                        accumulate, s);
+      e = launch_dw_fma(x, dy, dw_self, dw_off, rows, w, d, n, bidir, accumulate, b16, s);
   }
   return e;
 }
@@ -590,7 +594,7 @@ hcmix_status hcmix_stack_backward(int64_t batch, int64_t n, int64_t width, int32
     for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
       void* out = l == 0 ? dx : gbuf[l & 1];
       const int d = hcmix_dim(layers[l], n);
-      if (dtype == HCMIX_BF16 && num_layers > 1) {
+      if (mfma_path(dtype, w) && num_layers > 1) {
         // dX = W_self^T dy (+ partner W_off^T dy): the forward kernels on W^T
         e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g, wt + 2 * (size_t)l * ww,
                         wt + (2 * (size_t)l + 1) * ww, (bf16*)out, /*transpose_b=*/false, s);
@@ -671,7 +675,7 @@ hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
   if (need > 0) e = transpose_weights(w, num_layers, w_self, w_off, wt, s);
   for (int l = num_layers - 1; l >= 0 && e == hipSuccess; l--) {
     const int d = hcmix_dim(layers[l], n);
-    if (dtype == HCMIX_BF16) {
+    if (mfma_path(dtype, w)) {
       if (need > 0)
         e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g(l + 1), wt + 2 * (size_t)l * ww,
                         wt + (2 * (size_t)l + 1) * ww, (bf16*)g(l), /*transpose_b=*/false, s);
@@ -679,9 +683,8 @@ hcmix_status hcmix_stack_backward_data(int64_t batch, int64_t n, int64_t width,
         e = run_dx_bf16(rows, w, d, (int)n, bidir, (const bf16*)g(l + 1), (const bf16*)w_self[l],
                         (const bf16*)w_off[l], (bf16*)g(l), /*transpose_b=*/true, s);
     } else {
-      e = launch_mix_f32((const float*)g(l + 1), (const float*)w_self[l], (const float*)w_off[l],
-                         (float*)g(l), rows, w, d, 1, bidir, (int)n, /*shift=*/1,
-                         /*transpose_w=*/true, s);
+      e = launch_mix_fma(g(l + 1), w_self[l], w_off[l], g(l), rows, w, d, 1, bidir, (int)n,
+                         /*shift=*/1, /*transpose_w=*/true, dtype == HCMIX_BF16, s);
     }
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
@@ -744,12 +747,12 @@ hcmix_status hcmix_stack_weight_gradients(int64_t batch, int64_t n, int64_t widt
   } else {
     for (int l = 0; l < num_layers && e == hipSuccess; l++) {
       const int d = hcmix_dim(layers[l], n);
-      if (dtype == HCMIX_BF16)
+      if (mfma_path(dtype, w))
         e = launch_dw_bf16((const bf16*)xs_in[l], (const bf16*)dys[l], (float*)workspace,
                            dw_self[l], dw_off[l], rows, w, d, (int)n, bidir, accumulate != 0, s);
       else
-        e = launch_dw_f32((const float*)xs_in[l], (const float*)dys[l], dw_self[l], dw_off[l],
-                          rows, w, d, (int)n, bidir, accumulate != 0, s);
+        e = launch_dw_fma(xs_in[l], dys[l], dw_self[l], dw_off[l], rows, w, d, (int)n, bidir,
+                          accumulate != 0, dtype == HCMIX_BF16, s);
     }
   }
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
@@ -1006,7 +1009,7 @@ hcmix_status hcmix_decode_step(int64_t batch, int64_t n, int64_t width, int32_t 
       a.in_stride = a.partner_stride = a.out_stride = a.rec_stride = width;
       a.batch = (int)batch;
       a.width = (int)width;
-      e = launch_decode_bf16(a, s);
+      e = mfma_path(dtype, width) ? launch_decode_bf16(a, s) : launch_decode_bf16_fma(a, s);
     } else {
       DecodeLayerArgsF32 a = {};
       a.x_in = (const float*)in;

@@ -47,21 +47,24 @@ __device__ __forceinline__ bf16 to_bf16(float v) { return (bf16)v; }
 
 // ---- launchers (each returns hipGetLastError() of its launch) ----
 
-// out[r][j] = sum_k A[r][k] B1(j,k) + m(r) sum_k A[p(r)][k] B2(j,k), fp32.
+// FMA path (fp32 arithmetic; data fp32, or bf16 when bf16_data, widened
+// exactly and each output rounded once):
+// out[r][j] = sum_k A[r][k] B1(j,k) + m(r) sum_k A[p(r)][k] B2(j,k).
 // B(j,k) = W[j*width+k] when !transpose_w, W[k*width+j] when transpose_w.
 // d >= 0: p(r) = r ^ 2^d, m(r) = partner_lower for rows with bit d clear,
 // partner_upper otherwise.  d < 0 (local layer): p(r) = r + shift over windows
 // of n rows, shift = -1 (m = 0 at a window's first row) or +1 (at its last).
-// The weight gradients of a local layer (d < 0) pair row r with r - 1.
-hipError_t launch_mix_f32(const float* A, const float* W1, const float* W2, float* out,
-                          int rows, int width, int d, int partner_lower, int partner_upper,
-                          int n, int shift, bool transpose_w, hipStream_t st);
+// The weight gradients (fp32 out) of a local layer (d < 0) pair row r with
+// r - 1.
+hipError_t launch_mix_fma(const void* A, const void* W1, const void* W2, void* out, int rows,
+                          int width, int d, int partner_lower, int partner_upper, int n,
+                          int shift, bool transpose_w, bool bf16_data, hipStream_t st);
 
-hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo,
-                         int rows, int width, int d, int n, int bidir, int accumulate,
+hipError_t launch_dw_fma(const void* X, const void* dY, float* dws, float* dwo, int rows,
+                         int width, int d, int n, int bidir, int accumulate, bool bf16_data,
                          hipStream_t st);
 
-// bf16 MFMA: same contraction as launch_mix_f32.  B(j,k) = B[j*width+k] when
+// bf16 MFMA: same contraction as launch_mix_fma.  B(j,k) = B[j*width+k] when
 // !transpose_b, B[k*width+j] when transpose_b (read transposed from LDS).
 // width % 64 == 0.
 hipError_t launch_mix_bf16(const bf16* A, const bf16* B1, const bf16* B2, bf16* out,
@@ -273,5 +276,7 @@ struct DecodeLayerArgsF32 {
 };
 hipError_t launch_decode_bf16(const DecodeLayerArgs& a, hipStream_t st);   // width % 64 == 0
 hipError_t launch_decode_f32(const DecodeLayerArgsF32& a, hipStream_t st);
+// bf16 widths that are not a multiple of 64: plain fp32 FMAs, one rounding
+hipError_t launch_decode_bf16_fma(const DecodeLayerArgs& a, hipStream_t st);
 
 }  // namespace hcmix

@@ -81,20 +81,30 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_bf16_kernel(DecodeLayer
   *(bf16x4*)(a.out + (size_t)b * a.out_stride + o0 + 4 * q) = v;
 }
 
-// fp32: one thread per output (window b, column o), plain FMAs.
-__global__ __launch_bounds__(256) void decode_f32_kernel(DecodeLayerArgsF32 a) {
+// fp32 arithmetic, one thread per output (window b, column o), plain FMAs:
+// fp32 data, or bf16 widths that are not a multiple of 64 (operands widened
+// exactly, the output rounded once).
+__device__ __forceinline__ float dec_widen(float v) { return v; }
+__device__ __forceinline__ float dec_widen(bf16 v) { return (float)v; }
+__device__ __forceinline__ void dec_store(float* p, float v) { *p = v; }
+__device__ __forceinline__ void dec_store(bf16* p, float v) { *p = to_bf16(v); }
+
+template <typename Args>
+__global__ __launch_bounds__(256) void decode_fma_kernel(Args a) {
   const int o = blockIdx.x * 64 + (threadIdx.x & 63);
   const int b = blockIdx.y * 4 + (threadIdx.x >> 6);
   if (o >= a.width || b >= a.batch) return;
-  const float* xin = a.x_in + (size_t)b * a.in_stride;
+  const auto* xin = a.x_in + (size_t)b * a.in_stride;
   float acc = 0.f;
-  for (int c = 0; c < a.width; c++) acc = fmaf(a.w_self[(size_t)o * a.width + c], xin[c], acc);
+  for (int c = 0; c < a.width; c++)
+    acc = fmaf(dec_widen(a.w_self[(size_t)o * a.width + c]), dec_widen(xin[c]), acc);
   if (a.x_partner) {
-    const float* xp = a.x_partner + (size_t)b * a.partner_stride;
-    for (int c = 0; c < a.width; c++) acc = fmaf(a.w_off[(size_t)o * a.width + c], xp[c], acc);
+    const auto* xp = a.x_partner + (size_t)b * a.partner_stride;
+    for (int c = 0; c < a.width; c++)
+      acc = fmaf(dec_widen(a.w_off[(size_t)o * a.width + c]), dec_widen(xp[c]), acc);
   }
   if (a.record) a.record[(size_t)b * a.rec_stride + o] = xin[o];
-  a.out[(size_t)b * a.out_stride + o] = acc;
+  dec_store(a.out + (size_t)b * a.out_stride + o, acc);
 }
 
 }  // namespace
@@ -111,7 +121,12 @@ hipError_t launch_decode_bf16(const DecodeLayerArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_decode_f32(const DecodeLayerArgsF32& a, hipStream_t st) {
-  decode_f32_kernel<<<dim3((a.width + 63) / 64, (a.batch + 3) / 4), 256, 0, st>>>(a);
+  decode_fma_kernel<<<dim3((a.width + 63) / 64, (a.batch + 3) / 4), 256, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_bf16_fma(const DecodeLayerArgs& a, hipStream_t st) {
+  decode_fma_kernel<<<dim3((a.width + 63) / 64, (a.batch + 3) / 4), 256, 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -1,12 +1,20 @@
-// fp32 path of the mixing layer: LDS-tiled FMA kernels, no matrix
-// instructions, so every product and sum is an IEEE fp32 operation.
-// Used for fp32 inputs of any width; the bf16 MFMA path lives in
-// kernels_bf16.hip.
+// FMA path of the mixing layer: LDS-tiled kernels with no matrix
+// instructions, every product and sum an IEEE fp32 operation.  Used for fp32
+// inputs of any width, and for bf16 inputs whose width is a multiple of 8 but
+// not of 64 (the MFMA tiles of kernels_bf16.hip need 64): bf16 operands are
+// widened to fp32 exactly, and each bf16 output is rounded once (RNE), as on
+// the MFMA path.
 #include "hcmix_internal.h"
 
 namespace hcmix {
 
 namespace {
+
+__device__ __forceinline__ float widen(float v) { return v; }
+__device__ __forceinline__ float widen(bf16 v) { return (float)v; }
+template <typename E> __device__ __forceinline__ E narrow(float v);
+template <> __device__ __forceinline__ float narrow<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 narrow<bf16>(float v) { return to_bf16(v); }
 
 constexpr int T = 64;    // output tile edge
 constexpr int KC = 16;   // contraction chunk
@@ -16,10 +24,10 @@ constexpr int NT = 256;  // threads per block: 16 x 16, 4 x 4 outputs each
 // Hypercube layer (d >= 0): p(r) = r ^ 2^d, m(r) = partner_upper / partner_lower
 // by bit d of r.  Local layer (d < 0): p(r) = r + shift with shift = -1
 // (forward; m = 0 at a window's first row) or +1 (dX; m = 0 at its last row).
-template <bool TRANSPOSE_W>
-__global__ __launch_bounds__(NT) void mix_f32_kernel(
-    const float* __restrict__ A, const float* __restrict__ W1, const float* __restrict__ W2,
-    float* __restrict__ out, int rows, int width, int d, int partner_lower, int partner_upper,
+template <typename E, bool TRANSPOSE_W>
+__global__ __launch_bounds__(NT) void mix_fma_kernel(
+    const E* __restrict__ A, const E* __restrict__ W1, const E* __restrict__ W2,
+    E* __restrict__ out, int rows, int width, int d, int partner_lower, int partner_upper,
     int n, int shift) {
   __shared__ float sA[KC][T + 1];
   __shared__ float sP[KC][T + 1];
@@ -40,7 +48,7 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
         const int r = r0 + m, k = k0 + kk;
         float a = 0.f, p = 0.f;
         if (r < rows && k < width) {
-          a = A[(size_t)r * width + k];
+          a = widen(A[(size_t)r * width + k]);
           int take, pr;
           if (d >= 0) {
             take = ((r >> d) & 1) ? partner_upper : partner_lower;
@@ -50,7 +58,7 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
             take = shift < 0 ? pos != 0 : pos != n - 1;
             pr = r + shift;
           }
-          if (take) p = A[(size_t)pr * width + k];
+          if (take) p = widen(A[(size_t)pr * width + k]);
         }
         sA[kk][m] = a;
         sP[kk][m] = p;
@@ -64,8 +72,8 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
         float w1 = 0.f, w2 = 0.f;
         if (jj < width && k < width) {
           const size_t off = TRANSPOSE_W ? (size_t)k * width + jj : (size_t)jj * width + k;
-          w1 = W1[off];
-          w2 = W2[off];
+          w1 = widen(W1[off]);
+          w2 = widen(W2[off]);
         }
         sW1[kk][j] = w1;
         sW2[kk][j] = w2;
@@ -96,7 +104,7 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
 #pragma unroll
     for (int j = 0; j < 4; j++) {
       const int jj = j0 + tx * 4 + j;
-      if (jj < width) out[(size_t)r * width + jj] = acc[i][j];
+      if (jj < width) out[(size_t)r * width + jj] = narrow<E>(acc[i][j]);
     }
   }
 }
@@ -105,8 +113,9 @@ __global__ __launch_bounds__(NT) void mix_f32_kernel(
 // with p(r) = r ^ 2^d (hypercube layer) or r - 1 (local layer, d < 0; m = 0 at
 // a window's first row).  One block per 64 x 64 output tile walks every row in
 // a fixed order.
-__global__ __launch_bounds__(NT) void dw_f32_kernel(
-    const float* __restrict__ X, const float* __restrict__ dY, float* __restrict__ dws,
+template <typename E>
+__global__ __launch_bounds__(NT) void dw_fma_kernel(
+    const E* __restrict__ X, const E* __restrict__ dY, float* __restrict__ dws,
     float* __restrict__ dwo, int rows, int width, int d, int n, int bidir, int accumulate) {
   __shared__ float sG[KC][T + 1];
   __shared__ float sX[KC][T + 1];
@@ -124,13 +133,13 @@ __global__ __launch_bounds__(NT) void dw_f32_kernel(
       const int r = rb + kk;
       float g = 0.f, xv = 0.f, xp = 0.f;
       if (r < rows) {
-        if (o0 + j < width) g = dY[(size_t)r * width + o0 + j];
+        if (o0 + j < width) g = widen(dY[(size_t)r * width + o0 + j]);
         if (c0 + j < width) {
-          xv = X[(size_t)r * width + c0 + j];
+          xv = widen(X[(size_t)r * width + c0 + j]);
           if (d < 0) {
-            if (r & (n - 1)) xp = X[(size_t)(r - 1) * width + c0 + j];
+            if (r & (n - 1)) xp = widen(X[(size_t)(r - 1) * width + c0 + j]);
           } else if (bidir || ((r >> d) & 1)) {
-            xp = X[(size_t)(r ^ s) * width + c0 + j];
+            xp = widen(X[(size_t)(r ^ s) * width + c0 + j]);
           }
         }
       }
@@ -175,23 +184,40 @@ __global__ __launch_bounds__(NT) void dw_f32_kernel(
 
 }  // namespace
 
-hipError_t launch_mix_f32(const float* A, const float* W1, const float* W2, float* out, int rows,
-                          int width, int d, int partner_lower, int partner_upper, int n,
-                          int shift, bool transpose_w, hipStream_t st) {
+template <typename E>
+hipError_t mix_fma_launch(const void* A, const void* W1, const void* W2, void* out, int rows,
+                          int width, int d, int partner_lower, int partner_upper, int n, int shift,
+                          bool transpose_w, hipStream_t st) {
   dim3 grid((rows + T - 1) / T, (width + T - 1) / T);
+  const E *a = (const E*)A, *w1 = (const E*)W1, *w2 = (const E*)W2;
   if (transpose_w)
-    mix_f32_kernel<true><<<grid, NT, 0, st>>>(A, W1, W2, out, rows, width, d, partner_lower,
-                                              partner_upper, n, shift);
+    mix_fma_kernel<E, true><<<grid, NT, 0, st>>>(a, w1, w2, (E*)out, rows, width, d,
+                                                 partner_lower, partner_upper, n, shift);
   else
-    mix_f32_kernel<false><<<grid, NT, 0, st>>>(A, W1, W2, out, rows, width, d, partner_lower,
-                                               partner_upper, n, shift);
+    mix_fma_kernel<E, false><<<grid, NT, 0, st>>>(a, w1, w2, (E*)out, rows, width, d,
+                                                  partner_lower, partner_upper, n, shift);
   return hipGetLastError();
 }
 
-hipError_t launch_dw_f32(const float* X, const float* dY, float* dws, float* dwo, int rows,
-                         int width, int d, int n, int bidir, int accumulate, hipStream_t st) {
+hipError_t launch_mix_fma(const void* A, const void* W1, const void* W2, void* out, int rows,
+                          int width, int d, int partner_lower, int partner_upper, int n,
+                          int shift, bool transpose_w, bool bf16_data, hipStream_t st) {
+  return bf16_data ? mix_fma_launch<bf16>(A, W1, W2, out, rows, width, d, partner_lower,
+                                          partner_upper, n, shift, transpose_w, st)
+                   : mix_fma_launch<float>(A, W1, W2, out, rows, width, d, partner_lower,
+                                           partner_upper, n, shift, transpose_w, st);
+}
+
+hipError_t launch_dw_fma(const void* X, const void* dY, float* dws, float* dwo, int rows,
+                         int width, int d, int n, int bidir, int accumulate, bool bf16_data,
+                         hipStream_t st) {
   dim3 grid((width + T - 1) / T, (width + T - 1) / T);
-  dw_f32_kernel<<<grid, NT, 0, st>>>(X, dY, dws, dwo, rows, width, d, n, bidir, accumulate);
+  if (bf16_data)
+    dw_fma_kernel<bf16><<<grid, NT, 0, st>>>((const bf16*)X, (const bf16*)dY, dws, dwo, rows,
+                                             width, d, n, bidir, accumulate);
+  else
+    dw_fma_kernel<float><<<grid, NT, 0, st>>>((const float*)X, (const float*)dY, dws, dwo, rows,
+                                              width, d, n, bidir, accumulate);
   return hipGetLastError();
 }
 

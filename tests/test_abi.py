@@ -74,11 +74,11 @@ UNSUPPORTED = hcmix.HCMIX_ERR_UNSUPPORTED
     (dict(layer=-1), INVALID), (dict(mode=2), INVALID), (dict(dtype=7), INVALID),
     (dict(layer=-1, mode=0), INVALID),                # the local layer is causal only
     (dict(layer=-2, mode=1), INVALID), (dict(layer=-1, mode=1, n=12), INVALID),
-    (dict(layer=-1, mode=1, width=96), UNSUPPORTED),  # a valid local layer, unsupported width
+    (dict(layer=-1, mode=1, width=100), UNSUPPORTED),  # a valid local layer, unsupported width
     (dict(x=None), INVALID), (dict(ws=None), INVALID), (dict(wo=None), INVALID),
     (dict(y=None), INVALID), (dict(y=P[0]), INVALID),                      # y aliases x
     (dict(batch=1 << 40), INVALID),                                       # too many rows
-    (dict(width=96), UNSUPPORTED), (dict(width=8), UNSUPPORTED),          # bf16 needs 64 | width
+    (dict(width=100), UNSUPPORTED), (dict(width=4), UNSUPPORTED),         # bf16 needs 8 | width
     (dict(x=ctypes.c_void_p(0x100008)), UNSUPPORTED),                     # bf16 needs 16-byte alignment
     (dict(dtype=0, x=ctypes.c_void_p(0x100002)), UNSUPPORTED),            # fp32 needs 4-byte alignment
 ])
@@ -101,7 +101,7 @@ def test_forward_aliasing_checks_whole_extent():
     (dict(dws=FP[6]), INVALID),                       # dw_self aliases dw_off
     (dict(workspace=None), INVALID), (dict(wsb=16), INVALID),
     (dict(workspace=P[0]), INVALID),                  # workspace aliases x
-    (dict(width=32), UNSUPPORTED),
+    (dict(width=36), UNSUPPORTED),                    # bf16 needs 8 | width
     (dict(workspace=ctypes.c_void_p(0x800010)), UNSUPPORTED),   # workspace not 256-aligned
 ])
 def test_backward_rejects_bad_arguments(kw, code):
@@ -117,7 +117,7 @@ def bwd_no_alloc(batch=2, n=16, width=64, layer=0, mode=0, dtype=1, x=P[0], ws=P
 @pytest.mark.parametrize("kw,code", [
     (dict(n=3), INVALID), (dict(batch=0), INVALID), (dict(dy=None), INVALID),
     (dict(dx=P[3]), INVALID), (dict(dws=FP[6]), INVALID), (dict(dx=P[0]), INVALID),
-    (dict(width=32), UNSUPPORTED),
+    (dict(width=36), UNSUPPORTED),                    # bf16 needs 8 | width
     (dict(width=2112, n=64, batch=1), UNSUPPORTED),   # needs more than the 32 MiB scratch
 ])
 def test_backward_no_alloc_rejects_bad_arguments(kw, code):
@@ -156,7 +156,7 @@ def sfwd(batch=2, n=16, width=64, L=4, layers=LP, mode=0, dtype=1, x=P[0], ws=No
     (dict(x=None), INVALID), (dict(xs=PP(P[3], P[3], P[5], P[6])), INVALID),   # two outputs alias
     (dict(xs=PP(P[0], P[4], P[5], P[6])), INVALID),                            # output aliases x
     (dict(xs=PP(P[3], P[4], P[1], P[6])), INVALID),                            # output aliases a weight
-    (dict(width=96), UNSUPPORTED),
+    (dict(width=100), UNSUPPORTED),
 ])
 def test_stack_forward_rejects_bad_arguments(kw, code):
     assert sfwd(**kw) == code
@@ -180,7 +180,7 @@ def swg(batch=2, n=16, width=128, L=4, layers=LP, mode=0, dtype=1, xs=None, dys=
     (dict(dws=PP(P[2], P[2], P[4], P[5])), INVALID),                # two gradients alias
     (dict(dws=PP(P[0], P[2], P[4], P[5])), INVALID),                # a gradient aliases an input
     (dict(dws=PP(ctypes.c_void_p(P[2].value + 4), P[4], P[5], P[6])), UNSUPPORTED),   # misaligned
-    (dict(width=96), UNSUPPORTED),
+    (dict(width=100), UNSUPPORTED),
 ])
 def test_weight_gradients_reject_bad_arguments(kw, code):
     assert swg(**kw) == code
@@ -361,7 +361,7 @@ def dec(batch=2, n=16, width=64, L=4, layers=LP, dtype=1, pos=0, x=P[0], ws=None
     (dict(y=P[3]), INVALID),                          # y aliases the cache
     (dict(cache=P[1]), INVALID),                      # cache aliases a weight
     (dict(cache=ctypes.c_void_p(0x400010)), UNSUPPORTED),   # cache not 256-aligned
-    (dict(width=96), UNSUPPORTED),
+    (dict(width=100), UNSUPPORTED),
 ])
 def test_decode_rejects_bad_arguments(kw, code):
     assert dec(**kw) == code
@@ -410,7 +410,7 @@ def sbd(batch=2, n=16, width=128, L=4, layers=LP, mode=1, dtype=1, ws=None, wo=N
     (dict(wsp=None), INVALID),
     (dict(wsp=ctypes.c_void_p(P[7].value + 16)), UNSUPPORTED),      # not 256-aligned
     (dict(dy=ctypes.c_void_p(P[0].value + 2)), UNSUPPORTED),        # misaligned bf16 operand
-    (dict(width=96), UNSUPPORTED),
+    (dict(width=100), UNSUPPORTED),
     (dict(layers=(ctypes.c_int32 * 4)(0, -1, 2, 3), mode=0), INVALID),   # local layer, bidir
 ])
 def test_stack_backward_data_rejects_bad_arguments(kw, code):

@@ -31,6 +31,9 @@ SHAPES = [
     (2, 16, 64, "bf16"), (3, 8, 64, "bf16"), (1, 2, 64, "bf16"), (5, 64, 192, "bf16"),
     (4, 256, 128, "bf16"), (1, 4096, 64, "bf16"), (2, 512, 256, "bf16"),
     (1, 64, 1024, "bf16"), (3, 32, 1280, "bf16"),      # 256-column tiles, ragged row tiles
+    # bf16 widths that are a multiple of 8 but not of 64: the FMA kernels
+    (2, 16, 8, "bf16"), (3, 8, 24, "bf16"), (2, 64, 72, "bf16"), (1, 512, 200, "bf16"),
+    (2, 32, 96, "bf16"),
 ]
 
 
