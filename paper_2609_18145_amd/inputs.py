@@ -153,3 +153,36 @@ def make_shared_stack(batch: int, n: int, width: int, num_layers: int, causal: b
         layers = list(range(num_layers))
     return SharedInputs(x=_finish(x, dtype), tables=tables, layers=list(layers), dy=dy,
                         causal=causal, dtype=dtype)
+
+
+@dataclass
+class FieldInputs:
+    p: np.ndarray                      # [batch, n, coord_dim] float32 coordinates
+    x: np.ndarray                      # [batch, n, width] float32 (bf16 values)
+    dy: np.ndarray                     # [batch, n, width] float32 (bf16 values)
+    tau: float = 1.0
+    scaled: bool = True
+
+
+def make_field(batch: int, n: int, width: int, coord_dim: int = 32, tau: float = 1.0,
+               scaled: bool = True, mean_sq_dist: float = 100.0, kind: str = "normal",
+               seed: int = 0) -> FieldInputs:
+    """Inputs of the field coupling (Section 3.4's dynamics variant): x (drawn
+    as in make_stack), then coordinates N(0, s^2) per component with s chosen so
+    that the expected squared distance of two positions, 2 coord_dim s^2, is
+    mean_sq_dist (about 100 is the regime Section 7 describes at
+    initialisation), then dY N(0,1).  x and dY are rounded to bf16; the
+    coordinates stay fp32."""
+    rng = np.random.default_rng(seed)
+    if kind == "normal":
+        x = rng.standard_normal((batch, n, width))
+    elif kind == "zipf_bytes":
+        seq = zipf_byte_tokens(rng, (batch, n + 1))
+        table = rng.standard_normal((256, width))
+        x = table[seq[:, :n]]
+    else:
+        raise ValueError(kind)
+    s = np.sqrt(mean_sq_dist / (2.0 * coord_dim))
+    p = (rng.standard_normal((batch, n, coord_dim)) * s).astype(np.float32)
+    dy = _finish(rng.standard_normal((batch, n, width)), "bf16")
+    return FieldInputs(p=p, x=_finish(x, "bf16"), dy=dy, tau=tau, scaled=scaled)
