@@ -386,6 +386,60 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
                                       const void* qkv, const void* out, const float* lse,
                                       const void* dout, void* dqkv, void* stream);
 
+/* ---- Field coupling (Section 3.4's dynamics variant; Section 7) ----
+ *
+ * Every position i of a window carries a coordinate p_i with coord_dim
+ * components; positions are coupled by a Gaussian of their squared distance,
+ * and the scaled form ("field") divides each squared distance by its causal
+ * row mean first.  Reading taken here (the paper states the coupling in words;
+ * the force that moves the coordinates and the number of repetitions T belong
+ * to the model and stay with the caller, who passes the coordinates of each
+ * application):
+ *   D[i][j] = |p_i - p_j|^2,  m_i = (1 / (i + 1)) sum_{j <= i} D[i][j],
+ *   a[i][j] = -D[i][j] / (tau m_i)   (scaled = 1; all 0 when m_i = 0)
+ *           = -D[i][j] / tau         (scaled = 0),
+ *   C[i][j] = exp(a[i][j]) / Z_i,  Z_i = sum_{j <= i} exp(a[i][j]),  C = 0 for j > i,
+ *   y_i = sum_{j <= i} C[i][j] x_j,
+ *   partners_i = exp(-sum_j C[i][j] ln C[i][j])  (Section 7's effective number
+ *   of partners).
+ * Layouts: p [batch][n][coord_dim] fp32; x, y, dy, dx [batch][n][width] bf16;
+ * row_mean, lse, partners [batch][n] fp32 (lse = ln Z_i); dp like p.
+ * Precision: distances from a split-bf16 Gram product with fp32 accumulation
+ * (about 2^-17 of the squared norms of p_i - p_0), couplings and statistics in
+ * fp32, the two products with x and dy on bf16 matrix cores (couplings rounded
+ * to bf16, fp32 accumulation), outputs rounded once.  In the scaled form a
+ * positive row mean below 2^-100 is taken as 2^-100.
+ * HCMIX_ERR_INVALID_VALUE: null pointers (partners may be null), batch, n,
+ * width or coord_dim < 1, tau outside [2^-24, 2^24] or not finite, scaled not 0
+ * or 1, an output overlapping an input or another output, a workspace smaller
+ * than hcmix_field_workspace_bytes, sizes past the limits above.
+ * HCMIX_ERR_UNSUPPORTED: n above 256, coord_dim above 64, width not a
+ * multiple of 64, bf16 pointers not 16-byte aligned, fp32 pointers not 4-byte
+ * aligned, a workspace not 256-byte aligned. */
+hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
+                                 float tau, int32_t scaled, const float* p, const void* x,
+                                 void* y, float* row_mean, float* lse, float* partners,
+                                 void* stream);
+
+/* Bytes of device workspace hcmix_field_backward needs: batch * N * N * 4 with
+ * N = n rounded up to a multiple of 32 (the gradient of each window's squared
+ * distances); 0 for arguments outside the supported range. */
+size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n);
+
+/* Backward: dp = dL/dp and dx = dL/dx (both overwritten) from p, x, the
+ * forward's row_mean and lse (same coordinates, tau and scaled), and dy:
+ *   dx_j = sum_{i >= j} C[i][j] dy_i,
+ *   da[i][j] = C[i][j] (dy_i . x_j - dy_i . y_i),
+ *   dD[i][j] = -da[i][j] / (tau m_i) + (sum_k da[i][k] D[i][k]) / (tau m_i^2 (i + 1))
+ *              (scaled; -da[i][j] / tau unscaled; 0 for rows with m_i = 0),
+ *   dp_i = 2 sum_{j <= i} dD[i][j] (p_i - p_j) + 2 sum_{k >= i} dD[k][i] (p_i - p_k).
+ * dy_i . y_i is taken as sum_j C[i][j] (dy_i . x_j), so y is not read. */
+hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
+                                  float tau, int32_t scaled, const float* p, const void* x,
+                                  const float* row_mean, const float* lse, const void* dy,
+                                  float* dp, void* dx, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
 /* ---- Linear maps: the attention layers' projections in the hybrids ----
  *
  * The hybrid schedules' attention layers (Section 3.3) project each position

@@ -72,6 +72,26 @@ def forward(p, x, tau: float, scaled: bool = True):
     return np.stack(ys), np.stack(Cs), np.stack(effs)
 
 
+def row_stats(p, tau: float, scaled: bool = True):
+    """(m [batch, n], ln Z [batch, n]): each row's causal mean squared
+    distance and the log of its softmax denominator sum over j <= i of
+    exp(a[i][j]) (the row maximum is the diagonal's logit, 0)."""
+    p = np.asarray(p, dtype=np.float64)
+    ms, ls = [], []
+    for t in range(p.shape[0]):
+        n = p.shape[1]
+        _, _, D, m = _window(p[t], np.zeros((n, 1)), tau, scaled)
+        if scaled:
+            with np.errstate(divide="ignore", invalid="ignore"):
+                a = np.where(m[:, None] > 0, -D / (tau * m[:, None]), 0.0)
+        else:
+            a = -D / tau
+        a = np.where(np.tril(np.ones((n, n), dtype=bool)), a, -np.inf)
+        ms.append(m)
+        ls.append(np.log(np.exp(a).sum(axis=1)))
+    return np.stack(ms), np.stack(ls)
+
+
 def backward(p, x, dy, tau: float, scaled: bool = True):
     """Returns (dp [batch, n, c], dx [batch, n, width])."""
     p = np.asarray(p, dtype=np.float64)

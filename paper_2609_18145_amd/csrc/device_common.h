@@ -10,6 +10,14 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
+// Block index -> tile index, keeping consecutive tiles (the column tiles of
+// one row tile, the tiles of one window) on one XCD: blocks are dealt to the
+// 8 XCDs round-robin.
+__device__ __forceinline__ int xcd_tile(int bid, int total) {
+  if (total % 8 != 0) return bid;
+  return (bid % 8) * (total / 8) + bid / 8;
+}
+
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }

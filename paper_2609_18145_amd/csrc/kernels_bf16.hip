@@ -26,13 +26,6 @@ namespace hcmix {
 
 namespace {
 
-// Block index -> tile index, keeping consecutive tiles (the column tiles of
-// one row tile) on one XCD: blocks are dealt to the 8 XCDs round-robin.
-__device__ __forceinline__ int xcd_tile(int bid, int total) {
-  if (total % 8 != 0) return bid;
-  return (bid % 8) * (total / 8) + bid / 8;
-}
-
 // ---------------------------------------------------------------------------
 // Mix GEMM.  For the block's lower rows L and upper rows U:
 //   out_L = A_L B1^T + [PL] A_U B2^T

@@ -38,7 +38,8 @@ EXPORTS = ("hcmix_status_string", "hcmix_last_hip_error", "hcmix_dim", "hcmix_fo
            "hcmix_backward_no_alloc", "hcmix_shared_stack_forward",
            "hcmix_shared_stack_backward_workspace_bytes", "hcmix_shared_stack_backward",
            "hcmix_linear_forward", "hcmix_linear_backward_workspace_bytes",
-           "hcmix_linear_backward")
+           "hcmix_linear_backward", "hcmix_field_forward", "hcmix_field_workspace_bytes",
+           "hcmix_field_backward")
 
 _lib = None
 
@@ -99,6 +100,14 @@ def load():
         lib.hcmix_attention_forward.restype = i32
         lib.hcmix_attention_backward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp, vp, vp]
         lib.hcmix_attention_backward.restype = i32
+        lib.hcmix_field_forward.argtypes = [i64, i64, i64, i32, ctypes.c_float, i32, fp, vp, vp,
+                                            fp, fp, fp, vp]
+        lib.hcmix_field_forward.restype = i32
+        lib.hcmix_field_workspace_bytes.argtypes = [i64, i64]
+        lib.hcmix_field_workspace_bytes.restype = sz
+        lib.hcmix_field_backward.argtypes = [i64, i64, i64, i32, ctypes.c_float, i32, fp, vp, fp,
+                                             fp, vp, fp, vp, vp, sz, vp]
+        lib.hcmix_field_backward.restype = i32
         lib.hcmix_embedding_forward.argtypes = [i64, i64, i32, vp, vp, vp, vp]
         lib.hcmix_embedding_forward.restype = i32
         lib.hcmix_embedding_backward_workspace_bytes.argtypes = [i64, i64, i32]
@@ -503,6 +512,73 @@ def attention_backward(qkv, out, lse, dout, dqkv=None):
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_attention_backward")
     return dqkv
+
+
+def _field_shapes(p, x):
+    if not isinstance(p, torch.Tensor) or p.dim() != 3:
+        raise ValueError("p: expected a [batch, n, coord_dim] tensor")
+    batch, n, width = _act_shape(x)
+    if tuple(p.shape[:2]) != (batch, n):
+        raise ValueError(f"p: shape {tuple(p.shape)} does not match x {tuple(x.shape)}")
+    _need(p, "p", None, torch.float32)
+    _need(x, "x", None, torch.bfloat16, p.device)
+    return batch, n, width, p.shape[2]
+
+
+def field_forward(p, x, tau=1.0, scaled=True, partners=False, y=None, row_mean=None, lse=None):
+    """Field coupling (Section 3.4): p [batch, n, c] fp32 coordinates, x
+    [batch, n, width] bf16 -> (y bf16, row_mean fp32 [batch, n], lse fp32
+    [batch, n], partners fp32 [batch, n] or None)."""
+    batch, n, width, c = _field_shapes(p, x)
+    dev = x.device
+    if y is None:
+        y = torch.empty_like(x)
+    if row_mean is None:
+        row_mean = torch.empty((batch, n), dtype=torch.float32, device=dev)
+    if lse is None:
+        lse = torch.empty((batch, n), dtype=torch.float32, device=dev)
+    part = torch.empty((batch, n), dtype=torch.float32, device=dev) if partners else None
+    _need(y, "y", (batch, n, width), torch.bfloat16, dev)
+    _need(row_mean, "row_mean", (batch, n), torch.float32, dev)
+    _need(lse, "lse", (batch, n), torch.float32, dev)
+    _gpu(dev)
+    rc = load().hcmix_field_forward(batch, n, width, c, float(tau), int(bool(scaled)), _fptr(p),
+                                    _ptr(x), _ptr(y), _fptr(row_mean), _fptr(lse),
+                                    _fptr(part) if part is not None else None, _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_field_forward")
+    return y, row_mean, lse, part
+
+
+def field_workspace_bytes(batch: int, n: int) -> int:
+    return load().hcmix_field_workspace_bytes(batch, n)
+
+
+def field_backward(p, x, row_mean, lse, dy, tau=1.0, scaled=True, dp=None, dx=None,
+                   workspace=None):
+    """(dp fp32 [batch, n, c], dx bf16 [batch, n, width]) given dy = dL/dy and
+    the forward's row_mean and lse."""
+    batch, n, width, c = _field_shapes(p, x)
+    dev = x.device
+    _need(row_mean, "row_mean", (batch, n), torch.float32, dev)
+    _need(lse, "lse", (batch, n), torch.float32, dev)
+    _need(dy, "dy", (batch, n, width), torch.bfloat16, dev)
+    if dp is None:
+        dp = torch.empty_like(p)
+    if dx is None:
+        dx = torch.empty_like(x)
+    _need(dp, "dp", tuple(p.shape), torch.float32, dev)
+    _need(dx, "dx", (batch, n, width), torch.bfloat16, dev)
+    _gpu(dev)
+    if workspace is None:
+        need = field_workspace_bytes(batch, n)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = load().hcmix_field_backward(batch, n, width, c, float(tau), int(bool(scaled)), _fptr(p),
+                                     _ptr(x), _fptr(row_mean), _fptr(lse), _ptr(dy), _fptr(dp),
+                                     _ptr(dx), _ptr(workspace), _bytes(workspace), _stream(x))
+    if rc != HCMIX_OK:
+        raise HcmixError(rc, "hcmix_field_backward")
+    return dp, dx
 
 
 def _rows_of(t, name, width, dtype, dev):

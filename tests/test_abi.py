@@ -472,3 +472,54 @@ def test_shared_backward_workspace_and_rejections():
     assert call(dts=vp(P[6], P[2])) == INVALID        # a table gradient aliases a table
     assert call(wsb=nb - 4) == INVALID
     assert call(ws=ctypes.c_void_p(0x4000010)) == UNSUPPORTED
+
+
+def field_fwd(batch=2, n=40, width=64, c=3, tau=1.0, scaled=1, p=FP[0], x=P[1], y=P[2],
+              mean=FP[3], lse=FP[4], part=FP[5]):
+    return hcmix.load().hcmix_field_forward(batch, n, width, c, tau, scaled, p, x, y, mean, lse,
+                                            part, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=0), INVALID), (dict(n=0), INVALID), (dict(width=0), INVALID),
+    (dict(c=0), INVALID), (dict(tau=0.0), INVALID), (dict(tau=-1.0), INVALID),
+    (dict(tau=float("nan")), INVALID), (dict(tau=float("inf")), INVALID),
+    (dict(tau=2.0 ** -30), INVALID), (dict(scaled=2), INVALID),
+    (dict(p=None), INVALID), (dict(x=None), INVALID), (dict(y=None), INVALID),
+    (dict(mean=None), INVALID), (dict(lse=None), INVALID),
+    (dict(y=P[1]), INVALID),                                            # y aliases x
+    (dict(lse=FP[3]), INVALID),                                         # two outputs alias
+    (dict(part=ctypes.cast(ctypes.c_void_p(P[2].value + 256), ctypes.POINTER(ctypes.c_float))),
+     INVALID),                                                          # partners inside y
+    (dict(n=257), UNSUPPORTED), (dict(c=65), UNSUPPORTED), (dict(width=96), UNSUPPORTED),
+    (dict(x=ctypes.c_void_p(P[1].value + 8)), UNSUPPORTED),             # bf16 misaligned
+    (dict(p=ctypes.cast(ctypes.c_void_p(P[0].value + 2), ctypes.POINTER(ctypes.c_float))),
+     UNSUPPORTED),
+])
+def test_field_forward_rejects_bad_arguments(kw, code):
+    assert field_fwd(**kw) == code
+
+
+def test_field_backward_workspace_and_rejections():
+    lib = hcmix.load()
+    q = lib.hcmix_field_workspace_bytes
+    assert q(64, 256) == 64 * 256 * 256 * 4
+    assert q(2, 40) == 2 * 64 * 64 * 4           # n rounded up to a multiple of 32
+    assert q(1, 1) == 32 * 32 * 4
+    assert q(0, 16) == 0 and q(2, 257) == 0 and q(2, 0) == 0
+    need = q(2, 40)
+    ws = ctypes.c_void_p(0x4000000)
+    call = lambda **k: lib.hcmix_field_backward(   # noqa: E731
+        2, k.get("n", 40), 64, k.get("c", 3), k.get("tau", 1.0), 1, FP[0], P[1], FP[2], FP[3],
+        k.get("dy", P[4]), k.get("dp", FP[5]), k.get("dx", P[6]), k.get("ws", ws),
+        k.get("wsb", need), None)
+    assert call(wsb=need - 4) == INVALID
+    assert call(ws=None) == INVALID
+    assert call(dx=P[4]) == INVALID                                     # dx aliases dy
+    assert call(dp=FP[0]) == INVALID                                    # dp aliases p
+    assert call(ws=P[6]) == INVALID                                     # workspace aliases dx
+    assert call(dy=None) == INVALID
+    assert call(tau=0.0) == INVALID
+    assert call(n=300) == UNSUPPORTED
+    assert call(c=100) == UNSUPPORTED
+    assert call(ws=ctypes.c_void_p(0x4000010)) == UNSUPPORTED          # workspace alignment

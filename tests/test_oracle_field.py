@@ -182,3 +182,16 @@ def test_degenerate_rows_have_zero_coordinate_gradient():
     assert np.all(dp == 0)
     C = np.tril(np.ones((5, 5))) / np.arange(1, 6)[:, None]
     assert np.allclose(dx[0], C.T @ dy[0])
+
+
+def test_row_stats_closed_forms():
+    # two points at distance d: m_1 = d^2 / 2 and ln Z_1 = ln(1 + exp(-2 / tau)) (scaled),
+    # ln(1 + exp(-d^2 / tau)) (unscaled); row 0 always has m = 0 and ln Z = 0
+    p = np.array([[[0.0, 0.0], [3.0, 4.0]]])
+    m, lse = field.row_stats(p, 0.5, True)
+    assert np.allclose(m[0], [0.0, 12.5]) and np.allclose(lse[0], [0.0, np.log1p(np.exp(-4.0))])
+    m, lse = field.row_stats(p, 20.0, False)
+    assert np.allclose(lse[0], [0.0, np.log1p(np.exp(-25.0 / 20.0))])
+    # equal coordinates: m = 0, ln Z = ln(i + 1)
+    m, lse = field.row_stats(np.ones((1, 6, 3)), 1.0, True)
+    assert np.all(m == 0) and np.allclose(lse[0], np.log(np.arange(1, 7)))
