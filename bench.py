@@ -49,6 +49,10 @@ WORKLOADS = {
     "shared256": ("window n=256, width 512, batch 64, 16 rotated causal channel-shared layers "
                   "(per-position scalar maps from one 256 x 256 table per layer), Zipf byte-token "
                   "embedding inputs, bf16, fwd+bwd"),
+    "field256": ("window n=256, width 512, batch 64, the field coupling of Section 3.4 (scaled "
+                 "Gaussian distance kernel, 32 coordinates, tau 1, mean squared distance 100) "
+                 "applied T = 8 times in a chain, each application with its own coordinates, "
+                 "Zipf byte-token embedding inputs, bf16 with fp32 coordinates, fwd+bwd"),
 }
 # hybrid: positions of the attention layers in the 18-layer list
 HYBRID_ATTN_SLOTS = (3, 9)
@@ -316,6 +320,8 @@ def main():
         return run_decode(args, torch, hcmix, inputs, dev)
     if args.workload == "lm256_step":
         return run_lm_step(args, torch, hcmix, inputs, dev)
+    if args.workload == "field256":
+        return run_field(args, torch, hcmix, inputs, dev)
     if args.workload == "shared256":
         return run_shared(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
@@ -859,6 +865,110 @@ def run_shared(args, torch, hcmix, inputs, dev):
     return 0
 
 
+def run_field(args, torch, hcmix, inputs, dev):
+    """The field coupling (Section 3.4) at the window-256 LM shape: T = 8
+    applications x_t = C(p_t) x_{t-1} in a chain, each with its own
+    coordinates (the force that moves them between applications is the
+    model's and stays out), then the backward in reverse (dx chained, dp per
+    application); one step = T hcmix_field_forward and T hcmix_field_backward
+    calls, replayed as a graph.  Both calls are HBM-bound (about 60 flops per
+    byte against the bf16 ridge near 315), so the roofline is bytes: forward
+    reads p and x and writes y and two fp32 row statistics; backward reads p,
+    x, dy and the statistics and writes dp and dx (its fp32 squared-distance
+    gradient is a workspace, not algorithmic traffic).  Each call is timed
+    on its own with graph_timed, on the stream it runs on."""
+    B, n, w, c, T = 64, 256, 512, 32, 8
+    if args.batch > 0:
+        B = args.batch
+    x_h, ps_h, dy_h, tau, scaled = inputs.make_field_chain(B, n, w, c, T, seed=0)
+    x0 = torch.from_numpy(x_h).to(torch.bfloat16).to(dev)
+    dy = torch.from_numpy(dy_h).to(torch.bfloat16).to(dev)
+    ps = [torch.from_numpy(p).to(dev) for p in ps_h]
+    xs = [x0] + [torch.empty_like(x0) for _ in range(T)]
+    ms = [torch.empty((B, n), dtype=torch.float32, device=dev) for _ in range(T)]
+    lses = [torch.empty((B, n), dtype=torch.float32, device=dev) for _ in range(T)]
+    dps = [torch.empty_like(p) for p in ps]
+    gs = [torch.empty_like(x0) for _ in range(T)]
+    wsp = torch.empty(hcmix.field_workspace_bytes(B, n), dtype=torch.uint8, device=dev)
+
+    def fwd(t):
+        hcmix.field_forward(ps[t], xs[t], tau, scaled, y=xs[t + 1], row_mean=ms[t], lse=lses[t])
+
+    def bwd(t, g):
+        hcmix.field_backward(ps[t], xs[t], ms[t], lses[t], g, tau, scaled, dp=dps[t], dx=gs[t],
+                             workspace=wsp)
+
+    def step():
+        for t in range(T):
+            fwd(t)
+        g = dy
+        for t in reversed(range(T)):
+            bwd(t, g)
+            g = gs[t]
+
+    stream = torch.cuda.Stream(device=dev)
+    with torch.cuda.stream(stream):
+        step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = max(time.perf_counter() - t0, e0.elapsed_time(e1) / 1e3)
+    us = {"forward": graph_timed(torch, lambda: fwd(0), args.kernel_reps) * 1e6,
+          "backward": graph_timed(torch, lambda: bwd(0, dy), args.kernel_reps) * 1e6}
+    if args.calib_copy_mb > 0:
+        calibration_copy(torch, dev, args.calib_copy_mb)
+    rows = B * n
+    bytes_fwd = rows * (c * 4 + 2 * w * 2 + 2 * 4)
+    bytes_bwd = rows * (2 * c * 4 + 3 * w * 2 + 2 * 4)
+    # causal products with x or dy: sum over rows of (i + 1) w multiply-adds
+    pv_flops = B * n * (n + 1) * w
+    entries = {}
+    for name, nb, fl, kname in (
+            ("forward", bytes_fwd, pv_flops, "field_fwd_kernel"),
+            ("backward", bytes_bwd, 2 * pv_flops,
+             "field_bwd_rows_kernel + field_bwd_dx_kernel + field_bwd_coord_kernel")):
+        sec = us[name] * 1e-6
+        gbs = nb / sec / 1e9
+        entries[name] = {"bound": "hbm", "kernel": f"{kname} (one {name} call)",
+                         "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "traffic": profiled_traffic(args.workload, kname),
+                         "avg_launch_us": round(us[name], 2), "algorithmic_bytes": nb,
+                         "mfma_frac_bf16": round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    dom = "backward" if us["backward"] >= us["forward"] else "forward"
+    out = {
+        "metric": METRIC, "value": round(B * n * T * args.steps / t, 1), "unit": UNIT,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"field256: {WORKLOADS['field256']}", "batch": B, "n": n,
+                   "width": w, "coord_dim": c, "applications": T, "tau": tau,
+                   "form": "scaled" if scaled else "unscaled", "graph": True},
+        "roofline": entries[dom],
+        "roofline_" + ("forward" if dom == "backward" else "backward"):
+            entries["forward" if dom == "backward" else "backward"],
+    }
+    if args.cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_field(x_h, ps_h, dy_h, tau, scaled, n, T,
+                                                 args.cpu_windows)
+    if not args.calib_copy_mb:       # counter runs: the calibration copy stays the largest
+        out["context"] = device_copy_context(torch, dev)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def run_lm_step(args, torch, hcmix, inputs, dev):
     """The lm256 stack inside a whole training step of the byte-level language
     model: embedding (library gather), the 16-layer stack forward, the 256-way
@@ -1203,6 +1313,30 @@ def cpu_baseline_shared(s, n, L, windows):
 
     return timed_oracle_legs(run, s.x.shape[0], n, L, windows,
                              f", all {L} layers, forward+backward (numpy, one thread)",
+                             single_threaded=True)
+
+
+def cpu_baseline_field(x, ps, dy, tau, scaled, n, T, windows):
+    """The field oracle (oracle/field.py, float64 numpy) on a bounded sample of
+    the workload: windows through all T applications, forward and backward,
+    with numpy's BLAS held to one thread."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import field
+
+    def run(k):
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            xs = [x[:k]]
+            for t in range(T):
+                xs.append(field.forward(ps[t][:k], xs[-1], tau, scaled)[0])
+            g = dy[:k]
+            for t in reversed(range(T)):
+                _, g = field.backward(ps[t][:k], xs[t], g, tau, scaled)
+            return time.perf_counter() - t0
+
+    return timed_oracle_legs(run, x.shape[0], n, T, windows,
+                             f", all {T} applications, forward+backward (numpy, one thread)",
                              single_threaded=True)
 
 

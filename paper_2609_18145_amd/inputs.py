@@ -186,3 +186,21 @@ def make_field(batch: int, n: int, width: int, coord_dim: int = 32, tau: float =
     p = (rng.standard_normal((batch, n, coord_dim)) * s).astype(np.float32)
     dy = _finish(rng.standard_normal((batch, n, width)), "bf16")
     return FieldInputs(p=p, x=_finish(x, "bf16"), dy=dy, tau=tau, scaled=scaled)
+
+
+def make_field_chain(batch: int, n: int, width: int, coord_dim: int = 32, steps: int = 8,
+                     tau: float = 1.0, scaled: bool = True, mean_sq_dist: float = 100.0,
+                     seed: int = 0):
+    """Inputs of `steps` field applications in a chain: x (Zipf byte tokens
+    through an N(0,1) table, as in make_stack), then one coordinate array per
+    application drawn as in make_field, then dY.  Returns (x, [p_1..p_T], dy,
+    tau, scaled)."""
+    rng = np.random.default_rng(seed)
+    seq = zipf_byte_tokens(rng, (batch, n + 1))
+    table = rng.standard_normal((256, width))
+    x = _finish(table[seq[:, :n]], "bf16")
+    s = np.sqrt(mean_sq_dist / (2.0 * coord_dim))
+    ps = [(rng.standard_normal((batch, n, coord_dim)) * s).astype(np.float32)
+          for _ in range(steps)]
+    dy = _finish(rng.standard_normal((batch, n, width)), "bf16")
+    return x, ps, dy, tau, scaled
