@@ -38,8 +38,7 @@ namespace hcmix {
 
 namespace {
 
-constexpr int FT = 512;                       // threads per block, 8 waves (coordinate kernel: 256)
-constexpr int FTC = 256;
+constexpr int FT = 512;                       // threads per block, 8 waves
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
@@ -64,95 +63,197 @@ __device__ __forceinline__ bf16x8 ct_row(const bf16* t, int rs, int r, int c0, i
 // load coalesced, all of a thread's loads issued before its first LDS write);
 // the element -> (row, column) walk advances by a precomputed step, with no
 // division per element.
-template <int THREADS, int PER>
+struct NoIssue {
+  __device__ __forceinline__ void operator()() const {}
+};
+// `then` runs after the loads are issued and before their values are used
+// (loads it issues queue behind them).  vec: pw is 16-byte aligned and c a
+// multiple of 4, so 16-byte loads never straddle a row (a wave-wide memory
+// instruction costs about the same whatever its width, so wide loads move
+// four times the bytes per instruction).
+template <int THREADS, class Then = NoIssue>
 __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int rows, int c,
-                                             unsigned char* dst, int stride) {
+                                             unsigned char* dst, int stride, bool vec,
+                                             Then then = {}) {
   const int total = rows * c;
-  float v[PER];
+  if (vec) {
+    constexpr int PER = 256 * 64 / 4 / THREADS;     // float4 per thread at 256 rows x 64
+    const int total4 = total >> 2;
+    f32x4 v[PER];
 #pragma unroll
-  for (int u = 0; u < PER; u++) {   // unconditional loads (clamped): no branch waits per load
-    const int e = min(threadIdx.x + THREADS * u, total - 1);
-    v[u] = pw[e];
-  }
-  int r = threadIdx.x / c, k = threadIdx.x % c;
-  const int dr = THREADS / c, dk = THREADS % c;
+    for (int u = 0; u < PER; u++)
+      v[u] = ((const f32x4*)pw)[min((int)threadIdx.x + THREADS * u, total4 - 1)];
+    then();
+    int r = (4 * threadIdx.x) / c, k = (4 * threadIdx.x) % c;
+    const int dr = (4 * THREADS) / c, dk = (4 * THREADS) % c;
 #pragma unroll
-  for (int u = 0; u < PER; u++) {
-    if (threadIdx.x + THREADS * u < total) *(float*)(dst + r * stride + 4 * k) = v[u];
-    k += dk;
-    r += dr;
-    if (k >= c) {
-      k -= c;
-      r += 1;
+    for (int u = 0; u < PER; u++) {
+      if ((int)threadIdx.x + THREADS * u < total4) {
+        float* d = (float*)(dst + r * stride) + k;
+        d[0] = v[u][0];
+        d[1] = v[u][1];
+        d[2] = v[u][2];
+        d[3] = v[u][3];
+      }
+      k += dk;
+      r += dr;
+      if (k >= c) {
+        k -= c;
+        r += 1;
+      }
+    }
+  } else {
+    constexpr int PER = 256 * 64 / THREADS;
+    float v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; u++)   // unconditional loads (clamped): no branch waits per load
+      v[u] = pw[min((int)threadIdx.x + THREADS * u, total - 1)];
+    then();
+    int r = threadIdx.x / c, k = threadIdx.x % c;
+    const int dr = THREADS / c, dk = THREADS % c;
+#pragma unroll
+    for (int u = 0; u < PER; u++) {
+      if ((int)threadIdx.x + THREADS * u < total) *(float*)(dst + r * stride + 4 * k) = v[u];
+      k += dk;
+      r += dr;
+      if (k >= c) {
+        k -= c;
+        r += 1;
+      }
     }
   }
 }
 
-// The table rows [0, rows) (rows <= the block's threads) and their squared
-// norms N_r (of hi + lo, fp32), from the window's coordinates pw [n][c]:
-// the raw rows are staged into the table's own space, each thread reads its
-// row and row 0, and after a barrier overwrites its row with the split centred
-// values.  Ends with a barrier.
-__device__ __forceinline__ void build_coords(const float* __restrict__ pw, int n, int c, int cp,
-                                             int rows, bf16* sT, float* sN) {
-  const int rsb = ct_stride(cp) * 2;                 // bytes per table row
+// The coordinate table rows [0, rows) (rows <= 256) and their squared norms
+// N_r (of hi + lo, fp32), from the window's coordinates pw [n][c]; with TILES
+// also what a row's mean needs from the tiles before it:
+//   sTS[t][k] = sum over rows j < 32 t (of the window) of the centred p_j[k]
+//   (fp32, t = 0 .. NT; each tile's column sum by one thread, then a running
+//   sum over the tiles), and sPN[t] = sum of N_j over tile t.  Then, for
+//   query q in tile t,
+//   sum_{j < 32 t} D[q][j] = 32 t N_q + sum_{t' < t} sPN[t'] - 2 p'_q . sTS[t].
+// The raw rows are staged in the table's own space with a stride of c + 1
+// words (consecutive rows in distinct banks); each table row is then split by
+// two threads (cp / 2 columns each: thread tid takes row tid % 256, half
+// tid / 256), every LDS read of a phase issued before its values are used.
+// `then` is passed on to stage_coords.  Three barriers; ends with one.  sNh:
+// [2][NT * 32] scratch for the half-row norms.
+template <int NT, bool TILES, class Then>
+__device__ __forceinline__ void build_table(const float* __restrict__ pw, int n, int c, int cp,
+                                            int rows, bf16* sT, float* sN, float* sNh,
+                                            float* sTS, float* sPN, bool vec, Then then) {
+  constexpr int NP = NT * 32;
+  const int rws = (c + 1) * 4;                       // raw staging row stride (bytes)
   unsigned char* base = (unsigned char*)sT;
-  stage_coords<FT, 32>(pw, rows < n ? rows : n, c, base, rsb);
+  stage_coords<FT>(pw, rows < n ? rows : n, c, base, rws, vec, then);
   __syncthreads();
-  const int r = threadIdx.x;
+  const int r = threadIdx.x & 255, h = threadIdx.x >> 8;
+  const int hc = cp >> 1, k0 = h * hc;               // this thread's columns [k0, k0 + hc)
   const bool live = r < n && r < rows;
   const int rr = live ? r : 0;
-  float v[64];
+  float v[32];
+  {
+    float raw[32], p0[32];
 #pragma unroll
-  for (int k = 0; k < 64; k++) {
-    float t = 0.f;
-    if (k < c) t = *(const float*)(base + rr * rsb + 4 * k) - *(const float*)(base + 4 * k);
-    v[k] = live ? t : 0.f;
+    for (int k = 0; k < 32; k++) {
+      const int kk = min(k0 + k, c - 1);
+      raw[k] = *(const float*)(base + rr * rws + 4 * kk);
+      p0[k] = *(const float*)(base + 4 * kk);
+    }
+#pragma unroll
+    for (int k = 0; k < 32; k++) v[k] = (live && k < hc && k0 + k < c) ? raw[k] - p0[k] : 0.f;
+  }
+  if constexpr (TILES) {
+    // tile t's column k: thread (t, k) = (tid / 64, tid % 64); 8 tiles x 64 columns
+    const int t = threadIdx.x >> 6, k = threadIdx.x & 63;
+    if (t < NT) {
+      const int kk = min(k, c - 1);
+      const float p0k = *(const float*)(base + 4 * kk);
+      float col[32];
+#pragma unroll
+      for (int j = 0; j < 32; j++)
+        col[j] = *(const float*)(base + min(32 * t + j, n - 1) * rws + 4 * kk);
+      float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 32; j++) part[j & 3] += (32 * t + j < n) ? col[j] - p0k : 0.f;
+      sTS[(t + 1) * 64 + k] = k < c ? (part[0] + part[1]) + (part[2] + part[3]) : 0.f;
+    }
   }
   __syncthreads();
+  float nn = 0.f;
   if (r < rows) {
-    bf16* row = sT + r * ct_stride(cp);
-    float nn = 0.f;
+    bf16* row = sT + r * ct_stride(cp) + k0;
 #pragma unroll
-    for (int k = 0; k < 64; k += 2) {
-      const bf16 ha = to_bf16(v[k]), hb = to_bf16(v[k + 1]);
-      const bf16 la = to_bf16(v[k] - (float)ha), lb = to_bf16(v[k + 1] - (float)hb);
-      if (k < cp) {
-        *(bf16x2*)(row + k) = bf16x2{ha, hb};
-        *(bf16x2*)(row + cp + k) = bf16x2{la, lb};
+    for (int k = 0; k < 32; k += 2) {
+      const bf16x2 hi2 = {to_bf16(v[k]), to_bf16(v[k + 1])};
+      const float ha = (float)hi2[0], hb = (float)hi2[1];
+      const bf16x2 lo2 = {to_bf16(v[k] - ha), to_bf16(v[k + 1] - hb)};
+      if (k < hc) {
+        *(bf16x2*)(row + k) = hi2;
+        *(bf16x2*)(row + cp + k) = lo2;
       }
-      const float ta = (float)ha + (float)la, tb = (float)hb + (float)lb;
+      const float ta = ha + (float)lo2[0], tb = hb + (float)lo2[1];
       nn = fmaf(ta, ta, nn);
       nn = fmaf(tb, tb, nn);
     }
-    *(u32x4*)(row + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
-    sN[r] = nn;
+    if (h == 0) *(u32x4*)(sT + r * ct_stride(cp) + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
+  }
+  if (r < rows) sNh[h * NP + r] = nn;
+  if constexpr (TILES) {
+    if (threadIdx.x < 64) {
+      float acc = 0.f;
+      sTS[threadIdx.x] = 0.f;
+#pragma unroll
+      for (int t = 0; t < NT; t++) {
+        acc += sTS[(t + 1) * 64 + threadIdx.x];
+        sTS[(t + 1) * 64 + threadIdx.x] = acc;
+      }
+    }
+  }
+  __syncthreads();
+  // N_r from the two halves; tile sums of N (rows 32 t .. 32 t + 31 are one
+  // half of a wave)
+  if (threadIdx.x < rows) {
+    float nr = sNh[threadIdx.x] + sNh[NP + threadIdx.x];
+    sN[threadIdx.x] = nr;
+    if constexpr (TILES) {
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) nr += __shfl_xor(nr, o);
+      if ((threadIdx.x & 31) == 0) sPN[threadIdx.x >> 5] = nr;
+    }
   }
   __syncthreads();
 }
 
-// Rows [0, NT * 32) of one slab of SW columns (SW / 64 tiles of 64 columns;
-// src: row 0's first column, rows `stride` apart) into swizzled LDS tiles
-// NT * 32 * 64 elements apart; rows >= n are zero.  Every load is in flight
-// before the first LDS write.
+// One slab of SW columns (SW / 64 tiles of 64 columns; src: row 0's first
+// column, rows `stride` apart), rows [0, NT * 32), in two steps: issue every
+// load into registers (unconditional, rows clamped into the window), and later
+// write them to swizzled LDS tiles NT * 32 * 64 elements apart, rows >= n as
+// zero.  The loads can then overlap other work; vector-memory waits are in
+// issue order, so loads issued before them do not delay later ones' use.
 template <int NT, int SW>
-__device__ __forceinline__ void load_slab(const bf16* __restrict__ src, size_t stride, int n,
-                                          bf16* tile) {
-  constexpr int NP = NT * 32, TP = NP * 8, PIECES = TP * (SW / 64), PER = (PIECES + FT - 1) / FT;
+struct Slab {
+  static constexpr int NP = NT * 32, TP = NP * 8, PIECES = TP * (SW / 64),
+                       PER = (PIECES + FT - 1) / FT;
   u32x4 v[PER];
+  __device__ __forceinline__ void issue(const bf16* __restrict__ src, size_t stride, int n) {
 #pragma unroll
-  for (int j = 0; j < PER; j++) {   // unconditional loads (clamped), zeroed after
-    const int pi = min(threadIdx.x + FT * j, PIECES - 1), tl = pi / TP, r = (pi % TP) >> 3,
-              pc = pi & 7;
-    v[j] = *(const u32x4*)(src + (size_t)min(r, n - 1) * stride + 64 * tl + 8 * pc);
-    if (r >= n) v[j] = u32x4{0u, 0u, 0u, 0u};
+    for (int j = 0; j < PER; j++) {
+      const int pi = min((int)threadIdx.x + FT * j, PIECES - 1), tl = pi / TP,
+                r = (pi % TP) >> 3, pc = pi & 7;
+      v[j] = *(const u32x4*)(src + (size_t)min(r, n - 1) * stride + 64 * tl + 8 * pc);
+    }
   }
+  __device__ __forceinline__ void store(bf16* tile, int n) {
 #pragma unroll
-  for (int j = 0; j < PER; j++) {
-    const int pi = threadIdx.x + FT * j, tl = pi / TP, r = (pi % TP) >> 3, pc = pi & 7;
-    if (pi < PIECES) *(u32x4*)(tile + tl * NP * 64 + att_off(r, 8 * pc)) = v[j];
+    for (int j = 0; j < PER; j++) {
+      const int pi = threadIdx.x + FT * j, tl = pi / TP, r = (pi % TP) >> 3, pc = pi & 7;
+      if (pi < PIECES)
+        *(u32x4*)(tile + tl * NP * 64 + att_off(r, 8 * pc)) =
+            r < n ? v[j] : u32x4{0u, 0u, 0u, 0u};
+    }
   }
-}
+};
 
 // s_waitcnt vmcnt(n) for a wave-uniform runtime n <= 15.
 __device__ __forceinline__ void wait_vmcnt_upto(int n) {
@@ -177,40 +278,58 @@ __device__ __forceinline__ void wait_vmcnt_upto(int n) {
 // of the other side) sums to the same 9 for every SIMD at 8 tiles.
 __device__ __forceinline__ int wave_tile(int wave) { return wave < 4 ? wave : 11 - wave; }
 
-// Gram tile G^T[key][query] for keys kt*32.. (A operand, table rows) and the
-// lane's query q (B operand): hi.hi + lo.hi + hi.lo, in that order.
-__device__ __forceinline__ f32x16 gram_keys(const bf16* sT, int rs, int cp, int kt, int q,
-                                            int lane) {
-  const int half = lane >> 5;
+// The lane's own row of the table as B-operand fragments: hi and lo halves,
+// the 8 components of each 16-wide k step that lane half h contributes.
+struct RowFrags {
+  bf16x8 hi[4], lo[4];
+};
+__device__ __forceinline__ void row_frags(const bf16* sT, int rs, int cp, int r, int half,
+                                          RowFrags& f) {
+#pragma unroll
+  for (int ks = 0; ks < 4; ks++) {
+    f.hi[ks] = bf16x8{};
+    f.lo[ks] = bf16x8{};
+    if (16 * ks < cp) {
+      f.hi[ks] = ct_row(sT, rs, r, 16 * ks, half);
+      f.lo[ks] = ct_row(sT, rs, r, cp + 16 * ks, half);
+    }
+  }
+}
+
+// Gram tile of table rows t0 .. t0 + 31 (A operand) against the lane's row
+// fragments f (B operand): hi.hi, then key-lo . query-hi, then key-hi .
+// query-lo, so that both orientations (A_IS_KEY: the tile holds keys, f the
+// query; else the tile holds queries, f the key) add the same products in the
+// same order.
+template <bool A_IS_KEY>
+__device__ __forceinline__ f32x16 gram_tile(const bf16* sT, int rs, int cp, int t0,
+                                            const RowFrags& f, int lane) {
   f32x16 acc = {};
-  for (int k0 = 0; k0 < cp; k0 += 16) {
-    const bf16x8 khi = ct_frag(sT, rs, kt * 32, k0, lane);
-    const bf16x8 klo = ct_frag(sT, rs, kt * 32, cp + k0, lane);
-    const bf16x8 qhi = ct_row(sT, rs, q, k0, half);
-    const bf16x8 qlo = ct_row(sT, rs, q, cp + k0, half);
-    acc = mfma32(khi, qhi, acc);
-    acc = mfma32(klo, qhi, acc);
-    acc = mfma32(khi, qlo, acc);
+#pragma unroll
+  for (int ks = 0; ks < 4; ks++) {
+    if (16 * ks < cp) {
+      const bf16x8 ahi = ct_frag(sT, rs, t0, 16 * ks, lane);
+      const bf16x8 alo = ct_frag(sT, rs, t0, cp + 16 * ks, lane);
+      acc = mfma32(ahi, f.hi[ks], acc);
+      if constexpr (A_IS_KEY) {
+        acc = mfma32(alo, f.hi[ks], acc);
+        acc = mfma32(ahi, f.lo[ks], acc);
+      } else {
+        acc = mfma32(ahi, f.lo[ks], acc);
+        acc = mfma32(alo, f.hi[ks], acc);
+      }
+    }
   }
   return acc;
 }
 
-// Same products with queries qt*32.. as the A operand and the lane's key j as
-// the B operand (G[query][key]), in the same order of terms.
-__device__ __forceinline__ f32x16 gram_queries(const bf16* sT, int rs, int cp, int qt, int j,
-                                               int lane) {
-  const int half = lane >> 5;
-  f32x16 acc = {};
-  for (int k0 = 0; k0 < cp; k0 += 16) {
-    const bf16x8 qhi = ct_frag(sT, rs, qt * 32, k0, lane);
-    const bf16x8 qlo = ct_frag(sT, rs, qt * 32, cp + k0, lane);
-    const bf16x8 khi = ct_row(sT, rs, j, k0, half);
-    const bf16x8 klo = ct_row(sT, rs, j, cp + k0, half);
-    acc = mfma32(qhi, khi, acc);
-    acc = mfma32(qhi, klo, acc);
-    acc = mfma32(qlo, khi, acc);
-  }
-  return acc;
+// Gram tile G^T[key][query] for keys kt*32.. (A operand, table rows) and the
+// lane's query q (B operand): hi.hi + lo.hi + hi.lo, in that order.
+__device__ __forceinline__ f32x16 gram_keys(const bf16* sT, int rs, int cp, int kt, int q,
+                                            int lane) {
+  RowFrags f;
+  row_frags(sT, rs, cp, q, lane >> 5, f);
+  return gram_tile<true>(sT, rs, cp, kt * 32, f, lane);
 }
 
 // Scale of the logits of a row with mean squared distance m: a = -D * scale.
@@ -224,12 +343,17 @@ __device__ __forceinline__ float logit_scale(float m, float inv_tau, int scaled)
 }
 
 // Dynamic LDS layouts (bytes).
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
 constexpr int table_bytes(int NT, int cp) { return NT * 32 * (2 * cp + 8) * 2; }
+// (the forward's last phase reuses the space for (NT + 1) / 2 partial
+// readouts of (SW / 32 * 16 + 2) x 64 floats)
 constexpr int fwd_lds_bytes(int NT, int SW, int cp) {
-  return NT * 32 * SW * 2 + NT * 32 * 4 + table_bytes(NT, cp);
+  return cmax(NT * 32 * SW * 2 + NT * 32 * 4 + (NT + 1) * 64 * 4 + 16 * 4 + 2 * NT * 32 * 4 +
+                  table_bytes(NT, cp),
+              (NT + 1) / 2 * (SW / 32 * 16 + 2) * 64 * 4);
 }
 constexpr int dx_lds_bytes(int NT, int SW, int cp) {
-  return NT * 32 * SW * 2 + 3 * NT * 32 * 4 + table_bytes(NT, cp);
+  return NT * 32 * SW * 2 + 5 * NT * 32 * 4 + table_bytes(NT, cp);
 }
 // rows kernel: NS stages of [x rows (NT * 32)][64] + [dy rows (32)][64] bf16
 constexpr int rows_stage_elems(int NT) { return (NT * 32 + 32) * 64; }
@@ -240,115 +364,224 @@ constexpr int rows_stages(int NT, int cp) {
   return rows_lds_bytes(NT, 3, cp) <= 160 * 1024 ? 3 : 2;
 }
 // coordinate kernel: E tile [32][NP + 1] fp32, coordinates [NP][ck + 1] fp32,
-// row-sum parts [8][32], and the per-wave partial products [4][32][ck + 1]
+// row-sum parts [16][32], and the per-wave partial products [4][32][ck + 1]
 // (in the E tile's space where they fit, else after the rest)
 constexpr bool coord_part_in_e(int NT, int ck) { return 4 * 32 * (ck + 1) <= 32 * (NT * 32 + 1); }
 constexpr int coord_lds_bytes(int NT, int ck) {
-  return 32 * (NT * 32 + 1) * 4 + NT * 32 * (ck + 1) * 4 + 8 * 32 * 4 +
+  return 32 * (NT * 32 + 1) * 4 + NT * 32 * (ck + 1) * 4 + 16 * 32 * 4 +
          (coord_part_in_e(NT, ck) ? 0 : 4 * 32 * (ck + 1) * 4);
 }
 
 // ---------------------------------------------------------------------------
-// Forward.  Block = (window b, slab s of SW columns), 8 waves, wave w on query
-// tile wave_tile(w); grid = batch * slabs, dealt so that the slabs of one
-// window share an XCD (its coordinates are read from HBM once).  Per
-// coupling: D = N_key + N_q - 2 G (one add, one FMA), the row sum, then the
-// logit D * k2 and its exponential, its sum and (PARTNERS) the entropy term;
-// the causal mask only on the diagonal tile.
+// Forward.  Block = (window b, slab s of SW columns), 8 waves; grid = batch *
+// slabs, dealt so that the slabs of one window share an XCD (its coordinates
+// are read from HBM once).
+//
+// Work plan: the query tiles pair up as (i, NT - 1 - i), i < ceil(NT / 2),
+// and the two waves of SIMD i (waves i and i + 4) share pair i's causal work
+// (NT + 1 key tiles) evenly: wave i takes query tile i whole (when it differs
+// from the other) and key tiles [0, sA) of query tile qb = NT - 1 - i; wave
+// i + 4 takes key tiles [sA, qb] of qb, the diagonal first.  The two partial
+// readouts of qb (numerator and sums) meet in LDS at the end.
+//
+// A row's mean is known before any exponential: the earlier tiles' part from
+// the tile sums (build_table), the diagonal tile's from its Gram tile (wave i
+// recomputes qb's for its share).  Then per key tile: D = N_key + N_q - 2 G
+// (one add, one FMA), the exponential of D k2, its sum (and, PARTNERS, the
+// entropy term), and the tile's product with the x slab; the query's table
+// fragments stay in registers.
 // ---------------------------------------------------------------------------
 template <int NT, int SW, bool PARTNERS>
 __global__ __launch_bounds__(FT) void field_fwd_kernel(
     const float* __restrict__ p, const bf16* __restrict__ x, bf16* __restrict__ y,
     float* __restrict__ row_mean, float* __restrict__ lse, float* __restrict__ partners, int n,
-    int c, int cp, int width, int slabs, float inv_tau, int scaled) {
+    int c, int cp, int width, int slabs, float inv_tau, int scaled, int vec) {
   constexpr int NP = NT * 32, DT = SW / 32;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sX = (bf16*)smem;
   float* sN = (float*)(smem + NP * SW * 2);
-  bf16* sT = (bf16*)(smem + NP * SW * 2 + NP * 4);
+  float* sTS = sN + NP;                       // [NT + 1][64]
+  float* sPN = sTS + (NT + 1) * 64;           // [16]
+  float* sNh = sPN + 16;                      // [2][NP]
+  bf16* sT = (bf16*)(sNh + 2 * NP);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / slabs, s = lin % slabs;
-  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int lane = threadIdx.x & 63, half = lane >> 5, lq = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int rs = ct_stride(cp);
-  load_slab<NT, SW>(x + (size_t)b * n * width + (size_t)s * SW, width, n, sX);
-  build_coords(p + (size_t)b * n * c, n, c, cp, NP, sT, sN);
-  const int qt = wave_tile(wave);
-  if (qt >= NT) return;
-  const int q = qt * 32 + (lane & 31);
-  const float nq = sN[q];
-  f32x16 sc[NT];
-  float dsum = 0.f;
+  Slab<NT, SW> slab;
+  build_table<NT, true>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, sTS, sPN, vec,
+                        [&] { slab.issue(x + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  // the plan of this wave
+  const int pi = wave & 3;
+  const bool roleA = wave < 4, active = pi < (NT + 1) / 2;
+  const int qa = pi, qb = NT - 1 - pi;
+  const int sA = qa < qb ? (qb - qa) / 2 : (qb + 1) / 2;
+  const bool own = roleA && active && qa < qb;          // wave A's whole tile
+  f32x16 o[DT];
+  float z = 0.f, za = 0.f;
+  auto reset = [&] {
 #pragma unroll
-  for (int kt = 0; kt < NT; kt++) {
-    if (kt > qt) continue;
-    f32x16 acc = gram_keys(sT, rs, cp, kt, q, lane);
+    for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
+    z = 0.f;
+    za = 0.f;
+  };
+  // sum of D over the keys of the tiles before Q
+  auto row_off = [&](const RowFrags& fr, int Q, float nqv) {
+    float dotp = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ks++) {
+      if (16 * ks < cp) {
+        const float* ts = sTS + Q * 64 + 16 * ks + 8 * half;
+        const f32x4 t0 = *(const f32x4*)ts, t1 = *(const f32x4*)(ts + 4);
+#pragma unroll
+        for (int e = 0; e < 8; e++)
+          dotp = fmaf((float)fr.hi[ks][e] + (float)fr.lo[ks][e], e < 4 ? t0[e] : t1[e - 4], dotp);
+      }
+    }
+    dotp += __shfl_xor(dotp, 32);
+    float pn = 0.f;
+    for (int t = 0; t < Q; t++) pn += sPN[t];
+    return (float)(32 * Q) * nqv + pn - 2.f * dotp;
+  };
+  // the diagonal tile of Q: D (q itself and keys after q set to 0) and its row sum
+  auto diag = [&](const RowFrags& fr, int Q, float nqv, f32x16& d) {
+    d = gram_tile<true>(sT, rs, cp, Q * 32, fr, lane);
+    float dsum = 0.f;
 #pragma unroll
     for (int g = 0; g < 4; g++) {
-      const f32x4 n4 = *(const f32x4*)(sN + kt * 32 + 8 * g + 4 * half);
+      const f32x4 n4 = *(const f32x4*)(sN + Q * 32 + 8 * g + 4 * half);
 #pragma unroll
       for (int r = 0; r < 4; r++) {
         const int e = 4 * g + r;
-        float d = fmaf(acc[e], -2.f, n4[r] + nq);
-        if (kt == qt && 8 * g + 4 * half + r >= (lane & 31)) d = 0.f;  // q itself, keys after q
-        acc[e] = d;
-        dsum += d;
+        float dv = fmaf(d[e], -2.f, n4[r] + nqv);
+        if (8 * g + 4 * half + r >= lq) dv = 0.f;
+        d[e] = dv;
+        dsum += dv;
       }
     }
-    sc[kt] = acc;
-  }
-  dsum += __shfl_xor(dsum, 32);
-  const float m = dsum / (float)(q + 1);
-  const float k2 = -logit_scale(m, inv_tau, scaled) * LOG2E;
-  float z = 0.f, za = 0.f;                  // sum of exp, sum of exp * logit (log2 units)
-#pragma unroll
-  for (int kt = 0; kt < NT; kt++) {
-    if (kt > qt) continue;
-#pragma unroll
-    for (int e = 0; e < 16; e++) {
-      const float a = sc[kt][e] * k2;
-      float pe = __builtin_amdgcn_exp2f(a);
-      if (kt == qt && att_masked(e, lane)) pe = 0.f;
-      sc[kt][e] = pe;
-      z += pe;
-      if constexpr (PARTNERS) za += pe * a;
-    }
-  }
-  z += __shfl_xor(z, 32);
-  if constexpr (PARTNERS) za += __shfl_xor(za, 32);
-  f32x16 o[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
-#pragma unroll
-  for (int kt = 0; kt < NT; kt++) {
-    if (kt > qt) continue;
+    return dsum + __shfl_xor(dsum, 32);
+  };
+  auto readout = [&](f32x16& pe, int kt) {
 #pragma unroll
     for (int mm = 0; mm < 2; mm++) {
-      const bf16x8 pf = att_pack(sc[kt], mm);
+      const bf16x8 pf = att_pack(pe, mm);
 #pragma unroll
       for (int dt = 0; dt < DT; dt++)
         o[dt] = mfma32(att_trfrag(sX + (dt / 2) * NP * 64, kt * 32 + 16 * mm, 32 * (dt % 2), lane),
                        pf, o[dt]);
     }
-  }
-  if (q >= n) return;
-  // O^T register e of lane l: query q, column 32 dt + 8 (e / 4) + 4 half + e % 4
-  const float inv = 1.f / z;
-  bf16* yrow = y + ((size_t)b * n + q) * width + (size_t)s * SW;
+  };
+  // exponentials of a tile of D (diagonal: masked), their sums
+  auto expo = [&](f32x16& d, float k2, bool is_diag) {
 #pragma unroll
-  for (int dt = 0; dt < DT; dt++)
+    for (int e = 0; e < 16; e++) {
+      const float a = d[e] * k2;
+      float pe = __builtin_amdgcn_exp2f(a);
+      if (is_diag && att_masked(e, lane)) pe = 0.f;
+      d[e] = pe;
+      z += pe;
+      if constexpr (PARTNERS) za += pe * a;
+    }
+  };
+  // one off-diagonal key tile of query tile Q
+  auto tile = [&](const RowFrags& fr, int kt, float nqv, float k2) {
+    f32x16 acc = gram_tile<true>(sT, rs, cp, kt * 32, fr, lane);
 #pragma unroll
     for (int g = 0; g < 4; g++) {
-      const bf16x4 v = {to_bf16(o[dt][4 * g] * inv), to_bf16(o[dt][4 * g + 1] * inv),
-                        to_bf16(o[dt][4 * g + 2] * inv), to_bf16(o[dt][4 * g + 3] * inv)};
-      *(bf16x4*)(yrow + 32 * dt + 8 * g + 4 * half) = v;
+      const f32x4 n4 = *(const f32x4*)(sN + kt * 32 + 8 * g + 4 * half);
+#pragma unroll
+      for (int r = 0; r < 4; r++) acc[4 * g + r] = fmaf(acc[4 * g + r], -2.f, n4[r] + nqv);
     }
-  if (s == 0 && half == 0) {
-    const float l2z = __builtin_amdgcn_logf(z);         // log2 Z
-    const size_t at = (size_t)b * n + q;
-    row_mean[at] = m;
-    lse[at] = l2z * LN2;
-    if constexpr (PARTNERS) partners[at] = __builtin_amdgcn_exp2f(l2z - za * inv);
+    expo(acc, k2, false);
+    readout(acc, kt);
+  };
+  auto finish = [&](int Q, float m) {
+    const int q = Q * 32 + lq;
+    if (q >= n) return;
+    // O^T register e of lane l: query q, column 32 dt + 8 (e / 4) + 4 half + e % 4
+    const float inv = 1.f / z;
+    bf16* yrow = y + ((size_t)b * n + q) * width + (size_t)s * SW;
+#pragma unroll
+    for (int dt = 0; dt < DT; dt++)
+#pragma unroll
+      for (int g = 0; g < 4; g++) {
+        const bf16x4 v = {to_bf16(o[dt][4 * g] * inv), to_bf16(o[dt][4 * g + 1] * inv),
+                          to_bf16(o[dt][4 * g + 2] * inv), to_bf16(o[dt][4 * g + 3] * inv)};
+        *(bf16x4*)(yrow + 32 * dt + 8 * g + 4 * half) = v;
+      }
+    if (s == 0 && half == 0) {
+      const float l2z = __builtin_amdgcn_logf(z);       // log2 Z
+      const size_t at = (size_t)b * n + q;
+      row_mean[at] = m;
+      lse[at] = l2z * LN2;
+      if constexpr (PARTNERS) partners[at] = __builtin_amdgcn_exp2f(l2z - za * inv);
+    }
+  };
+
+  // before the slab barrier: every wave's diagonal tile (wave A: its own
+  // tile's, and qb's row sum for the mean of its share)
+  RowFrags fa, fb;
+  float nqa = 0.f, nqb = 0.f, ma = 0.f, mb = 0.f, k2a = 0.f, k2b = 0.f;
+  f32x16 dA = {}, dB = {};
+  if (active) {
+    row_frags(sT, rs, cp, qb * 32 + lq, half, fb);
+    nqb = sN[qb * 32 + lq];
+    const float dsb = diag(fb, qb, nqb, dB);
+    mb = (row_off(fb, qb, nqb) + dsb) / (float)(qb * 32 + lq + 1);
+    k2b = -logit_scale(mb, inv_tau, scaled) * LOG2E;
+    if (own) {
+      row_frags(sT, rs, cp, qa * 32 + lq, half, fa);
+      nqa = sN[qa * 32 + lq];
+      const float dsa = diag(fa, qa, nqa, dA);
+      ma = (row_off(fa, qa, nqa) + dsa) / (float)(qa * 32 + lq + 1);
+      k2a = -logit_scale(ma, inv_tau, scaled) * LOG2E;
+    }
+  }
+  slab.store(sX, n);
+  __syncthreads();
+  if (own) {                                  // wave A: query tile qa whole
+    reset();
+    expo(dA, k2a, true);
+    readout(dA, qa);
+    for (int kt = qa - 1; kt >= 0; kt--) tile(fa, kt, nqa, k2a);
+    z += __shfl_xor(z, 32);
+    if constexpr (PARTNERS) za += __shfl_xor(za, 32);
+    finish(qa, ma);
+  }
+  reset();
+  if (active) {
+    if (roleA) {                              // wave A: key tiles [0, sA) of qb
+      for (int kt = 0; kt < sA; kt++) tile(fb, kt, nqb, k2b);
+    } else {                                  // wave B: key tiles [sA, qb] of qb
+      expo(dB, k2b, true);
+      readout(dB, qb);
+      for (int kt = qb - 1; kt >= sA; kt--) tile(fb, kt, nqb, k2b);
+    }
+  }
+  // wave A's partial readout of qb joins wave B's through LDS (the slab and
+  // the table are no longer read)
+  __syncthreads();
+  float* part = (float*)smem + pi * (DT * 16 + 2) * 64;
+  if (active && roleA) {
+#pragma unroll
+    for (int dt = 0; dt < DT; dt++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) part[(dt * 16 + e) * 64 + lane] = o[dt][e];
+    part[DT * 16 * 64 + lane] = z;
+    part[(DT * 16 + 1) * 64 + lane] = za;
+  }
+  __syncthreads();
+  if (active && !roleA) {
+#pragma unroll
+    for (int dt = 0; dt < DT; dt++)
+#pragma unroll
+      for (int e = 0; e < 16; e++) o[dt][e] += part[(dt * 16 + e) * 64 + lane];
+    z += part[DT * 16 * 64 + lane];
+    za += part[(DT * 16 + 1) * 64 + lane];
+    z += __shfl_xor(z, 32);
+    if constexpr (PARTNERS) za += __shfl_xor(za, 32);
+    finish(qb, mb);
   }
 }
 
@@ -367,12 +600,12 @@ template <int NT, int NS>
 __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
     const float* __restrict__ p, const bf16* __restrict__ x, const bf16* __restrict__ dy,
     const float* __restrict__ row_mean, const float* __restrict__ lse, float* __restrict__ ddt,
-    int n, int c, int cp, int width, float inv_tau, int scaled) {
+    int n, int c, int cp, int width, float inv_tau, int scaled, int vec) {
   constexpr int NP = NT * 32, STAGE = rows_stage_elems(NT);
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sStage = (bf16*)smem;
   float* sN = (float*)(smem + NS * STAGE * 2);
-  float* sRed = sN + NP;                              // [2][8 waves][32]
+  float* sRed = sN + NP;                              // [2][8 waves][32]; first the half norms
   bf16* sT = (bf16*)(sRed + 2 * 8 * 32);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / NT, qt = NT - 1 - lin % NT;
@@ -413,7 +646,8 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
     if (st < steps) dma(st, st);
   const float m_ld = row_mean[(size_t)b * n + min(q, n - 1)];
   const float l_ld = lse[(size_t)b * n + min(q, n - 1)];
-  build_coords(p + (size_t)b * n * c, n, c, cp, (qt + 1) * 32, sT, sN);
+  build_table<NT, false>(p + (size_t)b * n * c, n, c, cp, (qt + 1) * 32, sT, sN, sRed, nullptr,
+                         nullptr, vec, NoIssue{});
   const float m = qvalid ? m_ld : 0.f;
   const float l2 = qvalid ? l_ld * LOG2E : 0.f;
   const float scale = qvalid ? logit_scale(m, inv_tau, scaled) : 0.f;
@@ -499,14 +733,15 @@ template <int NT, int SW>
 __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
     const float* __restrict__ p, const float* __restrict__ row_mean, const float* __restrict__ lse,
     const bf16* __restrict__ dy, bf16* __restrict__ dx, int n, int c, int cp, int width,
-    int slabs, float inv_tau, int scaled) {
+    int slabs, float inv_tau, int scaled, int vec) {
   constexpr int NP = NT * 32, DT = SW / 32;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sDY = (bf16*)smem;
   float* sN = (float*)(smem + NP * SW * 2);
   float* sK2 = sN + NP;                       // -scale_q log2 e
   float* sL2 = sK2 + NP;                      // -ln Z_q log2 e
-  bf16* sT = (bf16*)(sL2 + NP);
+  float* sNh = sL2 + NP;                      // [2][NP]
+  bf16* sT = (bf16*)(sNh + 2 * NP);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / slabs, s = lin % slabs;
   const int lane = threadIdx.x & 63, half = lane >> 5;
@@ -520,20 +755,35 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
     sK2[q] = v ? -logit_scale(m, inv_tau, scaled) * LOG2E : 0.f;
     sL2[q] = v ? -l * LOG2E : 0.f;
   }
-  load_slab<NT, SW>(dy + (size_t)b * n * width + (size_t)s * SW, width, n, sDY);
-  build_coords(p + (size_t)b * n * c, n, c, cp, NP, sT, sN);
+  Slab<NT, SW> slab;
+  build_table<NT, false>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, nullptr, nullptr, vec,
+                         [&] { slab.issue(dy + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  slab.store(sDY, n);
+  __syncthreads();
   const int kt = wave_tile(wave);
   if (kt >= NT) return;
-  const int j = kt * 32 + (lane & 31);
+  const int lj = lane & 31, j = kt * 32 + lj;
+  RowFrags f;
+  row_frags(sT, rs, cp, j, half, f);
   const float nj = sN[j];
   f32x16 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
+  auto readout = [&](f32x16& ce, int qt) {
 #pragma unroll
-  for (int qt = 0; qt < NT; qt++) {
-    if (qt < kt) continue;
-    f32x16 acc = gram_queries(sT, rs, cp, qt, j, lane);
-    // register e: query qt*32 + 8 (e/4) + 4 half + e%4, key j
+    for (int mm = 0; mm < 2; mm++) {
+      const bf16x8 pf = att_pack(ce, mm);
+#pragma unroll
+      for (int dt = 0; dt < DT; dt++)
+        o[dt] = mfma32(att_trfrag(sDY + (dt / 2) * NP * 64, qt * 32 + 16 * mm, 32 * (dt % 2), lane),
+                       pf, o[dt]);
+    }
+  };
+  // register e: query qt*32 + 8 (e/4) + 4 half + e%4, key j; the diagonal tile
+  // first (its own diagonal exactly 0, queries before j masked)
+  for (int qt = kt; qt < NT; qt++) {
+    f32x16 acc = gram_tile<false>(sT, rs, cp, qt * 32, f, lane);
+    const bool diag = qt == kt;
 #pragma unroll
     for (int gq = 0; gq < 4; gq++) {
       const int q0 = qt * 32 + 8 * gq + 4 * half;
@@ -542,23 +792,15 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
       const f32x4 l4 = *(const f32x4*)(sL2 + q0);
 #pragma unroll
       for (int r = 0; r < 4; r++) {
-        const int e = 4 * gq + r;
-        const int lq = 8 * gq + 4 * half + r, lj = lane & 31;   // within the tiles
+        const int e = 4 * gq + r, lq = 8 * gq + 4 * half + r;
         float d = fmaf(acc[e], -2.f, n4[r] + nj);
-        if (qt == kt && lq == lj) d = 0.f;                     // the diagonal
+        if (diag && lq == lj) d = 0.f;
         float ce = __builtin_amdgcn_exp2f(fmaf(d, k4[r], l4[r]));
-        if (qt == kt && lq < lj) ce = 0.f;                     // query before j
+        if (diag && lq < lj) ce = 0.f;
         acc[e] = ce;
       }
     }
-#pragma unroll
-    for (int mm = 0; mm < 2; mm++) {
-      const bf16x8 pf = att_pack(acc, mm);
-#pragma unroll
-      for (int dt = 0; dt < DT; dt++)
-        o[dt] = mfma32(att_trfrag(sDY + (dt / 2) * NP * 64, qt * 32 + 16 * mm, 32 * (dt % 2), lane),
-                       pf, o[dt]);
-    }
+    readout(acc, qt);
   }
   if (j >= n) return;
   bf16* xrow = dx + ((size_t)b * n + j) * width + (size_t)s * SW;
@@ -573,130 +815,158 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Backward, coordinates.  Block = (window b, row tile t), 4 waves: E[i][j] for
+// Backward, coordinates.  Block = (window b, row tile t), 8 waves: E[i][j] for
 // the tile's 32 rows i and every j (dD[i][j] = ddt[j][i] for j < i, dD[j][i] =
 // ddt[i][j] for j > i; 0 at j = i and outside the window) into LDS; then
 //   dp_i = 2 (sum_j E[i][j]) p'_i - 2 sum_j E[i][j] p'_j,  p' = p - p_0,
 // the second sum on the fp32 matrix cores (32 x 32 x 2: A = p'^T, B = E^T),
-// wave w taking a quarter of the j range; partial products meet in LDS.
+// waves 0-3 taking a quarter of the j range each; partial products meet in
+// LDS.
 // ---------------------------------------------------------------------------
 template <int NT, int CK>
-__global__ __launch_bounds__(FTC) void field_bwd_coord_kernel(const float* __restrict__ p,
-                                                             const float* __restrict__ ddt,
-                                                             float* __restrict__ dp, int n,
-                                                             int c) {
+__global__ __launch_bounds__(FT) void field_bwd_coord_kernel(const float* __restrict__ p,
+                                                            const float* __restrict__ ddt,
+                                                            float* __restrict__ dp, int n,
+                                                            int c, int vec) {
   constexpr int NP = NT * 32, ES = NP + 1, CKP = CK + 1;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   float* sE = (float*)smem;                          // [32][ES]
   float* sP = sE + 32 * ES;                          // [NP][CKP]
-  float* sRowPart = sP + NP * CKP;                   // [8][32]
-  float* sPart = coord_part_in_e(NT, CK) ? sE : sRowPart + 8 * 32;   // [4][32][CKP]
+  float* sRowPart = sP + NP * CKP;                   // [16][32]
+  float* sPart = coord_part_in_e(NT, CK) ? sE : sRowPart + 16 * 32;   // [4][32][CKP]
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / NT, t = lin % NT;
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const float* pw = p + (size_t)b * n * c;
   const float* dw = ddt + (size_t)b * NP * NP;
-  // E: element u of this thread is e = tid + 256 u of the 32 * NP entries,
-  // first those with j < (t + 1) * 32 (j = e / 32, consecutive i along ddt
-  // rows j, or ddt[i][j] for j > i), then the rest (i = e' / rest, j
-  // contiguous along ddt rows i).  All loads before the first LDS write; every
-  // address lies in the window's NP x NP workspace, and the entries that are
-  // not part of E (j = i, outside the window) are replaced by 0.
-  constexpr int PER = NT * 4;
-  const int split = (t + 1) * 32 * 32, rest = NP - (t + 1) * 32;
-  float ev[PER];
+  // E in three parts, 16-byte loads where the rows are contiguous, every load
+  // unconditional (indices inside the window's NP x NP workspace) and the
+  // entries outside E (j = i, outside the window) replaced by 0 afterwards:
+  //   j < 32 t: ddt[j][32 t .. 32 t + 31] (i consecutive): 8 float4 per j,
+  //     group g = tid + 512 u, j = g / 8;
+  //   the diagonal tile: ddt[j][i] for j < i, ddt[i][j] for j > i, scalar;
+  //   j >= 32 (t + 1): ddt[i][j] (j consecutive): wave w takes rows
+  //     ii = 4 w .. 4 w + 3, lane l the float4 at j = 32 (t + 1) + 4 l.
+  constexpr int PA = (NT + 1) / 2;
+  const int na = (t * 32 * 8 + FT - 1) / FT, j0 = (t + 1) * 32;
+  f32x4 ea[PA], eb[4];
+  float ed[2];
 #pragma unroll
-  for (int u = 0; u < PER; u++) {
-    const int e = threadIdx.x + FTC * u;
-    int ii, j;
-    if (e < split) {
-      j = e >> 5;
-      ii = e & 31;
-    } else {
-      ii = (e - split) / rest;
-      j = (t + 1) * 32 + (e - split) % rest;
-    }
-    const int i = t * 32 + ii;
-    const float v = dw[j < i ? (size_t)j * NP + i : (size_t)i * NP + j];
-    ev[u] = (i < n && j < n && j != i) ? v : 0.f;
+  for (int u = 0; u < PA; u++) {
+    const int g = min((int)threadIdx.x + FT * u, max(t * 32 * 8 - 1, 0));
+    ea[u] = *(const f32x4*)(dw + (size_t)(g >> 3) * NP + 32 * t + 4 * (g & 7));
+  }
+#pragma unroll
+  for (int u = 0; u < 2; u++) {
+    const int e = threadIdx.x + FT * u, jj = e >> 5, ii = e & 31;
+    const int i = 32 * t + ii, j = 32 * t + jj;
+    ed[u] = dw[jj < ii ? (size_t)j * NP + i : (size_t)i * NP + j];
+  }
+#pragma unroll
+  for (int u = 0; u < 4; u++) {
+    const int ii = 4 * wave + u, j = min(j0 + 4 * lane, NP - 4);
+    eb[u] = *(const f32x4*)(dw + (size_t)(32 * t + ii) * NP + j);
   }
   // coordinates: rows past the window zero (their E entries are 0, so they
   // must be finite); columns past c are left as they are (they only reach
   // output rows that are not used)
-  for (int idx = threadIdx.x; idx < (NP - n) * CKP; idx += FTC) sP[n * CKP + idx] = 0.f;
-  stage_coords<FTC, 64>(pw, n, c, (unsigned char*)sP, CKP * 4);
+  for (int idx = threadIdx.x; idx < (NP - n) * CKP; idx += FT) sP[n * CKP + idx] = 0.f;
+  stage_coords<FT>(pw, n, c, (unsigned char*)sP, CKP * 4, vec);
 #pragma unroll
-  for (int u = 0; u < PER; u++) {
-    const int e = threadIdx.x + FTC * u;
-    int ii, j;
-    if (e < split) {
-      j = e >> 5;
-      ii = e & 31;
-    } else {
-      ii = (e - split) / rest;
-      j = (t + 1) * 32 + (e - split) % rest;
+  for (int u = 0; u < PA; u++) {
+    if (u < na && (int)threadIdx.x + FT * u < t * 32 * 8) {
+      const int g = threadIdx.x + FT * u, j = g >> 3;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const int ii = 4 * (g & 7) + e, i = 32 * t + ii;
+        sE[ii * ES + j] = (i < n && j < n) ? ea[u][e] : 0.f;
+      }
     }
-    sE[ii * ES + j] = ev[u];
+  }
+#pragma unroll
+  for (int u = 0; u < 2; u++) {
+    const int e = threadIdx.x + FT * u, jj = e >> 5, ii = e & 31;
+    const int i = 32 * t + ii, j = 32 * t + jj;
+    sE[ii * ES + j] = (i < n && j < n && jj != ii) ? ed[u] : 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < 4; u++) {
+    const int ii = 4 * wave + u, i = 32 * t + ii, j = j0 + 4 * lane;
+    if (j < NP) {
+#pragma unroll
+      for (int e = 0; e < 4; e++) sE[ii * ES + j + e] = (i < n && j + e < n) ? eb[u][e] : 0.f;
+    }
   }
   __syncthreads();
   {
-    // row sums: lane group of 32 = the 32 rows at one j, 8 groups over j
+    // row sums: lane group of 32 = the 32 rows at one j, 16 groups over j
     const int ii = threadIdx.x & 31, part = threadIdx.x >> 5;
     float rsum = 0.f;
-    for (int j = part; j < NP; j += 8) rsum += sE[ii * ES + j];
+    for (int j = part; j < NP; j += 16) rsum += sE[ii * ES + j];
     sRowPart[part * 32 + ii] = rsum;
   }
-  constexpr int JW = NP / 4;                         // j range of one wave
+  constexpr int JW = NP / 4;                         // j range of one of waves 0-3
   f32x16 acc[CK / 32];
 #pragma unroll
   for (int kc = 0; kc < CK / 32; kc++) acc[kc] = f32x16{};
-  float p0[CK / 32];                                 // p_0 at this lane's coordinates
+  if (wave < 4) {
+    float p0[CK / 32];                               // p_0 at this lane's coordinates
 #pragma unroll
-  for (int kc = 0; kc < CK / 32; kc++) p0[kc] = sP[kc * 32 + (lane & 31)];
-  for (int js = 0; js < JW; js += 2) {
-    const int j = wave * JW + js + half;
-    const float bv = sE[(lane & 31) * ES + j];       // B[k = half][col i] = E[i][j]
+    for (int kc = 0; kc < CK / 32; kc++) p0[kc] = sP[kc * 32 + (lane & 31)];
+    for (int js = 0; js < JW; js += 2) {
+      const int j = wave * JW + js + half;
+      const float bv = sE[(lane & 31) * ES + j];     // B[k = half][col i] = E[i][j]
 #pragma unroll
-    for (int kc = 0; kc < CK / 32; kc++) {
-      // A[row k][half] = p'_j[k] = p_j[k] - p_0[k]
-      const float av = sP[j * CKP + kc * 32 + (lane & 31)] - p0[kc];
-      acc[kc] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[kc], 0, 0, 0);
+      for (int kc = 0; kc < CK / 32; kc++) {
+        // A[row k][half] = p'_j[k] = p_j[k] - p_0[k]
+        const float av = sP[j * CKP + kc * 32 + (lane & 31)] - p0[kc];
+        acc[kc] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[kc], 0, 0, 0);
+      }
     }
   }
   __syncthreads();                                   // sE may be reused for the partials
   // register e: coordinate k = kc*32 + 8 (e/4) + 4 half + e%4, row i = lane % 32
+  if (wave < 4) {
 #pragma unroll
-  for (int kc = 0; kc < CK / 32; kc++)
+    for (int kc = 0; kc < CK / 32; kc++)
 #pragma unroll
-    for (int e = 0; e < 16; e++) {
-      const int k = kc * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-      sPart[(wave * 32 + (lane & 31)) * CKP + k] = acc[kc][e];
-    }
+      for (int e = 0; e < 16; e++) {
+        const int k = kc * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+        sPart[(wave * 32 + (lane & 31)) * CKP + k] = acc[kc][e];
+      }
+  }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 32 * c; idx += FTC) {
+  for (int idx = threadIdx.x; idx < 32 * c; idx += FT) {
     const int ii = idx / c, k = idx % c, i = t * 32 + ii;
     if (i >= n) continue;
     float rsum = 0.f;
 #pragma unroll
-    for (int part = 0; part < 8; part++) rsum += sRowPart[part * 32 + ii];
+    for (int part = 0; part < 16; part++) rsum += sRowPart[part * 32 + ii];
     const float ep = sPart[(0 * 32 + ii) * CKP + k] + sPart[(1 * 32 + ii) * CKP + k] +
                      sPart[(2 * 32 + ii) * CKP + k] + sPart[(3 * 32 + ii) * CKP + k];
     dp[((size_t)b * n + i) * c + k] = 2.f * (rsum * (sP[i * CKP + k] - sP[k]) - ep);
   }
 }
 
+// Whether the coordinates take the 16-byte load path: p 16-byte aligned and
+// c a multiple of 4 (then every window's rows start 16-byte aligned too).
+inline int coords_vec(const float* p, int c) {
+  return ((uintptr_t)p % 16 == 0 && c % 4 == 0) ? 1 : 0;
+}
+
 template <int NT, int SW, bool PARTNERS>
 hipError_t field_fwd_launch(const float* p, const bf16* x, bf16* y, float* row_mean, float* lse,
                             float* partners, int batch, int n, int c, int cp, int width,
                             float inv_tau, int scaled, hipStream_t st) {
+  const int vec = coords_vec(p, c);
   static std::atomic<unsigned long long> done{0};
   hipError_t e = lds_limit_once(done, (const void*)field_fwd_kernel<NT, SW, PARTNERS>,
                                 fwd_lds_bytes(NT, SW, 64));
   if (e != hipSuccess) return e;
   const int slabs = width / SW;
   field_fwd_kernel<NT, SW, PARTNERS><<<batch * slabs, FT, fwd_lds_bytes(NT, SW, cp), st>>>(
-      p, x, y, row_mean, lse, partners, n, c, cp, width, slabs, inv_tau, scaled);
+      p, x, y, row_mean, lse, partners, n, c, cp, width, slabs, inv_tau, scaled, vec);
   return hipGetLastError();
 }
 
@@ -726,7 +996,7 @@ hipError_t field_dx_launch(const float* p, const float* row_mean, const float* l
   if (e != hipSuccess) return e;
   const int slabs = width / SW;
   field_bwd_dx_kernel<NT, SW><<<batch * slabs, FT, dx_lds_bytes(NT, SW, cp), st>>>(
-      p, row_mean, lse, dy, dx, n, c, cp, width, slabs, inv_tau, scaled);
+      p, row_mean, lse, dy, dx, n, c, cp, width, slabs, inv_tau, scaled, coords_vec(p, c));
   return hipGetLastError();
 }
 
@@ -738,7 +1008,7 @@ hipError_t field_rows_launch(const float* p, const bf16* x, const float* row_mea
   hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS>, 160 * 1024);
   if (e != hipSuccess) return e;
   field_bwd_rows_kernel<NT, NS><<<batch * NT, FT, rows_lds_bytes(NT, NS, cp), st>>>(
-      p, x, dy, row_mean, lse, ddt, n, c, cp, width, inv_tau, scaled);
+      p, x, dy, row_mean, lse, ddt, n, c, cp, width, inv_tau, scaled, coords_vec(p, c));
   return hipGetLastError();
 }
 
@@ -749,8 +1019,8 @@ hipError_t field_coord_launch(const float* p, const float* ddt, float* dp, int b
   hipError_t e = lds_limit_once(done, (const void*)field_bwd_coord_kernel<NT, CK>,
                                 coord_lds_bytes(NT, CK));
   if (e != hipSuccess) return e;
-  field_bwd_coord_kernel<NT, CK><<<batch * NT, FTC, coord_lds_bytes(NT, CK), st>>>(p, ddt, dp, n,
-                                                                                  c);
+  field_bwd_coord_kernel<NT, CK><<<batch * NT, FT, coord_lds_bytes(NT, CK), st>>>(
+      p, ddt, dp, n, c, coords_vec(p, c));
   return hipGetLastError();
 }
 
