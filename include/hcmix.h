@@ -409,22 +409,28 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
  * fp32, the two products with x and dy on bf16 matrix cores (couplings rounded
  * to bf16, fp32 accumulation), outputs rounded once.  In the scaled form a
  * positive row mean below 2^-100 is taken as 2^-100.
+ * workspace: hcmix_field_workspace_bytes(batch, n, coord_dim) bytes of device
+ * memory, 256-byte aligned, owned by the caller; it holds each window's
+ * prepared coordinate table during the call (and for the backward the gradient
+ * of the squared distances), so calls that share it must not overlap.
  * HCMIX_ERR_INVALID_VALUE: null pointers (partners may be null), batch, n,
  * width or coord_dim < 1, tau outside [2^-24, 2^24] or not finite, scaled not 0
  * or 1, an output overlapping an input or another output, a workspace smaller
- * than hcmix_field_workspace_bytes, sizes past the limits above.
+ * than the query, sizes past the limits above.
  * HCMIX_ERR_UNSUPPORTED: n above 256, coord_dim above 64, width not a
  * multiple of 64, bf16 pointers not 16-byte aligned, fp32 pointers not 4-byte
  * aligned, a workspace not 256-byte aligned. */
 hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
                                  float tau, int32_t scaled, const float* p, const void* x,
                                  void* y, float* row_mean, float* lse, float* partners,
-                                 void* stream);
+                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of device workspace hcmix_field_backward needs: batch * N * N * 4 with
- * N = n rounded up to a multiple of 32 (the gradient of each window's squared
- * distances); 0 for arguments outside the supported range. */
-size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n);
+/* Bytes of device workspace the field calls need: for each window its
+ * prepared coordinate table (about n (4 c' + 16) bytes, c' = coord_dim
+ * rounded up to 16), plus N * N * 4 with N = n rounded up to a multiple of 32
+ * (the gradient of the window's squared distances, used by the backward); 0
+ * for arguments outside the supported range. */
+size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n, int32_t coord_dim);
 
 /* Backward: dp = dL/dp and dx = dL/dx (both overwritten) from p, x, the
  * forward's row_mean and lse (same coordinates, tau and scaled), and dy:

@@ -1232,27 +1232,30 @@ hcmix_status check_field(int64_t batch, int64_t n, int64_t width, int32_t coord_
   return HCMIX_OK;
 }
 
-size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n) {
-  if (batch < 1 || n < 1 || n > 256 || batch > kMaxRows / n) return 0;
-  const size_t np = (size_t)(n + 31) / 32 * 32;
-  return (size_t)batch * np * np * sizeof(float);
+size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n, int32_t coord_dim) {
+  if (batch < 1 || n < 1 || n > 256 || coord_dim < 1 || coord_dim > 64) return 0;
+  if (batch > kMaxRows / n) return 0;
+  return field_workspace_bytes((int)batch, (int)n, coord_dim);
 }
 
 hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
                                  float tau, int32_t scaled, const float* p, const void* x,
                                  void* y, float* row_mean, float* lse, float* partners,
-                                 void* stream) {
+                                 void* workspace, size_t workspace_bytes, void* stream) {
   if (!p || !x || !y || !row_mean || !lse) return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_field(batch, n, width, coord_dim, tau, scaled);
   if (st != HCMIX_OK) return st;
+  const size_t need = hcmix_field_workspace_bytes(batch, n, coord_dim);
+  if (!workspace || workspace_bytes < need) return HCMIX_ERR_INVALID_VALUE;
   const size_t rows = (size_t)(batch * n), act = rows * width * sizeof(bf16);
   const size_t stat = rows * sizeof(float);
   const Span ins[2] = {{p, rows * coord_dim * sizeof(float)}, {x, act}};
-  const Span outs[4] = {{y, act}, {row_mean, stat}, {lse, stat}, {partners, partners ? stat : 0}};
-  st = check_spans(ins, 2, outs, 4, 4);
+  const Span outs[5] = {{y, act}, {row_mean, stat}, {lse, stat}, {partners, partners ? stat : 0},
+                        {workspace, need}};
+  st = check_spans(ins, 2, outs, 5, 4);
   if (st != HCMIX_OK) return st;
-  if (!aligned(x, 16) || !aligned(y, 16)) return HCMIX_ERR_UNSUPPORTED;
-  hipError_t e = launch_field_fwd(p, (const bf16*)x, (bf16*)y, row_mean, lse, partners,
+  if (!aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256)) return HCMIX_ERR_UNSUPPORTED;
+  hipError_t e = launch_field_fwd(p, (const bf16*)x, (bf16*)y, row_mean, lse, partners, workspace,
                                   (int)batch, (int)n, coord_dim, (int)width, 1.f / tau, scaled,
                                   (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
@@ -1266,7 +1269,7 @@ hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32
   if (!p || !x || !row_mean || !lse || !dy || !dp || !dx) return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_field(batch, n, width, coord_dim, tau, scaled);
   if (st != HCMIX_OK) return st;
-  const size_t need = hcmix_field_workspace_bytes(batch, n);
+  const size_t need = hcmix_field_workspace_bytes(batch, n, coord_dim);
   if (!workspace || workspace_bytes < need) return HCMIX_ERR_INVALID_VALUE;
   const size_t rows = (size_t)(batch * n), act = rows * width * sizeof(bf16);
   const size_t stat = rows * sizeof(float), coords = rows * coord_dim * sizeof(float);
@@ -1277,7 +1280,7 @@ hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32
   if (!aligned(x, 16) || !aligned(dy, 16) || !aligned(dx, 16) || !aligned(workspace, 256))
     return HCMIX_ERR_UNSUPPORTED;
   hipError_t e = launch_field_bwd(p, (const bf16*)x, row_mean, lse, (const bf16*)dy, dp,
-                                  (bf16*)dx, (float*)workspace, (int)batch, (int)n, coord_dim,
+                                  (bf16*)dx, workspace, (int)batch, (int)n, coord_dim,
                                   (int)width, 1.f / tau, scaled, (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }

@@ -101,9 +101,9 @@ def load():
         lib.hcmix_attention_backward.argtypes = [i64, i64, i32, i32, vp, vp, fp, vp, vp, vp]
         lib.hcmix_attention_backward.restype = i32
         lib.hcmix_field_forward.argtypes = [i64, i64, i64, i32, ctypes.c_float, i32, fp, vp, vp,
-                                            fp, fp, fp, vp]
+                                            fp, fp, fp, vp, sz, vp]
         lib.hcmix_field_forward.restype = i32
-        lib.hcmix_field_workspace_bytes.argtypes = [i64, i64]
+        lib.hcmix_field_workspace_bytes.argtypes = [i64, i64, i32]
         lib.hcmix_field_workspace_bytes.restype = sz
         lib.hcmix_field_backward.argtypes = [i64, i64, i64, i32, ctypes.c_float, i32, fp, vp, fp,
                                              fp, vp, fp, vp, vp, sz, vp]
@@ -525,7 +525,19 @@ def _field_shapes(p, x):
     return batch, n, width, p.shape[2]
 
 
-def field_forward(p, x, tau=1.0, scaled=True, partners=False, y=None, row_mean=None, lse=None):
+def field_workspace_bytes(batch: int, n: int, coord_dim: int) -> int:
+    return load().hcmix_field_workspace_bytes(batch, n, coord_dim)
+
+
+def _field_workspace(workspace, batch, n, c, dev):
+    if workspace is None:
+        need = field_workspace_bytes(batch, n, c)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    return workspace
+
+
+def field_forward(p, x, tau=1.0, scaled=True, partners=False, y=None, row_mean=None, lse=None,
+                  workspace=None):
     """Field coupling (Section 3.4): p [batch, n, c] fp32 coordinates, x
     [batch, n, width] bf16 -> (y bf16, row_mean fp32 [batch, n], lse fp32
     [batch, n], partners fp32 [batch, n] or None)."""
@@ -542,16 +554,14 @@ def field_forward(p, x, tau=1.0, scaled=True, partners=False, y=None, row_mean=N
     _need(row_mean, "row_mean", (batch, n), torch.float32, dev)
     _need(lse, "lse", (batch, n), torch.float32, dev)
     _gpu(dev)
+    workspace = _field_workspace(workspace, batch, n, c, dev)
     rc = load().hcmix_field_forward(batch, n, width, c, float(tau), int(bool(scaled)), _fptr(p),
                                     _ptr(x), _ptr(y), _fptr(row_mean), _fptr(lse),
-                                    _fptr(part) if part is not None else None, _stream(x))
+                                    _fptr(part) if part is not None else None, _ptr(workspace),
+                                    _bytes(workspace), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_field_forward")
     return y, row_mean, lse, part
-
-
-def field_workspace_bytes(batch: int, n: int) -> int:
-    return load().hcmix_field_workspace_bytes(batch, n)
 
 
 def field_backward(p, x, row_mean, lse, dy, tau=1.0, scaled=True, dp=None, dx=None,
@@ -570,9 +580,7 @@ def field_backward(p, x, row_mean, lse, dy, tau=1.0, scaled=True, dp=None, dx=No
     _need(dp, "dp", tuple(p.shape), torch.float32, dev)
     _need(dx, "dx", (batch, n, width), torch.bfloat16, dev)
     _gpu(dev)
-    if workspace is None:
-        need = field_workspace_bytes(batch, n)
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    workspace = _field_workspace(workspace, batch, n, c, dev)
     rc = load().hcmix_field_backward(batch, n, width, c, float(tau), int(bool(scaled)), _fptr(p),
                                      _ptr(x), _fptr(row_mean), _fptr(lse), _ptr(dy), _fptr(dp),
                                      _ptr(dx), _ptr(workspace), _bytes(workspace), _stream(x))

@@ -475,9 +475,12 @@ def test_shared_backward_workspace_and_rejections():
 
 
 def field_fwd(batch=2, n=40, width=64, c=3, tau=1.0, scaled=1, p=FP[0], x=P[1], y=P[2],
-              mean=FP[3], lse=FP[4], part=FP[5]):
-    return hcmix.load().hcmix_field_forward(batch, n, width, c, tau, scaled, p, x, y, mean, lse,
-                                            part, None)
+              mean=FP[3], lse=FP[4], part=FP[5], ws=ctypes.c_void_p(0x4000000), wsb=None):
+    lib = hcmix.load()
+    if wsb is None:
+        wsb = lib.hcmix_field_workspace_bytes(batch, n, c)
+    return lib.hcmix_field_forward(batch, n, width, c, tau, scaled, p, x, y, mean, lse, part, ws,
+                                   wsb, None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -495,6 +498,9 @@ def field_fwd(batch=2, n=40, width=64, c=3, tau=1.0, scaled=1, p=FP[0], x=P[1], 
     (dict(x=ctypes.c_void_p(P[1].value + 8)), UNSUPPORTED),             # bf16 misaligned
     (dict(p=ctypes.cast(ctypes.c_void_p(P[0].value + 2), ctypes.POINTER(ctypes.c_float))),
      UNSUPPORTED),
+    (dict(ws=None), INVALID), (dict(wsb=64), INVALID),                  # no or short workspace
+    (dict(ws=P[2]), INVALID),                                           # workspace aliases y
+    (dict(ws=ctypes.c_void_p(0x4000010)), UNSUPPORTED),                 # workspace alignment
 ])
 def test_field_forward_rejects_bad_arguments(kw, code):
     assert field_fwd(**kw) == code
@@ -503,11 +509,16 @@ def test_field_forward_rejects_bad_arguments(kw, code):
 def test_field_backward_workspace_and_rejections():
     lib = hcmix.load()
     q = lib.hcmix_field_workspace_bytes
-    assert q(64, 256) == 64 * 256 * 256 * 4
-    assert q(2, 40) == 2 * 64 * 64 * 4           # n rounded up to a multiple of 32
-    assert q(1, 1) == 32 * 32 * 4
-    assert q(0, 16) == 0 and q(2, 257) == 0 and q(2, 0) == 0
-    need = q(2, 40)
+    # per window: the prepared table (rows of 2 c' + 8 bf16, the norms, 8 tile
+    # sums of 64 and 16 tile norm sums, rounded up to 256 bytes), then the
+    # N x N fp32 squared-distance gradient
+    table = lambda np_, cp: -(-(np_ * (2 * cp + 8) * 2 + np_ * 4 + (np_ // 32) * 64 * 4 + 64) // 256) * 256  # noqa: E731
+    assert q(64, 256, 32) == 64 * (table(256, 32) + 256 * 256 * 4)
+    assert q(2, 40, 3) == 2 * (table(64, 16) + 64 * 64 * 4)      # n rounded up to a multiple of 32
+    assert q(1, 1, 64) == table(32, 64) + 32 * 32 * 4
+    assert q(0, 16, 4) == 0 and q(2, 257, 4) == 0 and q(2, 0, 4) == 0
+    assert q(2, 16, 0) == 0 and q(2, 16, 65) == 0
+    need = q(2, 40, 3)
     ws = ctypes.c_void_p(0x4000000)
     call = lambda **k: lib.hcmix_field_backward(   # noqa: E731
         2, k.get("n", 40), 64, k.get("c", 3), k.get("tau", 1.0), 1, FP[0], P[1], FP[2], FP[3],
