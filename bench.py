@@ -875,9 +875,11 @@ def run_field(args, torch, hcmix, inputs, dev):
     byte against the bf16 ridge near 315), so the roofline is bytes: forward
     reads p and x and writes y and two fp32 row statistics; backward reads p,
     x, dy and the statistics and writes dp and dx (its fp32 squared-distance
-    gradient and each window's prepared coordinate table are workspace, not
-    algorithmic traffic).  Each call is timed
-    on its own with graph_timed, on the stream it runs on."""
+    gradient and each window's coordinate table are workspace, not
+    algorithmic traffic).  Each application has its own workspace: the
+    forward leaves the coordinate tables there and the backward of the same
+    application takes them (reuse_table).  Each call is timed on its own with
+    graph_timed, on the stream it runs on."""
     B, n, w, c, T = 64, 256, 512, 32, 8
     if args.batch > 0:
         B = args.batch
@@ -890,15 +892,16 @@ def run_field(args, torch, hcmix, inputs, dev):
     lses = [torch.empty((B, n), dtype=torch.float32, device=dev) for _ in range(T)]
     dps = [torch.empty_like(p) for p in ps]
     gs = [torch.empty_like(x0) for _ in range(T)]
-    wsp = torch.empty(hcmix.field_workspace_bytes(B, n, c), dtype=torch.uint8, device=dev)
+    wsps = [torch.empty(hcmix.field_workspace_bytes(B, n, c), dtype=torch.uint8, device=dev)
+            for _ in range(T)]
 
     def fwd(t):
         hcmix.field_forward(ps[t], xs[t], tau, scaled, y=xs[t + 1], row_mean=ms[t], lse=lses[t],
-                            workspace=wsp)
+                            workspace=wsps[t])
 
     def bwd(t, g):
         hcmix.field_backward(ps[t], xs[t], ms[t], lses[t], g, tau, scaled, dp=dps[t], dx=gs[t],
-                             workspace=wsp)
+                             workspace=wsps[t], reuse_table=True)
 
     def step():
         for t in range(T):

@@ -410,9 +410,12 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
  * to bf16, fp32 accumulation), outputs rounded once.  In the scaled form a
  * positive row mean below 2^-100 is taken as 2^-100.
  * workspace: hcmix_field_workspace_bytes(batch, n, coord_dim) bytes of device
- * memory, 256-byte aligned, owned by the caller; it holds each window's
- * prepared coordinate table during the call (and for the backward the gradient
- * of the squared distances), so calls that share it must not overlap.
+ * memory, 256-byte aligned, owned by the caller.  The forward leaves each
+ * window's coordinate table (the split centred coordinates and their norms)
+ * in it, which the backward can take instead of building it again
+ * (reuse_table); the backward also keeps the gradient of the squared
+ * distances there during the call.  Calls that share a workspace must not
+ * overlap.
  * HCMIX_ERR_INVALID_VALUE: null pointers (partners may be null), batch, n,
  * width or coord_dim < 1, tau outside [2^-24, 2^24] or not finite, scaled not 0
  * or 1, an output overlapping an input or another output, a workspace smaller
@@ -426,7 +429,7 @@ hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_
                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* Bytes of device workspace the field calls need: for each window its
- * prepared coordinate table (about n (4 c' + 16) bytes, c' = coord_dim
+ * coordinate table (N (4 c' + 20) bytes rounded up to 256, c' = coord_dim
  * rounded up to 16), plus N * N * 4 with N = n rounded up to a multiple of 32
  * (the gradient of the window's squared distances, used by the backward); 0
  * for arguments outside the supported range. */
@@ -439,12 +442,19 @@ size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n, int32_t coord_dim);
  *   dD[i][j] = -da[i][j] / (tau m_i) + (sum_k da[i][k] D[i][k]) / (tau m_i^2 (i + 1))
  *              (scaled; -da[i][j] / tau unscaled; 0 for rows with m_i = 0),
  *   dp_i = 2 sum_{j <= i} dD[i][j] (p_i - p_j) + 2 sum_{k >= i} dD[k][i] (p_i - p_k).
- * dy_i . y_i is taken as sum_j C[i][j] (dy_i . x_j), so y is not read. */
+ * dy_i . y_i is taken as sum_j C[i][j] (dy_i . x_j), so y is not read.
+ * reuse_table = 1: the workspace still holds the tables hcmix_field_forward
+ * wrote for these same p, batch, n and coord_dim (no call has used the
+ * workspace since), and the backward reads them instead of building them
+ * (one launch fewer; the results are bitwise those of reuse_table = 0).  The
+ * library cannot check this; tables of other coordinates give wrong dp and
+ * dx, never an access outside the buffers.  reuse_table = 0 builds them from
+ * p.  Other values: HCMIX_ERR_INVALID_VALUE. */
 hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
                                   float tau, int32_t scaled, const float* p, const void* x,
                                   const float* row_mean, const float* lse, const void* dy,
-                                  float* dp, void* dx, void* workspace, size_t workspace_bytes,
-                                  void* stream);
+                                  float* dp, void* dx, int32_t reuse_table, void* workspace,
+                                  size_t workspace_bytes, void* stream);
 
 /* ---- Linear maps: the attention layers' projections in the hybrids ----
  *

@@ -1264,9 +1264,10 @@ hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_
 hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32_t coord_dim,
                                   float tau, int32_t scaled, const float* p, const void* x,
                                   const float* row_mean, const float* lse, const void* dy,
-                                  float* dp, void* dx, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
+                                  float* dp, void* dx, int32_t reuse_table, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
   if (!p || !x || !row_mean || !lse || !dy || !dp || !dx) return HCMIX_ERR_INVALID_VALUE;
+  if (reuse_table != 0 && reuse_table != 1) return HCMIX_ERR_INVALID_VALUE;
   hcmix_status st = check_field(batch, n, width, coord_dim, tau, scaled);
   if (st != HCMIX_OK) return st;
   const size_t need = hcmix_field_workspace_bytes(batch, n, coord_dim);
@@ -1280,7 +1281,7 @@ hcmix_status hcmix_field_backward(int64_t batch, int64_t n, int64_t width, int32
   if (!aligned(x, 16) || !aligned(dy, 16) || !aligned(dx, 16) || !aligned(workspace, 256))
     return HCMIX_ERR_UNSUPPORTED;
   hipError_t e = launch_field_bwd(p, (const bf16*)x, row_mean, lse, (const bf16*)dy, dp,
-                                  (bf16*)dx, workspace, (int)batch, (int)n, coord_dim,
+                                  (bf16*)dx, workspace, reuse_table, (int)batch, (int)n, coord_dim,
                                   (int)width, 1.f / tau, scaled, (hipStream_t)stream);
   return e == hipSuccess ? HCMIX_OK : hip_fail(e);
 }

@@ -236,16 +236,18 @@ hipError_t launch_attention_bwd_bf16(const bf16* qkv, const bf16* out, const flo
 // bf16 [batch][n][width], width % 64 == 0; n <= 256): row statistics
 // row_mean and lse fp32 [batch][n], partners fp32 [batch][n] or null.
 // workspace: field_workspace_bytes(batch, n, c) bytes, 256-byte aligned (each
-// window's prepared coordinate table, then for the backward the gradient of
-// the squared distances, fp32 [batch][NP][NP] with NP = n rounded up to 32).
+// window's coordinate table, written by the forward, then for the backward the
+// gradient of the squared distances, fp32 [batch][NP][NP] with NP = n rounded
+// up to 32).  reuse_table: the backward takes the tables the forward wrote to
+// this workspace for the same p instead of building them again.
 size_t field_workspace_bytes(int batch, int n, int c);
 hipError_t launch_field_fwd(const float* p, const bf16* x, bf16* y, float* row_mean, float* lse,
                             float* partners, void* workspace, int batch, int n, int c, int width,
                             float inv_tau, int scaled, hipStream_t st);
 hipError_t launch_field_bwd(const float* p, const bf16* x, const float* row_mean,
                             const float* lse, const bf16* dy, float* dp, bf16* dx, void* workspace,
-                            int batch, int n, int c, int width, float inv_tau, int scaled,
-                            hipStream_t st);
+                            int reuse_table, int batch, int n, int c, int width, float inv_tau,
+                            int scaled, hipStream_t st);
 
 // Language-model harness kernels (bf16, width % 64 == 0): embedding gather and
 // its fixed-order scatter sum (workspace embedding_workspace_bytes), fused

@@ -124,146 +124,83 @@ __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int r
   }
 }
 
-// ---------------------------------------------------------------------------
-// Prepared coordinate table of a window, in the caller's workspace (built once
-// per window by field_prep_kernel, copied into LDS by the other kernels):
-//   rows [NP][2 cp + 8] bf16: the table rows as in LDS (hi | lo | 8 zeros),
-//   nrm  [NP] fp32: N_r,
-//   ts   [NT][64] fp32: each tile's sum of the centred coordinates (0 past c),
-//   pn   [16] fp32: each tile's sum of N_r (0 past NT),
-// windows tab_stride bytes apart (a multiple of 256).
-// ---------------------------------------------------------------------------
-__host__ __device__ constexpr size_t tab_nrm(int NT, int cp) { return (size_t)NT * 32 * (2 * cp + 8) * 2; }
-__host__ __device__ constexpr size_t tab_ts(int NT, int cp) { return tab_nrm(NT, cp) + (size_t)NT * 32 * 4; }
-__host__ __device__ constexpr size_t tab_pn(int NT, int cp) { return tab_ts(NT, cp) + (size_t)NT * 64 * 4; }
-__host__ __device__ constexpr size_t tab_stride(int NT, int cp) {
-  return (tab_pn(NT, cp) + 16 * 4 + 255) / 256 * 256;
-}
-
-// Block = (window b, tile t), 256 threads: thread (row r = tid / 8 of the
-// tile, j = tid % 8) takes columns [j cp / 8, (j + 1) cp / 8) (an even count;
-// with vec and 4 or 8 of them, read as 16-byte pieces).
-template <int NT>
-__global__ __launch_bounds__(256) void field_prep_kernel(const float* __restrict__ p,
-                                                        unsigned char* __restrict__ tab, int n,
-                                                        int c, int cp, int vec) {
-  constexpr int NP = NT * 32;
-  __shared__ float sCol[4][64];
-  __shared__ float sNs[4];
-  const int b = blockIdx.x / NT, t = blockIdx.x % NT;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rl = threadIdx.x >> 3, j = threadIdx.x & 7, r = 32 * t + rl;
-  const int cq = cp >> 3, k0 = j * cq;                 // cq <= 8 columns
-  const float* pw = p + (size_t)b * n * c;
-  unsigned char* tw = tab + (size_t)b * tab_stride(NT, cp);
-  float raw[8], p0[8];
-  const float* prow = pw + (size_t)min(r, n - 1) * c;
-  if (vec && (cq == 8 || cq == 4)) {
-    // 16-byte loads (c a multiple of 4; columns past c read as clamped pieces)
-#pragma unroll
-    for (int h = 0; h < 2; h++) {
-      if (4 * h < cq) {
-        const int kk = min(k0 + 4 * h, c - 4);
-        const f32x4 a = *(const f32x4*)(prow + kk), q = *(const f32x4*)(pw + kk);
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-          raw[4 * h + e] = a[e];
-          p0[4 * h + e] = q[e];
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; e++) raw[4 * h + e] = p0[4 * h + e] = 0.f;
-      }
-    }
-  } else {
-#pragma unroll
-    for (int u = 0; u < 8; u++) {
-      const int kk = min(k0 + u, c - 1);
-      raw[u] = prow[kk];
-      p0[u] = pw[kk];
-    }
-  }
-  float v[8], nn = 0.f;
-  bf16 hi[8], lo[8];
-#pragma unroll
-  for (int u = 0; u < 8; u++) {
-    v[u] = (r < n && u < cq && k0 + u < c) ? raw[u] - p0[u] : 0.f;
-    hi[u] = to_bf16(v[u]);
-    lo[u] = to_bf16(v[u] - (float)hi[u]);
-    const float tv = (float)hi[u] + (float)lo[u];
-    nn = fmaf(tv, tv, nn);
-  }
-  bf16* row = (bf16*)tw + (size_t)r * (2 * cp + 8);
-#pragma unroll
-  for (int u = 0; u < 8; u += 2)                   // cq is even: pairs of bf16
-    if (u < cq) {
-      *(bf16x2*)(row + k0 + u) = bf16x2{hi[u], hi[u + 1]};
-      *(bf16x2*)(row + cp + k0 + u) = bf16x2{lo[u], lo[u + 1]};
-    }
-  if (j == 0) *(u32x4*)(row + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
-  nn += __shfl_xor(nn, 1);
-  nn += __shfl_xor(nn, 2);
-  nn += __shfl_xor(nn, 4);
-  if (j == 0) ((float*)(tw + tab_nrm(NT, cp)))[r] = nn;
-  // tile column sums: over the 8 rows of a wave (lanes 8 apart), then the 4 waves
-#pragma unroll
-  for (int u = 0; u < 8; u++) {
-    float cs = v[u];
-    cs += __shfl_xor(cs, 8);
-    cs += __shfl_xor(cs, 16);
-    cs += __shfl_xor(cs, 32);
-    if (lane < 8 && u < cq) sCol[wave][k0 + u] = cs;
-  }
-  float ns = nn;                                   // N of this lane's row (8 lanes each)
-  ns += __shfl_xor(ns, 8);
-  ns += __shfl_xor(ns, 16);
-  ns += __shfl_xor(ns, 32);
-  if (lane == 0) sNs[wave] = ns;
-  __syncthreads();
-  if (threadIdx.x < 64) {
-    const int k = threadIdx.x;
-    const float sum = k < cp ? sCol[0][k] + sCol[1][k] + sCol[2][k] + sCol[3][k] : 0.f;
-    ((float*)(tw + tab_ts(NT, cp)))[t * 64 + k] = k < c ? sum : 0.f;
-  }
-  if (threadIdx.x == 0) {
-    float* pn = (float*)(tw + tab_pn(NT, cp));
-    pn[t] = sNs[0] + sNs[1] + sNs[2] + sNs[3];
-    if (t == 0)
-      for (int u = NT; u < 16; u++) pn[u] = 0.f;
-  }
-}
-
-// Rows [0, rows) of window b's prepared table, its norms, and with TILES the
-// exclusive prefix over the tiles of the coordinate sums (sTS [NT + 1][64])
-// and the tile norm sums (sPN [16]), into LDS.  Every load is issued before the
-// first LDS write; `then` runs after the loads are issued.  Two barriers; ends
-// with one.
+// The coordinate table rows [0, rows) (rows <= 256) and their squared norms
+// N_r (of hi + lo, fp32), from the window's coordinates pw [n][c]; with TILES
+// also what a row's mean needs from the tiles before it:
+//   sTS[t][k] = sum over rows j < 32 t (of the window) of the centred p_j[k]
+//   (fp32, t = 0 .. NT; each tile's column sum by one thread, then a running
+//   sum over the tiles), and sPN[t] = sum of N_j over tile t.  Then, for
+//   query q in tile t,
+//   sum_{j < 32 t} D[q][j] = 32 t N_q + sum_{t' < t} sPN[t'] - 2 p'_q . sTS[t].
+// The raw rows are staged in the table's own space with a stride of c + 1
+// words (consecutive rows in distinct banks; (c + 1) * 4 <= (2 cp + 8) * 2
+// bytes, so they fit); each table row is then split by two threads (cp / 2
+// columns each: thread tid takes row tid % 256, half tid / 256), every LDS
+// read of a phase issued before its values are used.  Rows at or past n are
+// zero, N_r = 0.  `then` is passed on to stage_coords.  Three barriers; ends
+// with one.  sNh: [2][NT * 32] scratch for the half-row norms.
 template <int NT, bool TILES, class Then>
-__device__ __forceinline__ void load_table(const unsigned char* __restrict__ tw, int cp, int rows,
-                                           bf16* sT, float* sN, float* sTS, float* sPN,
-                                           Then then) {
-  constexpr int MAXP = (NT * 32 * 136 * 2 / 16 + FT - 1) / FT;   // 16-byte pieces per thread
-  const int pieces = rows * (2 * cp + 8) * 2 / 16;
-  u32x4 v[MAXP];
+__device__ __forceinline__ void build_table(const float* __restrict__ pw, int n, int c, int cp,
+                                            int rows, bf16* sT, float* sN, float* sNh,
+                                            float* sTS, float* sPN, bool vec, Then then) {
+  constexpr int NP = NT * 32;
+  const int rws = (c + 1) * 4;                       // raw staging row stride (bytes)
+  unsigned char* base = (unsigned char*)sT;
+  stage_coords<FT>(pw, rows < n ? rows : n, c, base, rws, vec, then);
+  __syncthreads();
+  const int r = threadIdx.x & 255, h = threadIdx.x >> 8;
+  const int hc = cp >> 1, k0 = h * hc;               // this thread's columns [k0, k0 + hc)
+  const bool live = r < n && r < rows;
+  const int rr = live ? r : 0;
+  float v[32];
+  {
+    float raw[32], p0[32];
 #pragma unroll
-  for (int u = 0; u < MAXP; u++)
-    v[u] = ((const u32x4*)tw)[min((int)threadIdx.x + FT * u, pieces - 1)];
-  const float* nrm = (const float*)(tw + tab_nrm(NT, cp));
-  const float nv = nrm[min((int)threadIdx.x, rows - 1)];
-  float tsv = 0.f, pnv = 0.f;
-  if constexpr (TILES) {
-    tsv = ((const float*)(tw + tab_ts(NT, cp)))[min((int)threadIdx.x, NT * 64 - 1)];
-    pnv = ((const float*)(tw + tab_pn(NT, cp)))[threadIdx.x & 15];
+    for (int k = 0; k < 32; k++) {
+      const int kk = min(k0 + k, c - 1);
+      raw[k] = *(const float*)(base + rr * rws + 4 * kk);
+      p0[k] = *(const float*)(base + 4 * kk);
+    }
+#pragma unroll
+    for (int k = 0; k < 32; k++) v[k] = (live && k < hc && k0 + k < c) ? raw[k] - p0[k] : 0.f;
   }
-  then();
-#pragma unroll
-  for (int u = 0; u < MAXP; u++)
-    if ((int)threadIdx.x + FT * u < pieces) ((u32x4*)sT)[threadIdx.x + FT * u] = v[u];
-  if ((int)threadIdx.x < rows) sN[threadIdx.x] = nv;
   if constexpr (TILES) {
-    if (threadIdx.x < NT * 64) sTS[64 + threadIdx.x] = tsv;
-    if (threadIdx.x < 16) sPN[threadIdx.x] = pnv;
-    __syncthreads();
+    // tile t's column k: thread (t, k) = (tid / 64, tid % 64); 8 tiles x 64 columns
+    const int t = threadIdx.x >> 6, k = threadIdx.x & 63;
+    if (t < NT) {
+      const int kk = min(k, c - 1);
+      const float p0k = *(const float*)(base + 4 * kk);
+      float col[32];
+#pragma unroll
+      for (int j = 0; j < 32; j++)
+        col[j] = *(const float*)(base + min(32 * t + j, n - 1) * rws + 4 * kk);
+      float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 32; j++) part[j & 3] += (32 * t + j < n) ? col[j] - p0k : 0.f;
+      sTS[(t + 1) * 64 + k] = k < c ? (part[0] + part[1]) + (part[2] + part[3]) : 0.f;
+    }
+  }
+  __syncthreads();
+  float nn = 0.f;
+  if (r < rows) {
+    bf16* row = sT + r * ct_stride(cp) + k0;
+#pragma unroll
+    for (int k = 0; k < 32; k += 2) {
+      const bf16x2 hi2 = {to_bf16(v[k]), to_bf16(v[k + 1])};
+      const float ha = (float)hi2[0], hb = (float)hi2[1];
+      const bf16x2 lo2 = {to_bf16(v[k] - ha), to_bf16(v[k + 1] - hb)};
+      if (k < hc) {
+        *(bf16x2*)(row + k) = hi2;
+        *(bf16x2*)(row + cp + k) = lo2;
+      }
+      const float ta = ha + (float)lo2[0], tb = hb + (float)lo2[1];
+      nn = fmaf(ta, ta, nn);
+      nn = fmaf(tb, tb, nn);
+    }
+    if (h == 0) *(u32x4*)(sT + r * ct_stride(cp) + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
+  }
+  if (r < rows) sNh[h * NP + r] = nn;
+  if constexpr (TILES) {
     if (threadIdx.x < 64) {
       float acc = 0.f;
       sTS[threadIdx.x] = 0.f;
@@ -274,6 +211,88 @@ __device__ __forceinline__ void load_table(const unsigned char* __restrict__ tw,
       }
     }
   }
+  __syncthreads();
+  // N_r from the two halves; tile sums of N (rows 32 t .. 32 t + 31 are one
+  // half of a wave)
+  if (threadIdx.x < rows) {
+    float nr = sNh[threadIdx.x] + sNh[NP + threadIdx.x];
+    sN[threadIdx.x] = nr;
+    if constexpr (TILES) {
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) nr += __shfl_xor(nr, o);
+      if ((threadIdx.x & 31) == 0) sPN[threadIdx.x >> 5] = nr;
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// A window's coordinate table as kept in the caller's workspace for the
+// backward (written by the forward, or by field_prep_kernel when the backward
+// is asked to build it), windows tab_stride bytes apart (a multiple of 256):
+//   rows [NP][2 cp + 8] bf16: the table rows as in LDS (hi | lo | 8 zeros),
+//   nrm  [NP] fp32: N_r.
+// Both writers run build_table over all NP rows, so the stored bytes do not
+// depend on which of them wrote them.
+// ---------------------------------------------------------------------------
+__host__ __device__ constexpr size_t tab_nrm(int NT, int cp) { return (size_t)NT * 32 * (2 * cp + 8) * 2; }
+__host__ __device__ constexpr size_t tab_stride(int NT, int cp) {
+  return (tab_nrm(NT, cp) + (size_t)NT * 32 * 4 + 255) / 256 * 256;
+}
+
+// Block `part` of `parts` blocks copies its share of the LDS table (rows and
+// norms, NP rows) to the window's place tw in the workspace, 16 bytes per
+// store.  No wait: nothing in the block reads it back.
+template <int NT>
+__device__ __forceinline__ void store_table(const bf16* sT, const float* sN,
+                                            unsigned char* __restrict__ tw, int cp, int part,
+                                            int parts) {
+  constexpr int NP = NT * 32;
+  const int rowp = NP * (2 * cp + 8) * 2 / 16, pieces = rowp + NP * 4 / 16;
+  const int per = (pieces + parts - 1) / parts;
+  const int lo = part * per, hi = min(pieces, lo + per);
+  for (int i = lo + (int)threadIdx.x; i < hi; i += FT) {
+    const u32x4 v = i < rowp ? ((const u32x4*)sT)[i] : ((const u32x4*)sN)[i - rowp];
+    ((u32x4*)tw)[i] = v;
+  }
+}
+
+// Block = window b, FT threads: the table built in LDS as the forward builds
+// it, then copied to the workspace.
+template <int NT>
+__global__ __launch_bounds__(FT) void field_prep_kernel(const float* __restrict__ p,
+                                                       unsigned char* __restrict__ tab, int n,
+                                                       int c, int cp, int vec) {
+  constexpr int NP = NT * 32;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  float* sN = (float*)smem;
+  float* sNh = sN + NP;                       // [2][NP]
+  bf16* sT = (bf16*)(sNh + 2 * NP);
+  const int b = blockIdx.x;
+  build_table<NT, false>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, nullptr, nullptr, vec,
+                         NoIssue{});
+  store_table<NT>(sT, sN, tab + (size_t)b * tab_stride(NT, cp), cp, 0, 1);
+}
+
+// Rows [0, rows) of window b's stored table and their norms, into LDS.  Every
+// load is issued before the first LDS write; `then` runs after the loads are
+// issued.  Ends with a barrier.
+template <int NT, class Then>
+__device__ __forceinline__ void load_table(const unsigned char* __restrict__ tw, int cp, int rows,
+                                           bf16* sT, float* sN, Then then) {
+  constexpr int MAXP = (NT * 32 * 136 * 2 / 16 + FT - 1) / FT;   // 16-byte pieces per thread
+  const int pieces = rows * (2 * cp + 8) * 2 / 16;
+  u32x4 v[MAXP];
+#pragma unroll
+  for (int u = 0; u < MAXP; u++)
+    v[u] = ((const u32x4*)tw)[min((int)threadIdx.x + FT * u, pieces - 1)];
+  const float* nrm = (const float*)(tw + tab_nrm(NT, cp));
+  const float nv = nrm[min((int)threadIdx.x, rows - 1)];
+  then();
+#pragma unroll
+  for (int u = 0; u < MAXP; u++)
+    if ((int)threadIdx.x + FT * u < pieces) ((u32x4*)sT)[threadIdx.x + FT * u] = v[u];
+  if ((int)threadIdx.x < rows) sN[threadIdx.x] = nv;
   __syncthreads();
 }
 
@@ -400,20 +419,23 @@ constexpr int table_bytes(int NT, int cp) { return NT * 32 * (2 * cp + 8) * 2; }
 // (the forward's last phase reuses the space for (NT + 1) / 2 partial
 // readouts of (SW / 32 * 16 + 2) x 64 floats)
 constexpr int fwd_lds_bytes(int NT, int SW, int cp) {
-  return cmax(NT * 32 * SW * 2 + NT * 32 * 4 + (NT + 1) * 64 * 4 + 16 * 4 + table_bytes(NT, cp),
+  return cmax(NT * 32 * SW * 2 + NT * 32 * 4 + (NT + 1) * 64 * 4 + 16 * 4 + 2 * NT * 32 * 4 +
+                  table_bytes(NT, cp),
               (NT + 1) / 2 * (SW / 32 * 16 + 2) * 64 * 4);
 }
+constexpr int prep_lds_bytes(int NT, int cp) { return 3 * NT * 32 * 4 + table_bytes(NT, cp); }
 constexpr int dx_lds_bytes(int NT, int SW, int cp) {
   return NT * 32 * SW * 2 + 3 * NT * 32 * 4 + table_bytes(NT, cp);
 }
-// rows kernel: NS stages of [x rows (NT * 32)][64] + [dy rows (32)][64] bf16
+// rows kernel: NS stages of [x rows (NT * 32)][64] + [dy rows (32)][64] bf16,
+// the coordinate table in the same space before the stages are used, then
+// the norms and the per-wave row sums.  At NS = 2 a block needs at most 77
+// KB, so two blocks share a CU.
 constexpr int rows_stage_elems(int NT) { return (NT * 32 + 32) * 64; }
 constexpr int rows_lds_bytes(int NT, int NS, int cp) {
-  return NS * rows_stage_elems(NT) * 2 + NT * 32 * 4 + 2 * 8 * 32 * 4 + table_bytes(NT, cp);
+  return cmax(NS * rows_stage_elems(NT) * 2, table_bytes(NT, cp)) + NT * 32 * 4 + 2 * 8 * 32 * 4;
 }
-constexpr int rows_stages(int NT, int cp) {
-  return rows_lds_bytes(NT, 3, cp) <= 160 * 1024 ? 3 : 2;
-}
+constexpr int ROWS_NS = 2;
 // coordinate kernel: E tile [32][NP + 1] fp32, coordinates [NP][ck + 1] fp32,
 // row-sum parts [16][32], and the per-wave partial products [4][32][ck + 1]
 // (in the E tile's space where they fit, else after the rest)
@@ -444,24 +466,28 @@ constexpr int coord_lds_bytes(int NT, int ck) {
 // ---------------------------------------------------------------------------
 template <int NT, int SW, bool PARTNERS>
 __global__ __launch_bounds__(FT) void field_fwd_kernel(
-    const unsigned char* __restrict__ tab, const bf16* __restrict__ x, bf16* __restrict__ y,
-    float* __restrict__ row_mean, float* __restrict__ lse, float* __restrict__ partners, int n,
-    int cp, int width, int slabs, float inv_tau, int scaled) {
+    const float* __restrict__ p, unsigned char* __restrict__ tab, const bf16* __restrict__ x,
+    bf16* __restrict__ y, float* __restrict__ row_mean, float* __restrict__ lse,
+    float* __restrict__ partners, int n, int c, int cp, int width, int slabs, float inv_tau,
+    int scaled, int vec) {
   constexpr int NP = NT * 32, DT = SW / 32;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sX = (bf16*)smem;
   float* sN = (float*)(smem + NP * SW * 2);
   float* sTS = sN + NP;                       // [NT + 1][64]
   float* sPN = sTS + (NT + 1) * 64;           // [16]
-  bf16* sT = (bf16*)(sPN + 16);
+  float* sNh = sPN + 16;                      // [2][NP]
+  bf16* sT = (bf16*)(sNh + 2 * NP);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / slabs, s = lin % slabs;
   const int lane = threadIdx.x & 63, half = lane >> 5, lq = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int rs = ct_stride(cp);
   Slab<NT, SW> slab;
-  load_table<NT, true>(tab + (size_t)b * tab_stride(NT, cp), cp, NP, sT, sN, sTS, sPN,
-                       [&] { slab.issue(x + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  build_table<NT, true>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, sTS, sPN, vec,
+                        [&] { slab.issue(x + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  // the window's slab blocks share the copy of its table for the backward
+  store_table<NT>(sT, sN, tab + (size_t)b * tab_stride(NT, cp), cp, s, slabs);
   // the plan of this wave
   const int pi = wave & 3;
   const bool roleA = wave < 4, active = pi < (NT + 1) / 2;
@@ -637,14 +663,17 @@ __global__ __launch_bounds__(FT) void field_fwd_kernel(
 
 // ---------------------------------------------------------------------------
 // Backward, rows.  Block = (window b, query tile qt), the heaviest tiles of a
-// window first; 8 waves, wave w owning key tile w (w <= qt).
-// dP^T[key][q] = x_key . dy_q sums over the width in 64-column steps: each
-// step's x rows [0, 32 (qt + 1)) and the tile's 32 dy rows go global -> LDS by
-// DMA (coalesced, 8 rows of 128 bytes per instruction, swizzled as the 64-
-// column tiles), NS stages in flight, the instructions of a step dealt over
-// the 8 waves.  The couplings, their squared distances and the row sums come
-// from the coordinate table first; the per-row sums Delta and sum(da D) across
-// the waves go through LDS.
+// window first; 8 waves, wave w owning key tile w (w <= qt).  Two blocks share
+// a CU (the grid's second half, the light tiles, beside the first), so one
+// block's set-up and reductions overlap the other's streaming.
+// The couplings, their squared distances and the row sums come first, from
+// the coordinate table (loaded into the stage space).  Then dP^T[key][q] =
+// x_key . dy_q sums over the width in 64-column steps: each step's x rows
+// [0, 32 (qt + 1)) and the tile's 32 dy rows go global -> LDS by DMA
+// (coalesced, 8 rows of 128 bytes per instruction, swizzled as the 64-column
+// tiles), NS stages in flight, the instructions of a step dealt over the 8
+// waves.  The per-row sums Delta and sum(da D) across the waves go through
+// LDS.
 // ---------------------------------------------------------------------------
 template <int NT, int NS>
 __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
@@ -654,9 +683,9 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
   constexpr int NP = NT * 32, STAGE = rows_stage_elems(NT);
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sStage = (bf16*)smem;
-  float* sN = (float*)(smem + NS * STAGE * 2);
+  bf16* sT = sStage;                                  // the table, until the first DMA
+  float* sN = (float*)(smem + cmax(NS * STAGE * 2, table_bytes(NT, cp)));
   float* sRed = sN + NP;                              // [2][8 waves][32]
-  bf16* sT = (bf16*)(sRed + 2 * 8 * 32);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / NT, qt = NT - 1 - lin % NT;
   const int lane = threadIdx.x & 63, half = lane >> 5;
@@ -691,13 +720,9 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
       }
     }
   };
-#pragma unroll
-  for (int st = 0; st < NS - 1; st++)
-    if (st < steps) dma(st, st);
   const float m_ld = row_mean[(size_t)b * n + min(q, n - 1)];
   const float l_ld = lse[(size_t)b * n + min(q, n - 1)];
-  load_table<NT, false>(tab + (size_t)b * tab_stride(NT, cp), cp, (qt + 1) * 32, sT, sN,
-                        nullptr, nullptr, NoIssue{});
+  load_table<NT>(tab + (size_t)b * tab_stride(NT, cp), cp, (qt + 1) * 32, sT, sN, NoIssue{});
   const float m = qvalid ? m_ld : 0.f;
   const float l2 = qvalid ? l_ld * LOG2E : 0.f;
   const float scale = qvalid ? logit_scale(m, inv_tau, scaled) : 0.f;
@@ -721,6 +746,10 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
       }
     }
   }
+  __syncthreads();                                    // the table's space becomes the stages
+#pragma unroll
+  for (int st = 0; st < NS - 1; st++)
+    if (st < steps) dma(st, st);
   for (int st = 0; st < steps; st++) {
     // this wave's DMA of step st has landed (those of the next NS - 2 steps may
     // still be in flight); after the barrier every wave's has, and every wave
@@ -805,8 +834,8 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
     sL2[q] = v ? -l * LOG2E : 0.f;
   }
   Slab<NT, SW> slab;
-  load_table<NT, false>(tab + (size_t)b * tab_stride(NT, cp), cp, NP, sT, sN, nullptr, nullptr,
-                        [&] { slab.issue(dy + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  load_table<NT>(tab + (size_t)b * tab_stride(NT, cp), cp, NP, sT, sN,
+                 [&] { slab.issue(dy + (size_t)b * n * width + (size_t)s * SW, width, n); });
   slab.store(sDY, n);
   __syncthreads();
   const int kt = wave_tile(wave);
@@ -1007,21 +1036,26 @@ inline int coords_vec(const float* p, int c) {
 template <int NT>
 hipError_t field_prep_launch(const float* p, unsigned char* tab, int batch, int n, int c, int cp,
                              hipStream_t st) {
-  field_prep_kernel<NT><<<batch * NT, 256, 0, st>>>(p, tab, n, c, cp, coords_vec(p, c));
+  static std::atomic<unsigned long long> done{0};
+  hipError_t e = lds_limit_once(done, (const void*)field_prep_kernel<NT>, prep_lds_bytes(NT, 64));
+  if (e != hipSuccess) return e;
+  field_prep_kernel<NT><<<batch, FT, prep_lds_bytes(NT, cp), st>>>(p, tab, n, c, cp,
+                                                                   coords_vec(p, c));
   return hipGetLastError();
 }
 
 template <int NT, int SW, bool PARTNERS>
-hipError_t field_fwd_launch(const unsigned char* tab, const bf16* x, bf16* y, float* row_mean,
-                            float* lse, float* partners, int batch, int n, int cp, int width,
-                            float inv_tau, int scaled, hipStream_t st) {
+hipError_t field_fwd_launch(const float* p, unsigned char* tab, const bf16* x, bf16* y,
+                            float* row_mean, float* lse, float* partners, int batch, int n, int c,
+                            int cp, int width, float inv_tau, int scaled, hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
   hipError_t e = lds_limit_once(done, (const void*)field_fwd_kernel<NT, SW, PARTNERS>,
                                 fwd_lds_bytes(NT, SW, 64));
   if (e != hipSuccess) return e;
   const int slabs = width / SW;
   field_fwd_kernel<NT, SW, PARTNERS><<<batch * slabs, FT, fwd_lds_bytes(NT, SW, cp), st>>>(
-      tab, x, y, row_mean, lse, partners, n, cp, width, slabs, inv_tau, scaled);
+      p, tab, x, y, row_mean, lse, partners, n, c, cp, width, slabs, inv_tau, scaled,
+      coords_vec(p, c));
   return hipGetLastError();
 }
 
@@ -1029,18 +1063,16 @@ template <int NT>
 hipError_t field_fwd_pick(const float* p, const bf16* x, bf16* y, float* row_mean, float* lse,
                           float* partners, unsigned char* tab, int batch, int n, int c, int cp,
                           int width, float inv_tau, int scaled, hipStream_t st) {
-  hipError_t e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
-  if (e != hipSuccess) return e;
   const bool wide = width % 128 == 0;
   if (partners)
-    return wide ? field_fwd_launch<NT, 128, true>(tab, x, y, row_mean, lse, partners, batch, n,
-                                                  cp, width, inv_tau, scaled, st)
-                : field_fwd_launch<NT, 64, true>(tab, x, y, row_mean, lse, partners, batch, n,
-                                                 cp, width, inv_tau, scaled, st);
-  return wide ? field_fwd_launch<NT, 128, false>(tab, x, y, row_mean, lse, partners, batch, n,
-                                                 cp, width, inv_tau, scaled, st)
-              : field_fwd_launch<NT, 64, false>(tab, x, y, row_mean, lse, partners, batch, n, cp,
-                                                width, inv_tau, scaled, st);
+    return wide ? field_fwd_launch<NT, 128, true>(p, tab, x, y, row_mean, lse, partners, batch,
+                                                  n, c, cp, width, inv_tau, scaled, st)
+                : field_fwd_launch<NT, 64, true>(p, tab, x, y, row_mean, lse, partners, batch, n,
+                                                 c, cp, width, inv_tau, scaled, st);
+  return wide ? field_fwd_launch<NT, 128, false>(p, tab, x, y, row_mean, lse, partners, batch, n,
+                                                 c, cp, width, inv_tau, scaled, st)
+              : field_fwd_launch<NT, 64, false>(p, tab, x, y, row_mean, lse, partners, batch, n,
+                                                c, cp, width, inv_tau, scaled, st);
 }
 
 template <int NT, int SW>
@@ -1062,7 +1094,8 @@ hipError_t field_rows_launch(const unsigned char* tab, const bf16* x, const floa
                              const float* lse, const bf16* dy, float* ddt, int batch, int n,
                              int cp, int width, float inv_tau, int scaled, hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
-  hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS>, 160 * 1024);
+  hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS>,
+                                rows_lds_bytes(NT, NS, 64));
   if (e != hipSuccess) return e;
   field_bwd_rows_kernel<NT, NS><<<batch * NT, FT, rows_lds_bytes(NT, NS, cp), st>>>(
       tab, x, dy, row_mean, lse, ddt, n, cp, width, inv_tau, scaled);
@@ -1084,17 +1117,17 @@ hipError_t field_coord_launch(const float* p, const float* ddt, float* dp, int b
 template <int NT>
 hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean,
                             const float* lse, const bf16* dy, float* dp, bf16* dx,
-                            unsigned char* ws, int batch, int n, int c, int cp, int width,
-                            float inv_tau, int scaled, hipStream_t st) {
+                            unsigned char* ws, int reuse_table, int batch, int n, int c, int cp,
+                            int width, float inv_tau, int scaled, hipStream_t st) {
   unsigned char* tab = ws;
   float* ddt = (float*)(ws + (size_t)batch * tab_stride(NT, cp));
-  hipError_t e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
-  if (e != hipSuccess) return e;
-  e = rows_stages(NT, cp) == 3
-          ? field_rows_launch<NT, 3>(tab, x, row_mean, lse, dy, ddt, batch, n, cp, width,
-                                     inv_tau, scaled, st)
-          : field_rows_launch<NT, 2>(tab, x, row_mean, lse, dy, ddt, batch, n, cp, width,
-                                     inv_tau, scaled, st);
+  hipError_t e = hipSuccess;
+  if (!reuse_table) {
+    e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
+    if (e != hipSuccess) return e;
+  }
+  e = field_rows_launch<NT, ROWS_NS>(tab, x, row_mean, lse, dy, ddt, batch, n, cp, width, inv_tau,
+                                     scaled, st);
   if (e != hipSuccess) return e;
   e = width % 128 == 0 ? field_dx_launch<NT, 128>(tab, row_mean, lse, dy, dx, batch, n, cp, width,
                                                    inv_tau, scaled, st)
@@ -1150,11 +1183,11 @@ hipError_t launch_field_fwd(const float* p, const bf16* x, bf16* y, float* row_m
 
 hipError_t launch_field_bwd(const float* p, const bf16* x, const float* row_mean,
                             const float* lse, const bf16* dy, float* dp, bf16* dx, void* workspace,
-                            int batch, int n, int c, int width, float inv_tau, int scaled,
-                            hipStream_t st) {
+                            int reuse_table, int batch, int n, int c, int width, float inv_tau,
+                            int scaled, hipStream_t st) {
   const int cp = (c + 15) / 16 * 16;
   HCMIX_FIELD_CASES(field_bwd_launch, p, x, row_mean, lse, dy, dp, dx, (unsigned char*)workspace,
-                    batch, n, c, cp, width, inv_tau, scaled, st)
+                    reuse_table, batch, n, c, cp, width, inv_tau, scaled, st)
 }
 #undef HCMIX_FIELD_CASES
 

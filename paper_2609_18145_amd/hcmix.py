@@ -106,7 +106,7 @@ def load():
         lib.hcmix_field_workspace_bytes.argtypes = [i64, i64, i32]
         lib.hcmix_field_workspace_bytes.restype = sz
         lib.hcmix_field_backward.argtypes = [i64, i64, i64, i32, ctypes.c_float, i32, fp, vp, fp,
-                                             fp, vp, fp, vp, vp, sz, vp]
+                                             fp, vp, fp, vp, i32, vp, sz, vp]
         lib.hcmix_field_backward.restype = i32
         lib.hcmix_embedding_forward.argtypes = [i64, i64, i32, vp, vp, vp, vp]
         lib.hcmix_embedding_forward.restype = i32
@@ -565,10 +565,14 @@ def field_forward(p, x, tau=1.0, scaled=True, partners=False, y=None, row_mean=N
 
 
 def field_backward(p, x, row_mean, lse, dy, tau=1.0, scaled=True, dp=None, dx=None,
-                   workspace=None):
+                   workspace=None, reuse_table=False):
     """(dp fp32 [batch, n, c], dx bf16 [batch, n, width]) given dy = dL/dy and
-    the forward's row_mean and lse."""
+    the forward's row_mean and lse.  reuse_table: `workspace` is the one the
+    forward of these same coordinates used, untouched since, and its
+    coordinate tables are taken as they are."""
     batch, n, width, c = _field_shapes(p, x)
+    if reuse_table and workspace is None:
+        raise ValueError("reuse_table needs the workspace the forward wrote its tables to")
     dev = x.device
     _need(row_mean, "row_mean", (batch, n), torch.float32, dev)
     _need(lse, "lse", (batch, n), torch.float32, dev)
@@ -583,7 +587,8 @@ def field_backward(p, x, row_mean, lse, dy, tau=1.0, scaled=True, dp=None, dx=No
     workspace = _field_workspace(workspace, batch, n, c, dev)
     rc = load().hcmix_field_backward(batch, n, width, c, float(tau), int(bool(scaled)), _fptr(p),
                                      _ptr(x), _fptr(row_mean), _fptr(lse), _ptr(dy), _fptr(dp),
-                                     _ptr(dx), _ptr(workspace), _bytes(workspace), _stream(x))
+                                     _ptr(dx), int(bool(reuse_table)), _ptr(workspace),
+                                     _bytes(workspace), _stream(x))
     if rc != HCMIX_OK:
         raise HcmixError(rc, "hcmix_field_backward")
     return dp, dx

@@ -509,10 +509,9 @@ def test_field_forward_rejects_bad_arguments(kw, code):
 def test_field_backward_workspace_and_rejections():
     lib = hcmix.load()
     q = lib.hcmix_field_workspace_bytes
-    # per window: the prepared table (rows of 2 c' + 8 bf16, the norms, 8 tile
-    # sums of 64 and 16 tile norm sums, rounded up to 256 bytes), then the
-    # N x N fp32 squared-distance gradient
-    table = lambda np_, cp: -(-(np_ * (2 * cp + 8) * 2 + np_ * 4 + (np_ // 32) * 64 * 4 + 64) // 256) * 256  # noqa: E731
+    # per window: the coordinate table (rows of 2 c' + 8 bf16 and the norms,
+    # rounded up to 256 bytes), then the N x N fp32 squared-distance gradient
+    table = lambda np_, cp: -(-(np_ * (2 * cp + 8) * 2 + np_ * 4) // 256) * 256  # noqa: E731
     assert q(64, 256, 32) == 64 * (table(256, 32) + 256 * 256 * 4)
     assert q(2, 40, 3) == 2 * (table(64, 16) + 64 * 64 * 4)      # n rounded up to a multiple of 32
     assert q(1, 1, 64) == table(32, 64) + 32 * 32 * 4
@@ -522,8 +521,8 @@ def test_field_backward_workspace_and_rejections():
     ws = ctypes.c_void_p(0x4000000)
     call = lambda **k: lib.hcmix_field_backward(   # noqa: E731
         2, k.get("n", 40), 64, k.get("c", 3), k.get("tau", 1.0), 1, FP[0], P[1], FP[2], FP[3],
-        k.get("dy", P[4]), k.get("dp", FP[5]), k.get("dx", P[6]), k.get("ws", ws),
-        k.get("wsb", need), None)
+        k.get("dy", P[4]), k.get("dp", FP[5]), k.get("dx", P[6]), k.get("reuse", 0),
+        k.get("ws", ws), k.get("wsb", need), None)
     assert call(wsb=need - 4) == INVALID
     assert call(ws=None) == INVALID
     assert call(dx=P[4]) == INVALID                                     # dx aliases dy
@@ -534,3 +533,4 @@ def test_field_backward_workspace_and_rejections():
     assert call(n=300) == UNSUPPORTED
     assert call(c=100) == UNSUPPORTED
     assert call(ws=ctypes.c_void_p(0x4000010)) == UNSUPPORTED          # workspace alignment
+    assert call(reuse=2) == INVALID and call(reuse=-1) == INVALID       # reuse_table is 0 or 1

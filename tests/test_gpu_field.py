@@ -29,12 +29,21 @@ def _need_gpu():
 
 
 def run(inp, want_partners=True):
+    """Forward, then the backward twice: on the forward's workspace taking its
+    coordinate tables (reuse_table), and on a fresh workspace building them;
+    the two must agree bitwise."""
     p = torch.from_numpy(inp.p).cuda()
     x = to_dev(inp.x, "bf16")
     dy = to_dev(inp.dy, "bf16")
-    y, m, lse, part = hcmix.field_forward(p, x, inp.tau, inp.scaled, partners=want_partners)
-    dp, dx = hcmix.field_backward(p, x, m, lse, dy, inp.tau, inp.scaled)
+    batch, n, c = inp.p.shape
+    ws = torch.empty(hcmix.field_workspace_bytes(batch, n, c), dtype=torch.uint8, device="cuda")
+    y, m, lse, part = hcmix.field_forward(p, x, inp.tau, inp.scaled, partners=want_partners,
+                                          workspace=ws)
+    dp, dx = hcmix.field_backward(p, x, m, lse, dy, inp.tau, inp.scaled, workspace=ws,
+                                  reuse_table=True)
+    dp2, dx2 = hcmix.field_backward(p, x, m, lse, dy, inp.tau, inp.scaled)
     torch.cuda.synchronize()
+    assert torch.equal(dp, dp2) and torch.equal(dx, dx2), "tables from the forward differ"
     return dict(y=to_host(y), m=to_host(m), lse=to_host(lse),
                 part=to_host(part) if part is not None else None, dp=to_host(dp), dx=to_host(dx))
 
