@@ -413,8 +413,8 @@ hcmix_status hcmix_attention_backward(int64_t batch, int64_t n, int32_t heads, i
  * memory, 256-byte aligned, owned by the caller.  The forward leaves each
  * window's coordinate table (the split centred coordinates and their norms)
  * in it, which the backward can take instead of building it again
- * (reuse_table); the backward also keeps the gradient of the squared
- * distances there during the call.  Calls that share a workspace must not
+ * (reuse_table); the backward also keeps the couplings and the gradient of
+ * the squared distances there during the call.  Calls that share a workspace must not
  * overlap.
  * HCMIX_ERR_INVALID_VALUE: null pointers (partners may be null), batch, n,
  * width or coord_dim < 1, tau outside [2^-24, 2^24] or not finite, scaled not 0
@@ -430,9 +430,9 @@ hcmix_status hcmix_field_forward(int64_t batch, int64_t n, int64_t width, int32_
 
 /* Bytes of device workspace the field calls need: for each window its
  * coordinate table (N (4 c' + 20) bytes rounded up to 256, c' = coord_dim
- * rounded up to 16), plus N * N * 4 with N = n rounded up to a multiple of 32
- * (the gradient of the window's squared distances, used by the backward); 0
- * for arguments outside the supported range. */
+ * rounded up to 16), plus N * N * 6 with N = n rounded up to a multiple of 32
+ * (the gradient of the window's squared distances in fp32 and its couplings in
+ * bf16, used by the backward); 0 for arguments outside the supported range. */
 size_t hcmix_field_workspace_bytes(int64_t batch, int64_t n, int32_t coord_dim);
 
 /* Backward: dp = dL/dp and dx = dL/dx (both overwritten) from p, x, the

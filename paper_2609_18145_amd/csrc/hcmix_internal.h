@@ -238,8 +238,9 @@ hipError_t launch_attention_bwd_bf16(const bf16* qkv, const bf16* out, const flo
 // workspace: field_workspace_bytes(batch, n, c) bytes, 256-byte aligned (each
 // window's coordinate table, written by the forward, then for the backward the
 // gradient of the squared distances, fp32 [batch][NP][NP] with NP = n rounded
-// up to 32).  reuse_table: the backward takes the tables the forward wrote to
-// this workspace for the same p instead of building them again.
+// up to 32, and the couplings, bf16 [batch][NP][NP]).  reuse_table: the
+// backward takes the tables the forward wrote to this workspace for the same
+// p instead of building them again.
 size_t field_workspace_bytes(int batch, int n, int c);
 hipError_t launch_field_fwd(const float* p, const bf16* x, bf16* y, float* row_mean, float* lse,
                             float* partners, void* workspace, int batch, int n, int c, int width,

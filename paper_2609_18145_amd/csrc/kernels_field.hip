@@ -23,11 +23,13 @@
 // Kernels (one window's coordinates and one 64-column slab per block, the
 // whole causal row of a 32-query tile in registers as in the attention core):
 //   field_fwd_kernel        y slab, and (slab 0) m_i, ln Z_i, partners;
-//   field_bwd_rows_kernel   per query tile: dP[i][j] = dy_i . x_j over the full
-//                           width, Delta_i = sum_j C dP (= dy_i . y_i),
-//                           da = C (dP - Delta), and the gradient of the
-//                           squared distances dD (written, fp32, [key][query]);
-//   field_bwd_dx_kernel     dx slab = C^T dy (keys in lanes);
+//   field_bwd_rows_kernel   per query tile: the couplings C (written, bf16,
+//                           transposed, for the dx kernel), dP[i][j] = dy_i .
+//                           x_j over the full width, Delta_i = sum_j C dP (=
+//                           dy_i . y_i), da = C (dP - Delta), and the gradient
+//                           of the squared distances dD (written, fp32,
+//                           [key][query]);
+//   field_bwd_dx_kernel     dx slab = C^T dy (keys in lanes, C as written);
 //   field_bwd_coord_kernel  dp_i = 2 sum_j E[i][j] (p_i - p_j), E = dD + dD^T,
 //                           on the fp32 matrix cores.
 #include "hcmix_internal.h"
@@ -424,9 +426,15 @@ constexpr int fwd_lds_bytes(int NT, int SW, int cp) {
               (NT + 1) / 2 * (SW / 32 * 16 + 2) * 64 * 4);
 }
 constexpr int prep_lds_bytes(int NT, int cp) { return 3 * NT * 32 * 4 + table_bytes(NT, cp); }
-constexpr int dx_lds_bytes(int NT, int SW, int cp) {
-  return NT * 32 * SW * 2 + 3 * NT * 32 * 4 + table_bytes(NT, cp);
-}
+constexpr int dx_lds_bytes(int NT, int SW) { return NT * 32 * SW * 2; }
+
+// Transposed coupling tiles as the rows kernel writes them and the dx kernel
+// reads them: per window NT x NT tiles of 32 x 32 bf16 (tile (kt, qt) at kt *
+// NT + qt; only qt >= kt written), row = key, and within a row the 32
+// queries in the order of a key lane's score registers: query 8 g + 4 h + r
+// (g, r < 4, h < 2) at 16 h + 4 g + r.  A lane of half h then finds its 16
+// couplings of a tile in 32 contiguous bytes.
+__device__ __forceinline__ int ct_pos(int lq) { return 16 * ((lq >> 2) & 1) + 4 * (lq >> 3) + (lq & 3); }
 // rows kernel: NS stages of [x rows (NT * 32)][64] + [dy rows (32)][64] bf16,
 // the coordinate table in the same space before the stages are used, then
 // the norms and the per-wave row sums.  At NS = 2 a block needs at most 77
@@ -679,7 +687,7 @@ template <int NT, int NS>
 __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
     const unsigned char* __restrict__ tab, const bf16* __restrict__ x, const bf16* __restrict__ dy,
     const float* __restrict__ row_mean, const float* __restrict__ lse, float* __restrict__ ddt,
-    int n, int cp, int width, float inv_tau, int scaled) {
+    bf16* __restrict__ ct, int n, int cp, int width, float inv_tau, int scaled) {
   constexpr int NP = NT * 32, STAGE = rows_stage_elems(NT);
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sStage = (bf16*)smem;
@@ -745,6 +753,10 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
         cc[e] = diag && lk > lq ? 0.f : __builtin_amdgcn_exp2f(d * k2 - l2);
       }
     }
+    // C^T tile (key tile = wave, query tile qt) for the dx kernel
+    bf16* cw = ct + ((size_t)b * NT * NT + wave * NT + qt) * 1024 + ct_pos(lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; e++) cw[(8 * (e >> 2) + 4 * half + (e & 3)) * 32] = to_bf16(cc[e]);
   }
   __syncthreads();                                    // the table's space becomes the stages
 #pragma unroll
@@ -803,83 +815,59 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
 
 // ---------------------------------------------------------------------------
 // Backward, dx.  Block = (window b, slab s of SW columns), 8 waves, wave w on
-// key tile wave_tile(w), a lane one key j; C[q][j] is recomputed from the
-// forward's m and ln Z (one add, two FMAs and the exponential per coupling,
-// the mask only on the diagonal tile), and dx^T[col][j] += dy^T[col][q]
-// C[q][j] as in the attention core's dV.
+// key tile wave_tile(w), a lane one key j; the couplings come as the rows
+// kernel wrote them (bf16, the lane's 16 queries of a tile in one 32-byte
+// load, PF tiles in flight), and dx^T[col][j] += dy^T[col][q] C[q][j] as in
+// the attention core's dV, dy^T read transposed from the LDS slab.
 // ---------------------------------------------------------------------------
 template <int NT, int SW>
-__global__ __launch_bounds__(FT) void field_bwd_dx_kernel(
-    const unsigned char* __restrict__ tab, const float* __restrict__ row_mean,
-    const float* __restrict__ lse, const bf16* __restrict__ dy, bf16* __restrict__ dx, int n,
-    int cp, int width, int slabs, float inv_tau, int scaled) {
-  constexpr int NP = NT * 32, DT = SW / 32;
+__global__ __launch_bounds__(FT) void field_bwd_dx_kernel(const bf16* __restrict__ ct,
+                                                         const bf16* __restrict__ dy,
+                                                         bf16* __restrict__ dx, int n, int width,
+                                                         int slabs) {
+  constexpr int NP = NT * 32, DT = SW / 32, PF = NT < 3 ? NT : 3;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sDY = (bf16*)smem;
-  float* sN = (float*)(smem + NP * SW * 2);
-  float* sK2 = sN + NP;                       // -scale_q log2 e
-  float* sL2 = sK2 + NP;                      // -ln Z_q log2 e
-  bf16* sT = (bf16*)(sL2 + NP);
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
   const int b = lin / slabs, s = lin % slabs;
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-  const int rs = ct_stride(cp);
-  if (threadIdx.x < NP) {
-    const int q = threadIdx.x;
-    const bool v = q < n;
-    const float m = row_mean[(size_t)b * n + min(q, n - 1)];
-    const float l = lse[(size_t)b * n + min(q, n - 1)];
-    sK2[q] = v ? -logit_scale(m, inv_tau, scaled) * LOG2E : 0.f;
-    sL2[q] = v ? -l * LOG2E : 0.f;
-  }
+  const int kt = wave_tile(wave);
   Slab<NT, SW> slab;
-  load_table<NT>(tab + (size_t)b * tab_stride(NT, cp), cp, NP, sT, sN,
-                 [&] { slab.issue(dy + (size_t)b * n * width + (size_t)s * SW, width, n); });
+  slab.issue(dy + (size_t)b * n * width + (size_t)s * SW, width, n);
+  // tile (kt, kt + u) for u < NT - kt; past that (and for waves without a key
+  // tile) the loads are clamped to tile (min(kt, NT - 1), NT - 1), in bounds
+  const bf16* cw = ct + ((size_t)b * NT * NT + (size_t)min(kt, NT - 1) * NT) * 1024 +
+                   (lane & 31) * 32 + 16 * half;
+  bf16x8 cf[PF][2];
+  auto fetch = [&](int u, bf16x8* dst) {
+    const bf16* src = cw + (size_t)min(kt + u, NT - 1) * 1024;
+    dst[0] = *(const bf16x8*)src;
+    dst[1] = *(const bf16x8*)(src + 8);
+  };
+#pragma unroll
+  for (int u = 0; u < PF; u++) fetch(u, cf[u]);
   slab.store(sDY, n);
   __syncthreads();
-  const int kt = wave_tile(wave);
   if (kt >= NT) return;
-  const int lj = lane & 31, j = kt * 32 + lj;
-  RowFrags f;
-  row_frags(sT, rs, cp, j, half, f);
-  const float nj = sN[j];
   f32x16 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
-  auto readout = [&](f32x16& ce, int qt) {
 #pragma unroll
-    for (int mm = 0; mm < 2; mm++) {
-      const bf16x8 pf = att_pack(ce, mm);
+  for (int u = 0; u < NT; u++) {
+    if (u < NT - kt) {
+      const int qt = kt + u;
+      bf16x8 cur[2] = {cf[u % PF][0], cf[u % PF][1]};
+      if (u + PF < NT) fetch(u + PF, cf[u % PF]);
 #pragma unroll
-      for (int dt = 0; dt < DT; dt++)
-        o[dt] = mfma32(att_trfrag(sDY + (dt / 2) * NP * 64, qt * 32 + 16 * mm, 32 * (dt % 2), lane),
-                       pf, o[dt]);
+      for (int mm = 0; mm < 2; mm++)
+#pragma unroll
+        for (int dt = 0; dt < DT; dt++)
+          o[dt] = mfma32(att_trfrag(sDY + (dt / 2) * NP * 64, qt * 32 + 16 * mm, 32 * (dt % 2), lane),
+                         cur[mm], o[dt]);
     }
-  };
-  // register e: query qt*32 + 8 (e/4) + 4 half + e%4, key j; the diagonal tile
-  // first (its own diagonal exactly 0, queries before j masked)
-  for (int qt = kt; qt < NT; qt++) {
-    f32x16 acc = gram_tile<false>(sT, rs, cp, qt * 32, f, lane);
-    const bool diag = qt == kt;
-#pragma unroll
-    for (int gq = 0; gq < 4; gq++) {
-      const int q0 = qt * 32 + 8 * gq + 4 * half;
-      const f32x4 n4 = *(const f32x4*)(sN + q0);
-      const f32x4 k4 = *(const f32x4*)(sK2 + q0);
-      const f32x4 l4 = *(const f32x4*)(sL2 + q0);
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        const int e = 4 * gq + r, lq = 8 * gq + 4 * half + r;
-        float d = fmaf(acc[e], -2.f, n4[r] + nj);
-        if (diag && lq == lj) d = 0.f;
-        float ce = __builtin_amdgcn_exp2f(fmaf(d, k4[r], l4[r]));
-        if (diag && lq < lj) ce = 0.f;
-        acc[e] = ce;
-      }
-    }
-    readout(acc, qt);
   }
+  const int j = kt * 32 + (lane & 31);
   if (j >= n) return;
   bf16* xrow = dx + ((size_t)b * n + j) * width + (size_t)s * SW;
 #pragma unroll
@@ -1076,29 +1064,28 @@ hipError_t field_fwd_pick(const float* p, const bf16* x, bf16* y, float* row_mea
 }
 
 template <int NT, int SW>
-hipError_t field_dx_launch(const unsigned char* tab, const float* row_mean, const float* lse,
-                           const bf16* dy, bf16* dx, int batch, int n, int cp, int width,
-                           float inv_tau, int scaled, hipStream_t st) {
+hipError_t field_dx_launch(const bf16* ct, const bf16* dy, bf16* dx, int batch, int n, int width,
+                           hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
   hipError_t e = lds_limit_once(done, (const void*)field_bwd_dx_kernel<NT, SW>,
-                                dx_lds_bytes(NT, SW, 64));
+                                dx_lds_bytes(NT, SW));
   if (e != hipSuccess) return e;
   const int slabs = width / SW;
-  field_bwd_dx_kernel<NT, SW><<<batch * slabs, FT, dx_lds_bytes(NT, SW, cp), st>>>(
-      tab, row_mean, lse, dy, dx, n, cp, width, slabs, inv_tau, scaled);
+  field_bwd_dx_kernel<NT, SW><<<batch * slabs, FT, dx_lds_bytes(NT, SW), st>>>(ct, dy, dx, n,
+                                                                               width, slabs);
   return hipGetLastError();
 }
 
 template <int NT, int NS>
 hipError_t field_rows_launch(const unsigned char* tab, const bf16* x, const float* row_mean,
-                             const float* lse, const bf16* dy, float* ddt, int batch, int n,
+                             const float* lse, const bf16* dy, float* ddt, bf16* ct, int batch, int n,
                              int cp, int width, float inv_tau, int scaled, hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
   hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS>,
                                 rows_lds_bytes(NT, NS, 64));
   if (e != hipSuccess) return e;
   field_bwd_rows_kernel<NT, NS><<<batch * NT, FT, rows_lds_bytes(NT, NS, cp), st>>>(
-      tab, x, dy, row_mean, lse, ddt, n, cp, width, inv_tau, scaled);
+      tab, x, dy, row_mean, lse, ddt, ct, n, cp, width, inv_tau, scaled);
   return hipGetLastError();
 }
 
@@ -1121,18 +1108,17 @@ hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean
                             int width, float inv_tau, int scaled, hipStream_t st) {
   unsigned char* tab = ws;
   float* ddt = (float*)(ws + (size_t)batch * tab_stride(NT, cp));
+  bf16* ct = (bf16*)(ddt + (size_t)batch * NT * 32 * NT * 32);
   hipError_t e = hipSuccess;
   if (!reuse_table) {
     e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
     if (e != hipSuccess) return e;
   }
-  e = field_rows_launch<NT, ROWS_NS>(tab, x, row_mean, lse, dy, ddt, batch, n, cp, width, inv_tau,
-                                     scaled, st);
+  e = field_rows_launch<NT, ROWS_NS>(tab, x, row_mean, lse, dy, ddt, ct, batch, n, cp, width,
+                                     inv_tau, scaled, st);
   if (e != hipSuccess) return e;
-  e = width % 128 == 0 ? field_dx_launch<NT, 128>(tab, row_mean, lse, dy, dx, batch, n, cp, width,
-                                                   inv_tau, scaled, st)
-                       : field_dx_launch<NT, 64>(tab, row_mean, lse, dy, dx, batch, n, cp, width,
-                                                 inv_tau, scaled, st);
+  e = width % 128 == 0 ? field_dx_launch<NT, 128>(ct, dy, dx, batch, n, width, st)
+                       : field_dx_launch<NT, 64>(ct, dy, dx, batch, n, width, st);
   if (e != hipSuccess) return e;
   return c <= 32 ? field_coord_launch<NT, 32>(p, ddt, dp, batch, n, c, st)
                  : field_coord_launch<NT, 64>(p, ddt, dp, batch, n, c, st);
@@ -1140,7 +1126,7 @@ hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean
 
 template <int NT>
 size_t field_ws_bytes(int batch, int cp) {
-  return (size_t)batch * (tab_stride(NT, cp) + (size_t)NT * 32 * NT * 32 * 4);
+  return (size_t)batch * (tab_stride(NT, cp) + (size_t)NT * 32 * NT * 32 * 6);
 }
 
 }  // namespace

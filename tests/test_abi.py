@@ -511,10 +511,11 @@ def test_field_backward_workspace_and_rejections():
     q = lib.hcmix_field_workspace_bytes
     # per window: the coordinate table (rows of 2 c' + 8 bf16 and the norms,
     # rounded up to 256 bytes), then the N x N fp32 squared-distance gradient
+    # and the N x N bf16 couplings
     table = lambda np_, cp: -(-(np_ * (2 * cp + 8) * 2 + np_ * 4) // 256) * 256  # noqa: E731
-    assert q(64, 256, 32) == 64 * (table(256, 32) + 256 * 256 * 4)
-    assert q(2, 40, 3) == 2 * (table(64, 16) + 64 * 64 * 4)      # n rounded up to a multiple of 32
-    assert q(1, 1, 64) == table(32, 64) + 32 * 32 * 4
+    assert q(64, 256, 32) == 64 * (table(256, 32) + 256 * 256 * 6)
+    assert q(2, 40, 3) == 2 * (table(64, 16) + 64 * 64 * 6)      # n rounded up to a multiple of 32
+    assert q(1, 1, 64) == table(32, 64) + 32 * 32 * 6
     assert q(0, 16, 4) == 0 and q(2, 257, 4) == 0 and q(2, 0, 4) == 0
     assert q(2, 16, 0) == 0 and q(2, 16, 65) == 0
     need = q(2, 40, 3)
