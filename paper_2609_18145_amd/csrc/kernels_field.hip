@@ -20,9 +20,14 @@
 // that rounding and the diagonal's is 0, so each row's maximum is known: the
 // exponentials need no running maximum and Z_i lies in [1, i + 1].
 //
-// Kernels (one window's coordinates and one 64-column slab per block, the
-// whole causal row of a 32-query tile in registers as in the attention core):
-//   field_fwd_kernel        y slab, and (slab 0) m_i, ln Z_i, partners;
+// Kernels (a 32-query or 32-key tile of one window per wave, its scores in
+// registers as in the attention core):
+//   field_couple_kernel     per query tile: m_i, ln Z_i, partners, and the
+//                           couplings C (written, bf16, in the readout's
+//                           operand order); the window's table for the
+//                           backward;
+//   field_readout_kernel    y slab = C x (queries in lanes, C as written);
+//   field_prep_kernel       the window's table, when the backward builds it;
 //   field_bwd_rows_kernel   per query tile: the couplings C (written, bf16,
 //                           transposed, for the dx kernel), dP[i][j] = dy_i .
 //                           x_j over the full width, Delta_i = sum_j C dP (=
@@ -126,104 +131,71 @@ __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int r
   }
 }
 
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+// bytes of a window's table rows (NT * 32 rows of 2 cp + 8 bf16)
+constexpr int table_bytes(int NT, int cp) { return NT * 32 * (2 * cp + 8) * 2; }
+
 // The coordinate table rows [0, rows) (rows <= 256) and their squared norms
-// N_r (of hi + lo, fp32), from the window's coordinates pw [n][c]; with TILES
-// also what a row's mean needs from the tiles before it:
-//   sTS[t][k] = sum over rows j < 32 t (of the window) of the centred p_j[k]
-//   (fp32, t = 0 .. NT; each tile's column sum by one thread, then a running
-//   sum over the tiles), and sPN[t] = sum of N_j over tile t.  Then, for
-//   query q in tile t,
-//   sum_{j < 32 t} D[q][j] = 32 t N_q + sum_{t' < t} sPN[t'] - 2 p'_q . sTS[t].
-// The raw rows are staged in the table's own space with a stride of c + 1
-// words (consecutive rows in distinct banks; (c + 1) * 4 <= (2 cp + 8) * 2
-// bytes, so they fit); each table row is then split by two threads (cp / 2
-// columns each: thread tid takes row tid % 256, half tid / 256), every LDS
-// read of a phase issued before its values are used.  Rows at or past n are
-// zero, N_r = 0.  `then` is passed on to stage_coords.  Three barriers; ends
-// with one.  sNh: [2][NT * 32] scratch for the half-row norms.
-template <int NT, bool TILES, class Then>
+// N_r (of hi + lo, fp32), from the window's coordinates pw [n][c].  Work is
+// dealt in pieces of 4 columns, consecutive threads on consecutive pieces of
+// a row (so a wave's 16-byte loads, with vec, cover contiguous memory; every
+// load unconditional, indices clamped into the window): a piece is centred on
+// the window's first row, split into hi + lo, written to its row, and the sum
+// of the squares of hi + lo over its 4 columns goes to sNp[piece][row]; after
+// a barrier each row adds its pieces in column order.  Rows at or past n are
+// zero, N_r = 0.  sNp: (cp / 4) x NT * 32 floats.  Two barriers; ends with one.
+template <int NT>
 __device__ __forceinline__ void build_table(const float* __restrict__ pw, int n, int c, int cp,
-                                            int rows, bf16* sT, float* sN, float* sNh,
-                                            float* sTS, float* sPN, bool vec, Then then) {
-  constexpr int NP = NT * 32;
-  const int rws = (c + 1) * 4;                       // raw staging row stride (bytes)
-  unsigned char* base = (unsigned char*)sT;
-  stage_coords<FT>(pw, rows < n ? rows : n, c, base, rws, vec, then);
-  __syncthreads();
-  const int r = threadIdx.x & 255, h = threadIdx.x >> 8;
-  const int hc = cp >> 1, k0 = h * hc;               // this thread's columns [k0, k0 + hc)
-  const bool live = r < n && r < rows;
-  const int rr = live ? r : 0;
-  float v[32];
-  {
-    float raw[32], p0[32];
+                                            int rows, bf16* sT, float* sN, float* sNp, bool vec) {
+  constexpr int NP = NT * 32, MAXI = (NP * 16 + FT - 1) / FT;
+  const int cp4 = cp >> 2, pieces = rows * cp4, rs = ct_stride(cp);
+  const float inv4 = 1.f / (float)cp4;             // (idx + 0.5) * inv4 never rounds across an integer
+  f32x4 raw[MAXI], p0[MAXI];
 #pragma unroll
-    for (int k = 0; k < 32; k++) {
-      const int kk = min(k0 + k, c - 1);
-      raw[k] = *(const float*)(base + rr * rws + 4 * kk);
-      p0[k] = *(const float*)(base + 4 * kk);
-    }
+  for (int u = 0; u < MAXI; u++) {
+    const int idx = min((int)threadIdx.x + FT * u, pieces - 1);
+    const int r = (int)(((float)idx + 0.5f) * inv4), j = idx - r * cp4;
+    const float* prow = pw + (size_t)min(r, n - 1) * c;
+    if (vec) {
+      const int kk = min(4 * j, c - 4);
+      raw[u] = *(const f32x4*)(prow + kk);
+      p0[u] = *(const f32x4*)(pw + kk);
+    } else {
 #pragma unroll
-    for (int k = 0; k < 32; k++) v[k] = (live && k < hc && k0 + k < c) ? raw[k] - p0[k] : 0.f;
-  }
-  if constexpr (TILES) {
-    // tile t's column k: thread (t, k) = (tid / 64, tid % 64); 8 tiles x 64 columns
-    const int t = threadIdx.x >> 6, k = threadIdx.x & 63;
-    if (t < NT) {
-      const int kk = min(k, c - 1);
-      const float p0k = *(const float*)(base + 4 * kk);
-      float col[32];
-#pragma unroll
-      for (int j = 0; j < 32; j++)
-        col[j] = *(const float*)(base + min(32 * t + j, n - 1) * rws + 4 * kk);
-      float part[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < 32; j++) part[j & 3] += (32 * t + j < n) ? col[j] - p0k : 0.f;
-      sTS[(t + 1) * 64 + k] = k < c ? (part[0] + part[1]) + (part[2] + part[3]) : 0.f;
-    }
-  }
-  __syncthreads();
-  float nn = 0.f;
-  if (r < rows) {
-    bf16* row = sT + r * ct_stride(cp) + k0;
-#pragma unroll
-    for (int k = 0; k < 32; k += 2) {
-      const bf16x2 hi2 = {to_bf16(v[k]), to_bf16(v[k + 1])};
-      const float ha = (float)hi2[0], hb = (float)hi2[1];
-      const bf16x2 lo2 = {to_bf16(v[k] - ha), to_bf16(v[k + 1] - hb)};
-      if (k < hc) {
-        *(bf16x2*)(row + k) = hi2;
-        *(bf16x2*)(row + cp + k) = lo2;
-      }
-      const float ta = ha + (float)lo2[0], tb = hb + (float)lo2[1];
-      nn = fmaf(ta, ta, nn);
-      nn = fmaf(tb, tb, nn);
-    }
-    if (h == 0) *(u32x4*)(sT + r * ct_stride(cp) + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
-  }
-  if (r < rows) sNh[h * NP + r] = nn;
-  if constexpr (TILES) {
-    if (threadIdx.x < 64) {
-      float acc = 0.f;
-      sTS[threadIdx.x] = 0.f;
-#pragma unroll
-      for (int t = 0; t < NT; t++) {
-        acc += sTS[(t + 1) * 64 + threadIdx.x];
-        sTS[(t + 1) * 64 + threadIdx.x] = acc;
+      for (int e = 0; e < 4; e++) {
+        const int kk = min(4 * j + e, c - 1);
+        raw[u][e] = prow[kk];
+        p0[u][e] = pw[kk];
       }
     }
   }
+#pragma unroll
+  for (int u = 0; u < MAXI; u++) {
+    const int idx = threadIdx.x + FT * u;
+    if (idx < pieces) {
+      const int r = (int)(((float)idx + 0.5f) * inv4), j = idx - r * cp4;
+      float nn = 0.f;
+      bf16x4 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 4; e++) {
+        const float v = (r < n && 4 * j + e < c) ? raw[u][e] - p0[u][e] : 0.f;
+        hi[e] = to_bf16(v);
+        const float hv = (float)hi[e];
+        lo[e] = to_bf16(v - hv);
+        const float t = hv + (float)lo[e];
+        nn = fmaf(t, t, nn);
+      }
+      *(bf16x4*)(sT + r * rs + 4 * j) = hi;
+      *(bf16x4*)(sT + r * rs + cp + 4 * j) = lo;
+      if (j == 0) *(u32x4*)(sT + r * rs + 2 * cp) = u32x4{0u, 0u, 0u, 0u};
+      sNp[j * NP + r] = nn;
+    }
+  }
   __syncthreads();
-  // N_r from the two halves; tile sums of N (rows 32 t .. 32 t + 31 are one
-  // half of a wave)
-  if (threadIdx.x < rows) {
-    float nr = sNh[threadIdx.x] + sNh[NP + threadIdx.x];
+  if ((int)threadIdx.x < rows) {
+    float nr = 0.f;
+    for (int j = 0; j < cp4; j++) nr += sNp[j * NP + threadIdx.x];
     sN[threadIdx.x] = nr;
-    if constexpr (TILES) {
-#pragma unroll
-      for (int o = 16; o >= 1; o >>= 1) nr += __shfl_xor(nr, o);
-      if ((threadIdx.x & 31) == 0) sPN[threadIdx.x >> 5] = nr;
-    }
   }
   __syncthreads();
 }
@@ -267,21 +239,19 @@ __global__ __launch_bounds__(FT) void field_prep_kernel(const float* __restrict_
                                                        int c, int cp, int vec) {
   constexpr int NP = NT * 32;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
-  float* sN = (float*)smem;
-  float* sNh = sN + NP;                       // [2][NP]
-  bf16* sT = (bf16*)(sNh + 2 * NP);
+  bf16* sT = (bf16*)smem;
+  float* sN = (float*)(smem + table_bytes(NT, cp));
+  float* sNp = sN + NP;                       // [cp / 4][NP]
   const int b = blockIdx.x;
-  build_table<NT, false>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, nullptr, nullptr, vec,
-                         NoIssue{});
+  build_table<NT>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNp, vec);
   store_table<NT>(sT, sN, tab + (size_t)b * tab_stride(NT, cp), cp, 0, 1);
 }
 
 // Rows [0, rows) of window b's stored table and their norms, into LDS.  Every
-// load is issued before the first LDS write; `then` runs after the loads are
-// issued.  Ends with a barrier.
-template <int NT, class Then>
+// load is issued before the first LDS write.  Ends with a barrier.
+template <int NT>
 __device__ __forceinline__ void load_table(const unsigned char* __restrict__ tw, int cp, int rows,
-                                           bf16* sT, float* sN, Then then) {
+                                           bf16* sT, float* sN) {
   constexpr int MAXP = (NT * 32 * 136 * 2 / 16 + FT - 1) / FT;   // 16-byte pieces per thread
   const int pieces = rows * (2 * cp + 8) * 2 / 16;
   u32x4 v[MAXP];
@@ -290,7 +260,6 @@ __device__ __forceinline__ void load_table(const unsigned char* __restrict__ tw,
     v[u] = ((const u32x4*)tw)[min((int)threadIdx.x + FT * u, pieces - 1)];
   const float* nrm = (const float*)(tw + tab_nrm(NT, cp));
   const float nv = nrm[min((int)threadIdx.x, rows - 1)];
-  then();
 #pragma unroll
   for (int u = 0; u < MAXP; u++)
     if ((int)threadIdx.x + FT * u < pieces) ((u32x4*)sT)[threadIdx.x + FT * u] = v[u];
@@ -369,40 +338,27 @@ __device__ __forceinline__ void row_frags(const bf16* sT, int rs, int cp, int r,
   }
 }
 
-// Gram tile of table rows t0 .. t0 + 31 (A operand) against the lane's row
-// fragments f (B operand): hi.hi, then key-lo . query-hi, then key-hi .
-// query-lo, so that both orientations (A_IS_KEY: the tile holds keys, f the
-// query; else the tile holds queries, f the key) add the same products in the
-// same order.
-template <bool A_IS_KEY>
-__device__ __forceinline__ f32x16 gram_tile(const bf16* sT, int rs, int cp, int t0,
-                                            const RowFrags& f, int lane) {
-  f32x16 acc = {};
-#pragma unroll
-  for (int ks = 0; ks < 4; ks++) {
-    if (16 * ks < cp) {
-      const bf16x8 ahi = ct_frag(sT, rs, t0, 16 * ks, lane);
-      const bf16x8 alo = ct_frag(sT, rs, t0, cp + 16 * ks, lane);
-      acc = mfma32(ahi, f.hi[ks], acc);
-      if constexpr (A_IS_KEY) {
-        acc = mfma32(alo, f.hi[ks], acc);
-        acc = mfma32(ahi, f.lo[ks], acc);
-      } else {
-        acc = mfma32(ahi, f.lo[ks], acc);
-        acc = mfma32(alo, f.hi[ks], acc);
-      }
-    }
-  }
-  return acc;
-}
-
-// Gram tile G^T[key][query] for keys kt*32.. (A operand, table rows) and the
-// lane's query q (B operand): hi.hi + lo.hi + hi.lo, in that order.
+// Gram tile G^T[key][query] for keys kt*32 .. kt*32 + 31 (A operand, table
+// rows) and the lane's query q (B operand, its own row's fragments):
+// hi.hi, then key-lo . query-hi, then key-hi . query-lo.  The forward's
+// couplings and the backward's rows kernel both take D from here, so they
+// agree bitwise.
 __device__ __forceinline__ f32x16 gram_keys(const bf16* sT, int rs, int cp, int kt, int q,
                                             int lane) {
   RowFrags f;
   row_frags(sT, rs, cp, q, lane >> 5, f);
-  return gram_tile<true>(sT, rs, cp, kt * 32, f, lane);
+  f32x16 acc = {};
+#pragma unroll
+  for (int ks = 0; ks < 4; ks++) {
+    if (16 * ks < cp) {
+      const bf16x8 ahi = ct_frag(sT, rs, kt * 32, 16 * ks, lane);
+      const bf16x8 alo = ct_frag(sT, rs, kt * 32, cp + 16 * ks, lane);
+      acc = mfma32(ahi, f.hi[ks], acc);
+      acc = mfma32(alo, f.hi[ks], acc);
+      acc = mfma32(ahi, f.lo[ks], acc);
+    }
+  }
+  return acc;
 }
 
 // Scale of the logits of a row with mean squared distance m: a = -D * scale.
@@ -416,16 +372,7 @@ __device__ __forceinline__ float logit_scale(float m, float inv_tau, int scaled)
 }
 
 // Dynamic LDS layouts (bytes).
-constexpr int cmax(int a, int b) { return a > b ? a : b; }
-constexpr int table_bytes(int NT, int cp) { return NT * 32 * (2 * cp + 8) * 2; }
-// (the forward's last phase reuses the space for (NT + 1) / 2 partial
-// readouts of (SW / 32 * 16 + 2) x 64 floats)
-constexpr int fwd_lds_bytes(int NT, int SW, int cp) {
-  return cmax(NT * 32 * SW * 2 + NT * 32 * 4 + (NT + 1) * 64 * 4 + 16 * 4 + 2 * NT * 32 * 4 +
-                  table_bytes(NT, cp),
-              (NT + 1) / 2 * (SW / 32 * 16 + 2) * 64 * 4);
-}
-constexpr int prep_lds_bytes(int NT, int cp) { return 3 * NT * 32 * 4 + table_bytes(NT, cp); }
+constexpr int prep_lds_bytes(int NT, int cp) { return table_bytes(NT, cp) + (1 + cp / 4) * NT * 32 * 4; }
 constexpr int dx_lds_bytes(int NT, int SW) { return NT * 32 * SW * 2; }
 
 // Transposed coupling tiles as the rows kernel writes them and the dx kernel
@@ -454,219 +401,176 @@ constexpr int coord_lds_bytes(int NT, int ck) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward.  Block = (window b, slab s of SW columns), 8 waves; grid = batch *
-// slabs, dealt so that the slabs of one window share an XCD (its coordinates
-// are read from HBM once).
-//
-// Work plan: the query tiles pair up as (i, NT - 1 - i), i < ceil(NT / 2),
-// and the two waves of SIMD i (waves i and i + 4) share pair i's causal work
-// (NT + 1 key tiles) evenly: wave i takes query tile i whole (when it differs
-// from the other) and key tiles [0, sA) of query tile qb = NT - 1 - i; wave
-// i + 4 takes key tiles [sA, qb] of qb, the diagonal first.  The two partial
-// readouts of qb (numerator and sums) meet in LDS at the end.
-//
-// A row's mean is known before any exponential: the earlier tiles' part from
-// the tile sums (build_table), the diagonal tile's from its Gram tile (wave i
-// recomputes qb's for its share).  Then per key tile: D = N_key + N_q - 2 G
-// (one add, one FMA), the exponential of D k2, its sum (and, PARTNERS, the
-// entropy term), and the tile's product with the x slab; the query's table
-// fragments stay in registers.
+// Forward, couplings.  Block = (window b, query tile qt), 8 waves; grid =
+// batch * NT, dealt so that the tiles of one window share an XCD.
+//   1. The table rows [0, 32 (qt + 1)) are built in LDS; the block of the
+//      last tile, which has every row, leaves the table in the workspace for
+//      the backward.
+//   2. Wave w <= qt takes key tile w: D for the tile's 32 queries (lanes) and
+//      32 keys (registers) from the Gram tile; the row sums of D meet in LDS
+//      (in wave order), giving each query's mean and logit scale; then the
+//      weights exp2(D k2) (<= 1; keys after the query 0), whose sums (and the
+//      entropy term) meet in LDS the same way.
+//   3. The couplings C = weight / Z, as the bf16 MFMA operand fragments of the
+//      readout (lane = query, the 8 keys of a k step in score-register
+//      order), go to the workspace: tile (qt, kt) at qt * NT + kt, [2][64
+//      lanes][8].  Each coupling is computed once.
 // ---------------------------------------------------------------------------
-template <int NT, int SW, bool PARTNERS>
-__global__ __launch_bounds__(FT) void field_fwd_kernel(
-    const float* __restrict__ p, unsigned char* __restrict__ tab, const bf16* __restrict__ x,
-    bf16* __restrict__ y, float* __restrict__ row_mean, float* __restrict__ lse,
-    float* __restrict__ partners, int n, int c, int cp, int width, int slabs, float inv_tau,
-    int scaled, int vec) {
-  constexpr int NP = NT * 32, DT = SW / 32;
+constexpr int couple_lds_bytes(int NT, int cp) {
+  return table_bytes(NT, cp) + NT * 32 * 4 + cmax(cp / 4 * NT * 32 * 4, 3 * 8 * 32 * 4);
+}
+
+template <int NT, bool PARTNERS>
+__global__ __launch_bounds__(FT) void field_couple_kernel(
+    const float* __restrict__ p, unsigned char* __restrict__ tab, bf16x8* __restrict__ cq,
+    float* __restrict__ row_mean, float* __restrict__ lse, float* __restrict__ partners, int n,
+    int c, int cp, float inv_tau, int scaled, int vec) {
+  constexpr int NP = NT * 32;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
-  bf16* sX = (bf16*)smem;
-  float* sN = (float*)(smem + NP * SW * 2);
-  float* sTS = sN + NP;                       // [NT + 1][64]
-  float* sPN = sTS + (NT + 1) * 64;           // [16]
-  float* sNh = sPN + 16;                      // [2][NP]
-  bf16* sT = (bf16*)(sNh + 2 * NP);
+  bf16* sT = (bf16*)smem;
+  float* sN = (float*)(smem + table_bytes(NT, cp));
+  float* sNp = sN + NP;                               // [cp / 4][NP] while the table is built,
+  float* sRed = sNp;                                  // then [3][8 waves][32]: D, Z, entropy sums
   const int lin = xcd_tile(blockIdx.x, gridDim.x);
-  const int b = lin / slabs, s = lin % slabs;
+  const int b = lin / NT, qt = NT - 1 - lin % NT;
   const int lane = threadIdx.x & 63, half = lane >> 5, lq = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int rs = ct_stride(cp);
-  Slab<NT, SW> slab;
-  build_table<NT, true>(p + (size_t)b * n * c, n, c, cp, NP, sT, sN, sNh, sTS, sPN, vec,
-                        [&] { slab.issue(x + (size_t)b * n * width + (size_t)s * SW, width, n); });
-  // the window's slab blocks share the copy of its table for the backward
-  store_table<NT>(sT, sN, tab + (size_t)b * tab_stride(NT, cp), cp, s, slabs);
-  // the plan of this wave
-  const int pi = wave & 3;
-  const bool roleA = wave < 4, active = pi < (NT + 1) / 2;
-  const int qa = pi, qb = NT - 1 - pi;
-  const int sA = qa < qb ? (qb - qa) / 2 : (qb + 1) / 2;
-  const bool own = roleA && active && qa < qb;          // wave A's whole tile
-  f32x16 o[DT];
-  float z = 0.f, za = 0.f;
-  auto reset = [&] {
-#pragma unroll
-    for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
-    z = 0.f;
-    za = 0.f;
-  };
-  // sum of D over the keys of the tiles before Q
-  auto row_off = [&](const RowFrags& fr, int Q, float nqv) {
-    float dotp = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < 4; ks++) {
-      if (16 * ks < cp) {
-        const float* ts = sTS + Q * 64 + 16 * ks + 8 * half;
-        const f32x4 t0 = *(const f32x4*)ts, t1 = *(const f32x4*)(ts + 4);
-#pragma unroll
-        for (int e = 0; e < 8; e++)
-          dotp = fmaf((float)fr.hi[ks][e] + (float)fr.lo[ks][e], e < 4 ? t0[e] : t1[e - 4], dotp);
-      }
-    }
-    dotp += __shfl_xor(dotp, 32);
-    float pn = 0.f;
-    for (int t = 0; t < Q; t++) pn += sPN[t];
-    return (float)(32 * Q) * nqv + pn - 2.f * dotp;
-  };
-  // the diagonal tile of Q: D (q itself and keys after q set to 0) and its row sum
-  auto diag = [&](const RowFrags& fr, int Q, float nqv, f32x16& d) {
-    d = gram_tile<true>(sT, rs, cp, Q * 32, fr, lane);
-    float dsum = 0.f;
+  const int q = qt * 32 + lq;
+  const bool qvalid = q < n;
+  build_table<NT>(p + (size_t)b * n * c, n, c, cp, (qt + 1) * 32, sT, sN, sNp, vec);
+  if (qt == NT - 1) store_table<NT>(sT, sN, tab + (size_t)b * tab_stride(NT, cp), cp, 0, 1);
+  const bool own = wave <= qt;                        // this wave's key tile kt = wave
+  const bool diag = wave == qt;
+  const float nq = sN[q];
+  f32x16 d = {};
+  if (own) {
+    const f32x16 acc = gram_keys(sT, rs, cp, wave, q, lane);
+    float ds = 0.f;
 #pragma unroll
     for (int g = 0; g < 4; g++) {
-      const f32x4 n4 = *(const f32x4*)(sN + Q * 32 + 8 * g + 4 * half);
+      const f32x4 n4 = *(const f32x4*)(sN + wave * 32 + 8 * g + 4 * half);
 #pragma unroll
       for (int r = 0; r < 4; r++) {
         const int e = 4 * g + r;
-        float dv = fmaf(d[e], -2.f, n4[r] + nqv);
-        if (8 * g + 4 * half + r >= lq) dv = 0.f;
+        float dv = fmaf(acc[e], -2.f, n4[r] + nq);
+        if (diag && 8 * g + 4 * half + r >= lq) dv = 0.f;   // q itself, keys after q
         d[e] = dv;
-        dsum += dv;
+        ds += dv;
       }
     }
-    return dsum + __shfl_xor(dsum, 32);
-  };
-  auto readout = [&](f32x16& pe, int kt) {
-#pragma unroll
-    for (int mm = 0; mm < 2; mm++) {
-      const bf16x8 pf = att_pack(pe, mm);
-#pragma unroll
-      for (int dt = 0; dt < DT; dt++)
-        o[dt] = mfma32(att_trfrag(sX + (dt / 2) * NP * 64, kt * 32 + 16 * mm, 32 * (dt % 2), lane),
-                       pf, o[dt]);
-    }
-  };
-  // exponentials of a tile of D (diagonal: masked), their sums
-  auto expo = [&](f32x16& d, float k2, bool is_diag) {
+    ds += __shfl_xor(ds, 32);
+    if (half == 0) sRed[wave * 32 + lq] = ds;
+  }
+  __syncthreads();
+  float dsum = 0.f;
+  for (int w = 0; w <= qt; w++) dsum += sRed[w * 32 + lq];
+  const float m = qvalid ? dsum / (float)(q + 1) : 0.f;
+  const float k2 = qvalid ? -logit_scale(m, inv_tau, scaled) * LOG2E : 0.f;
+  if (own) {
+    float z = 0.f, za = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; e++) {
       const float a = d[e] * k2;
       float pe = __builtin_amdgcn_exp2f(a);
-      if (is_diag && att_masked(e, lane)) pe = 0.f;
+      if (diag && att_masked(e, lane)) pe = 0.f;
       d[e] = pe;
       z += pe;
       if constexpr (PARTNERS) za += pe * a;
     }
-  };
-  // one off-diagonal key tile of query tile Q
-  auto tile = [&](const RowFrags& fr, int kt, float nqv, float k2) {
-    f32x16 acc = gram_tile<true>(sT, rs, cp, kt * 32, fr, lane);
-#pragma unroll
-    for (int g = 0; g < 4; g++) {
-      const f32x4 n4 = *(const f32x4*)(sN + kt * 32 + 8 * g + 4 * half);
-#pragma unroll
-      for (int r = 0; r < 4; r++) acc[4 * g + r] = fmaf(acc[4 * g + r], -2.f, n4[r] + nqv);
-    }
-    expo(acc, k2, false);
-    readout(acc, kt);
-  };
-  auto finish = [&](int Q, float m) {
-    const int q = Q * 32 + lq;
-    if (q >= n) return;
-    // O^T register e of lane l: query q, column 32 dt + 8 (e / 4) + 4 half + e % 4
-    const float inv = 1.f / z;
-    bf16* yrow = y + ((size_t)b * n + q) * width + (size_t)s * SW;
-#pragma unroll
-    for (int dt = 0; dt < DT; dt++)
-#pragma unroll
-      for (int g = 0; g < 4; g++) {
-        const bf16x4 v = {to_bf16(o[dt][4 * g] * inv), to_bf16(o[dt][4 * g + 1] * inv),
-                          to_bf16(o[dt][4 * g + 2] * inv), to_bf16(o[dt][4 * g + 3] * inv)};
-        *(bf16x4*)(yrow + 32 * dt + 8 * g + 4 * half) = v;
-      }
-    if (s == 0 && half == 0) {
-      const float l2z = __builtin_amdgcn_logf(z);       // log2 Z
-      const size_t at = (size_t)b * n + q;
-      row_mean[at] = m;
-      lse[at] = l2z * LN2;
-      if constexpr (PARTNERS) partners[at] = __builtin_amdgcn_exp2f(l2z - za * inv);
-    }
-  };
-
-  // before the slab barrier: every wave's diagonal tile (wave A: its own
-  // tile's, and qb's row sum for the mean of its share)
-  RowFrags fa, fb;
-  float nqa = 0.f, nqb = 0.f, ma = 0.f, mb = 0.f, k2a = 0.f, k2b = 0.f;
-  f32x16 dA = {}, dB = {};
-  if (active) {
-    row_frags(sT, rs, cp, qb * 32 + lq, half, fb);
-    nqb = sN[qb * 32 + lq];
-    const float dsb = diag(fb, qb, nqb, dB);
-    mb = (row_off(fb, qb, nqb) + dsb) / (float)(qb * 32 + lq + 1);
-    k2b = -logit_scale(mb, inv_tau, scaled) * LOG2E;
-    if (own) {
-      row_frags(sT, rs, cp, qa * 32 + lq, half, fa);
-      nqa = sN[qa * 32 + lq];
-      const float dsa = diag(fa, qa, nqa, dA);
-      ma = (row_off(fa, qa, nqa) + dsa) / (float)(qa * 32 + lq + 1);
-      k2a = -logit_scale(ma, inv_tau, scaled) * LOG2E;
+    z += __shfl_xor(z, 32);
+    if constexpr (PARTNERS) za += __shfl_xor(za, 32);
+    if (half == 0) {
+      sRed[256 + wave * 32 + lq] = z;
+      if constexpr (PARTNERS) sRed[512 + wave * 32 + lq] = za;
     }
   }
+  __syncthreads();
+  float z = 0.f, za = 0.f;
+  for (int w = 0; w <= qt; w++) {
+    z += sRed[256 + w * 32 + lq];
+    if constexpr (PARTNERS) za += sRed[512 + w * 32 + lq];
+  }
+  const float inv = 1.f / z;
+  if (wave == 0 && half == 0 && qvalid) {
+    const float l2z = __builtin_amdgcn_logf(z);       // log2 Z
+    const size_t at = (size_t)b * n + q;
+    row_mean[at] = m;
+    lse[at] = l2z * LN2;
+    if constexpr (PARTNERS) partners[at] = __builtin_amdgcn_exp2f(l2z - za * inv);
+  }
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 16; e++) d[e] *= inv;
+    bf16x8* dst = cq + ((size_t)(b * NT + qt) * NT + wave) * 128 + lane;
+    dst[0] = att_pack(d, 0);
+    dst[64] = att_pack(d, 1);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward, readout.  Block = (window b, slab s of SW columns), 8 waves, wave w
+// on query tile wave_tile(w) (lane = query); y^T[col][q] = sum over key tiles
+// kt <= qt of x^T[col][k] C[q][k], with C as the couplings kernel wrote it
+// (PF tiles in flight) and x^T read transposed from the LDS slab.
+// ---------------------------------------------------------------------------
+template <int NT, int SW>
+__global__ __launch_bounds__(FT) void field_readout_kernel(const bf16x8* __restrict__ cq,
+                                                          const bf16* __restrict__ x,
+                                                          bf16* __restrict__ y, int n, int width,
+                                                          int slabs) {
+  constexpr int NP = NT * 32, DT = SW / 32, PF = NT < 3 ? NT : 3;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  bf16* sX = (bf16*)smem;
+  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int b = lin / slabs, s = lin % slabs;
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+  const int qt = wave_tile(wave);
+  Slab<NT, SW> slab;
+  slab.issue(x + (size_t)b * n * width + (size_t)s * SW, width, n);
+  // tile (qt, u) for u <= qt; past that (and for waves without a query tile)
+  // the loads are clamped to a tile of the window, in bounds
+  const bf16x8* cw = cq + ((size_t)b * NT + min(qt, NT - 1)) * NT * 128 + lane;
+  bf16x8 cf[PF][2];
+  auto fetch = [&](int u, bf16x8* dst) {
+    const bf16x8* src = cw + (size_t)min(u, NT - 1) * 128;
+    dst[0] = src[0];
+    dst[1] = src[64];
+  };
+#pragma unroll
+  for (int u = 0; u < PF; u++) fetch(u, cf[u]);
   slab.store(sX, n);
   __syncthreads();
-  if (own) {                                  // wave A: query tile qa whole
-    reset();
-    expo(dA, k2a, true);
-    readout(dA, qa);
-    for (int kt = qa - 1; kt >= 0; kt--) tile(fa, kt, nqa, k2a);
-    z += __shfl_xor(z, 32);
-    if constexpr (PARTNERS) za += __shfl_xor(za, 32);
-    finish(qa, ma);
-  }
-  reset();
-  if (active) {
-    if (roleA) {                              // wave A: key tiles [0, sA) of qb
-      for (int kt = 0; kt < sA; kt++) tile(fb, kt, nqb, k2b);
-    } else {                                  // wave B: key tiles [sA, qb] of qb
-      expo(dB, k2b, true);
-      readout(dB, qb);
-      for (int kt = qb - 1; kt >= sA; kt--) tile(fb, kt, nqb, k2b);
+  if (qt >= NT) return;
+  f32x16 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; dt++) o[dt] = f32x16{};
+#pragma unroll
+  for (int u = 0; u < NT; u++) {
+    if (u <= qt) {
+      bf16x8 cur[2] = {cf[u % PF][0], cf[u % PF][1]};
+      if (u + PF < NT) fetch(u + PF, cf[u % PF]);
+#pragma unroll
+      for (int mm = 0; mm < 2; mm++)
+#pragma unroll
+        for (int dt = 0; dt < DT; dt++)
+          o[dt] = mfma32(att_trfrag(sX + (dt / 2) * NP * 64, u * 32 + 16 * mm, 32 * (dt % 2), lane),
+                         cur[mm], o[dt]);
     }
   }
-  // wave A's partial readout of qb joins wave B's through LDS (the slab and
-  // the table are no longer read)
-  __syncthreads();
-  float* part = (float*)smem + pi * (DT * 16 + 2) * 64;
-  if (active && roleA) {
+  const int q = qt * 32 + (lane & 31);
+  if (q >= n) return;
+  // register e of o[dt]: column 32 dt + 8 (e / 4) + 4 half + e % 4
+  bf16* yrow = y + ((size_t)b * n + q) * width + (size_t)s * SW;
 #pragma unroll
-    for (int dt = 0; dt < DT; dt++)
+  for (int dt = 0; dt < DT; dt++)
 #pragma unroll
-      for (int e = 0; e < 16; e++) part[(dt * 16 + e) * 64 + lane] = o[dt][e];
-    part[DT * 16 * 64 + lane] = z;
-    part[(DT * 16 + 1) * 64 + lane] = za;
-  }
-  __syncthreads();
-  if (active && !roleA) {
-#pragma unroll
-    for (int dt = 0; dt < DT; dt++)
-#pragma unroll
-      for (int e = 0; e < 16; e++) o[dt][e] += part[(dt * 16 + e) * 64 + lane];
-    z += part[DT * 16 * 64 + lane];
-    za += part[(DT * 16 + 1) * 64 + lane];
-    z += __shfl_xor(z, 32);
-    if constexpr (PARTNERS) za += __shfl_xor(za, 32);
-    finish(qb, mb);
-  }
+    for (int g = 0; g < 4; g++) {
+      const bf16x4 v = {to_bf16(o[dt][4 * g]), to_bf16(o[dt][4 * g + 1]), to_bf16(o[dt][4 * g + 2]),
+                        to_bf16(o[dt][4 * g + 3])};
+      *(bf16x4*)(yrow + 32 * dt + 8 * g + 4 * half) = v;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -730,7 +634,7 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
   };
   const float m_ld = row_mean[(size_t)b * n + min(q, n - 1)];
   const float l_ld = lse[(size_t)b * n + min(q, n - 1)];
-  load_table<NT>(tab + (size_t)b * tab_stride(NT, cp), cp, (qt + 1) * 32, sT, sN, NoIssue{});
+  load_table<NT>(tab + (size_t)b * tab_stride(NT, cp), cp, (qt + 1) * 32, sT, sN);
   const float m = qvalid ? m_ld : 0.f;
   const float l2 = qvalid ? l_ld * LOG2E : 0.f;
   const float scale = qvalid ? logit_scale(m, inv_tau, scaled) : 0.f;
@@ -1032,35 +936,52 @@ hipError_t field_prep_launch(const float* p, unsigned char* tab, int batch, int 
   return hipGetLastError();
 }
 
-template <int NT, int SW, bool PARTNERS>
-hipError_t field_fwd_launch(const float* p, unsigned char* tab, const bf16* x, bf16* y,
-                            float* row_mean, float* lse, float* partners, int batch, int n, int c,
-                            int cp, int width, float inv_tau, int scaled, hipStream_t st) {
+template <int NT, bool PARTNERS>
+hipError_t field_couple_launch(const float* p, unsigned char* tab, bf16x8* cq, float* row_mean,
+                               float* lse, float* partners, int batch, int n, int c, int cp,
+                               float inv_tau, int scaled, hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
-  hipError_t e = lds_limit_once(done, (const void*)field_fwd_kernel<NT, SW, PARTNERS>,
-                                fwd_lds_bytes(NT, SW, 64));
+  hipError_t e = lds_limit_once(done, (const void*)field_couple_kernel<NT, PARTNERS>,
+                                couple_lds_bytes(NT, 64));
+  if (e != hipSuccess) return e;
+  field_couple_kernel<NT, PARTNERS><<<batch * NT, FT, couple_lds_bytes(NT, cp), st>>>(
+      p, tab, cq, row_mean, lse, partners, n, c, cp, inv_tau, scaled, coords_vec(p, c));
+  return hipGetLastError();
+}
+
+template <int NT, int SW>
+hipError_t field_readout_launch(const bf16x8* cq, const bf16* x, bf16* y, int batch, int n,
+                                int width, hipStream_t st) {
+  static std::atomic<unsigned long long> done{0};
+  hipError_t e = lds_limit_once(done, (const void*)field_readout_kernel<NT, SW>,
+                                dx_lds_bytes(NT, SW));
   if (e != hipSuccess) return e;
   const int slabs = width / SW;
-  field_fwd_kernel<NT, SW, PARTNERS><<<batch * slabs, FT, fwd_lds_bytes(NT, SW, cp), st>>>(
-      p, tab, x, y, row_mean, lse, partners, n, c, cp, width, slabs, inv_tau, scaled,
-      coords_vec(p, c));
+  field_readout_kernel<NT, SW><<<batch * slabs, FT, dx_lds_bytes(NT, SW), st>>>(cq, x, y, n,
+                                                                                width, slabs);
   return hipGetLastError();
+}
+
+// Workspace: the tables, then the squared-distance gradient (backward), then
+// the couplings: the forward's [batch][NT][NT] fragment tiles, later the
+// backward's transposed tiles (each call's use ends with the call).
+template <int NT>
+unsigned char* field_coupling_space(unsigned char* ws, int batch, int cp) {
+  return ws + (size_t)batch * tab_stride(NT, cp) + (size_t)batch * NT * 32 * NT * 32 * 4;
 }
 
 template <int NT>
 hipError_t field_fwd_pick(const float* p, const bf16* x, bf16* y, float* row_mean, float* lse,
-                          float* partners, unsigned char* tab, int batch, int n, int c, int cp,
+                          float* partners, unsigned char* ws, int batch, int n, int c, int cp,
                           int width, float inv_tau, int scaled, hipStream_t st) {
-  const bool wide = width % 128 == 0;
-  if (partners)
-    return wide ? field_fwd_launch<NT, 128, true>(p, tab, x, y, row_mean, lse, partners, batch,
-                                                  n, c, cp, width, inv_tau, scaled, st)
-                : field_fwd_launch<NT, 64, true>(p, tab, x, y, row_mean, lse, partners, batch, n,
-                                                 c, cp, width, inv_tau, scaled, st);
-  return wide ? field_fwd_launch<NT, 128, false>(p, tab, x, y, row_mean, lse, partners, batch, n,
-                                                 c, cp, width, inv_tau, scaled, st)
-              : field_fwd_launch<NT, 64, false>(p, tab, x, y, row_mean, lse, partners, batch, n,
-                                                c, cp, width, inv_tau, scaled, st);
+  bf16x8* cq = (bf16x8*)field_coupling_space<NT>(ws, batch, cp);
+  hipError_t e = partners ? field_couple_launch<NT, true>(p, ws, cq, row_mean, lse, partners, batch,
+                                                          n, c, cp, inv_tau, scaled, st)
+                          : field_couple_launch<NT, false>(p, ws, cq, row_mean, lse, partners,
+                                                           batch, n, c, cp, inv_tau, scaled, st);
+  if (e != hipSuccess) return e;
+  return width % 128 == 0 ? field_readout_launch<NT, 128>(cq, x, y, batch, n, width, st)
+                          : field_readout_launch<NT, 64>(cq, x, y, batch, n, width, st);
 }
 
 template <int NT, int SW>
@@ -1108,7 +1029,7 @@ hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean
                             int width, float inv_tau, int scaled, hipStream_t st) {
   unsigned char* tab = ws;
   float* ddt = (float*)(ws + (size_t)batch * tab_stride(NT, cp));
-  bf16* ct = (bf16*)(ddt + (size_t)batch * NT * 32 * NT * 32);
+  bf16* ct = (bf16*)field_coupling_space<NT>(ws, batch, cp);
   hipError_t e = hipSuccess;
   if (!reuse_table) {
     e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
