@@ -718,21 +718,20 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Backward, dx.  Block = (window b, slab s of SW columns), 8 waves, wave w on
+// Backward, dx.  Block bid of nblk = (window b, slab s of SW columns), 8 waves, wave w on
 // key tile wave_tile(w), a lane one key j; the couplings come as the rows
 // kernel wrote them (bf16, the lane's 16 queries of a tile in one 32-byte
 // load, PF tiles in flight), and dx^T[col][j] += dy^T[col][q] C[q][j] as in
 // the attention core's dV, dy^T read transposed from the LDS slab.
 // ---------------------------------------------------------------------------
 template <int NT, int SW>
-__global__ __launch_bounds__(FT) void field_bwd_dx_kernel(const bf16* __restrict__ ct,
-                                                         const bf16* __restrict__ dy,
-                                                         bf16* __restrict__ dx, int n, int width,
-                                                         int slabs) {
+__device__ __forceinline__ void dx_block(int bid, int nblk, const bf16* __restrict__ ct,
+                                         const bf16* __restrict__ dy, bf16* __restrict__ dx, int n,
+                                         int width, int slabs) {
   constexpr int NP = NT * 32, DT = SW / 32, PF = NT < 3 ? NT : 3;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sDY = (bf16*)smem;
-  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int lin = xcd_tile(bid, nblk);
   const int b = lin / slabs, s = lin % slabs;
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
@@ -785,7 +784,7 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(const bf16* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// Backward, coordinates.  Block = (window b, row tile t), 8 waves: E[i][j] for
+// Backward, coordinates.  Block bid of nblk = (window b, row tile t), 8 waves: E[i][j] for
 // the tile's 32 rows i and every j (dD[i][j] = ddt[j][i] for j < i, dD[j][i] =
 // ddt[i][j] for j > i; 0 at j = i and outside the window) into LDS; then
 //   dp_i = 2 (sum_j E[i][j]) p'_i - 2 sum_j E[i][j] p'_j,  p' = p - p_0,
@@ -794,17 +793,16 @@ __global__ __launch_bounds__(FT) void field_bwd_dx_kernel(const bf16* __restrict
 // LDS.
 // ---------------------------------------------------------------------------
 template <int NT, int CK>
-__global__ __launch_bounds__(FT) void field_bwd_coord_kernel(const float* __restrict__ p,
-                                                            const float* __restrict__ ddt,
-                                                            float* __restrict__ dp, int n,
-                                                            int c, int vec) {
+__device__ __forceinline__ void coord_block(int bid, int nblk, const float* __restrict__ p,
+                                            const float* __restrict__ ddt, float* __restrict__ dp,
+                                            int n, int c, int vec) {
   constexpr int NP = NT * 32, ES = NP + 1, CKP = CK + 1;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   float* sE = (float*)smem;                          // [32][ES]
   float* sP = sE + 32 * ES;                          // [NP][CKP]
   float* sRowPart = sP + NP * CKP;                   // [16][32]
   float* sPart = coord_part_in_e(NT, CK) ? sE : sRowPart + 16 * 32;   // [4][32][CKP]
-  const int lin = xcd_tile(blockIdx.x, gridDim.x);
+  const int lin = xcd_tile(bid, nblk);
   const int b = lin / NT, t = lin % NT;
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
@@ -919,6 +917,23 @@ __global__ __launch_bounds__(FT) void field_bwd_coord_kernel(const float* __rest
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward, dx and coordinates in one launch: blocks [0, dx_blocks) are dx
+// blocks, the rest coordinate blocks.  Both read only what the rows kernel
+// wrote, so the coordinate blocks' latency-bound work overlaps the dx
+// blocks' memory traffic, and one kernel boundary goes.
+// ---------------------------------------------------------------------------
+template <int NT, int SW, int CK>
+__global__ __launch_bounds__(FT) void field_bwd_tail_kernel(
+    const bf16* __restrict__ ct, const bf16* __restrict__ dy, bf16* __restrict__ dx, int width,
+    int slabs, const float* __restrict__ p, const float* __restrict__ ddt, float* __restrict__ dp,
+    int n, int c, int vec, int dx_blocks) {
+  if ((int)blockIdx.x < dx_blocks)
+    dx_block<NT, SW>(blockIdx.x, dx_blocks, ct, dy, dx, n, width, slabs);
+  else
+    coord_block<NT, CK>(blockIdx.x - dx_blocks, gridDim.x - dx_blocks, p, ddt, dp, n, c, vec);
+}
+
 // Whether the coordinates take the 16-byte load path: p 16-byte aligned and
 // c a multiple of 4 (then every window's rows start 16-byte aligned too).
 inline int coords_vec(const float* p, int c) {
@@ -984,19 +999,6 @@ hipError_t field_fwd_pick(const float* p, const bf16* x, bf16* y, float* row_mea
                           : field_readout_launch<NT, 64>(cq, x, y, batch, n, width, st);
 }
 
-template <int NT, int SW>
-hipError_t field_dx_launch(const bf16* ct, const bf16* dy, bf16* dx, int batch, int n, int width,
-                           hipStream_t st) {
-  static std::atomic<unsigned long long> done{0};
-  hipError_t e = lds_limit_once(done, (const void*)field_bwd_dx_kernel<NT, SW>,
-                                dx_lds_bytes(NT, SW));
-  if (e != hipSuccess) return e;
-  const int slabs = width / SW;
-  field_bwd_dx_kernel<NT, SW><<<batch * slabs, FT, dx_lds_bytes(NT, SW), st>>>(ct, dy, dx, n,
-                                                                               width, slabs);
-  return hipGetLastError();
-}
-
 template <int NT, int NS>
 hipError_t field_rows_launch(const unsigned char* tab, const bf16* x, const float* row_mean,
                              const float* lse, const bf16* dy, float* ddt, bf16* ct, int batch, int n,
@@ -1010,16 +1012,26 @@ hipError_t field_rows_launch(const unsigned char* tab, const bf16* x, const floa
   return hipGetLastError();
 }
 
-template <int NT, int CK>
-hipError_t field_coord_launch(const float* p, const float* ddt, float* dp, int batch, int n,
-                              int c, hipStream_t st) {
+template <int NT, int SW, int CK>
+hipError_t field_tail_launch(const bf16* ct, const bf16* dy, bf16* dx, const float* p,
+                             const float* ddt, float* dp, int batch, int n, int c, int width,
+                             hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
-  hipError_t e = lds_limit_once(done, (const void*)field_bwd_coord_kernel<NT, CK>,
-                                coord_lds_bytes(NT, CK));
+  constexpr int lds = cmax(dx_lds_bytes(NT, SW), coord_lds_bytes(NT, CK));
+  hipError_t e = lds_limit_once(done, (const void*)field_bwd_tail_kernel<NT, SW, CK>, lds);
   if (e != hipSuccess) return e;
-  field_bwd_coord_kernel<NT, CK><<<batch * NT, FT, coord_lds_bytes(NT, CK), st>>>(
-      p, ddt, dp, n, c, coords_vec(p, c));
+  const int slabs = width / SW, dxb = batch * slabs;
+  field_bwd_tail_kernel<NT, SW, CK><<<dxb + batch * NT, FT, lds, st>>>(
+      ct, dy, dx, width, slabs, p, ddt, dp, n, c, coords_vec(p, c), dxb);
   return hipGetLastError();
+}
+
+template <int NT, int SW>
+hipError_t field_tail_pick(const bf16* ct, const bf16* dy, bf16* dx, const float* p,
+                           const float* ddt, float* dp, int batch, int n, int c, int width,
+                           hipStream_t st) {
+  return c <= 32 ? field_tail_launch<NT, SW, 32>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st)
+                 : field_tail_launch<NT, SW, 64>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st);
 }
 
 template <int NT>
@@ -1038,11 +1050,8 @@ hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean
   e = field_rows_launch<NT, ROWS_NS>(tab, x, row_mean, lse, dy, ddt, ct, batch, n, cp, width,
                                      inv_tau, scaled, st);
   if (e != hipSuccess) return e;
-  e = width % 128 == 0 ? field_dx_launch<NT, 128>(ct, dy, dx, batch, n, width, st)
-                       : field_dx_launch<NT, 64>(ct, dy, dx, batch, n, width, st);
-  if (e != hipSuccess) return e;
-  return c <= 32 ? field_coord_launch<NT, 32>(p, ddt, dp, batch, n, c, st)
-                 : field_coord_launch<NT, 64>(p, ddt, dp, batch, n, c, st);
+  return width % 128 == 0 ? field_tail_pick<NT, 128>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st)
+                          : field_tail_pick<NT, 64>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st);
 }
 
 template <int NT>
