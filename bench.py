@@ -874,9 +874,9 @@ def run_field(args, torch, hcmix, inputs, dev):
     calls, replayed as a graph.  Both calls are HBM-bound (about 60 flops per
     byte against the bf16 ridge near 315), so the roofline is bytes: forward
     reads p and x and writes y and two fp32 row statistics; backward reads p,
-    x, dy and the statistics and writes dp and dx (its fp32 squared-distance
-    gradient and each window's coordinate table are workspace, not
-    algorithmic traffic).  Each application has its own workspace: the
+    x, dy and the statistics and writes dp and dx (the couplings, the fp32
+    squared-distance gradient and each window's coordinate table are
+    workspace, not algorithmic traffic).  Each application has its own workspace: the
     forward leaves the coordinate tables there and the backward of the same
     application takes them (reuse_table).  Each call is timed on its own with
     graph_timed, on the stream it runs on."""
@@ -940,9 +940,8 @@ def run_field(args, torch, hcmix, inputs, dev):
     pv_flops = B * n * (n + 1) * w
     entries = {}
     for name, nb, fl, kname in (
-            ("forward", bytes_fwd, pv_flops, "field_fwd_kernel"),
-            ("backward", bytes_bwd, 2 * pv_flops,
-             "field_bwd_rows_kernel + field_bwd_dx_kernel + field_bwd_coord_kernel")):
+            ("forward", bytes_fwd, pv_flops, "field_couple_kernel + field_readout_kernel"),
+            ("backward", bytes_bwd, 2 * pv_flops, "field_bwd_rows_kernel + field_bwd_tail_kernel")):
         sec = us[name] * 1e-6
         gbs = nb / sec / 1e9
         entries[name] = {"bound": "hbm", "kernel": f"{kname} (one {name} call)",
