@@ -34,8 +34,9 @@
 //                           dy_i . y_i), da = C (dP - Delta), and the gradient
 //                           of the squared distances dD (written, fp32,
 //                           [key][query]);
-//   field_bwd_dx_kernel     dx slab = C^T dy (keys in lanes, C as written);
-//   field_bwd_coord_kernel  dp_i = 2 sum_j E[i][j] (p_i - p_j), E = dD + dD^T,
+//   field_bwd_tail_kernel   one launch, two block roles: dx slab = C^T dy
+//                           (keys in lanes, C as written), and
+//                           dp_i = 2 sum_j E[i][j] (p_i - p_j), E = dD + dD^T,
 //                           on the fp32 matrix cores.
 #include "hcmix_internal.h"
 #include "device_common.h"
