@@ -70,19 +70,13 @@ __device__ __forceinline__ bf16x8 ct_row(const bf16* t, int rs, int r, int c0, i
 // `stride` bytes apart: consecutive threads take consecutive elements (every
 // load coalesced, all of a thread's loads issued before its first LDS write);
 // the element -> (row, column) walk advances by a precomputed step, with no
-// division per element.
-struct NoIssue {
-  __device__ __forceinline__ void operator()() const {}
-};
-// `then` runs after the loads are issued and before their values are used
-// (loads it issues queue behind them).  vec: pw is 16-byte aligned and c a
-// multiple of 4, so 16-byte loads never straddle a row (a wave-wide memory
-// instruction costs about the same whatever its width, so wide loads move
-// four times the bytes per instruction).
-template <int THREADS, class Then = NoIssue>
+// division per element.  vec: pw is 16-byte aligned and c a multiple of 4, so
+// 16-byte loads never straddle a row (a wave-wide memory instruction costs
+// about the same whatever its width, so wide loads move four times the bytes
+// per instruction).
+template <int THREADS>
 __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int rows, int c,
-                                             unsigned char* dst, int stride, bool vec,
-                                             Then then = {}) {
+                                             unsigned char* dst, int stride, bool vec) {
   const int total = rows * c;
   if (vec) {
     constexpr int PER = 256 * 64 / 4 / THREADS;     // float4 per thread at 256 rows x 64
@@ -91,7 +85,6 @@ __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int r
 #pragma unroll
     for (int u = 0; u < PER; u++)
       v[u] = ((const f32x4*)pw)[min((int)threadIdx.x + THREADS * u, total4 - 1)];
-    then();
     int r = (4 * threadIdx.x) / c, k = (4 * threadIdx.x) % c;
     const int dr = (4 * THREADS) / c, dk = (4 * THREADS) % c;
 #pragma unroll
@@ -116,7 +109,6 @@ __device__ __forceinline__ void stage_coords(const float* __restrict__ pw, int r
 #pragma unroll
     for (int u = 0; u < PER; u++)   // unconditional loads (clamped): no branch waits per load
       v[u] = pw[min((int)threadIdx.x + THREADS * u, total - 1)];
-    then();
     int r = threadIdx.x / c, k = threadIdx.x % c;
     const int dr = THREADS / c, dk = THREADS % c;
 #pragma unroll
@@ -298,7 +290,7 @@ struct Slab {
   }
 };
 
-// s_waitcnt vmcnt(n) for a wave-uniform runtime n <= 15.
+// s_waitcnt vmcnt(n) for a wave-uniform runtime n (n > 10 waits for all).
 __device__ __forceinline__ void wait_vmcnt_upto(int n) {
   switch (n) {
     case 0: wait_vmcnt<0>(); break;
@@ -383,15 +375,30 @@ constexpr int dx_lds_bytes(int NT, int SW) { return NT * 32 * SW * 2; }
 // (g, r < 4, h < 2) at 16 h + 4 g + r.  A lane of half h then finds its 16
 // couplings of a tile in 32 contiguous bytes.
 __device__ __forceinline__ int ct_pos(int lq) { return 16 * ((lq >> 2) & 1) + 4 * (lq >> 3) + (lq & 3); }
-// rows kernel: NS stages of [x rows (NT * 32)][64] + [dy rows (32)][64] bf16,
+// rows kernel: NS stages of [x rows (NT * 32)][SC] + [dy rows (32)][SC] bf16,
 // the coordinate table in the same space before the stages are used, then
-// the norms and the per-wave row sums.  At NS = 2 a block needs at most 77
-// KB, so two blocks share a CU.
-constexpr int rows_stage_elems(int NT) { return (NT * 32 + 32) * 64; }
-constexpr int rows_lds_bytes(int NT, int NS, int cp) {
-  return cmax(NS * rows_stage_elems(NT) * 2, table_bytes(NT, cp)) + NT * 32 * 4 + 2 * 8 * 32 * 4;
+// the norms and the per-wave row sums.  NS * SC = 128 keeps a block within 77
+// KB, so two blocks share a CU.  Two stages of 64 columns (one step in flight)
+// ran 17.7 us at 64 windows x 256 x 512; four of 32 columns (three in flight,
+// twice the steps and barriers) 20.0 us.
+constexpr int rows_stage_elems(int NT, int SC) { return (NT * 32 + 32) * SC; }
+constexpr int rows_lds_bytes(int NT, int NS, int SC, int cp) {
+  return cmax(NS * rows_stage_elems(NT, SC) * 2, table_bytes(NT, cp)) + NT * 32 * 4 +
+         2 * 8 * 32 * 4;
 }
-constexpr int ROWS_NS = 2;
+constexpr int ROWS_NS = 2, ROWS_SC = 64;
+
+// 32 x 16 operand fragment of a [rows][SC] stage tile (lane l: row r0 + l % 32,
+// columns c0 + 8 (l / 32) .. + 8): SC = 64 in the attention tiles' layout, SC
+// = 32 in the 32-wide k-contiguous swizzle.
+template <int SC>
+__device__ __forceinline__ bf16x8 stage_frag(const bf16* t, int r0, int c0, int lane) {
+  if constexpr (SC == 64) {
+    return att_frag(t, r0, c0, lane);
+  } else {
+    return *(const bf16x8*)(t + swz<32>(r0 + (lane & 31), (c0 >> 3) + (lane >> 5)));
+  }
+}
 // coordinate kernel: E tile [32][NP + 1] fp32, coordinates [NP][ck + 1] fp32,
 // row-sum parts [16][32], and the per-wave partial products [4][32][ck + 1]
 // (in the E tile's space where they fit, else after the rest)
@@ -581,19 +588,21 @@ __global__ __launch_bounds__(FT) void field_readout_kernel(const bf16x8* __restr
 // block's set-up and reductions overlap the other's streaming.
 // The couplings, their squared distances and the row sums come first, from
 // the coordinate table (loaded into the stage space).  Then dP^T[key][q] =
-// x_key . dy_q sums over the width in 64-column steps: each step's x rows
+// x_key . dy_q sums over the width in SC-column steps: each step's x rows
 // [0, 32 (qt + 1)) and the tile's 32 dy rows go global -> LDS by DMA
-// (coalesced, 8 rows of 128 bytes per instruction, swizzled as the 64-column
-// tiles), NS stages in flight, the instructions of a step dealt over the 8
-// waves.  The per-row sums Delta and sum(da D) across the waves go through
+// (coalesced, 1 KB of whole rows per instruction, swizzled as stage_frag
+// reads them), NS - 1 steps in flight, the instructions of a step dealt over
+// the 8 waves.  The per-row sums Delta and sum(da D) across the waves go through
 // LDS.
 // ---------------------------------------------------------------------------
-template <int NT, int NS>
+template <int NT, int NS, int SC>
 __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
     const unsigned char* __restrict__ tab, const bf16* __restrict__ x, const bf16* __restrict__ dy,
     const float* __restrict__ row_mean, const float* __restrict__ lse, float* __restrict__ ddt,
     bf16* __restrict__ ct, int n, int cp, int width, float inv_tau, int scaled) {
-  constexpr int NP = NT * 32, STAGE = rows_stage_elems(NT);
+  constexpr int NP = NT * 32, STAGE = rows_stage_elems(NT, SC);
+  constexpr int RPI = 512 / SC, LPR = SC / 8;         // rows per DMA instruction, lanes per row
+  constexpr int VMAX = ((NP + 32) / RPI + 7) / 8;     // DMA instructions per wave and step
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   bf16* sStage = (bf16*)smem;
   bf16* sT = sStage;                                  // the table, until the first DMA
@@ -607,28 +616,29 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
   const int q = qt * 32 + (lane & 31);
   const bool qvalid = q < n;
   const bool own = wave <= qt;                        // this wave's key tile kt = wave
-  const int steps = width / 64;
-  // DMA plan of one step: instructions u < XI are x rows 8u .. 8u + 7, the
-  // next 4 the tile's dy rows; wave w issues u = w, w + 8, ...  Rows past the
-  // window read its last row (finite values that only reach couplings the
-  // causal mask removes, or rows whose results are not used).
-  const int XI = (qt + 1) * 4, TI = XI + 4;
+  const int steps = width / SC;
+  // DMA plan of one step: instructions u < XI are x rows RPI u .. RPI u +
+  // RPI - 1, the next 32 / RPI the tile's dy rows; wave w issues u = w, w + 8,
+  // ...  Rows past the window read its last row (finite values that only reach
+  // couplings the causal mask removes, or rows whose results are not used).
+  const int XI = (qt + 1) * 32 / RPI, TI = XI + 32 / RPI;
   const int cnt = wave < TI ? (TI - 1 - wave) / 8 + 1 : 0;
   const bf16* xw = x + (size_t)b * n * width;
   const bf16* dyw = dy + (size_t)b * n * width;
   auto dma = [&](int st, int slot) {
     bf16* dst = sStage + slot * STAGE;
 #pragma unroll
-    for (int v = 0; v < 5; v++) {
+    for (int v = 0; v < VMAX; v++) {
       if (v < cnt) {
         const int u = wave + 8 * v;
-        const int lr = 8 * u + (lane >> 3);               // row in the stage (x rows, then dy)
-        const int tr = u < XI ? lr : qt * 32 + (lr - 8 * XI);   // row in the window
+        const int lr = RPI * u + lane / LPR;              // row in the stage (x rows, then dy)
+        const int tr = u < XI ? lr : qt * 32 + (lr - RPI * XI);   // row in the window
         const int gr = tr < n ? tr : n - 1;
-        const int tile_row = u < XI ? lr : lr - 8 * XI;
-        const int piece = (lane & 7) ^ att_sw(tile_row);
-        const bf16* src = (u < XI ? xw : dyw) + (size_t)gr * width + st * 64 + 8 * piece;
-        bf16* d0 = u < XI ? dst + u * 512 : dst + NP * 64 + (u - XI) * 512;
+        const int tile_row = u < XI ? lr : lr - RPI * XI;
+        const int lp = lane % LPR;
+        const int piece = SC == 64 ? lp ^ att_sw(tile_row) : lp ^ ((tile_row >> 2) & 3);
+        const bf16* src = (u < XI ? xw : dyw) + (size_t)gr * width + st * SC + 8 * piece;
+        bf16* d0 = u < XI ? dst + u * 512 : dst + NP * SC + (u - XI) * 512;
         dma16(src, d0);
       }
     }
@@ -678,9 +688,9 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
     if (own) {
       const bf16* cur = sStage + (st % NS) * STAGE;
 #pragma unroll
-      for (int ks = 0; ks < 4; ks++)
-        g = mfma32(att_frag(cur, wave * 32, 16 * ks, lane),
-                   att_frag(cur + NP * 64, 0, 16 * ks, lane), g);
+      for (int ks = 0; ks < SC / 16; ks++)
+        g = mfma32(stage_frag<SC>(cur, wave * 32, 16 * ks, lane),
+                   stage_frag<SC>(cur + NP * SC, 0, 16 * ks, lane), g);
     }
   }
   // Delta_q = sum_j C dP (in-lane, the lane ^ 32 exchange, then the 8 waves)
@@ -1000,15 +1010,15 @@ hipError_t field_fwd_pick(const float* p, const bf16* x, bf16* y, float* row_mea
                           : field_readout_launch<NT, 64>(cq, x, y, batch, n, width, st);
 }
 
-template <int NT, int NS>
+template <int NT, int NS, int SC>
 hipError_t field_rows_launch(const unsigned char* tab, const bf16* x, const float* row_mean,
                              const float* lse, const bf16* dy, float* ddt, bf16* ct, int batch, int n,
                              int cp, int width, float inv_tau, int scaled, hipStream_t st) {
   static std::atomic<unsigned long long> done{0};
-  hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS>,
-                                rows_lds_bytes(NT, NS, 64));
+  hipError_t e = lds_limit_once(done, (const void*)field_bwd_rows_kernel<NT, NS, SC>,
+                                rows_lds_bytes(NT, NS, SC, 64));
   if (e != hipSuccess) return e;
-  field_bwd_rows_kernel<NT, NS><<<batch * NT, FT, rows_lds_bytes(NT, NS, cp), st>>>(
+  field_bwd_rows_kernel<NT, NS, SC><<<batch * NT, FT, rows_lds_bytes(NT, NS, SC, cp), st>>>(
       tab, x, dy, row_mean, lse, ddt, ct, n, cp, width, inv_tau, scaled);
   return hipGetLastError();
 }
@@ -1048,8 +1058,8 @@ hipError_t field_bwd_launch(const float* p, const bf16* x, const float* row_mean
     e = field_prep_launch<NT>(p, tab, batch, n, c, cp, st);
     if (e != hipSuccess) return e;
   }
-  e = field_rows_launch<NT, ROWS_NS>(tab, x, row_mean, lse, dy, ddt, ct, batch, n, cp, width,
-                                     inv_tau, scaled, st);
+  e = field_rows_launch<NT, ROWS_NS, ROWS_SC>(tab, x, row_mean, lse, dy, ddt, ct, batch, n, cp,
+                                              width, inv_tau, scaled, st);
   if (e != hipSuccess) return e;
   return width % 128 == 0 ? field_tail_pick<NT, 128>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st)
                           : field_tail_pick<NT, 64>(ct, dy, dx, p, ddt, dp, batch, n, c, width, st);
