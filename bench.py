@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--cpu-windows", type=int, default=0,
                     help="windows in the oracle sample (0: sized for ~10-30 s)")
     ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--mode", default="preset", choices=["preset", "causal", "bidir"],
+                    help="lm256, reach, long4096: run the stack causal or bidirectional instead "
+                         "of the preset's mode")
     ap.add_argument("--attention", default="native", choices=["native", "sdpa"],
                     help="hybrid workloads: the library's attention core, or PyTorch SDPA")
     ap.add_argument("--proj", default="library", choices=["library", "torch"],
@@ -242,6 +245,8 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
     import torch
     reps = args.kernel_reps
     xs = [x0, *xs_out[:L - 1]]
+    # committed counter figures belong to the preset's mode only
+    pkey = args.workload if args.mode == "preset" else f"{args.workload} ({args.mode})"
 
     def timed(fn, count):
         return graph_timed(torch, fn, count)
@@ -256,7 +261,7 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
         return {"roofline": {"bound": "hbm", "kernel": kname + " (one hcmix_stack_backward call)",
                              "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                              "frac": round(gbs / PEAK_HBM_GBS, 4),
-                             "traffic": profiled_traffic(args.workload, kname),
+                             "traffic": profiled_traffic(pkey, kname),
                              "avg_launch_us": round(sec * 1e6, 2), "algorithmic_bytes": nbytes}}
 
     def fwd_layers():
@@ -271,9 +276,9 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
     out = {"roofline": {"bound": "mfma", "kernel": kname + " (one forward layer launch)",
                         "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                        "traffic": profiled_traffic(args.workload, kname),
+                        "traffic": profiled_traffic(pkey, kname),
                         "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops,
-                        "counters": profiled_mfma(args.workload, kname, sec, flops)}}
+                        "counters": profiled_mfma(pkey, kname, sec, flops)}}
     if deferred_path(n, w, L):
         # the saved activations stand in for the output gradients: the same
         # shapes and magnitudes, and the kernel's work does not depend on values
@@ -287,9 +292,9 @@ def dominant_kernel(args, hcmix, stream, x0, ws, wo, dy, xs_out, dx_out, dws, dw
                               "layers, one launch)", "achieved": round(tflops, 2),
                               "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                              "traffic": profiled_traffic(args.workload, kname),
+                              "traffic": profiled_traffic(pkey, kname),
                               "avg_launch_us": round(sec * 1e6, 2), "algorithmic_flops": flops,
-                              "counters": profiled_mfma(args.workload, kname, sec, flops)}
+                              "counters": profiled_mfma(pkey, kname, sec, flops)}
     sec = timed(lambda: hcmix.stack_backward(xs, ws, wo, layers, dy, causal, dx=dx_out[0],
                                              dws=dws, dwo=dwo, workspace=workspace), reps)
     out["backward_call_us"] = round(sec * 1e6, 2)
@@ -310,6 +315,10 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
+    if args.mode != "preset" and args.workload not in inputs.PRESETS:
+        print(f"bench.py: --mode applies to the stack workloads {sorted(inputs.PRESETS)}",
+              file=sys.stderr)
+        return 2
     hcmix.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -325,6 +334,8 @@ def main():
     if args.workload == "shared256":
         return run_shared(args, torch, hcmix, inputs, dev)
     over = {"batch": args.batch} if args.batch > 0 else {}
+    if args.mode != "preset":
+        over["causal"] = args.mode == "causal"
     cfg = dict(inputs.PRESETS[args.workload], **over)
     s = inputs.make_preset(args.workload, **over)
     B, n, w, L, causal = cfg["batch"], cfg["n"], cfg["width"], cfg["num_layers"], cfg["causal"]
@@ -388,7 +399,9 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOADS[args.workload]}"
-                               + (f" (batch overridden to {B})" if over else ""), "batch": B,
+                               + (f" (batch overridden to {B})" if args.batch > 0 else "")
+                               + (f" (mode overridden to {args.mode})" if args.mode != "preset"
+                                  else ""), "batch": B,
                    "n": n, "width": w, "layers": L, "mode": "causal" if causal else "bidir",
                    "graph": bool(args.graph)},
         "pct_bf16_peak": round(flops / t * args.steps / 1e12 / PEAK_BF16_TFLOPS * 100, 2),
