@@ -313,6 +313,22 @@ __device__ __forceinline__ void wait_vmcnt_upto(int n) {
 // of the other side) sums to the same 9 for every SIMD at 8 tiles.
 __device__ __forceinline__ int wave_tile(int wave) { return wave < 4 ? wave : 11 - wave; }
 
+// Block bid of total -> (window b, query tile qt) for the kernels with one
+// block per query tile, two of them per CU.  Blocks go to the 8 XCDs round
+// robin (xcd_tile keeps a window's tiles on one XCD) and, within an XCD, to
+// its CUs in order, so the first and the second half of an XCD's blocks meet
+// on the same CUs.  The first half takes its windows' tiles heaviest first,
+// the second half lightest first: each CU then pairs tile t with tile NT - 1 -
+// t (NT + 1 key tiles of causal work) instead of holding two copies of one.
+// When an XCD's half is not a whole number of windows, all go heaviest first.
+__device__ __forceinline__ void query_tile_of(int bid, int total, int NT, int* b, int* qt) {
+  const int lin = xcd_tile(bid, total);
+  const int t = lin % NT, group = total / 8;
+  *b = lin / NT;
+  const bool paired = total % (16 * NT) == 0 && lin % group >= group / 2;
+  *qt = paired ? t : NT - 1 - t;
+}
+
 // The lane's own row of the table as B-operand fragments: hi and lo halves,
 // the 8 components of each 16-wide k step that lane half h contributes.
 struct RowFrags {
@@ -409,8 +425,8 @@ constexpr int coord_lds_bytes(int NT, int ck) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward, couplings.  Block = (window b, query tile qt), 8 waves; grid =
-// batch * NT, dealt so that the tiles of one window share an XCD.
+// Forward, couplings.  Block = (window b, query tile qt) (query_tile_of), 8
+// waves; grid = batch * NT.
 //   1. The table rows [0, 32 (qt + 1)) are built in LDS; the block of the
 //      last tile, which has every row, leaves the table in the workspace for
 //      the backward.
@@ -439,8 +455,8 @@ __global__ __launch_bounds__(FT) void field_couple_kernel(
   float* sN = (float*)(smem + table_bytes(NT, cp));
   float* sNp = sN + NP;                               // [cp / 4][NP] while the table is built,
   float* sRed = sNp;                                  // then [3][8 waves][32]: D, Z, entropy sums
-  const int lin = xcd_tile(blockIdx.x, gridDim.x);
-  const int b = lin / NT, qt = NT - 1 - lin % NT;
+  int b, qt;
+  query_tile_of(blockIdx.x, gridDim.x, NT, &b, &qt);
   const int lane = threadIdx.x & 63, half = lane >> 5, lq = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int rs = ct_stride(cp);
@@ -582,10 +598,10 @@ __global__ __launch_bounds__(FT) void field_readout_kernel(const bf16x8* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Backward, rows.  Block = (window b, query tile qt), the heaviest tiles of a
-// window first; 8 waves, wave w owning key tile w (w <= qt).  Two blocks share
-// a CU (the grid's second half, the light tiles, beside the first), so one
-// block's set-up and reductions overlap the other's streaming.
+// Backward, rows.  Block = (window b, query tile qt) (query_tile_of); 8 waves,
+// wave w owning key tile w (w <= qt).  Two blocks share a CU, a heavy tile
+// beside a light one, so one block's set-up and reductions overlap the
+// other's streaming.
 // The couplings, their squared distances and the row sums come first, from
 // the coordinate table (loaded into the stage space).  Then dP^T[key][q] =
 // x_key . dy_q sums over the width in SC-column steps: each step's x rows
@@ -608,8 +624,8 @@ __global__ __launch_bounds__(FT) void field_bwd_rows_kernel(
   bf16* sT = sStage;                                  // the table, until the first DMA
   float* sN = (float*)(smem + cmax(NS * STAGE * 2, table_bytes(NT, cp)));
   float* sRed = sN + NP;                              // [2][8 waves][32]
-  const int lin = xcd_tile(blockIdx.x, gridDim.x);
-  const int b = lin / NT, qt = NT - 1 - lin % NT;
+  int b, qt;
+  query_tile_of(blockIdx.x, gridDim.x, NT, &b, &qt);
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int rs = ct_stride(cp);
@@ -939,10 +955,11 @@ __global__ __launch_bounds__(FT) void field_bwd_tail_kernel(
     const bf16* __restrict__ ct, const bf16* __restrict__ dy, bf16* __restrict__ dx, int width,
     int slabs, const float* __restrict__ p, const float* __restrict__ ddt, float* __restrict__ dp,
     int n, int c, int vec, int dx_blocks) {
-  if ((int)blockIdx.x < dx_blocks)
-    dx_block<NT, SW>(blockIdx.x, dx_blocks, ct, dy, dx, n, width, slabs);
+  const int coord_blocks = gridDim.x - dx_blocks;
+  if ((int)blockIdx.x < coord_blocks)
+    coord_block<NT, CK>(blockIdx.x, coord_blocks, p, ddt, dp, n, c, vec);
   else
-    coord_block<NT, CK>(blockIdx.x - dx_blocks, gridDim.x - dx_blocks, p, ddt, dp, n, c, vec);
+    dx_block<NT, SW>(blockIdx.x - coord_blocks, dx_blocks, ct, dy, dx, n, width, slabs);
 }
 
 // Whether the coordinates take the 16-byte load path: p 16-byte aligned and
