@@ -80,8 +80,10 @@ def check(got, ref, tag):
 
 # (batch, n, width, coord_dim, tau, scaled, mean squared distance): every tile
 # count, ragged windows, one and several 32-wide coordinate tiles, both forms,
-# the saturated regime of Section 7 (unscaled, d^2 about 100, tau 1) and an
-# unscaled kernel with spread-out partners
+# the saturated regime of Section 7 (unscaled, d^2 about 100, tau 1), an
+# unscaled kernel with spread-out partners, and full 8-tile windows with the
+# widest coordinates (64, and 61 padded to 64) and widths that are not a
+# multiple of 128
 CASES = [
     (2, 256, 128, 32, 1.0, True, 100.0),
     (2, 256, 64, 32, 1.0, False, 100.0),
@@ -95,6 +97,8 @@ CASES = [
     (2, 128, 128, 8, 1.0, False, 2.0),
     (1, 224, 256, 40, 0.25, False, 0.5),
     (2, 96, 64, 2, 3.0, True, 1e4),
+    (2, 256, 192, 64, 1.0, True, 100.0),
+    (1, 250, 128, 61, 0.8, False, 30.0),
 ]
 
 
