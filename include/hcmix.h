@@ -22,9 +22,11 @@
  *
  * Ownership and ordering: the caller owns every buffer (device memory) and
  * keeps it alive until the enqueued work finishes.  The library allocates and
- * frees nothing, keeps no state between calls, never synchronises, and
- * enqueues all work on `stream` in call order.  Calls on different streams
- * that share an output buffer race.
+ * frees nothing, keeps no state between calls (two exceptions, stated where
+ * they apply: hcmix_backward_no_alloc's scratch array, and the coordinate
+ * tables the field forward leaves in the caller's workspace), never
+ * synchronises, and enqueues all work on `stream` in call order.  Calls on
+ * different streams that share an output buffer race.
  *
  * Errors: arguments are validated before anything is enqueued; a rejected
  * call has no effect.  HCMIX_ERR_INVALID_VALUE: null pointer, batch < 1, n not

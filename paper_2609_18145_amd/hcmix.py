@@ -7,6 +7,8 @@ raises on first use: there is no CPU or PyTorch fallback.
     y = forward(x, w_self, w_off, layer, causal)
     dx, dws, dwo = backward(x, w_self, w_off, dy, layer, causal)
     y = Stack.apply(x, layers, causal, *w_selfs, *w_offs)   # autograd over L layers
+    y, m, lse, partners = field_forward(p, x, tau, scaled, workspace=ws)
+    dp, dx = field_backward(p, x, m, lse, dy, tau, scaled, workspace=ws, reuse_table=True)
 """
 from __future__ import annotations
 
