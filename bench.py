@@ -312,13 +312,14 @@ def main():
     import torch
     from paper_2609_18145_amd import hcmix, inputs
 
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        return 1
     if args.mode != "preset" and args.workload not in inputs.PRESETS:
         print(f"bench.py: --mode applies to the stack workloads {sorted(inputs.PRESETS)}",
               file=sys.stderr)
         return 2
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
     hcmix.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
