@@ -196,11 +196,14 @@ def _act_dtype(x, name="x"):
 
 
 def _bytes(t):
-    """Byte extent of a workspace or cache tensor (any dtype, contiguous)."""
+    """Byte extent of a workspace or cache tensor (any dtype, contiguous, in GPU
+    memory: the library hands it to kernels as it is)."""
     if t is None:
         return 0
     if not isinstance(t, torch.Tensor) or not t.is_contiguous():
         raise ValueError("workspace/cache: expected a contiguous tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"workspace/cache: on {t.device}, expected GPU memory")
     return t.numel() * t.element_size()
 
 

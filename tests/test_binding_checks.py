@@ -155,3 +155,13 @@ def test_shared_stack_checks():
     refused(hcmix.shared_stack_backward, [x, x], [t, t], [0, 1], x, True,
             dtables=[t, z(n, n)], match="dtables")
     refused(hcmix.shared_stack_backward, [x, x], [t, t], [0, 1], x, True, match="GPU")
+
+
+def test_workspace_must_be_gpu_memory():
+    """A caller's workspace or cache reaches kernels as a raw pointer, so one in
+    host memory is refused before the library is called."""
+    with pytest.raises(ValueError, match="GPU memory"):
+        hcmix._bytes(torch.zeros(64, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="contiguous"):
+        hcmix._bytes(torch.zeros(8, 8, dtype=torch.uint8).t())
+    assert hcmix._bytes(None) == 0
